@@ -1,0 +1,257 @@
+"""ctypes wrapper of the plain CPU oracle (msao_oracle.c).
+
+TEST INFRASTRUCTURE ONLY: the oracle is the reference the GPU path is checked
+against. Only the test suite, the smoke check and the benchmark's CPU-baseline
+leg may import it; the library under paper_2604_02945_amd never does.
+
+Every function here marshals numpy arrays into the C oracle; no arithmetic of
+the method is done in Python.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "msao_oracle.c")
+_LIB = os.path.join(_HERE, "libmsao_oracle.so")
+
+NMOD = 4
+F32, BF16 = 0, 1
+FLAG_TEMPORAL_LITERAL = 1
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (plain -O2, no fast-math, no FMA contraction)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + f".tmp{os.getpid()}"
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-ffp-contract=off",
+                               "-fPIC", "-shared", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Segment(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("row_stride", ctypes.c_int64),
+                ("request", ctypes.c_int32), ("modality", ctypes.c_int32),
+                ("n_frames", ctypes.c_int32), ("tokens_per_frame", ctypes.c_int32),
+                ("hidden", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("keep_ratio", ctypes.c_float)]
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_float), ("tau_s", ctypes.c_float),
+                ("lambda_s", ctypes.c_float * NMOD), ("lambda_t", ctypes.c_float * NMOD),
+                ("flags", ctypes.c_uint32)]
+
+
+_P = ctypes.c_void_p
+
+
+class _Outputs(ctypes.Structure):
+    _fields_ = [(n, _P) for n in ("z", "l1", "l2", "info", "d", "res", "dframe", "sim", "gamma",
+                                  "agg", "rho", "temporal", "beta", "mas", "present",
+                                  "k", "keep", "kept_idx")]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        L = ctypes.CDLL(_LIB)
+        L.orc_run.argtypes = [ctypes.POINTER(_Segment), ctypes.c_int, ctypes.c_int,
+                              ctypes.POINTER(_Params), _P, ctypes.POINTER(_Outputs)]
+        L.orc_run.restype = ctypes.c_int
+        L.orc_select.argtypes = [ctypes.POINTER(_Segment), ctypes.c_int, ctypes.c_int,
+                                 ctypes.POINTER(_Params), _P, _P, _P, _P, _P, _P]
+        L.orc_select.restype = ctypes.c_int
+        L.orc_compact.argtypes = [ctypes.POINTER(_Segment), ctypes.c_int, _P, _P, _P, _P]
+        L.orc_compact.restype = None
+        L.orc_token_stats.argtypes = [_P, ctypes.c_int, ctypes.c_int, ctypes.c_float, _P, _P, _P]
+        L.orc_temporal_pair.argtypes = [_P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_float, _P, _P]
+        L.orc_is_sparse.argtypes = [ctypes.c_uint32, ctypes.c_int, ctypes.c_float]
+        L.orc_is_sparse.restype = ctypes.c_int
+        L.orc_modal_softmax.argtypes = [_P, _P, _P]
+        L.orc_mas_value.argtypes = [ctypes.c_double] * 5 + [ctypes.c_int]
+        L.orc_mas_value.restype = ctypes.c_double
+        L.orc_keep_count.argtypes = [ctypes.c_double, ctypes.c_int64]
+        L.orc_keep_count.restype = ctypes.c_int64
+        L.orc_q24.argtypes = [ctypes.c_float]
+        L.orc_q24.restype = ctypes.c_uint64
+        _lib = L
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+def _dtype_code(seg) -> int:
+    return F32 if seg.dtype == "f32" else BF16
+
+
+def _segment_table(segments: Sequence) -> ctypes.Array:
+    arr = (_Segment * max(1, len(segments)))()
+    for i, s in enumerate(segments):
+        data = s.data
+        if data.ndim != 2:
+            raise ValueError("segment data must be [tokens, row_stride]")
+        arr[i].data = data.ctypes.data if data.size else None
+        arr[i].row_stride = data.shape[1] if data.size else s.hidden
+        arr[i].request = s.request
+        arr[i].modality = s.modality
+        arr[i].n_frames = s.n_frames
+        arr[i].tokens_per_frame = s.tokens_per_frame
+        arr[i].hidden = s.hidden
+        arr[i].dtype = _dtype_code(s)
+        arr[i].keep_ratio = s.keep_ratio
+    return arr
+
+
+def _params(p: dict) -> _Params:
+    q = _Params()
+    q.tau = p["tau"]
+    q.tau_s = p["tau_s"]
+    for m in range(NMOD):
+        q.lambda_s[m] = p["lambda_s"][m]
+        q.lambda_t[m] = p["lambda_t"][m]
+    q.flags = p.get("flags", 0)
+    return q
+
+
+def _is_temporal(s) -> bool:
+    return s.modality == 2 and s.n_frames >= 2 and s.tokens_per_frame > 0
+
+
+def run(segments: Sequence, n_requests: int, params: dict, alpha: Optional[np.ndarray] = None,
+        compact: bool = True) -> dict:
+    """Run every step of the analysis on the CPU; returns numpy arrays.
+
+    `segments` carry request, modality, n_frames, tokens_per_frame, hidden,
+    dtype ("f32"/"bf16"), keep_ratio and data ([tokens, row_stride], float32
+    or uint16 bf16 bits).
+    """
+    L = lib()
+    n = len(segments)
+    ntok = sum(s.n_frames * s.tokens_per_frame for s in segments)
+    nframe = sum(s.n_frames for s in segments if _is_temporal(s))
+    R = n_requests
+    o = {
+        "z": np.zeros(ntok, np.uint32), "l1": np.zeros(ntok, np.float32),
+        "l2": np.zeros(ntok, np.float32), "info": np.zeros(ntok, np.float32),
+        "d": np.zeros(ntok, np.uint32), "res": np.zeros(ntok, np.float32),
+        "dframe": np.zeros(nframe, np.uint64), "sim": np.zeros(nframe, np.float32),
+        "gamma": np.zeros(nframe, np.float32),
+        "agg": np.zeros(R * NMOD * 4, np.uint64), "rho": np.zeros(R * NMOD, np.float32),
+        "temporal": np.zeros(R * NMOD, np.float32), "beta": np.zeros(R * NMOD, np.float32),
+        "mas": np.zeros(R * NMOD, np.float32), "present": np.zeros(R * NMOD, np.uint8),
+        "k": np.zeros(max(n, 1), np.int32), "keep": np.zeros(ntok, np.uint8),
+        "kept_idx": np.zeros(ntok, np.int32),
+    }
+    outs = _Outputs(**{k: _ptr(v) for k, v in o.items()})
+    segt = _segment_table(segments)
+    prm = _params(params)
+    al = None if alpha is None else np.ascontiguousarray(alpha, dtype=np.float32).reshape(-1)
+    if al is not None and al.size != R * NMOD:
+        raise ValueError("alpha must hold n_requests * 4 logits")
+    rc = L.orc_run(segt, n, R, ctypes.byref(prm), _ptr(al), ctypes.byref(outs))
+    if rc != 0:
+        raise RuntimeError(f"orc_run failed ({rc})")
+    o["k"] = o["k"][:n]
+    if compact:
+        o["compact"] = compact_rows(segments, o["k"], o["kept_idx"])
+    return o
+
+
+def select(segments: Sequence, n_requests: int, params: dict, z: np.ndarray,
+           d: Optional[np.ndarray], mas: Optional[np.ndarray]) -> dict:
+    """Selection only, from given per-token z, d and per-(request, modality) MAS."""
+    L = lib()
+    n = len(segments)
+    ntok = sum(s.n_frames * s.tokens_per_frame for s in segments)
+    z = np.ascontiguousarray(z, dtype=np.uint32)
+    d = None if d is None else np.ascontiguousarray(d, dtype=np.uint32)
+    mas = None if mas is None else np.ascontiguousarray(mas, dtype=np.float32)
+    k = np.zeros(max(n, 1), np.int32)
+    keep = np.zeros(ntok, np.uint8)
+    kept = np.zeros(ntok, np.int32)
+    rc = L.orc_select(_segment_table(segments), n, n_requests, ctypes.byref(_params(params)),
+                      _ptr(z), _ptr(d), _ptr(mas), _ptr(k), _ptr(keep), _ptr(kept))
+    if rc != 0:
+        raise RuntimeError(f"orc_select failed ({rc})")
+    return {"k": k[:n], "keep": keep, "kept_idx": kept}
+
+
+def compact_rows(segments: Sequence, k: np.ndarray, kept_idx: np.ndarray) -> list:
+    """Packed kept rows per segment (list of [k_s, hidden] arrays, input dtype)."""
+    L = lib()
+    offs = []
+    total = 0
+    for s, ks in zip(segments, k):
+        offs.append(total)
+        total += int(ks) * s.hidden * (4 if s.dtype == "f32" else 2)
+    buf = np.zeros(max(total, 1), np.uint8)
+    off_arr = np.asarray(offs if offs else [0], dtype=np.int64)
+    k32 = np.ascontiguousarray(k, dtype=np.int32)
+    L.orc_compact(_segment_table(segments), len(segments), _ptr(k32),
+                  _ptr(np.ascontiguousarray(kept_idx, dtype=np.int32)), _ptr(buf), _ptr(off_arr))
+    rows = []
+    for s, ks, off in zip(segments, k, offs):
+        nb = int(ks) * s.hidden * (4 if s.dtype == "f32" else 2)
+        dt = np.float32 if s.dtype == "f32" else np.uint16
+        rows.append(buf[off:off + nb].view(dt).reshape(int(ks), s.hidden))
+    return rows
+
+
+# ---- single steps, for pinning each on its own --------------------------------
+
+def token_stats(row: np.ndarray, dtype: str, tau: float):
+    row = np.ascontiguousarray(row)
+    a = np.zeros(1, np.uint32)
+    l1 = np.zeros(1, np.float64)
+    l2 = np.zeros(1, np.float64)
+    lib().orc_token_stats(_ptr(row), F32 if dtype == "f32" else BF16, row.shape[-1], tau,
+                          _ptr(a), _ptr(l1), _ptr(l2))
+    return int(a[0]), float(l1[0]), float(l2[0])
+
+
+def temporal_pair(cur: np.ndarray, prev: Optional[np.ndarray], dtype: str, tau: float):
+    cur = np.ascontiguousarray(cur)
+    prev = None if prev is None else np.ascontiguousarray(prev)
+    d = np.zeros(1, np.uint32)
+    res = np.zeros(1, np.float64)
+    lib().orc_temporal_pair(_ptr(cur), _ptr(prev), F32 if dtype == "f32" else BF16,
+                            cur.shape[-1], tau, _ptr(d), _ptr(res))
+    return int(d[0]), float(res[0])
+
+
+def is_sparse(a: int, C: int, tau_s: float) -> bool:
+    return bool(lib().orc_is_sparse(a, C, tau_s))
+
+
+def modal_softmax(alpha: Sequence[float], present: Sequence[int]) -> np.ndarray:
+    al = np.ascontiguousarray(alpha, dtype=np.float64)
+    pr = np.ascontiguousarray(present, dtype=np.int32)
+    beta = np.zeros(NMOD, np.float64)
+    lib().orc_modal_softmax(_ptr(al), _ptr(pr), _ptr(beta))
+    return beta
+
+
+def mas_value(beta, lam_s, rho, lam_t, tterm, has_t) -> float:
+    return lib().orc_mas_value(beta, lam_s, rho, lam_t, tterm, int(has_t))
+
+
+def keep_count(kappa: float, N: int) -> int:
+    return int(lib().orc_keep_count(kappa, N))
+
+
+def q24(lam: float) -> int:
+    return int(lib().orc_q24(lam))
