@@ -1,0 +1,193 @@
+"""Benchmark of the MAS hot path on one MI355X.
+
+One step = one msao_run over one batch: per-token statistics (and the temporal
+term for video), per-modality aggregation and MAS, per-segment top-k selection
+and compaction of the kept rows. Inputs are seeded synthetic tensors already
+resident in HBM; several replicas of the batch are rotated so that every step
+reads from HBM and not from the 256 MB Infinity Cache.
+
+Prints one JSON line (see the repository's design notes for every field).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "tokens scored+selected/sec and achieved HBM GB/s vs MI355X peak"
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=4, help="workload 1..5 (default 4: tri-modal batch)")
+    ap.add_argument("--replicas", type=int, default=0, help="input replicas rotated per step (0: enough for 1 GB)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU time budget of the oracle baseline")
+    ap.add_argument("--no-compact", action="store_true", help="time score+select only (no compaction)")
+    return ap.parse_args()
+
+
+def pack_replicas(w, n_rep, dev):
+    """Copy the workload's segments into n_rep contiguous device buffers."""
+    import numpy as np
+    import torch
+
+    import paper_2604_02945_amd as msao
+
+    offs, total = [], 0
+    for s in w.segments:
+        offs.append(total)
+        total += (s.data.nbytes + 255) // 256 * 256
+    host = np.zeros(total, np.uint8)
+    for s, o in zip(w.segments, offs):
+        host[o:o + s.data.nbytes] = np.ascontiguousarray(s.data).view(np.uint8).reshape(-1)
+    first = torch.from_numpy(host).to(dev)
+    bufs = [first] + [first.clone() for _ in range(n_rep - 1)]
+    reps = []
+    for b in bufs:
+        segs = []
+        for s, o in zip(w.segments, offs):
+            nb = s.data.nbytes
+            t = b[o:o + nb]
+            t = t.view(torch.float32) if s.dtype == "f32" else t.view(torch.bfloat16)
+            segs.append(msao.DeviceSegment(t.view(s.n_tokens, s.hidden), s.request, s.modality, s.keep_ratio,
+                                           s.n_frames))
+        reps.append(segs)
+    return reps, total
+
+
+def algorithmic_bytes(w, kept_rows_bytes, kept_total):
+    """Bytes the method must move (see the design notes): input rows read once,
+    16 B/token of statistics (z, l1, l2, info), 8 B/token more for video tokens
+    (d, res), 1 B/token keep flag, 4 B per kept index, and the kept rows written."""
+    ntok = w.n_tokens
+    nvid = sum(s.n_tokens for s in w.segments if s.modality == 2 and s.n_frames >= 2)
+    score = w.input_bytes + 16 * ntok + 8 * nvid
+    select = ntok * 1 + 4 * kept_total
+    return score, select, kept_rows_bytes
+
+
+def cpu_baseline(w, budget_s):
+    import oracle
+
+    runs, t0 = 0, time.perf_counter()
+    t_oracle = 0.0
+    while True:
+        a = time.perf_counter()
+        oracle.run(w.segments, w.n_requests, w.params, compact=True)
+        t_oracle += time.perf_counter() - a
+        runs += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    return {"value": w.n_tokens * runs / t_oracle, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"whole workload ({w.n_tokens} tokens) x {runs} runs of the single-threaded C oracle "
+                      f"(fp64 sums, sort-based selection, compaction), {t_oracle:.1f} s",
+            "host_cpu": platform.processor() or platform.machine()}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the analysis shards by request "
+              "with no exchange, so more GPUs would repeat the one-GPU line", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2604_02945_amd as msao
+    from workloads import CONFIG_NAMES, make_workload
+
+    dev = torch.device("cuda", 0)
+    w = make_workload(args.config)
+    n_rep = args.replicas or max(2, -(-1_000_000_000 // w.input_bytes))
+    reps, buf_bytes = pack_replicas(w, n_rep, dev)
+    R, n = w.n_requests, len(w.segments)
+    has_video = any(s.modality == 2 and s.n_frames >= 2 for s in w.segments)
+    fields = ("z", "l1", "l2", "info", "d", "res") if has_video else ("z", "l1", "l2", "info")
+    ctx = msao.Context(0)
+    out = msao.Outputs(reps[0], R, token_fields=fields, compact=not args.no_compact)
+    calls = [msao.prepare("msao_run", segs, R, out, w.params, ctx=ctx, compact=not args.no_compact)
+             for segs in reps]
+    stream = torch.cuda.current_stream()
+
+    for i in range(args.warmup):
+        calls[i % n_rep](stream)
+    torch.cuda.synchronize()
+    kept_count = out.sel["kept_count"][:n].cpu().numpy()
+    kept_total = int(kept_count.sum())
+    kept_rows_bytes = int(sum(int(k) * s.hidden * (4 if s.dtype == "f32" else 2)
+                              for k, s in zip(kept_count, w.segments)))
+    if args.no_compact:
+        kept_rows_bytes = 0
+
+    # timed region: K whole steps, replicas rotated
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for i in range(args.steps):
+        calls[i % n_rep](stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    ms_step = e0.elapsed_time(e1) / args.steps
+
+    # per-kernel durations: HIP events recorded by the library around each launch on this stream
+    ctx.set_profiling(True)
+    ksum = np.zeros(3)
+    kn = max(20, args.steps // 4)
+    for i in range(kn):
+        calls[i % n_rep](stream)
+        ksum += np.array(ctx.kernel_times())
+    ctx.set_profiling(False)
+    k_ms = ksum / kn
+
+    b_score, b_select, b_compact = algorithmic_bytes(w, kept_rows_bytes, kept_total)
+    b_step = b_score + b_select + b_compact
+    score_gbs = b_score / (k_ms[0] * 1e-3) / 1e9
+    line = {
+        "metric": METRIC,
+        "value": w.n_tokens / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{CONFIG_NAMES[args.config]} (config {args.config})",
+            "requests": R, "segments": n, "tokens": w.n_tokens, "input_dtype": sorted({s.dtype for s in w.segments}),
+            "input_bytes": w.input_bytes, "kept_tokens": kept_total, "replicas_rotated": n_rep,
+            "compaction": not args.no_compact,
+        },
+        "hbm_gbps_step": b_step / (ms_step * 1e-3) / 1e9,
+        "hbm_frac_step": b_step / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS,
+        "algorithmic_bytes": {"score": b_score, "select": b_select, "compact_write": b_compact},
+        "kernel_ms": {"score": k_ms[0], "post": k_ms[1], "gather": k_ms[2]},
+        "roofline": {"bound": "hbm", "kernel": "k_score", "achieved": score_gbs, "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": score_gbs / PEAK_HBM_GBS, "traffic": None},
+        "wall_s_timed": wall,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    ctx.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,238 @@
+/*
+ * msao.h -- C ABI of the MI355X (gfx950) implementation of MSAO's
+ * fine-grained sparsity analysis: per-token activation-sparsity statistics,
+ * the temporal-redundancy term between consecutive video frames, per-modality
+ * aggregation into MAS (Modal Activation Sparsity), and the MAS-guided
+ * selection and compaction of the tokens that are kept.
+ *
+ * Paper: "MSAO" (arXiv 2604.02945). Sec. 4.1 defines the probing module:
+ * spatial sparsity (Sec. 4.1.1, Eq. 3-4), temporal sparsity (Sec. 4.1.2,
+ * Eq. 5), modal sparsity (Sec. 4.1.3, Eq. 6 and the softmax after it) and
+ * MAS (Sec. 4.1.4, Eq. 7). Eq. 11's last constraint (retained proportion at
+ * least 1 - MAS) sets the MAS-guided keep ratio; Sec. 4.1.1 prunes the patches
+ * of low importance.
+ *
+ * Stand-ins for what the paper leaves open (all exact and parameter-free):
+ *  - importance of a token = fraction of its C channels that are active, a
+ *    channel being active iff NOT(|x| <= tau) (NaN is active, -0 is not);
+ *  - the LSH of Eq. 5 = bit sampling over the activity bits, every channel
+ *    sampled once; frame 0 is compared with an all-zero frame and left out of
+ *    the averages; a clip with one frame has no temporal term;
+ *  - the temporal term of Eq. 7 is the redundancy 1 - gamma_avg, or gamma_avg
+ *    as printed under MSAO_FLAG_TEMPORAL_LITERAL; the bracket of Eq. 7 is
+ *    clamped to [0, 1];
+ *  - relevance logits alpha (Eq. 6) are supplied by the caller (0 if absent);
+ *  - a token's redundancy key is the exact integer
+ *        key = Ls*z + Lt*e,  Ls = rne(lambda_s[m] * 2^24), Lt = rne(lambda_t[m] * 2^24),
+ *    z = inactive channels, e = C - d (channels whose activity equals the
+ *    previous frame's; temporal segments only, else the term is absent);
+ *    each segment keeps its k smallest (key, index) pairs, ties by ascending
+ *    index, with k = min(N, ceil(kappa * N)) computed in double from the
+ *    float keep ratio kappa (kappa = 1 - MAS of the segment's request and
+ *    modality when the keep ratio is negative).
+ *
+ * Conventions
+ *  - Every data pointer is HIP device memory owned by the caller unless it is
+ *    marked "host". The library allocates no device memory: scratch comes
+ *    from the caller's workspace (size from msao_workspace_size). The context
+ *    owns host state only (pinned staging for the small per-call tables, HIP
+ *    events, the last error message).
+ *  - Calls are asynchronous: they enqueue on `stream` (a hipStream_t; NULL is
+ *    the null stream) and return; outputs are valid once the caller has
+ *    synchronised with that stream. Pointers are not retained after return.
+ *  - Validation runs entirely on the host before anything is enqueued: an
+ *    invalid call returns a specific status, writes nothing and records a
+ *    message for msao_last_error. Runtime and launch failures return
+ *    MSAO_ERR_HIP.
+ *  - One context per concurrently used stream (a context is not thread-safe).
+ *  - Token t*P + p of a segment is row (t*P + p) of its data; global token ids
+ *    concatenate the segments in table order. Per-token outputs are indexed by
+ *    global token id. Frames are numbered over the temporal segments only
+ *    (VIDEO, n_frames >= 2, tokens_per_frame > 0), in table order.
+ *    Per-(request, modality) outputs are indexed r*4 + m.
+ *  - Layout: data and row_stride*element_size must be multiples of 16 bytes;
+ *    hidden a multiple of 8 (bf16) or 4 (fp32), at most 65536; n_frames > 1
+ *    only for VIDEO; total tokens below 2^31.
+ */
+#ifndef MSAO_H
+#define MSAO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MSAO_NUM_MODALITIES 4
+#define MSAO_MAX_HIDDEN 65536
+
+typedef enum {
+    MSAO_OK = 0,
+    MSAO_ERR_INVALID_ARG = 1,   /* bad pointer, size, enum value, parameter or output set */
+    MSAO_ERR_ALIGNMENT = 2,     /* data, row pitch or output not aligned as required */
+    MSAO_ERR_WORKSPACE = 3,     /* workspace missing, not 256-byte aligned or too small */
+    MSAO_ERR_UNSUPPORTED = 4,   /* valid request this build does not handle */
+    MSAO_ERR_HIP = 5            /* a HIP runtime call or a kernel launch failed */
+} msao_status;
+
+typedef enum { MSAO_TEXT = 0, MSAO_IMAGE = 1, MSAO_VIDEO = 2, MSAO_AUDIO = 3 } msao_modality;
+typedef enum { MSAO_F32 = 0, MSAO_BF16 = 1 } msao_dtype;
+
+/* Eq. 7 takes gamma_avg itself as the temporal term (default: 1 - gamma_avg). */
+#define MSAO_FLAG_TEMPORAL_LITERAL 1u
+
+typedef struct msao_ctx msao_ctx;
+
+/* One modality-tagged activation tensor of one request (Sec. 3 Eq. 1-2, the
+ * early-layer features F of Eq. 3 and f_t of Eq. 5). */
+typedef struct {
+    const void* data;          /* device; row i at data + i*row_stride elements */
+    int64_t row_stride;        /* elements between consecutive rows, >= hidden */
+    int32_t request;           /* 0 .. n_requests-1 */
+    int32_t modality;          /* msao_modality */
+    int32_t n_frames;          /* T >= 1 (> 1 only for VIDEO) */
+    int32_t tokens_per_frame;  /* P >= 0; the segment has N = T*P tokens */
+    int32_t hidden;            /* C */
+    int32_t dtype;             /* msao_dtype */
+    float keep_ratio;          /* kappa in [0, 1]; negative: MAS-guided, kappa = 1 - MAS */
+} msao_segment;
+
+/* Thresholds and weights (Sec. 5.1.4 defaults from msao_default_params). */
+typedef struct {
+    float tau;                          /* channel activity threshold, >= 0, finite */
+    float tau_s;                        /* Eq. 4 importance threshold, in [0, 1] */
+    float lambda_s[MSAO_NUM_MODALITIES];/* Eq. 7 spatial weight per modality, in [0, 1] */
+    float lambda_t[MSAO_NUM_MODALITIES];/* Eq. 7 temporal weight per modality, in [0, 1] */
+    uint32_t flags;                     /* MSAO_FLAG_* */
+} msao_params;
+
+/* Per-token outputs, [total tokens] each; any pointer may be NULL (not written)
+ * unless the entry point says otherwise. d and res are 0 for tokens of
+ * non-temporal segments. */
+typedef struct {
+    uint32_t* z;     /* inactive channels (importance = 1 - z/C, Eq. 3 stand-in) */
+    float* l1;       /* sum |x| */
+    float* l2;       /* sum x^2 */
+    float* info;     /* 1 - (lambda_s*z + lambda_t*e)/C: informativeness, orders like -key */
+    uint32_t* d;     /* Hamming distance of activity bits to the previous frame (Eq. 5) */
+    float* res;      /* sum (x_t - x_{t-1})^2, the residual energy of Sec. 4.1.2 */
+} msao_token_out;
+
+/* Per-frame outputs of temporal segments, [total temporal frames] each; NULL skips. */
+typedef struct {
+    uint64_t* dframe;/* D_t = sum over the frame's tokens of d */
+    float* sim;      /* Eq. 5: 1 - D_t/(P*C) */
+    float* gamma;    /* 1 - sim (Sec. 4.1.2) */
+} msao_frame_out;
+
+/* Per-(request, modality) outputs, index r*4 + m; NULL skips. */
+typedef struct {
+    uint64_t* agg;   /* [R*4*4]: Ntok, Nsparse (Eq. 4 count), Dsum, Qbits (hash bits compared) */
+    float* rho;      /* Eq. 4 over the modality: Nsparse/Ntok */
+    float* temporal; /* temporal term of Eq. 7 (0 where absent) */
+    float* beta;     /* softmax of alpha over the modalities present (Sec. 4.1.3) */
+    float* mas;      /* Eq. 7 */
+    uint8_t* present;/* 1 if the request has tokens of the modality */
+} msao_req_out;
+
+/* Selection outputs. kept_idx is [total tokens]: segment s owns the range
+ * starting at its global token offset; its first kept_count[s] entries are the
+ * kept token indices (local to the segment) in ascending order, the rest -1. */
+typedef struct {
+    uint8_t* keep;       /* [total tokens] 1 kept / 0 dropped; may be NULL */
+    int32_t* kept_idx;   /* [total tokens], required */
+    int32_t* kept_count; /* [n segments], required */
+} msao_select_out;
+
+/* ---- context and helpers (host only) ------------------------------------ */
+
+/* Create a context bound to HIP device `device`. MSAO_ERR_HIP if it is absent. */
+msao_status msao_create(msao_ctx** ctx, int device);
+/* Destroy a context (NULL is ignored). Waits for the context's pending uploads. */
+void msao_destroy(msao_ctx* ctx);
+/* Message of the last failed call on this context ("" if none). */
+const char* msao_last_error(const msao_ctx* ctx);
+/* Message of the last failed context-free call in this thread ("" if none). */
+const char* msao_last_error_global(void);
+/* Static name of a status code. */
+const char* msao_status_string(msao_status s);
+/* tau 0.1, tau_s 0.3, lambda_s {0, .6, .6, .6}, lambda_t {0, 0, .4, 0}, flags 0. */
+msao_params msao_default_params(void);
+
+/* Check a segment table and parameters without touching any device. */
+msao_status msao_validate(const msao_segment* segs, int n, int n_requests, const msao_params* params);
+/* Total tokens and total temporal frames of a segment table (host only). */
+msao_status msao_count(const msao_segment* segs, int n, int64_t* n_tokens, int64_t* n_frames);
+/* Workspace bytes any entry point needs for this table (host only). */
+msao_status msao_workspace_size(const msao_segment* segs, int n, int n_requests, size_t* bytes);
+/* Default packed compaction layout (host only): out_byte_off[s] (host, [n]) is
+ * where segment s's kept rows start; a segment with a fixed keep ratio gets
+ * room for exactly its k rows, a MAS-guided one for all N rows; offsets are
+ * 256-byte aligned. *total_bytes receives the buffer size needed. */
+msao_status msao_compact_layout(const msao_segment* segs, int n, int64_t* out_byte_off, int64_t* total_bytes);
+
+/* ---- entry points (enqueue on `stream`) ---------------------------------- */
+
+/* Sec. 4.1.1-4.1.4: per-token statistics, per-frame similarity, per-modality
+ * aggregation, softmax and MAS. alpha is host [n_requests*4] logits or NULL. */
+msao_status msao_mas_score(msao_ctx* ctx, const msao_segment* segs, int n, int n_requests,
+                           const msao_params* params, const float* alpha,
+                           const msao_token_out* tok, const msao_frame_out* frm, const msao_req_out* req,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Sec. 4.1.2 Eq. 5 only: d and res per token (0 outside temporal segments),
+ * per-frame D_t, sim and gamma, and the temporal term of Eq. 7 per (request,
+ * modality) (`temporal`, device [n_requests*4], may be NULL). */
+msao_status msao_temporal_redundancy(msao_ctx* ctx, const msao_segment* segs, int n, int n_requests,
+                                     const msao_params* params, uint32_t* d, float* res,
+                                     const msao_frame_out* frm, float* temporal,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Sec. 4.1.1 pruning with the Eq. 11 floor: per-segment top-k selection from
+ * per-token z (and d for temporal segments; may be NULL if there are none).
+ * mas (device [n_requests*4]) is read for segments with a negative keep ratio
+ * and may be NULL if there are none. */
+msao_status msao_select_tokens(msao_ctx* ctx, const msao_segment* segs, int n, int n_requests,
+                               const msao_params* params, const uint32_t* z, const uint32_t* d,
+                               const float* mas, const msao_select_out* sel,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Packed copy of each segment's kept rows: row j of segment s (j <
+ * kept_count[s]) is row kept_idx[off_s + j] of its data, written bitwise at
+ * out + out_byte_off[s] + j*hidden*element_size. out_byte_off is host [n],
+ * 16-byte aligned; each segment needs room for min(N, k) rows where k is its
+ * fixed keep count, or N rows if its keep ratio is negative; out_bytes bounds
+ * every write. */
+msao_status msao_compact(msao_ctx* ctx, const msao_segment* segs, int n,
+                         const int32_t* kept_idx, const int32_t* kept_count,
+                         void* out, const int64_t* out_byte_off, int64_t out_bytes,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* All of the above in one call: scoring, MAS, selection and (if out != NULL)
+ * compaction. tok->z is required, and tok->d if any segment is temporal. */
+msao_status msao_run(msao_ctx* ctx, const msao_segment* segs, int n, int n_requests,
+                     const msao_params* params, const float* alpha,
+                     const msao_token_out* tok, const msao_frame_out* frm, const msao_req_out* req,
+                     const msao_select_out* sel, void* out, const int64_t* out_byte_off, int64_t out_bytes,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---- profiling ----------------------------------------------------------- */
+
+/* Kernels of the hot path, for msao_kernel_times. */
+#define MSAO_KERNEL_SCORE 0   /* per-token statistics and temporal term */
+#define MSAO_KERNEL_POST 1    /* aggregation, MAS, per-frame terms, selection */
+#define MSAO_KERNEL_GATHER 2  /* compaction */
+#define MSAO_NUM_KERNELS 3
+
+/* When enabled, every launch is bracketed by HIP events on the caller's
+ * stream. */
+msao_status msao_set_profiling(msao_ctx* ctx, int enable);
+/* Milliseconds each kernel took in the last profiled call (0 if not
+ * launched); blocks until that call's events have completed. */
+msao_status msao_kernel_times(msao_ctx* ctx, float* ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MSAO_H */

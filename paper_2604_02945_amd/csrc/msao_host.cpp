@@ -1,0 +1,747 @@
+// msao_host.cpp -- host side of the C ABI declared in include/msao.h:
+// validation (before any device work), planning of the per-call tables
+// (token/frame offsets, work items, Eq. 4 integer thresholds, Q24 selection
+// weights, keep counts), upload into the caller's workspace from pinned
+// staging, and the kernel launches on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/msao.h"
+#include "msao_internal.h"
+
+using namespace msao;
+
+struct msao_ctx {
+    int device = 0;
+    std::string err;
+    // two pinned staging slots, each guarded by the event of its last upload
+    void* stage[2] = {nullptr, nullptr};
+    size_t stage_cap[2] = {0, 0};
+    hipEvent_t stage_ev[2] = {nullptr, nullptr};
+    bool stage_used[2] = {false, false};
+    int next_slot = 0;
+    // profiling
+    bool profiling = false;
+    hipEvent_t kev[MSAO_NUM_KERNELS][2] = {};
+    bool kran[MSAO_NUM_KERNELS] = {};
+    // tuning
+    int row_item_bytes = 16384;
+    int chain_frames = 0;       // frames per temporal work item; 0 = automatic
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+constexpr size_t kWsAlign = 256;
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+int elt_size(int dtype) { return dtype == MSAO_F32 ? 4 : 2; }
+
+bool is_temporal(const msao_segment& s)
+{
+    return s.modality == MSAO_VIDEO && s.n_frames >= 2 && s.tokens_per_frame > 0;
+}
+
+msao_status fail(std::string* err, msao_status st, const std::string& msg)
+{
+    if (err) *err = msg;
+    return st;
+}
+
+// Keep count: k = min(N, ceil(kappa * N)) in double.
+int64_t keep_count(float kappa, int64_t N)
+{
+    double k = std::ceil((double)kappa * (double)N);
+    if (k > (double)N) k = (double)N;
+    if (k < 0.0) k = 0.0;
+    return (int64_t)k;
+}
+
+// Q24 weight: round-to-nearest-even of lambda * 2^24.
+uint32_t q24(float lambda) { return (uint32_t)std::nearbyint((double)lambda * 16777216.0); }
+
+msao_status validate_impl(const msao_segment* segs, int n, int R, const msao_params* p, std::string* err)
+{
+    char buf[256];
+    if (n < 0) return fail(err, MSAO_ERR_INVALID_ARG, "segment count is negative");
+    if (n > 0 && !segs) return fail(err, MSAO_ERR_INVALID_ARG, "segment table is NULL");
+    if (R < 0) return fail(err, MSAO_ERR_INVALID_ARG, "request count is negative");
+    if (!p) return fail(err, MSAO_ERR_INVALID_ARG, "params is NULL");
+    if (!(std::isfinite(p->tau) && p->tau >= 0.0f))
+        return fail(err, MSAO_ERR_INVALID_ARG, "tau must be finite and >= 0");
+    if (!(p->tau_s >= 0.0f && p->tau_s <= 1.0f))
+        return fail(err, MSAO_ERR_INVALID_ARG, "tau_s must be in [0, 1]");
+    for (int m = 0; m < MSAO_NUM_MODALITIES; ++m) {
+        if (!(p->lambda_s[m] >= 0.0f && p->lambda_s[m] <= 1.0f) || !(p->lambda_t[m] >= 0.0f && p->lambda_t[m] <= 1.0f))
+            return fail(err, MSAO_ERR_INVALID_ARG, "lambda_s and lambda_t must be in [0, 1]");
+    }
+    if (p->flags & ~MSAO_FLAG_TEMPORAL_LITERAL) return fail(err, MSAO_ERR_INVALID_ARG, "unknown flag bits");
+    int64_t total = 0;
+    for (int i = 0; i < n; ++i) {
+        const msao_segment& s = segs[i];
+        auto bad = [&](msao_status st, const char* what) {
+            std::snprintf(buf, sizeof buf, "segment %d: %s", i, what);
+            return fail(err, st, buf);
+        };
+        if (s.modality < 0 || s.modality >= MSAO_NUM_MODALITIES) return bad(MSAO_ERR_INVALID_ARG, "unknown modality");
+        if (s.dtype != MSAO_F32 && s.dtype != MSAO_BF16) return bad(MSAO_ERR_INVALID_ARG, "unknown dtype");
+        if (s.request < 0 || s.request >= R) return bad(MSAO_ERR_INVALID_ARG, "request id out of range");
+        if (s.n_frames < 1) return bad(MSAO_ERR_INVALID_ARG, "n_frames must be >= 1");
+        if (s.n_frames > 1 && s.modality != MSAO_VIDEO) return bad(MSAO_ERR_INVALID_ARG, "n_frames > 1 on a non-video segment");
+        if (s.tokens_per_frame < 0) return bad(MSAO_ERR_INVALID_ARG, "tokens_per_frame is negative");
+        if (s.hidden < 1 || s.hidden > MSAO_MAX_HIDDEN) return bad(MSAO_ERR_INVALID_ARG, "hidden out of range");
+        if (s.hidden % (16 / elt_size(s.dtype)) != 0)
+            return bad(MSAO_ERR_ALIGNMENT, "hidden must be a multiple of 8 (bf16) or 4 (fp32)");
+        if (std::isnan(s.keep_ratio) || s.keep_ratio > 1.0f) return bad(MSAO_ERR_INVALID_ARG, "keep_ratio must be <= 1 (negative: MAS-guided)");
+        const int64_t N = (int64_t)s.n_frames * s.tokens_per_frame;
+        if (N > INT32_MAX) return bad(MSAO_ERR_UNSUPPORTED, "more than 2^31-1 tokens");
+        total += N;
+        if (total > INT32_MAX - 1) return bad(MSAO_ERR_UNSUPPORTED, "more than 2^31-2 tokens in total");
+        if (N > 0) {
+            if (!s.data) return bad(MSAO_ERR_INVALID_ARG, "data is NULL");
+            if (s.row_stride < s.hidden) return bad(MSAO_ERR_INVALID_ARG, "row_stride < hidden");
+            if (((uintptr_t)s.data) % 16 != 0) return bad(MSAO_ERR_ALIGNMENT, "data is not 16-byte aligned");
+            if ((s.row_stride * elt_size(s.dtype)) % 16 != 0)
+                return bad(MSAO_ERR_ALIGNMENT, "row pitch is not a multiple of 16 bytes");
+        }
+    }
+    return MSAO_OK;
+}
+
+// Per-call tables, built on the host and uploaded into the workspace.
+struct Plan {
+    std::vector<DevSeg> seg;
+    std::vector<int32_t> seg_wi, seg_gi, rm_off, rm_seg, tseg;
+    std::vector<float> alpha;
+    int64_t ntok = 0, nframes = 0;
+    int n_wi = 0, n_gwi = 0;
+    bool any_temporal = false, any_guided = false;
+    size_t off_seg = 0, off_wi = 0, off_gi = 0, off_rmoff = 0, off_rmseg = 0, off_tseg = 0, off_alpha = 0;
+    size_t table_bytes = 0, off_partial = 0, total_bytes = 0;
+};
+
+size_t table_layout(Plan& pl, int n, int R)
+{
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o = align_up(o + bytes, 16);
+        return at;
+    };
+    pl.off_seg = take(sizeof(DevSeg) * (size_t)std::max(n, 1));
+    pl.off_wi = take(sizeof(int32_t) * (size_t)(n + 1));
+    pl.off_gi = take(sizeof(int32_t) * (size_t)(n + 1));
+    pl.off_rmoff = take(sizeof(int32_t) * (size_t)(R * kNumMod + 1));
+    pl.off_rmseg = take(sizeof(int32_t) * (size_t)std::max(n, 1));
+    pl.off_tseg = take(sizeof(int32_t) * (size_t)std::max(n, 1));
+    pl.off_alpha = take(sizeof(float) * (size_t)std::max(R * kNumMod, 1));
+    pl.table_bytes = o;
+    return o;
+}
+
+// Workspace bound that does not depend on tuning: one Partial per token at most.
+size_t workspace_bytes_for(int n, int R, int64_t ntok)
+{
+    Plan pl;
+    const size_t tb = table_layout(pl, n, R);
+    return align_up(tb, kWsAlign) + sizeof(Partial) * (size_t)std::max<int64_t>(ntok + n, 1);
+}
+
+void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* p,
+                const float* alpha, const int64_t* out_off, Plan& pl)
+{
+    pl.seg.resize((size_t)n);
+    pl.seg_wi.assign((size_t)n + 1, 0);
+    pl.seg_gi.assign((size_t)n + 1, 0);
+    pl.tseg.clear();
+    int64_t tok = 0, frame = 0;
+    int wi = 0, gi = 0;
+    int64_t chains_total = 0;
+    for (int i = 0; i < n; ++i)
+        if (is_temporal(segs[i])) chains_total += segs[i].tokens_per_frame;
+    for (int i = 0; i < n; ++i) {
+        const msao_segment& s = segs[i];
+        DevSeg& d = pl.seg[(size_t)i];
+        std::memset(&d, 0, sizeof d);
+        const int64_t N = (int64_t)s.n_frames * s.tokens_per_frame;
+        const int es = elt_size(s.dtype);
+        d.data = (const uint8_t*)s.data;
+        d.stride_bytes = s.row_stride * es;
+        d.out_off = out_off ? out_off[i] : 0;
+        d.tok_off = (int32_t)tok;
+        d.n_tok = (int32_t)N;
+        d.T = s.n_frames;
+        d.P = s.tokens_per_frame;
+        d.C = s.hidden;
+        d.dtype = s.dtype;
+        d.modality = s.modality;
+        d.request = s.request;
+        d.temporal = is_temporal(s) ? 1 : 0;
+        d.frame_off = d.temporal ? (int32_t)frame : -1;
+        d.nchunk = s.hidden * es / 16;
+        d.A_s = (int32_t)std::ceil((double)p->tau_s * (double)s.hidden);
+        d.L_s = q24(p->lambda_s[s.modality]);
+        d.L_t = q24(p->lambda_t[s.modality]);
+        d.lam_s = p->lambda_s[s.modality];
+        d.lam_t = p->lambda_t[s.modality];
+        d.k = s.keep_ratio < 0.0f ? -1 : (int32_t)keep_count(s.keep_ratio, N);
+        d.cap = d.k < 0 ? (int32_t)N : d.k;
+        // scoring work items, one wavefront each
+        int items = 0;
+        if (d.temporal) {
+            int fpi = ctx && ctx->chain_frames > 0 ? ctx->chain_frames : s.n_frames;
+            if (!(ctx && ctx->chain_frames > 0)) {
+                // split long chains until there are enough wavefronts to cover the chip
+                while (fpi > 8 && chains_total * ((s.n_frames + fpi - 1) / fpi) < 4096) fpi = (fpi + 1) / 2;
+            }
+            fpi = std::min(fpi, s.n_frames);
+            d.per_item = fpi;
+            items = s.tokens_per_frame * ((s.n_frames + fpi - 1) / fpi);
+            pl.tseg.push_back(i);
+            pl.any_temporal = true;
+        } else if (N > 0) {
+            const int rb = (int)std::max<int64_t>(1, (ctx ? ctx->row_item_bytes : 16384) / ((int64_t)s.hidden * es));
+            d.per_item = rb;
+            items = (int)((N + rb - 1) / rb);
+        } else {
+            d.per_item = 1;
+        }
+        d.wi_begin = wi;
+        wi += items;
+        pl.seg_wi[(size_t)i + 1] = wi;
+        d.g_begin = gi;
+        gi += (d.cap + kGatherRows - 1) / kGatherRows;
+        pl.seg_gi[(size_t)i + 1] = gi;
+        if (d.k < 0) pl.any_guided = true;
+        tok += N;
+        if (d.temporal) frame += s.n_frames;
+    }
+    pl.ntok = tok;
+    pl.nframes = frame;
+    pl.n_wi = wi;
+    pl.n_gwi = gi;
+    // segments grouped by (request, modality), table order inside a group
+    pl.rm_off.assign((size_t)R * kNumMod + 1, 0);
+    for (int i = 0; i < n; ++i) pl.rm_off[(size_t)(segs[i].request * kNumMod + segs[i].modality) + 1]++;
+    for (size_t x = 1; x < pl.rm_off.size(); ++x) pl.rm_off[x] += pl.rm_off[x - 1];
+    pl.rm_seg.assign((size_t)std::max(n, 1), 0);
+    {
+        std::vector<int32_t> fill(pl.rm_off.begin(), pl.rm_off.end() - 1);
+        for (int i = 0; i < n; ++i) pl.rm_seg[(size_t)fill[(size_t)(segs[i].request * kNumMod + segs[i].modality)]++] = i;
+    }
+    pl.alpha.assign((size_t)std::max(R * kNumMod, 1), 0.0f);
+    if (alpha)
+        for (int x = 0; x < R * kNumMod; ++x) pl.alpha[(size_t)x] = alpha[x];
+    table_layout(pl, n, R);
+    pl.off_partial = align_up(pl.table_bytes, kWsAlign);
+    pl.total_bytes = pl.off_partial + sizeof(Partial) * (size_t)std::max(pl.n_wi, 1);
+}
+
+msao_status hip_fail(msao_ctx* ctx, hipError_t e, const char* what)
+{
+    ctx->err = std::string(what) + ": " + hipGetErrorString(e);
+    return MSAO_ERR_HIP;
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    bool changed = false;
+    explicit DeviceGuard(int dev)
+    {
+        if (hipGetDevice(&prev) == hipSuccess && prev != dev) changed = hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard()
+    {
+        if (changed) (void)hipSetDevice(prev);
+    }
+};
+
+// Copy the tables into a pinned slot and enqueue its upload into the workspace.
+msao_status upload(msao_ctx* ctx, const Plan& pl, void* ws, hipStream_t stream)
+{
+    const int slot = ctx->next_slot;
+    ctx->next_slot ^= 1;
+    hipError_t e;
+    if (ctx->stage_used[slot]) {
+        if ((e = hipEventSynchronize(ctx->stage_ev[slot])) != hipSuccess) return hip_fail(ctx, e, "hipEventSynchronize");
+    }
+    if (ctx->stage_cap[slot] < pl.table_bytes) {
+        if (ctx->stage[slot]) (void)hipHostFree(ctx->stage[slot]);
+        ctx->stage[slot] = nullptr;
+        ctx->stage_cap[slot] = 0;
+        const size_t cap = align_up(std::max<size_t>(pl.table_bytes, 65536), 65536);
+        if ((e = hipHostMalloc(&ctx->stage[slot], cap, hipHostMallocDefault)) != hipSuccess)
+            return hip_fail(ctx, e, "hipHostMalloc");
+        ctx->stage_cap[slot] = cap;
+    }
+    uint8_t* h = (uint8_t*)ctx->stage[slot];
+    std::memset(h, 0, pl.table_bytes);
+    auto put = [&](size_t off, const void* src, size_t bytes) {
+        if (bytes) std::memcpy(h + off, src, bytes);
+    };
+    put(pl.off_seg, pl.seg.data(), sizeof(DevSeg) * pl.seg.size());
+    put(pl.off_wi, pl.seg_wi.data(), sizeof(int32_t) * pl.seg_wi.size());
+    put(pl.off_gi, pl.seg_gi.data(), sizeof(int32_t) * pl.seg_gi.size());
+    put(pl.off_rmoff, pl.rm_off.data(), sizeof(int32_t) * pl.rm_off.size());
+    put(pl.off_rmseg, pl.rm_seg.data(), sizeof(int32_t) * pl.rm_seg.size());
+    put(pl.off_tseg, pl.tseg.data(), sizeof(int32_t) * pl.tseg.size());
+    put(pl.off_alpha, pl.alpha.data(), sizeof(float) * pl.alpha.size());
+    if ((e = hipMemcpyAsync(ws, h, pl.table_bytes, hipMemcpyHostToDevice, stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipMemcpyAsync");
+    if ((e = hipEventRecord(ctx->stage_ev[slot], stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
+    ctx->stage_used[slot] = true;
+    return MSAO_OK;
+}
+
+Tables device_tables(const Plan& pl, void* ws, int n, int R, const msao_params* p)
+{
+    uint8_t* b = (uint8_t*)ws;
+    Tables t;
+    t.seg = (const DevSeg*)(b + pl.off_seg);
+    t.seg_wi = (const int32_t*)(b + pl.off_wi);
+    t.seg_gi = (const int32_t*)(b + pl.off_gi);
+    t.rm_off = (const int32_t*)(b + pl.off_rmoff);
+    t.rm_seg = (const int32_t*)(b + pl.off_rmseg);
+    t.tseg = (const int32_t*)(b + pl.off_tseg);
+    t.alpha = (const float*)(b + pl.off_alpha);
+    t.partial = (Partial*)(b + pl.off_partial);
+    t.n = n;
+    t.R = R;
+    t.n_wi = pl.n_wi;
+    t.n_gwi = pl.n_gwi;
+    t.n_tseg = (int)pl.tseg.size();
+    t.n_frames = (int)pl.nframes;
+    t.tau = p->tau;
+    t.tau_s = p->tau_s;
+    for (int m = 0; m < kNumMod; ++m) {
+        t.lam_s[m] = p->lambda_s[m];
+        t.lam_t[m] = p->lambda_t[m];
+    }
+    t.flags = p->flags;
+    return t;
+}
+
+msao_status check_ws(msao_ctx* ctx, const Plan& pl, void* ws, size_t ws_bytes)
+{
+    if (!ws) return fail(&ctx->err, MSAO_ERR_WORKSPACE, "workspace is NULL");
+    if (((uintptr_t)ws) % kWsAlign != 0) return fail(&ctx->err, MSAO_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    if (ws_bytes < pl.total_bytes) {
+        char buf[160];
+        std::snprintf(buf, sizeof buf, "workspace too small: %zu bytes given, %zu needed", ws_bytes, pl.total_bytes);
+        return fail(&ctx->err, MSAO_ERR_WORKSPACE, buf);
+    }
+    return MSAO_OK;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p) % a == 0; }
+
+// Output arrays of 4 or 8 bytes must be naturally aligned.
+msao_status check_out_alignment(msao_ctx* ctx, std::initializer_list<std::pair<const void*, size_t>> ptrs)
+{
+    for (const auto& pr : ptrs)
+        if (pr.first && !aligned(pr.first, pr.second))
+            return fail(&ctx->err, MSAO_ERR_ALIGNMENT, "an output array is not naturally aligned");
+    return MSAO_OK;
+}
+
+// Launch with optional profiling events around it.
+msao_status launched(msao_ctx* ctx, int kernel, hipStream_t stream, int (*fn)(const void*, void*), const void* args)
+{
+    hipError_t e;
+    if (ctx->profiling && (e = hipEventRecord(ctx->kev[kernel][0], stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventRecord");
+    const int rc = fn(args, stream);
+    if (rc != 0) return hip_fail(ctx, (hipError_t)rc, "kernel launch");
+    if (ctx->profiling) {
+        if ((e = hipEventRecord(ctx->kev[kernel][1], stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
+        ctx->kran[kernel] = true;
+    }
+    return MSAO_OK;
+}
+
+int run_score(const void* a, void* s) { return launch_score(*(const ScoreArgs*)a, s); }
+int run_post(const void* a, void* s) { return launch_post(*(const PostArgs*)a, s); }
+int run_gather(const void* a, void* s) { return launch_gather(*(const GatherArgs*)a, s); }
+
+#define MSAO_TRY(x)                                                                                                   \
+    do {                                                                                                              \
+        msao_status st_ = (x);                                                                                        \
+        if (st_ != MSAO_OK) return st_;                                                                               \
+    } while (0)
+
+TokenOut token_out(const msao_token_out* t)
+{
+    TokenOut o{};
+    if (t) o = TokenOut{t->z, t->l1, t->l2, t->info, t->d, t->res};
+    return o;
+}
+
+msao_status check_compact_out(msao_ctx* ctx, const Plan& pl, const msao_segment* segs, int n, void* out,
+                              const int64_t* off, int64_t out_bytes)
+{
+    if (!out) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "compaction output is NULL");
+    if (!off) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "out_byte_off is NULL");
+    if (!aligned(out, 16)) return fail(&ctx->err, MSAO_ERR_ALIGNMENT, "out is not 16-byte aligned");
+    for (int i = 0; i < n; ++i) {
+        const DevSeg& d = pl.seg[(size_t)i];
+        const int64_t need = (int64_t)d.cap * segs[i].hidden * elt_size(segs[i].dtype);
+        if (off[i] < 0 || off[i] % 16 != 0) return fail(&ctx->err, MSAO_ERR_ALIGNMENT, "out_byte_off entry negative or not 16-byte aligned");
+        if (off[i] + need > out_bytes) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "compaction output too small for a segment's rows");
+    }
+    return MSAO_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- C ABI
+
+extern "C" {
+
+const char* msao_status_string(msao_status s)
+{
+    switch (s) {
+    case MSAO_OK: return "MSAO_OK";
+    case MSAO_ERR_INVALID_ARG: return "MSAO_ERR_INVALID_ARG";
+    case MSAO_ERR_ALIGNMENT: return "MSAO_ERR_ALIGNMENT";
+    case MSAO_ERR_WORKSPACE: return "MSAO_ERR_WORKSPACE";
+    case MSAO_ERR_UNSUPPORTED: return "MSAO_ERR_UNSUPPORTED";
+    case MSAO_ERR_HIP: return "MSAO_ERR_HIP";
+    }
+    return "unknown status";
+}
+
+msao_params msao_default_params(void)
+{
+    msao_params p;
+    std::memset(&p, 0, sizeof p);
+    p.tau = 0.1f;
+    p.tau_s = 0.3f;
+    p.lambda_s[MSAO_TEXT] = 0.0f;
+    p.lambda_s[MSAO_IMAGE] = 0.6f;
+    p.lambda_s[MSAO_VIDEO] = 0.6f;
+    p.lambda_s[MSAO_AUDIO] = 0.6f;
+    p.lambda_t[MSAO_VIDEO] = 0.4f;
+    p.flags = 0;
+    return p;
+}
+
+const char* msao_last_error(const msao_ctx* ctx) { return ctx ? ctx->err.c_str() : "context is NULL"; }
+
+const char* msao_last_error_global(void) { return g_err.c_str(); }
+
+msao_status msao_validate(const msao_segment* segs, int n, int n_requests, const msao_params* params)
+{
+    return validate_impl(segs, n, n_requests, params, &g_err);
+}
+
+msao_status msao_count(const msao_segment* segs, int n, int64_t* n_tokens, int64_t* n_frames)
+{
+    if (n < 0 || (n > 0 && !segs) || !n_tokens || !n_frames)
+        return fail(&g_err, MSAO_ERR_INVALID_ARG, "msao_count: bad arguments");
+    int64_t t = 0, f = 0;
+    for (int i = 0; i < n; ++i) {
+        if (segs[i].n_frames < 1 || segs[i].tokens_per_frame < 0)
+            return fail(&g_err, MSAO_ERR_INVALID_ARG, "msao_count: bad segment shape");
+        t += (int64_t)segs[i].n_frames * segs[i].tokens_per_frame;
+        if (is_temporal(segs[i])) f += segs[i].n_frames;
+    }
+    *n_tokens = t;
+    *n_frames = f;
+    return MSAO_OK;
+}
+
+msao_status msao_workspace_size(const msao_segment* segs, int n, int n_requests, size_t* bytes)
+{
+    if (!bytes) return fail(&g_err, MSAO_ERR_INVALID_ARG, "bytes is NULL");
+    msao_params p = msao_default_params();
+    MSAO_TRY(validate_impl(segs, n, n_requests, &p, &g_err));
+    int64_t t = 0, f = 0;
+    MSAO_TRY(msao_count(segs, n, &t, &f));
+    *bytes = workspace_bytes_for(n, n_requests, t);
+    return MSAO_OK;
+}
+
+msao_status msao_compact_layout(const msao_segment* segs, int n, int64_t* out_byte_off, int64_t* total_bytes)
+{
+    if (n < 0 || (n > 0 && (!segs || !out_byte_off)) || !total_bytes)
+        return fail(&g_err, MSAO_ERR_INVALID_ARG, "msao_compact_layout: bad arguments");
+    int64_t o = 0;
+    for (int i = 0; i < n; ++i) {
+        const msao_segment& s = segs[i];
+        const int64_t N = (int64_t)s.n_frames * s.tokens_per_frame;
+        if (s.n_frames < 1 || s.tokens_per_frame < 0 || std::isnan(s.keep_ratio))
+            return fail(&g_err, MSAO_ERR_INVALID_ARG, "msao_compact_layout: bad segment");
+        const int64_t cap = s.keep_ratio < 0.0f ? N : keep_count(s.keep_ratio, N);
+        out_byte_off[i] = o;
+        o = (int64_t)align_up((size_t)(o + cap * (int64_t)s.hidden * elt_size(s.dtype)), kWsAlign);
+    }
+    *total_bytes = o;
+    return MSAO_OK;
+}
+
+msao_status msao_create(msao_ctx** out, int device)
+{
+    if (!out) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx pointer is NULL");
+    *out = nullptr;
+    int count = 0;
+    hipError_t e = hipGetDeviceCount(&count);
+    if (e != hipSuccess || count <= 0) return fail(&g_err, MSAO_ERR_HIP, "no HIP device available");
+    if (device < 0 || device >= count) return fail(&g_err, MSAO_ERR_INVALID_ARG, "device id out of range");
+    msao_ctx* c = new msao_ctx();
+    c->device = device;
+    DeviceGuard guard(device);
+    for (int i = 0; i < 2; ++i) {
+        if ((e = hipEventCreateWithFlags(&c->stage_ev[i], hipEventDisableTiming)) != hipSuccess) {
+            g_err = std::string("hipEventCreate: ") + hipGetErrorString(e);
+            msao_destroy(c);
+            return MSAO_ERR_HIP;
+        }
+    }
+    for (int k = 0; k < MSAO_NUM_KERNELS; ++k)
+        for (int j = 0; j < 2; ++j)
+            if ((e = hipEventCreate(&c->kev[k][j])) != hipSuccess) {
+                g_err = std::string("hipEventCreate: ") + hipGetErrorString(e);
+                msao_destroy(c);
+                return MSAO_ERR_HIP;
+            }
+    if (const char* v = std::getenv("MSAO_ROW_ITEM_BYTES")) c->row_item_bytes = std::max(1, std::atoi(v));
+    if (const char* v = std::getenv("MSAO_CHAIN_FRAMES")) c->chain_frames = std::max(0, std::atoi(v));
+    *out = c;
+    return MSAO_OK;
+}
+
+void msao_destroy(msao_ctx* ctx)
+{
+    if (!ctx) return;
+    DeviceGuard guard(ctx->device);
+    for (int i = 0; i < 2; ++i) {
+        if (ctx->stage_ev[i]) {
+            if (ctx->stage_used[i]) (void)hipEventSynchronize(ctx->stage_ev[i]);
+            (void)hipEventDestroy(ctx->stage_ev[i]);
+        }
+        if (ctx->stage[i]) (void)hipHostFree(ctx->stage[i]);
+    }
+    for (int k = 0; k < MSAO_NUM_KERNELS; ++k)
+        for (int j = 0; j < 2; ++j)
+            if (ctx->kev[k][j]) (void)hipEventDestroy(ctx->kev[k][j]);
+    delete ctx;
+}
+
+msao_status msao_set_profiling(msao_ctx* ctx, int enable)
+{
+    if (!ctx) return MSAO_ERR_INVALID_ARG;
+    ctx->profiling = enable != 0;
+    return MSAO_OK;
+}
+
+msao_status msao_kernel_times(msao_ctx* ctx, float* ms)
+{
+    if (!ctx || !ms) return MSAO_ERR_INVALID_ARG;
+    DeviceGuard guard(ctx->device);
+    for (int k = 0; k < MSAO_NUM_KERNELS; ++k) {
+        ms[k] = 0.0f;
+        if (!ctx->kran[k]) continue;
+        hipError_t e = hipEventSynchronize(ctx->kev[k][1]);
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms[k], ctx->kev[k][0], ctx->kev[k][1]);
+        if (e != hipSuccess) return hip_fail(ctx, e, "msao_kernel_times");
+    }
+    return MSAO_OK;
+}
+
+msao_status msao_mas_score(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
+                           const float* alpha, const msao_token_out* tok, const msao_frame_out* frm,
+                           const msao_req_out* req, void* ws, size_t ws_bytes, void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
+    Plan pl;
+    build_plan(ctx, segs, n, R, params, alpha, nullptr, pl);
+    MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
+    const bool want_frames = frm && (frm->dframe || frm->sim || frm->gamma) && pl.nframes > 0;
+    if (want_frames && !(tok && tok->d))
+        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "per-frame outputs need tok->d");
+    if (tok) MSAO_TRY(check_out_alignment(ctx, {{tok->z, 4}, {tok->l1, 4}, {tok->l2, 4}, {tok->info, 4}, {tok->d, 4}, {tok->res, 4}}));
+    if (frm) MSAO_TRY(check_out_alignment(ctx, {{frm->dframe, 8}, {frm->sim, 4}, {frm->gamma, 4}}));
+    if (req) MSAO_TRY(check_out_alignment(ctx, {{req->agg, 8}, {req->rho, 4}, {req->temporal, 4}, {req->beta, 4}, {req->mas, 4}}));
+    for (int k = 0; k < MSAO_NUM_KERNELS; ++k) ctx->kran[k] = false;
+    DeviceGuard guard(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    MSAO_TRY(upload(ctx, pl, ws, st));
+    ScoreArgs sa;
+    sa.t = device_tables(pl, ws, n, R, params);
+    sa.tok = token_out(tok);
+    sa.mode = kModeScore;
+    MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
+    PostArgs pa;
+    std::memset(&pa, 0, sizeof pa);
+    pa.t = sa.t;
+    if (req) pa.req = ReqOut{req->agg, req->rho, req->temporal, req->beta, req->mas, req->present};
+    if (frm) pa.frm = FrameOut{frm->dframe, frm->sim, frm->gamma};
+    pa.d = tok ? tok->d : nullptr;
+    const bool want_req = req && (req->agg || req->rho || req->temporal || req->beta || req->mas || req->present);
+    pa.n_req_blocks = want_req ? R : 0;
+    pa.n_frame_blocks = want_frames ? (int)pl.nframes : 0;
+    pa.n_sel_blocks = 0;
+    return launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa);
+}
+
+msao_status msao_temporal_redundancy(msao_ctx* ctx, const msao_segment* segs, int n, int R,
+                                     const msao_params* params, uint32_t* d, float* res,
+                                     const msao_frame_out* frm, float* temporal, void* ws, size_t ws_bytes,
+                                     void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
+    Plan pl;
+    build_plan(ctx, segs, n, R, params, nullptr, nullptr, pl);
+    MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
+    const bool want_frames = frm && (frm->dframe || frm->sim || frm->gamma) && pl.nframes > 0;
+    if (want_frames && !d) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "per-frame outputs need d");
+    MSAO_TRY(check_out_alignment(ctx, {{d, 4}, {res, 4}, {temporal, 4}}));
+    if (frm) MSAO_TRY(check_out_alignment(ctx, {{frm->dframe, 8}, {frm->sim, 4}, {frm->gamma, 4}}));
+    for (int k = 0; k < MSAO_NUM_KERNELS; ++k) ctx->kran[k] = false;
+    DeviceGuard guard(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    MSAO_TRY(upload(ctx, pl, ws, st));
+    ScoreArgs sa;
+    std::memset(&sa, 0, sizeof sa);
+    sa.t = device_tables(pl, ws, n, R, params);
+    sa.tok.d = d;
+    sa.tok.res = res;
+    sa.mode = kModeTemporal;
+    MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
+    PostArgs pa;
+    std::memset(&pa, 0, sizeof pa);
+    pa.t = sa.t;
+    if (frm) pa.frm = FrameOut{frm->dframe, frm->sim, frm->gamma};
+    pa.req.temporal = temporal;
+    pa.d = d;
+    pa.temporal_only = 1;
+    pa.n_req_blocks = temporal ? R : 0;
+    pa.n_frame_blocks = want_frames ? (int)pl.nframes : 0;
+    return launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa);
+}
+
+msao_status msao_select_tokens(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
+                               const uint32_t* z, const uint32_t* d, const float* mas, const msao_select_out* sel,
+                               void* ws, size_t ws_bytes, void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
+    Plan pl;
+    build_plan(ctx, segs, n, R, params, nullptr, nullptr, pl);
+    MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
+    if (!sel || !sel->kept_idx || !sel->kept_count)
+        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "selection needs kept_idx and kept_count");
+    if (pl.ntok > 0 && !z) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "z is NULL");
+    if (pl.any_temporal && !d) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "d is NULL but a segment is temporal");
+    if (pl.any_guided && !mas) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "mas is NULL but a keep ratio is negative");
+    MSAO_TRY(check_out_alignment(ctx, {{z, 4}, {d, 4}, {mas, 4}, {sel->kept_idx, 4}, {sel->kept_count, 4}}));
+    for (int k = 0; k < MSAO_NUM_KERNELS; ++k) ctx->kran[k] = false;
+    DeviceGuard guard(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    MSAO_TRY(upload(ctx, pl, ws, st));
+    PostArgs pa;
+    std::memset(&pa, 0, sizeof pa);
+    pa.t = device_tables(pl, ws, n, R, params);
+    pa.sel = SelOut{sel->keep, sel->kept_idx, sel->kept_count};
+    pa.z = z;
+    pa.d = d;
+    pa.mas_in = mas;
+    pa.n_sel_blocks = n;
+    return launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa);
+}
+
+msao_status msao_compact(msao_ctx* ctx, const msao_segment* segs, int n, const int32_t* kept_idx,
+                         const int32_t* kept_count, void* out, const int64_t* out_byte_off, int64_t out_bytes,
+                         void* ws, size_t ws_bytes, void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    int R = 0;
+    for (int i = 0; i < n && segs; ++i) R = std::max(R, segs[i].request + 1);
+    msao_params p = msao_default_params();
+    MSAO_TRY(validate_impl(segs, n, R, &p, &ctx->err));
+    Plan pl;
+    build_plan(ctx, segs, n, R, &p, nullptr, out_byte_off, pl);
+    MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
+    if (pl.ntok > 0 && (!kept_idx || !kept_count))
+        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "kept_idx and kept_count are required");
+    MSAO_TRY(check_out_alignment(ctx, {{kept_idx, 4}, {kept_count, 4}}));
+    MSAO_TRY(check_compact_out(ctx, pl, segs, n, out, out_byte_off, out_bytes));
+    for (int k = 0; k < MSAO_NUM_KERNELS; ++k) ctx->kran[k] = false;
+    DeviceGuard guard(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    MSAO_TRY(upload(ctx, pl, ws, st));
+    GatherArgs ga;
+    ga.t = device_tables(pl, ws, n, R, &p);
+    ga.kept_idx = kept_idx;
+    ga.kept_count = kept_count;
+    ga.out = (uint8_t*)out;
+    ga.out_bytes = out_bytes;
+    return launched(ctx, MSAO_KERNEL_GATHER, st, run_gather, &ga);
+}
+
+msao_status msao_run(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
+                     const float* alpha, const msao_token_out* tok, const msao_frame_out* frm,
+                     const msao_req_out* req, const msao_select_out* sel, void* out, const int64_t* out_byte_off,
+                     int64_t out_bytes, void* ws, size_t ws_bytes, void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
+    Plan pl;
+    build_plan(ctx, segs, n, R, params, alpha, out_byte_off, pl);
+    MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
+    if (pl.ntok > 0 && !(tok && tok->z)) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "msao_run needs tok->z");
+    if (pl.any_temporal && !(tok && tok->d))
+        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "msao_run needs tok->d for temporal segments");
+    if (!sel || !sel->kept_idx || !sel->kept_count)
+        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "selection needs kept_idx and kept_count");
+    const bool want_frames = frm && (frm->dframe || frm->sim || frm->gamma) && pl.nframes > 0;
+    if (tok) MSAO_TRY(check_out_alignment(ctx, {{tok->z, 4}, {tok->l1, 4}, {tok->l2, 4}, {tok->info, 4}, {tok->d, 4}, {tok->res, 4}}));
+    if (frm) MSAO_TRY(check_out_alignment(ctx, {{frm->dframe, 8}, {frm->sim, 4}, {frm->gamma, 4}}));
+    if (req) MSAO_TRY(check_out_alignment(ctx, {{req->agg, 8}, {req->rho, 4}, {req->temporal, 4}, {req->beta, 4}, {req->mas, 4}}));
+    MSAO_TRY(check_out_alignment(ctx, {{sel->kept_idx, 4}, {sel->kept_count, 4}}));
+    if (out) MSAO_TRY(check_compact_out(ctx, pl, segs, n, out, out_byte_off, out_bytes));
+    for (int k = 0; k < MSAO_NUM_KERNELS; ++k) ctx->kran[k] = false;
+    DeviceGuard guard(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    MSAO_TRY(upload(ctx, pl, ws, st));
+    ScoreArgs sa;
+    sa.t = device_tables(pl, ws, n, R, params);
+    sa.tok = token_out(tok);
+    sa.mode = kModeScore;
+    MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
+    PostArgs pa;
+    std::memset(&pa, 0, sizeof pa);
+    pa.t = sa.t;
+    if (req) pa.req = ReqOut{req->agg, req->rho, req->temporal, req->beta, req->mas, req->present};
+    if (frm) pa.frm = FrameOut{frm->dframe, frm->sim, frm->gamma};
+    pa.sel = SelOut{sel->keep, sel->kept_idx, sel->kept_count};
+    pa.z = tok ? tok->z : nullptr;
+    pa.d = tok ? tok->d : nullptr;
+    pa.mas_in = nullptr;
+    const bool want_req = req && (req->agg || req->rho || req->temporal || req->beta || req->mas || req->present);
+    pa.n_req_blocks = want_req ? R : 0;
+    pa.n_frame_blocks = want_frames ? (int)pl.nframes : 0;
+    pa.n_sel_blocks = n;
+    MSAO_TRY(launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa));
+    if (!out) return MSAO_OK;
+    GatherArgs ga;
+    ga.t = sa.t;
+    ga.kept_idx = sel->kept_idx;
+    ga.kept_count = sel->kept_count;
+    ga.out = (uint8_t*)out;
+    ga.out_bytes = out_bytes;
+    return launched(ctx, MSAO_KERNEL_GATHER, st, run_gather, &ga);
+}
+
+}  // extern "C"

@@ -1,0 +1,115 @@
+// msao_internal.h -- device-side tables shared by the host planner
+// (msao_host.cpp) and the gfx950 kernels (msao_kernels.hip). Not part of the
+// public ABI.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace msao {
+
+enum : int { kText = 0, kImage = 1, kVideo = 2, kAudio = 3, kNumMod = 4 };
+enum : int { kF32 = 0, kBF16 = 1 };
+enum : int { kModeScore = 0, kModeTemporal = 1 };
+
+// One segment as the kernels see it. Built on the host for every call and
+// uploaded into the caller's workspace with the other tables.
+struct DevSeg {
+    const uint8_t* data;   // first row
+    int64_t stride_bytes;  // bytes between consecutive rows
+    int64_t out_off;       // compaction: byte offset of the segment's packed rows
+    int32_t tok_off;       // global token id of row 0
+    int32_t n_tok;         // N = T*P
+    int32_t T, P, C;
+    int32_t dtype;         // kF32 / kBF16
+    int32_t modality, request;
+    int32_t temporal;      // VIDEO with T >= 2 and P > 0
+    int32_t frame_off;     // global frame id of frame 0 (temporal segments)
+    int32_t wi_begin;      // first scoring work item (one wavefront each)
+    int32_t per_item;      // rows per item, or frames per item for temporal segments
+    int32_t nchunk;        // 16-byte chunks per row
+    int32_t A_s;           // Eq. 4 as an integer test: sparse iff active < A_s = ceil(tau_s*C)
+    uint32_t L_s, L_t;     // Q24 selection weights of the segment's modality
+    float lam_s, lam_t;    // the same weights as floats (informativeness)
+    int32_t k;             // fixed keep count, or -1 when MAS-guided
+    int32_t cap;           // compaction capacity in rows
+    int32_t g_begin;       // first gather work item
+    int32_t pad_;
+};
+
+// Integer partial sums of one scoring work item (no atomics, no zeroing).
+struct Partial {
+    uint32_t nsparse;      // tokens with active < A_s
+    uint32_t pad_;
+    uint64_t dsum;         // sum of d over frames t >= 1
+};
+
+// Device pointers into the workspace, plus scalars, passed by value.
+struct Tables {
+    const DevSeg* seg;
+    const int32_t* seg_wi;   // [n+1] prefix of scoring work items
+    const int32_t* seg_gi;   // [n+1] prefix of gather work items
+    const int32_t* rm_off;   // [R*4+1] CSR offsets into rm_seg
+    const int32_t* rm_seg;   // segment ids grouped by (request, modality)
+    const int32_t* tseg;     // [n_tseg] temporal segment ids in table order
+    const float* alpha;      // [R*4] relevance logits
+    Partial* partial;        // [n_wi]
+    int32_t n, R, n_wi, n_gwi, n_tseg, n_frames;
+    float tau, tau_s;
+    float lam_s[kNumMod], lam_t[kNumMod];
+    uint32_t flags;
+};
+
+struct TokenOut {
+    uint32_t* z; float* l1; float* l2; float* info; uint32_t* d; float* res;
+};
+struct FrameOut {
+    uint64_t* dframe; float* sim; float* gamma;
+};
+struct ReqOut {
+    uint64_t* agg; float* rho; float* temporal; float* beta; float* mas; uint8_t* present;
+};
+struct SelOut {
+    uint8_t* keep; int32_t* kept_idx; int32_t* kept_count;
+};
+
+// Roles of the post-scoring launch.
+struct PostArgs {
+    Tables t;
+    ReqOut req;           // request role outputs
+    FrameOut frm;         // frame role outputs
+    SelOut sel;           // selection role outputs
+    const uint32_t* z;    // selection inputs
+    const uint32_t* d;
+    const float* mas_in;  // MAS from the caller (selection only); NULL: recompute
+    int32_t n_req_blocks; // blocks [0, n_req_blocks): one per request
+    int32_t n_frame_blocks;
+    int32_t n_sel_blocks; // one per segment
+    int32_t temporal_only;// request role writes only the temporal term
+};
+
+struct ScoreArgs {
+    Tables t;
+    TokenOut tok;
+    int32_t mode;
+};
+
+struct GatherArgs {
+    Tables t;
+    const int32_t* kept_idx;
+    const int32_t* kept_count;
+    uint8_t* out;
+    int64_t out_bytes;
+};
+
+// Launchers (msao_kernels.hip). Return the HIP error code of the launch.
+int launch_score(const ScoreArgs& a, void* stream);
+int launch_post(const PostArgs& a, void* stream);
+int launch_gather(const GatherArgs& a, void* stream);
+
+constexpr int kScoreBlock = 256;   // 4 wavefronts, one work item each
+constexpr int kPostBlock = 256;
+constexpr int kGatherBlock = 256;
+constexpr int kGatherRows = 4;     // kept rows per gather work item
+
+}  // namespace msao

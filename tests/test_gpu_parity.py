@@ -1,0 +1,376 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle, on the
+same seeded inputs.
+
+Bar: integer outputs (z, d, per-frame D, aggregates, keep flags, kept indices,
+keep counts) and compacted rows bit-exact; l1/l2/res within 1e-5 relative for
+fp32 inputs and 2e-3 relative for bf16 inputs (sums of non-negative terms, so
+a relative bound holds); per-frame sim/gamma and per-modality rho and temporal
+term exact (both sides divide the same integers in double and round once);
+beta/MAS within 1e-6 relative; informativeness within 1e-5 relative + 2e-6.
+Where a MAS-guided keep count sits on a ceil boundary, a keep count from either
+side's MAS is accepted and the kept set is checked for the GPU's count.
+"""
+import math
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2604_02945_amd as msao
+from paper_2604_02945_amd import binding as B
+from workloads import AUDIO, IMAGE, TEXT, VIDEO, Segment, default_params, f32_to_bf16_bits, make_workload
+
+pytestmark = pytest.mark.gpu
+
+RTOL = {"f32": 1e-5, "bf16": 2e-3}
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda", 0)
+
+
+def to_device(segments, dev, pad=0):
+    out = []
+    for s in segments:
+        a = s.data
+        if pad:
+            a = np.concatenate([a, np.zeros((a.shape[0], pad), a.dtype)], axis=1)
+        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16 if s.dtype == "bf16" else np.float32)).to(dev)
+        if s.dtype == "bf16":
+            t = t.view(torch.bfloat16)
+        if pad:
+            t = t[:, : s.hidden]
+        out.append(msao.DeviceSegment(t, s.request, s.modality, s.keep_ratio, s.n_frames))
+    return out
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def token_tolerances(segments):
+    rt = np.concatenate([np.full(s.n_tokens, RTOL[s.dtype]) for s in segments]) if segments else np.zeros(0)
+    return rt
+
+
+def assert_close_rel(got, want, rtol, name):
+    got = got.astype(np.float64)
+    want = want.astype(np.float64)
+    both_nan = np.isnan(got) & np.isnan(want)
+    same_inf = np.isinf(got) & np.isinf(want) & (np.sign(got) == np.sign(want))
+    ok = both_nan | same_inf | (np.abs(got - want) <= rtol * np.abs(want))
+    if not ok.all():
+        i = int(np.flatnonzero(~ok)[0])
+        raise AssertionError(f"{name}[{i}]: got {got[i]!r} want {want[i]!r} ({(~ok).sum()} mismatches)")
+    fin = np.isfinite(want) & (want != 0)
+    return float(np.max(np.abs(got[fin] - want[fin]) / np.abs(want[fin]))) if fin.any() else 0.0
+
+
+def compare_scores(segments, R, got, ref, check_tokens=("z", "l1", "l2", "info", "d", "res")):
+    rt = token_tolerances(segments)
+    errs = {}
+    if "z" in check_tokens:
+        assert np.array_equal(host(got["z"]).astype(np.uint32), ref["z"]), "z"
+    if "d" in check_tokens:
+        assert np.array_equal(host(got["d"]).astype(np.uint32), ref["d"]), "d"
+    for f in ("l1", "l2", "res"):
+        if f in check_tokens:
+            errs[f] = assert_close_rel(host(got[f]), ref[f], rt, f)
+    if "info" in check_tokens:
+        g, w = host(got["info"]).astype(np.float64), ref["info"].astype(np.float64)
+        bad = ~(np.abs(g - w) <= 1e-5 * np.abs(w) + 2e-6)
+        assert not bad.any(), f"info mismatch at {np.flatnonzero(bad)[:5]}"
+    return errs
+
+
+def compare_frames(got, ref):
+    assert np.array_equal(host(got["dframe"]).astype(np.uint64), ref["dframe"]), "dframe"
+    assert np.array_equal(host(got["sim"]), ref["sim"]), "sim"
+    assert np.array_equal(host(got["gamma"]), ref["gamma"]), "gamma"
+
+
+def compare_requests(got, ref):
+    assert np.array_equal(host(got["agg"]).astype(np.uint64), ref["agg"]), "agg"
+    assert np.array_equal(host(got["present"]), ref["present"]), "present"
+    assert np.array_equal(host(got["rho"]), ref["rho"]), "rho"
+    assert np.array_equal(host(got["temporal"]), ref["temporal"]), "temporal"
+    assert np.allclose(host(got["beta"]), ref["beta"], rtol=1e-6, atol=0), "beta"
+    assert np.allclose(host(got["mas"]), ref["mas"], rtol=1e-6, atol=1e-7), "mas"
+
+
+def compare_selection(segments, R, got, ref, p, gpu_mas=None):
+    kc = host(got["kept_count"])
+    if np.array_equal(kc, ref["k"]):
+        assert np.array_equal(host(got["kept_idx"]), ref["kept_idx"]), "kept_idx"
+        assert np.array_equal(host(got["keep"]), ref["keep"]), "keep"
+        return
+    # a MAS-guided count on a ceil boundary: accept the count from the GPU's MAS
+    assert gpu_mas is not None, f"keep counts differ: {kc} vs {ref['k']}"
+    for i, s in enumerate(segments):
+        if kc[i] != ref["k"][i]:
+            assert s.keep_ratio < 0
+            alt = oracle.keep_count(1.0 - float(gpu_mas[s.request * 4 + s.modality]), s.n_tokens)
+            assert kc[i] == alt
+    redo = oracle.select(segments, R, p, ref["z"], ref["d"], gpu_mas)
+    assert np.array_equal(kc, redo["k"])
+    assert np.array_equal(host(got["kept_idx"]), redo["kept_idx"])
+    assert np.array_equal(host(got["keep"]), redo["keep"])
+
+
+def compare_compaction(dsegs, segments, out, ref_rows, kc):
+    rows = msao.compacted_rows(dsegs, out, kc)
+    for i, (r, want) in enumerate(zip(rows, ref_rows)):
+        g = host(r.view(torch.int16) if r.dtype == torch.bfloat16 else r)
+        w = want.view(np.int16) if segments[i].dtype == "bf16" else want
+        assert g.shape == w.shape and np.array_equal(g.view(np.uint8), np.ascontiguousarray(w).view(np.uint8)), \
+            f"compacted rows of segment {i}"
+
+
+def run_and_compare(segments, R, params, dev, alpha=None, pad=0, ctx=None, compact=True):
+    dsegs = to_device(segments, dev, pad)
+    out = msao.msao_run(dsegs, R, params, alpha, ctx=ctx, compact=compact)
+    torch.cuda.synchronize()
+    got = out.results(R, len(segments))
+    ref = oracle.run(segments, R, params, alpha)
+    errs = compare_scores(segments, R, got, ref)
+    compare_frames(got, ref)
+    compare_requests(got, ref)
+    compare_selection(segments, R, got, ref, params, gpu_mas=host(got["mas"]))
+    if compact:
+        compare_compaction(dsegs, segments, out, oracle.compact_rows(segments, host(got["kept_count"]),
+                                                                     host(got["kept_idx"])), host(got["kept_count"]))
+    return got, ref, errs
+
+
+# ------------------------------------------------------------- the five workloads
+
+@pytest.mark.parametrize("config", [1, 2, 3, 4])
+def test_config_full_size(config, dev):
+    log(f"[parity] config {config} full size")
+    w = make_workload(config)
+    _, ref, errs = run_and_compare(w.segments, w.n_requests, w.params, dev)
+    log(f"[parity] config {config}: max rel err {errs}; MAS[:8] {ref['mas'][:8]}")
+
+
+def test_config5_full_size_fused(dev):
+    log("[parity] config 5 full size (1.5 GB, fused run)")
+    w = make_workload(5)
+    _, ref, errs = run_and_compare(w.segments, w.n_requests, w.params, dev)
+    assert np.all(ref["k"] == 720)
+    log(f"[parity] config 5: max rel err {errs}")
+
+
+# ---------------------------------------------------------------- adversarial
+
+def _rand_seg(rng, request, modality, T, P, C, dtype, keep, kind="normal"):
+    n = T * P
+    if kind == "normal":
+        x = rng.standard_normal((n, C)).astype(np.float32)
+    elif kind == "relu_bg":
+        x = np.maximum(rng.standard_normal((n, C)), 0).astype(np.float32)
+        x[rng.random(n) < 0.5] *= np.float32(0.05)
+    elif kind == "same":
+        x = np.repeat(rng.standard_normal((1, C)).astype(np.float32), n, axis=0)
+    elif kind == "zero":
+        x = np.zeros((n, C), np.float32)
+    elif kind == "special":
+        x = rng.standard_normal((n, C)).astype(np.float32)
+        specials = np.array([np.nan, np.inf, -np.inf, -0.0, 0.0, 0.1, -0.1], np.float32)
+        mask = rng.random((n, C)) < 0.05
+        x[mask] = rng.choice(specials, size=int(mask.sum()))
+    elif kind == "static_video":
+        base = rng.standard_normal((P, C)).astype(np.float32)
+        frames = [base]
+        for _ in range(T - 1):
+            frames.append(frames[-1] + np.float32(0.02) * rng.standard_normal((P, C)).astype(np.float32))
+        x = np.concatenate(frames)
+    else:
+        raise ValueError(kind)
+    data = x if dtype == "f32" else f32_to_bf16_bits(x)
+    return Segment(request, modality, T, P, C, dtype, keep, data)
+
+
+def adversarial_cases():
+    rng = np.random.default_rng(2024)
+    cases = {}
+    cases["widths"] = [
+        _rand_seg(rng, 0, IMAGE, 1, 37, 8, "bf16", 0.5),          # one partial unit, N < 64
+        _rand_seg(rng, 0, TEXT, 1, 65, 24, "f32", 1.0),
+        _rand_seg(rng, 0, AUDIO, 1, 70, 1288, "bf16", 0.3),       # 161 chunks: ragged third unit
+        _rand_seg(rng, 1, IMAGE, 1, 33, 4104, "bf16", 0.2),       # 513 chunks: generic row path
+        _rand_seg(rng, 1, AUDIO, 1, 19, 2052, "f32", 0.75),       # 513 chunks (fp32), generic
+        _rand_seg(rng, 1, TEXT, 1, 3, 72, "f32", 0.01),
+    ]
+    cases["video"] = [
+        _rand_seg(rng, 0, VIDEO, 2, 9, 1024, "bf16", 0.3),        # T = 2
+        _rand_seg(rng, 0, VIDEO, 1, 11, 1024, "bf16", 0.3),       # T = 1: an image
+        _rand_seg(rng, 1, VIDEO, 7, 5, 520, "f32", 0.4),          # fp32 chains, ragged units
+        _rand_seg(rng, 1, VIDEO, 5, 6, 4096, "bf16", 0.5),        # 8 units: generic chain path
+        _rand_seg(rng, 2, VIDEO, 40, 3, 1024, "bf16", 0.25, "static_video"),
+        _rand_seg(rng, 2, IMAGE, 1, 50, 1024, "bf16", 0.25, "relu_bg"),
+    ]
+    cases["ties_and_specials"] = [
+        _rand_seg(rng, 0, IMAGE, 1, 300, 64, "bf16", 0.37, "same"),   # tie storm
+        _rand_seg(rng, 0, AUDIO, 1, 100, 64, "f32", 0.5, "zero"),      # all sparse, all tied
+        _rand_seg(rng, 0, TEXT, 1, 200, 256, "f32", 0.5, "special"),   # NaN / inf / -0 / +-tau
+        _rand_seg(rng, 1, VIDEO, 6, 16, 64, "bf16", 0.5, "same"),      # identical frames
+        _rand_seg(rng, 1, IMAGE, 1, 1, 64, "bf16", 0.5),               # single token
+    ]
+    cases["keep_extremes"] = [
+        _rand_seg(rng, 0, IMAGE, 1, 100, 128, "bf16", 0.0),
+        _rand_seg(rng, 0, AUDIO, 1, 100, 128, "bf16", 1.0),
+        _rand_seg(rng, 0, TEXT, 1, 100, 128, "bf16", 0.01),            # k = 1
+        _rand_seg(rng, 1, IMAGE, 1, 100, 128, "bf16", 0.999),          # k = N
+    ]
+    cases["empty_and_multi"] = [
+        _rand_seg(rng, 0, IMAGE, 1, 0, 64, "bf16", 0.5),
+        _rand_seg(rng, 0, IMAGE, 1, 40, 64, "bf16", 0.5, "relu_bg"),
+        _rand_seg(rng, 0, IMAGE, 1, 60, 64, "bf16", 0.5),              # two segments, one (r, m)
+        _rand_seg(rng, 2, AUDIO, 1, 30, 64, "f32", 0.5),               # request 1 absent
+        _rand_seg(rng, 2, VIDEO, 4, 0, 64, "bf16", 0.5),               # empty video
+        _rand_seg(rng, 2, VIDEO, 3, 10, 64, "bf16", 0.5),
+        _rand_seg(rng, 2, VIDEO, 3, 10, 64, "bf16", 0.5),              # two videos in one (r, m)
+    ]
+    cases["guided"] = [
+        _rand_seg(rng, 0, IMAGE, 1, 576, 1024, "bf16", -1.0, "relu_bg"),
+        _rand_seg(rng, 0, AUDIO, 1, 300, 1280, "bf16", -1.0),
+        _rand_seg(rng, 0, TEXT, 1, 64, 256, "bf16", -1.0),
+        _rand_seg(rng, 1, VIDEO, 8, 32, 1024, "bf16", -1.0, "static_video"),
+        _rand_seg(rng, 1, IMAGE, 1, 100, 512, "f32", 0.5),
+    ]
+    return cases
+
+
+ADV = adversarial_cases()
+
+
+@pytest.mark.parametrize("name", sorted(ADV))
+def test_adversarial(name, dev):
+    segs = ADV[name]
+    R = max(s.request for s in segs) + 1
+    log(f"[parity] adversarial {name}: {len(segs)} segments, R={R}")
+    run_and_compare(segs, R, default_params(), dev)
+
+
+@pytest.mark.parametrize("variant", ["alpha", "literal", "lambda_s0", "lambda_t0", "tau0", "tau_s_extremes"])
+def test_parameter_variants(variant, dev):
+    segs = ADV["guided"] + ADV["video"][:3]
+    segs = [Segment(s.request if s.request < 2 else 1, s.modality, s.n_frames, s.tokens_per_frame, s.hidden,
+                    s.dtype, s.keep_ratio, s.data) for s in segs]
+    R = 2
+    p = default_params()
+    alpha = None
+    if variant == "alpha":
+        alpha = np.random.default_rng(5).normal(size=R * 4).astype(np.float32)
+    elif variant == "literal":
+        p["flags"] = oracle.FLAG_TEMPORAL_LITERAL
+    elif variant == "lambda_s0":
+        p["lambda_s"] = [0.0] * 4
+    elif variant == "lambda_t0":
+        p["lambda_t"] = [0.0] * 4
+    elif variant == "tau0":
+        p["tau"] = 0.0
+    elif variant == "tau_s_extremes":
+        p["tau_s"] = 1.0
+    log(f"[parity] parameter variant {variant}")
+    run_and_compare(segs, R, p, dev, alpha=alpha)
+
+
+def test_row_stride_padding(dev):
+    segs = ADV["widths"][:3] + ADV["video"][:1]
+    R = max(s.request for s in segs) + 1
+    log("[parity] padded row stride")
+    run_and_compare(segs, R, default_params(), dev, pad=24)
+
+
+# ------------------------------------------------------ separate entry points
+
+def test_separate_entry_points(dev):
+    w = make_workload(4, n_requests=3)
+    segs = w.segments + ADV["video"]
+    segs = [Segment(min(s.request, 2), s.modality, s.n_frames, s.tokens_per_frame, s.hidden, s.dtype,
+                    -1.0 if i % 4 == 1 else s.keep_ratio, s.data) for i, s in enumerate(segs)]
+    R, p = 3, default_params()
+    log("[parity] msao_mas_score / temporal_redundancy / select_tokens / compact")
+    dsegs = to_device(segs, dev)
+    ref = oracle.run(segs, R, p)
+    o1 = msao.msao_mas_score(dsegs, R, p)
+    torch.cuda.synchronize()
+    g1 = o1.results(R, len(segs))
+    compare_scores(segs, R, g1, ref)
+    compare_frames(g1, ref)
+    compare_requests(g1, ref)
+    o2 = msao.msao_temporal_redundancy(dsegs, R, p)
+    torch.cuda.synchronize()
+    g2 = o2.results(R, len(segs))
+    assert np.array_equal(host(g2["d"]).astype(np.uint32), ref["d"])
+    assert_close_rel(host(g2["res"]), ref["res"], token_tolerances(segs), "res")
+    compare_frames(g2, ref)
+    assert np.array_equal(host(g2["temporal"]), ref["temporal"])
+    # selection from the oracle's z, d and MAS (inputs from the oracle, not from the GPU)
+    z = torch.from_numpy(ref["z"].view(np.int32)).to(dev)
+    d = torch.from_numpy(ref["d"].view(np.int32)).to(dev)
+    mas = torch.from_numpy(ref["mas"]).to(dev)
+    o3 = msao.msao_select_tokens(dsegs, R, z, d, mas, p)
+    torch.cuda.synchronize()
+    g3 = o3.results(R, len(segs))
+    assert np.array_equal(host(g3["kept_count"]), ref["k"])
+    assert np.array_equal(host(g3["kept_idx"]), ref["kept_idx"])
+    assert np.array_equal(host(g3["keep"]), ref["keep"])
+    # compaction from the oracle's kept indices
+    o4 = msao.Outputs(dsegs, R)
+    o4.sel["kept_idx"][: len(ref["kept_idx"])].copy_(torch.from_numpy(ref["kept_idx"]))
+    o4.sel["kept_count"][: len(segs)].copy_(torch.from_numpy(ref["k"]))
+    msao.msao_compact(dsegs, o4)
+    torch.cuda.synchronize()
+    compare_compaction(dsegs, segs, o4, oracle.compact_rows(segs, ref["k"], ref["kept_idx"]), ref["k"])
+
+
+# ------------------------------------------------- determinism and launch shapes
+
+def test_repeat_runs_bitwise_identical(dev):
+    w = make_workload(4, n_requests=4)
+    segs = w.segments + ADV["video"]
+    R = 4
+    segs = [Segment(min(s.request, 3), s.modality, s.n_frames, s.tokens_per_frame, s.hidden, s.dtype,
+                    s.keep_ratio, s.data) for s in segs]
+    dsegs = to_device(segs, dev)
+    log("[parity] 20 repeated runs")
+    first = None
+    out = msao.Outputs(dsegs, R)
+    call = msao.prepare("msao_run", dsegs, R, out, w.params)
+    for i in range(20):
+        call()
+        torch.cuda.synchronize()
+        snap = {k: host(v).copy() for k, v in out.results(R, len(segs)).items()}
+        snap["out"] = host(out.out).copy()
+        if first is None:
+            first = snap
+        else:
+            for k in first:
+                assert np.array_equal(first[k].view(np.uint8), snap[k].view(np.uint8)), (i, k)
+
+
+@pytest.mark.parametrize("row_bytes,chain", [("2048", "4"), ("65536", "32"), ("1", "1")])
+def test_launch_shapes_same_results(row_bytes, chain, dev, monkeypatch):
+    """Different work-item sizes (rows per wavefront, frames per video run)
+    give bit-identical outputs."""
+    segs = make_workload(4, n_requests=2).segments + ADV["video"][:3]
+    R = 3
+    log(f"[parity] launch shape rows={row_bytes}B chain={chain}")
+    monkeypatch.setenv("MSAO_ROW_ITEM_BYTES", row_bytes)
+    monkeypatch.setenv("MSAO_CHAIN_FRAMES", chain)
+    ctx = B.Context(0)
+    run_and_compare(segs, R, default_params(), dev, ctx=ctx)
+    ctx.close()
