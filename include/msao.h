@@ -217,6 +217,29 @@ msao_status msao_run(msao_ctx* ctx, const msao_segment* segs, int n, int n_reque
                      const msao_select_out* sel, void* out, const int64_t* out_byte_off, int64_t out_bytes,
                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- plans: tables uploaded once, runs with no host-to-device copy -------- */
+
+/* A plan holds the per-call tables of msao_run (offsets, work items, integer
+ * thresholds, Q24 weights, keep counts, data pointers) for one segment table.
+ * msao_plan_create validates, builds the tables and enqueues their upload into
+ * `workspace` on `stream`; msao_plan_run then enqueues the three launches of
+ * msao_run with no host-to-device copy, so a fixed-shape serving loop (new
+ * data written into the same input buffers each time) pays no per-call
+ * upload. The workspace must stay allocated and must not be written by the
+ * caller while the plan exists; runs on other streams must be ordered after
+ * `stream`. out_byte_off (host [n], may be NULL if no run compacts) is copied.
+ * Runs of one plan that overlap on the GPU race on the workspace. */
+typedef struct msao_plan msao_plan;
+msao_status msao_plan_create(msao_ctx* ctx, const msao_segment* segs, int n, int n_requests,
+                             const msao_params* params, const float* alpha, const int64_t* out_byte_off,
+                             void* workspace, size_t workspace_bytes, void* stream, msao_plan** plan);
+/* Same outputs and rules as msao_run. */
+msao_status msao_plan_run(msao_plan* plan, const msao_token_out* tok, const msao_frame_out* frm,
+                          const msao_req_out* req, const msao_select_out* sel, void* out, int64_t out_bytes,
+                          void* stream);
+/* Free a plan (NULL is ignored); the caller must have synchronised its runs. */
+void msao_plan_destroy(msao_plan* plan);
+
 /* ---- profiling ----------------------------------------------------------- */
 
 /* Kernels of the hot path, for msao_kernel_times. */
@@ -225,11 +248,12 @@ msao_status msao_run(msao_ctx* ctx, const msao_segment* segs, int n, int n_reque
 #define MSAO_KERNEL_GATHER 2  /* compaction */
 #define MSAO_NUM_KERNELS 3
 
-/* When enabled, every launch is bracketed by HIP events on the caller's
- * stream. */
+/* When enabled, every launch is bracketed by a pair of HIP events recorded on
+ * the caller's stream. */
 msao_status msao_set_profiling(msao_ctx* ctx, int enable);
-/* Milliseconds each kernel took in the last profiled call (0 if not
- * launched); blocks until that call's events have completed. */
+/* ms[MSAO_NUM_KERNELS]: mean milliseconds per launch of each kernel over the
+ * launches recorded since the previous query (0 if none); blocks until they
+ * have completed, then forgets them. */
 msao_status msao_kernel_times(msao_ctx* ctx, float* ms);
 
 #ifdef __cplusplus

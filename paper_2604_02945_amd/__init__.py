@@ -6,6 +6,6 @@ it with the same entry-point names.
 """
 from .binding import (  # noqa: F401
     AUDIO, BF16, F32, FLAG_TEMPORAL_LITERAL, IMAGE, TEXT, VIDEO,
-    Context, DeviceSegment, MsaoError, Outputs, compact_layout, compacted_rows, default_params, lib,
+    Context, DeviceSegment, MsaoError, Outputs, Plan, compact_layout, compacted_rows, default_params, lib,
     msao_compact, msao_mas_score, msao_run, msao_select_tokens, msao_temporal_redundancy, prepare, sizes,
 )

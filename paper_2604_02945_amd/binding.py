@@ -88,6 +88,10 @@ SIGNATURES = [
                                     ctypes.c_size_t, _P]),
     ("msao_run", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P,
                                 ctypes.c_int64, _P, ctypes.c_size_t, _P]),
+    ("msao_plan_create", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, ctypes.c_size_t, _P,
+                                        ctypes.POINTER(_P)]),
+    ("msao_plan_run", ctypes.c_int, [_P, _P, _P, _P, _P, _P, ctypes.c_int64, _P]),
+    ("msao_plan_destroy", None, [_P]),
     ("msao_set_profiling", ctypes.c_int, [_P, ctypes.c_int]),
     ("msao_kernel_times", ctypes.c_int, [_P, _P]),
 ]
@@ -362,6 +366,53 @@ def prepare(entry: str, segments: Sequence[DeviceSegment], n_requests: int, outp
     else:
         raise ValueError(f"unknown entry point {entry}")
     return Call(entry, args, ctx, keep)
+
+
+class Plan:
+    """msao_plan: the tables of one segment table uploaded once into the
+    workspace of `outputs`; each call enqueues the three launches of msao_run
+    with no host-to-device copy. The segments' input buffers and `outputs`
+    must outlive the plan."""
+
+    def __init__(self, segments: Sequence[DeviceSegment], n_requests: int, outputs: Outputs,
+                 params: Optional[dict] = None, alpha: Optional[Sequence[float]] = None,
+                 ctx: Optional[Context] = None, compact: bool = True, stream=None):
+        device = _device_of(segments)
+        self.ctx = ctx or default_context(device.index if device.index is not None else torch.cuda.current_device())
+        self.segt = segment_table(segments)
+        self.prm = params_struct(params)
+        n, R = len(segments), n_requests
+        self.al = None
+        if alpha is not None:
+            vals = list(alpha)
+            if len(vals) != R * NMOD:
+                raise ValueError("alpha needs n_requests * 4 logits")
+            self.al = (ctypes.c_float * len(vals))(*vals)
+        o = self.outputs = outputs
+        self.compact = compact and o.out is not None
+        h = ctypes.c_void_p()
+        _check(lib().msao_plan_create(self.ctx.handle, self.segt, n, R, _addr(self.prm), self.al,
+                                      o.out_off if self.compact else None, _ptr(o.workspace),
+                                      ctypes.c_size_t(o.ws_bytes), _stream_ptr(stream), ctypes.byref(h)), self.ctx)
+        self.handle = h
+        self.segments = list(segments)
+        self._args = [h, _addr(o.c_tok), _addr(o.c_frm), _addr(o.c_req), _addr(o.c_sel),
+                      _ptr(o.out) if self.compact else None,
+                      ctypes.c_int64(o.out_bytes if self.compact else 0)]
+
+    def __call__(self, stream=None):
+        _check(lib().msao_plan_run(*self._args, _stream_ptr(stream)), self.ctx)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().msao_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def _one_shot(entry, segments, n_requests, params=None, alpha=None, ctx=None, outputs=None, stream=None,

@@ -27,10 +27,10 @@ struct msao_ctx {
     hipEvent_t stage_ev[2] = {nullptr, nullptr};
     bool stage_used[2] = {false, false};
     int next_slot = 0;
-    // profiling
+    // profiling: an event pair around every launch, averaged per kernel on query
     bool profiling = false;
-    hipEvent_t kev[MSAO_NUM_KERNELS][2] = {};
-    bool kran[MSAO_NUM_KERNELS] = {};
+    std::vector<hipEvent_t> pool;                       // free events
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> rec[MSAO_NUM_KERNELS];
     // tuning
     int row_item_bytes = 16384;
     int chain_frames = 0;       // frames per temporal work item; 0 = automatic
@@ -120,10 +120,13 @@ msao_status validate_impl(const msao_segment* segs, int n, int R, const msao_par
 // Per-call tables, built on the host and uploaded into the workspace.
 struct Plan {
     std::vector<DevSeg> seg;
-    std::vector<int32_t> seg_wi, seg_gi, rm_off, rm_seg, tseg;
+    std::vector<int32_t> seg_wi, seg_gi, tseg;
+    std::vector<RmEntry> rm;
+    std::vector<WiRange> rm_rng;
     std::vector<float> alpha;
     int64_t ntok = 0, nframes = 0;
     int n_wi = 0, n_gwi = 0;
+    int max_n = 0;                 // largest segment (LDS key staging)
     bool any_temporal = false, any_guided = false;
     size_t off_seg = 0, off_wi = 0, off_gi = 0, off_rmoff = 0, off_rmseg = 0, off_tseg = 0, off_alpha = 0;
     size_t table_bytes = 0, off_partial = 0, total_bytes = 0;
@@ -140,8 +143,8 @@ size_t table_layout(Plan& pl, int n, int R)
     pl.off_seg = take(sizeof(DevSeg) * (size_t)std::max(n, 1));
     pl.off_wi = take(sizeof(int32_t) * (size_t)(n + 1));
     pl.off_gi = take(sizeof(int32_t) * (size_t)(n + 1));
-    pl.off_rmoff = take(sizeof(int32_t) * (size_t)(R * kNumMod + 1));
-    pl.off_rmseg = take(sizeof(int32_t) * (size_t)std::max(n, 1));
+    pl.off_rmoff = take(sizeof(RmEntry) * (size_t)std::max(R * kNumMod, 1));
+    pl.off_rmseg = take(sizeof(WiRange) * (size_t)std::max(n, 1));
     pl.off_tseg = take(sizeof(int32_t) * (size_t)std::max(n, 1));
     pl.off_alpha = take(sizeof(float) * (size_t)std::max(R * kNumMod, 1));
     pl.table_bytes = o;
@@ -222,6 +225,7 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         gi += (d.cap + kGatherRows - 1) / kGatherRows;
         pl.seg_gi[(size_t)i + 1] = gi;
         if (d.k < 0) pl.any_guided = true;
+        pl.max_n = std::max(pl.max_n, (int)N);
         tok += N;
         if (d.temporal) frame += s.n_frames;
     }
@@ -230,13 +234,22 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
     pl.n_wi = wi;
     pl.n_gwi = gi;
     // segments grouped by (request, modality), table order inside a group
-    pl.rm_off.assign((size_t)R * kNumMod + 1, 0);
-    for (int i = 0; i < n; ++i) pl.rm_off[(size_t)(segs[i].request * kNumMod + segs[i].modality) + 1]++;
-    for (size_t x = 1; x < pl.rm_off.size(); ++x) pl.rm_off[x] += pl.rm_off[x - 1];
-    pl.rm_seg.assign((size_t)std::max(n, 1), 0);
-    {
-        std::vector<int32_t> fill(pl.rm_off.begin(), pl.rm_off.end() - 1);
-        for (int i = 0; i < n; ++i) pl.rm_seg[(size_t)fill[(size_t)(segs[i].request * kNumMod + segs[i].modality)]++] = i;
+    pl.rm.assign((size_t)std::max(R * kNumMod, 1), RmEntry{});
+    std::vector<int32_t> count((size_t)R * kNumMod + 1, 0);
+    for (int i = 0; i < n; ++i) count[(size_t)(segs[i].request * kNumMod + segs[i].modality) + 1]++;
+    for (size_t x = 1; x < count.size(); ++x) count[x] += count[x - 1];
+    for (int x = 0; x < R * kNumMod; ++x) {
+        pl.rm[(size_t)x].rng_begin = count[(size_t)x];
+        pl.rm[(size_t)x].rng_end = count[(size_t)x + 1];
+    }
+    pl.rm_rng.assign((size_t)std::max(n, 1), WiRange{0, 0});
+    for (int i = 0; i < n; ++i) {
+        const msao_segment& s = segs[i];
+        const DevSeg& d = pl.seg[(size_t)i];
+        RmEntry& e = pl.rm[(size_t)(s.request * kNumMod + s.modality)];
+        e.ntok += (uint64_t)d.n_tok;
+        if (d.temporal) e.qbits += (uint64_t)(d.T - 1) * (uint64_t)d.P * (uint64_t)d.C;
+        pl.rm_rng[(size_t)count[(size_t)(s.request * kNumMod + s.modality)]++] = WiRange{pl.seg_wi[(size_t)i], pl.seg_wi[(size_t)i + 1]};
     }
     pl.alpha.assign((size_t)std::max(R * kNumMod, 1), 0.0f);
     if (alpha)
@@ -291,8 +304,8 @@ msao_status upload(msao_ctx* ctx, const Plan& pl, void* ws, hipStream_t stream)
     put(pl.off_seg, pl.seg.data(), sizeof(DevSeg) * pl.seg.size());
     put(pl.off_wi, pl.seg_wi.data(), sizeof(int32_t) * pl.seg_wi.size());
     put(pl.off_gi, pl.seg_gi.data(), sizeof(int32_t) * pl.seg_gi.size());
-    put(pl.off_rmoff, pl.rm_off.data(), sizeof(int32_t) * pl.rm_off.size());
-    put(pl.off_rmseg, pl.rm_seg.data(), sizeof(int32_t) * pl.rm_seg.size());
+    put(pl.off_rmoff, pl.rm.data(), sizeof(RmEntry) * pl.rm.size());
+    put(pl.off_rmseg, pl.rm_rng.data(), sizeof(WiRange) * pl.rm_rng.size());
     put(pl.off_tseg, pl.tseg.data(), sizeof(int32_t) * pl.tseg.size());
     put(pl.off_alpha, pl.alpha.data(), sizeof(float) * pl.alpha.size());
     if ((e = hipMemcpyAsync(ws, h, pl.table_bytes, hipMemcpyHostToDevice, stream)) != hipSuccess)
@@ -309,8 +322,8 @@ Tables device_tables(const Plan& pl, void* ws, int n, int R, const msao_params* 
     t.seg = (const DevSeg*)(b + pl.off_seg);
     t.seg_wi = (const int32_t*)(b + pl.off_wi);
     t.seg_gi = (const int32_t*)(b + pl.off_gi);
-    t.rm_off = (const int32_t*)(b + pl.off_rmoff);
-    t.rm_seg = (const int32_t*)(b + pl.off_rmseg);
+    t.rm = (const RmEntry*)(b + pl.off_rmoff);
+    t.rm_rng = (const WiRange*)(b + pl.off_rmseg);
     t.tseg = (const int32_t*)(b + pl.off_tseg);
     t.alpha = (const float*)(b + pl.off_alpha);
     t.partial = (Partial*)(b + pl.off_partial);
@@ -353,17 +366,33 @@ msao_status check_out_alignment(msao_ctx* ctx, std::initializer_list<std::pair<c
     return MSAO_OK;
 }
 
+hipEvent_t pooled_event(msao_ctx* ctx)
+{
+    if (!ctx->pool.empty()) {
+        hipEvent_t e = ctx->pool.back();
+        ctx->pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    return hipEventCreate(&e) == hipSuccess ? e : nullptr;
+}
+
 // Launch with optional profiling events around it.
 msao_status launched(msao_ctx* ctx, int kernel, hipStream_t stream, int (*fn)(const void*, void*), const void* args)
 {
     hipError_t e;
-    if (ctx->profiling && (e = hipEventRecord(ctx->kev[kernel][0], stream)) != hipSuccess)
-        return hip_fail(ctx, e, "hipEventRecord");
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (ctx->profiling) {
+        e0 = pooled_event(ctx);
+        e1 = pooled_event(ctx);
+        if (!e0 || !e1) return fail(&ctx->err, MSAO_ERR_HIP, "hipEventCreate failed");
+        if ((e = hipEventRecord(e0, stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
+    }
     const int rc = fn(args, stream);
     if (rc != 0) return hip_fail(ctx, (hipError_t)rc, "kernel launch");
     if (ctx->profiling) {
-        if ((e = hipEventRecord(ctx->kev[kernel][1], stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
-        ctx->kran[kernel] = true;
+        if ((e = hipEventRecord(e1, stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
+        ctx->rec[kernel].push_back({e0, e1});
     }
     return MSAO_OK;
 }
@@ -506,13 +535,6 @@ msao_status msao_create(msao_ctx** out, int device)
             return MSAO_ERR_HIP;
         }
     }
-    for (int k = 0; k < MSAO_NUM_KERNELS; ++k)
-        for (int j = 0; j < 2; ++j)
-            if ((e = hipEventCreate(&c->kev[k][j])) != hipSuccess) {
-                g_err = std::string("hipEventCreate: ") + hipGetErrorString(e);
-                msao_destroy(c);
-                return MSAO_ERR_HIP;
-            }
     if (const char* v = std::getenv("MSAO_ROW_ITEM_BYTES")) c->row_item_bytes = std::max(1, std::atoi(v));
     if (const char* v = std::getenv("MSAO_CHAIN_FRAMES")) c->chain_frames = std::max(0, std::atoi(v));
     *out = c;
@@ -531,8 +553,12 @@ void msao_destroy(msao_ctx* ctx)
         if (ctx->stage[i]) (void)hipHostFree(ctx->stage[i]);
     }
     for (int k = 0; k < MSAO_NUM_KERNELS; ++k)
-        for (int j = 0; j < 2; ++j)
-            if (ctx->kev[k][j]) (void)hipEventDestroy(ctx->kev[k][j]);
+        for (auto& pr : ctx->rec[k]) {
+            (void)hipEventSynchronize(pr.second);
+            ctx->pool.push_back(pr.first);
+            ctx->pool.push_back(pr.second);
+        }
+    for (hipEvent_t e : ctx->pool) (void)hipEventDestroy(e);
     delete ctx;
 }
 
@@ -547,14 +573,22 @@ msao_status msao_kernel_times(msao_ctx* ctx, float* ms)
 {
     if (!ctx || !ms) return MSAO_ERR_INVALID_ARG;
     DeviceGuard guard(ctx->device);
+    msao_status st = MSAO_OK;
     for (int k = 0; k < MSAO_NUM_KERNELS; ++k) {
-        ms[k] = 0.0f;
-        if (!ctx->kran[k]) continue;
-        hipError_t e = hipEventSynchronize(ctx->kev[k][1]);
-        if (e == hipSuccess) e = hipEventElapsedTime(&ms[k], ctx->kev[k][0], ctx->kev[k][1]);
-        if (e != hipSuccess) return hip_fail(ctx, e, "msao_kernel_times");
+        double sum = 0.0;
+        for (auto& pr : ctx->rec[k]) {
+            float t = 0.0f;
+            hipError_t e = hipEventSynchronize(pr.second);
+            if (e == hipSuccess) e = hipEventElapsedTime(&t, pr.first, pr.second);
+            if (e != hipSuccess && st == MSAO_OK) st = hip_fail(ctx, e, "msao_kernel_times");
+            sum += t;
+            ctx->pool.push_back(pr.first);
+            ctx->pool.push_back(pr.second);
+        }
+        ms[k] = ctx->rec[k].empty() ? 0.0f : (float)(sum / (double)ctx->rec[k].size());
+        ctx->rec[k].clear();
     }
-    return MSAO_OK;
+    return st;
 }
 
 msao_status msao_mas_score(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
@@ -572,7 +606,6 @@ msao_status msao_mas_score(msao_ctx* ctx, const msao_segment* segs, int n, int R
     if (tok) MSAO_TRY(check_out_alignment(ctx, {{tok->z, 4}, {tok->l1, 4}, {tok->l2, 4}, {tok->info, 4}, {tok->d, 4}, {tok->res, 4}}));
     if (frm) MSAO_TRY(check_out_alignment(ctx, {{frm->dframe, 8}, {frm->sim, 4}, {frm->gamma, 4}}));
     if (req) MSAO_TRY(check_out_alignment(ctx, {{req->agg, 8}, {req->rho, 4}, {req->temporal, 4}, {req->beta, 4}, {req->mas, 4}}));
-    for (int k = 0; k < MSAO_NUM_KERNELS; ++k) ctx->kran[k] = false;
     DeviceGuard guard(ctx->device);
     hipStream_t st = (hipStream_t)stream;
     MSAO_TRY(upload(ctx, pl, ws, st));
@@ -608,7 +641,6 @@ msao_status msao_temporal_redundancy(msao_ctx* ctx, const msao_segment* segs, in
     if (want_frames && !d) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "per-frame outputs need d");
     MSAO_TRY(check_out_alignment(ctx, {{d, 4}, {res, 4}, {temporal, 4}}));
     if (frm) MSAO_TRY(check_out_alignment(ctx, {{frm->dframe, 8}, {frm->sim, 4}, {frm->gamma, 4}}));
-    for (int k = 0; k < MSAO_NUM_KERNELS; ++k) ctx->kran[k] = false;
     DeviceGuard guard(ctx->device);
     hipStream_t st = (hipStream_t)stream;
     MSAO_TRY(upload(ctx, pl, ws, st));
@@ -646,7 +678,6 @@ msao_status msao_select_tokens(msao_ctx* ctx, const msao_segment* segs, int n, i
     if (pl.any_temporal && !d) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "d is NULL but a segment is temporal");
     if (pl.any_guided && !mas) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "mas is NULL but a keep ratio is negative");
     MSAO_TRY(check_out_alignment(ctx, {{z, 4}, {d, 4}, {mas, 4}, {sel->kept_idx, 4}, {sel->kept_count, 4}}));
-    for (int k = 0; k < MSAO_NUM_KERNELS; ++k) ctx->kran[k] = false;
     DeviceGuard guard(ctx->device);
     hipStream_t st = (hipStream_t)stream;
     MSAO_TRY(upload(ctx, pl, ws, st));
@@ -658,6 +689,7 @@ msao_status msao_select_tokens(msao_ctx* ctx, const msao_segment* segs, int n, i
     pa.d = d;
     pa.mas_in = mas;
     pa.n_sel_blocks = n;
+    pa.keys_cap = std::min(pl.max_n, kMaxLdsKeys);
     return launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa);
 }
 
@@ -677,7 +709,6 @@ msao_status msao_compact(msao_ctx* ctx, const msao_segment* segs, int n, const i
         return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "kept_idx and kept_count are required");
     MSAO_TRY(check_out_alignment(ctx, {{kept_idx, 4}, {kept_count, 4}}));
     MSAO_TRY(check_compact_out(ctx, pl, segs, n, out, out_byte_off, out_bytes));
-    for (int k = 0; k < MSAO_NUM_KERNELS; ++k) ctx->kran[k] = false;
     DeviceGuard guard(ctx->device);
     hipStream_t st = (hipStream_t)stream;
     MSAO_TRY(upload(ctx, pl, ws, st));
@@ -690,6 +721,77 @@ msao_status msao_compact(msao_ctx* ctx, const msao_segment* segs, int n, const i
     return launched(ctx, MSAO_KERNEL_GATHER, st, run_gather, &ga);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Output checks of a full run (scoring, MAS, selection, optional compaction).
+msao_status check_run_outputs(msao_ctx* ctx, const Plan& pl, const std::vector<msao_segment>& segs,
+                              const msao_token_out* tok, const msao_frame_out* frm, const msao_req_out* req,
+                              const msao_select_out* sel, void* out, const int64_t* out_byte_off, int64_t out_bytes)
+{
+    if (pl.ntok > 0 && !(tok && tok->z)) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "a full run needs tok->z");
+    if (pl.any_temporal && !(tok && tok->d))
+        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "a full run needs tok->d for temporal segments");
+    if (!sel || !sel->kept_idx || !sel->kept_count)
+        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "selection needs kept_idx and kept_count");
+    if (tok) MSAO_TRY(check_out_alignment(ctx, {{tok->z, 4}, {tok->l1, 4}, {tok->l2, 4}, {tok->info, 4}, {tok->d, 4}, {tok->res, 4}}));
+    if (frm) MSAO_TRY(check_out_alignment(ctx, {{frm->dframe, 8}, {frm->sim, 4}, {frm->gamma, 4}}));
+    if (req) MSAO_TRY(check_out_alignment(ctx, {{req->agg, 8}, {req->rho, 4}, {req->temporal, 4}, {req->beta, 4}, {req->mas, 4}}));
+    MSAO_TRY(check_out_alignment(ctx, {{sel->kept_idx, 4}, {sel->kept_count, 4}}));
+    if (out) MSAO_TRY(check_compact_out(ctx, pl, segs.data(), (int)segs.size(), out, out_byte_off, out_bytes));
+    return MSAO_OK;
+}
+
+// The three launches of a full run, on tables already in the workspace.
+msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const msao_token_out* tok,
+                        const msao_frame_out* frm, const msao_req_out* req, const msao_select_out* sel, void* out,
+                        int64_t out_bytes, hipStream_t st)
+{
+    ScoreArgs sa;
+    sa.t = t;
+    sa.tok = token_out(tok);
+    sa.mode = kModeScore;
+    MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
+    PostArgs pa;
+    std::memset(&pa, 0, sizeof pa);
+    pa.t = t;
+    if (req) pa.req = ReqOut{req->agg, req->rho, req->temporal, req->beta, req->mas, req->present};
+    if (frm) pa.frm = FrameOut{frm->dframe, frm->sim, frm->gamma};
+    pa.sel = SelOut{sel->keep, sel->kept_idx, sel->kept_count};
+    pa.z = tok ? tok->z : nullptr;
+    pa.d = tok ? tok->d : nullptr;
+    pa.mas_in = nullptr;
+    const bool want_req = req && (req->agg || req->rho || req->temporal || req->beta || req->mas || req->present);
+    const bool want_frames = frm && (frm->dframe || frm->sim || frm->gamma) && pl.nframes > 0;
+    pa.n_req_blocks = want_req ? t.R : 0;
+    pa.n_frame_blocks = want_frames ? (int)pl.nframes : 0;
+    pa.n_sel_blocks = t.n;
+    pa.keys_cap = std::min(pl.max_n, kMaxLdsKeys);
+    MSAO_TRY(launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa));
+    if (!out) return MSAO_OK;
+    GatherArgs ga;
+    ga.t = t;
+    ga.kept_idx = sel->kept_idx;
+    ga.kept_count = sel->kept_count;
+    ga.out = (uint8_t*)out;
+    ga.out_bytes = out_bytes;
+    return launched(ctx, MSAO_KERNEL_GATHER, st, run_gather, &ga);
+}
+
+}  // namespace
+
+struct msao_plan {
+    msao_ctx* ctx = nullptr;
+    Plan pl;
+    Tables t{};
+    std::vector<msao_segment> segs;
+    std::vector<int64_t> out_off;
+    msao_params params{};
+};
+
+extern "C" {
+
 msao_status msao_run(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
                      const float* alpha, const msao_token_out* tok, const msao_frame_out* frm,
                      const msao_req_out* req, const msao_select_out* sel, void* out, const int64_t* out_byte_off,
@@ -700,48 +802,55 @@ msao_status msao_run(msao_ctx* ctx, const msao_segment* segs, int n, int R, cons
     Plan pl;
     build_plan(ctx, segs, n, R, params, alpha, out_byte_off, pl);
     MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
-    if (pl.ntok > 0 && !(tok && tok->z)) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "msao_run needs tok->z");
-    if (pl.any_temporal && !(tok && tok->d))
-        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "msao_run needs tok->d for temporal segments");
-    if (!sel || !sel->kept_idx || !sel->kept_count)
-        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "selection needs kept_idx and kept_count");
-    const bool want_frames = frm && (frm->dframe || frm->sim || frm->gamma) && pl.nframes > 0;
-    if (tok) MSAO_TRY(check_out_alignment(ctx, {{tok->z, 4}, {tok->l1, 4}, {tok->l2, 4}, {tok->info, 4}, {tok->d, 4}, {tok->res, 4}}));
-    if (frm) MSAO_TRY(check_out_alignment(ctx, {{frm->dframe, 8}, {frm->sim, 4}, {frm->gamma, 4}}));
-    if (req) MSAO_TRY(check_out_alignment(ctx, {{req->agg, 8}, {req->rho, 4}, {req->temporal, 4}, {req->beta, 4}, {req->mas, 4}}));
-    MSAO_TRY(check_out_alignment(ctx, {{sel->kept_idx, 4}, {sel->kept_count, 4}}));
-    if (out) MSAO_TRY(check_compact_out(ctx, pl, segs, n, out, out_byte_off, out_bytes));
-    for (int k = 0; k < MSAO_NUM_KERNELS; ++k) ctx->kran[k] = false;
+    const std::vector<msao_segment> sv(segs, segs + n);
+    MSAO_TRY(check_run_outputs(ctx, pl, sv, tok, frm, req, sel, out, out_byte_off, out_bytes));
     DeviceGuard guard(ctx->device);
     hipStream_t st = (hipStream_t)stream;
     MSAO_TRY(upload(ctx, pl, ws, st));
-    ScoreArgs sa;
-    sa.t = device_tables(pl, ws, n, R, params);
-    sa.tok = token_out(tok);
-    sa.mode = kModeScore;
-    MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
-    PostArgs pa;
-    std::memset(&pa, 0, sizeof pa);
-    pa.t = sa.t;
-    if (req) pa.req = ReqOut{req->agg, req->rho, req->temporal, req->beta, req->mas, req->present};
-    if (frm) pa.frm = FrameOut{frm->dframe, frm->sim, frm->gamma};
-    pa.sel = SelOut{sel->keep, sel->kept_idx, sel->kept_count};
-    pa.z = tok ? tok->z : nullptr;
-    pa.d = tok ? tok->d : nullptr;
-    pa.mas_in = nullptr;
-    const bool want_req = req && (req->agg || req->rho || req->temporal || req->beta || req->mas || req->present);
-    pa.n_req_blocks = want_req ? R : 0;
-    pa.n_frame_blocks = want_frames ? (int)pl.nframes : 0;
-    pa.n_sel_blocks = n;
-    MSAO_TRY(launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa));
-    if (!out) return MSAO_OK;
-    GatherArgs ga;
-    ga.t = sa.t;
-    ga.kept_idx = sel->kept_idx;
-    ga.kept_count = sel->kept_count;
-    ga.out = (uint8_t*)out;
-    ga.out_bytes = out_bytes;
-    return launched(ctx, MSAO_KERNEL_GATHER, st, run_gather, &ga);
+    return enqueue_run(ctx, pl, device_tables(pl, ws, n, R, params), tok, frm, req, sel, out, out_bytes, st);
 }
+
+msao_status msao_plan_create(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
+                             const float* alpha, const int64_t* out_byte_off, void* ws, size_t ws_bytes,
+                             void* stream, msao_plan** plan)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    if (!plan) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "plan pointer is NULL");
+    *plan = nullptr;
+    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
+    msao_plan* p = new msao_plan();
+    p->ctx = ctx;
+    p->segs.assign(segs, segs + n);
+    if (out_byte_off) p->out_off.assign(out_byte_off, out_byte_off + n);
+    p->params = *params;
+    build_plan(ctx, segs, n, R, params, alpha, out_byte_off, p->pl);
+    msao_status st = check_ws(ctx, p->pl, ws, ws_bytes);
+    if (st == MSAO_OK) {
+        DeviceGuard guard(ctx->device);
+        st = upload(ctx, p->pl, ws, (hipStream_t)stream);
+    }
+    if (st != MSAO_OK) {
+        delete p;
+        return st;
+    }
+    p->t = device_tables(p->pl, ws, n, R, params);
+    *plan = p;
+    return MSAO_OK;
+}
+
+msao_status msao_plan_run(msao_plan* plan, const msao_token_out* tok, const msao_frame_out* frm,
+                          const msao_req_out* req, const msao_select_out* sel, void* out, int64_t out_bytes,
+                          void* stream)
+{
+    if (!plan) return fail(&g_err, MSAO_ERR_INVALID_ARG, "plan is NULL");
+    msao_ctx* ctx = plan->ctx;
+    if (out && plan->out_off.size() != plan->segs.size())
+        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "the plan was created without out_byte_off");
+    MSAO_TRY(check_run_outputs(ctx, plan->pl, plan->segs, tok, frm, req, sel, out, plan->out_off.data(), out_bytes));
+    DeviceGuard guard(ctx->device);
+    return enqueue_run(ctx, plan->pl, plan->t, tok, frm, req, sel, out, out_bytes, (hipStream_t)stream);
+}
+
+void msao_plan_destroy(msao_plan* plan) { delete plan; }
 
 }  // extern "C"

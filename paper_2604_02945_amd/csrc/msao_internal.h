@@ -44,13 +44,26 @@ struct Partial {
     uint64_t dsum;         // sum of d over frames t >= 1
 };
 
+// One (request, modality): its sizes and its run of work-item ranges in rm_rng
+// (one range per segment of that request and modality).
+struct RmEntry {
+    uint64_t ntok;         // tokens
+    uint64_t qbits;        // activity bits compared by Eq. 5: sum over its video clips of (T-1)*P*C
+    int32_t rng_begin, rng_end;
+    int32_t pad_[2];
+};
+
+struct WiRange {
+    int32_t begin, end;    // scoring work items of one segment
+};
+
 // Device pointers into the workspace, plus scalars, passed by value.
 struct Tables {
     const DevSeg* seg;
     const int32_t* seg_wi;   // [n+1] prefix of scoring work items
     const int32_t* seg_gi;   // [n+1] prefix of gather work items
-    const int32_t* rm_off;   // [R*4+1] CSR offsets into rm_seg
-    const int32_t* rm_seg;   // segment ids grouped by (request, modality)
+    const RmEntry* rm;       // [R*4]
+    const WiRange* rm_rng;   // [n] work-item ranges grouped by (request, modality)
     const int32_t* tseg;     // [n_tseg] temporal segment ids in table order
     const float* alpha;      // [R*4] relevance logits
     Partial* partial;        // [n_wi]
@@ -86,6 +99,7 @@ struct PostArgs {
     int32_t n_frame_blocks;
     int32_t n_sel_blocks; // one per segment
     int32_t temporal_only;// request role writes only the temporal term
+    int32_t keys_cap;     // selection keys staged in LDS per block (larger segments re-read z, d)
 };
 
 struct ScoreArgs {
@@ -109,7 +123,14 @@ int launch_gather(const GatherArgs& a, void* stream);
 
 constexpr int kScoreBlock = 256;   // 4 wavefronts, one work item each
 constexpr int kPostBlock = 256;
-constexpr int kGatherBlock = 256;
-constexpr int kGatherRows = 4;     // kept rows per gather work item
+#ifndef MSAO_GATHER_BLOCK
+#define MSAO_GATHER_BLOCK 64
+#endif
+constexpr int kGatherBlock = MSAO_GATHER_BLOCK;
+#ifndef MSAO_GATHER_ROWS
+#define MSAO_GATHER_ROWS 1
+#endif
+constexpr int kGatherRows = MSAO_GATHER_ROWS;  // kept rows per gather work item
+constexpr int kMaxLdsKeys = 16384; // 128 KiB of LDS per selection block
 
 }  // namespace msao

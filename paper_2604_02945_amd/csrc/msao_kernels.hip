@@ -33,30 +33,108 @@ __device__ __forceinline__ float dpp_f(float v)
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
 }
 
-// Sum over the 64 lanes; the result is the same in every lane. Fixed order,
-// so it is bit-reproducible. quad_perm [1,0,3,2], quad_perm [2,3,0,1],
-// row_half_mirror and row_mirror give each 16-lane row its sum; the four
-// row sums are then read out and added.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_rows(float v)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, false));
+}
+
+// Sum over the 64 lanes, returned as a wave-uniform value. Fixed order, so it
+// is bit-reproducible: quad_perm [1,0,3,2], quad_perm [2,3,0,1],
+// row_half_mirror and row_mirror give every 16-lane row its sum; row_bcast:15
+// and row_bcast:31 then fold the rows into lane 63.
 __device__ __forceinline__ float wave_sum(float v)
 {
     v += dpp_f<0xB1>(v);
     v += dpp_f<0x4E>(v);
     v += dpp_f<0x141>(v);
     v += dpp_f<0x140>(v);
-    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
-    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
-    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-    return (r0 + r1) + (r2 + r3);
+    v += dpp_rows<0x142, 0xA>(v);
+    v += dpp_rows<0x143, 0xC>(v);
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
-__device__ __forceinline__ uint4 ld16(const uint8_t* p) { return *reinterpret_cast<const uint4*>(p); }
+typedef unsigned int vec4 __attribute__((ext_vector_type(4)));
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+// Raw buffer resources (GFX9 word 3): a load whose offset lies past
+// num_records returns 0 and a store there is dropped, so ragged row tails
+// and absent rows need no lane predicates.
+constexpr int kRsrcWord3 = 0x00020000;
+#ifndef MSAO_LOAD_AUX
+#define MSAO_LOAD_AUX 2  // nontemporal: every input row is read once
+#endif
+#ifndef MSAO_STORE_AUX
+#define MSAO_STORE_AUX 0
+#endif
+#ifndef MSAO_GATHER_LOAD_AUX
+#define MSAO_GATHER_LOAD_AUX 0  // kept rows may still be cached from the scoring pass
+#endif
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, int bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kRsrcWord3);
+}
+
+__device__ __forceinline__ vec4 bload(rsrc_t r, int off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, MSAO_LOAD_AUX);
+}
+
+__device__ __forceinline__ vec4 bload_gather(rsrc_t r, int off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, MSAO_GATHER_LOAD_AUX);
+}
+
+__device__ __forceinline__ void bstore(vec4 v, rsrc_t r, int off)
+{
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, MSAO_STORE_AUX);
+}
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m)
+{
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o)
+{
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, o);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), o);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += shfl_xor_u64(v, o);
+    return v;
+}
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint64_t w = shfl_xor_u64(v, o);
+        v = w < v ? w : v;
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint64_t w = shfl_xor_u64(v, o);
+        v = w > v ? w : v;
+    }
+    return v;
+}
 
 // Widening of one 16-byte chunk to floats (exact).
 template <int DT> struct Lane;
 template <> struct Lane<kBF16> {
     static constexpr int EPC = 8;
-    __device__ static __forceinline__ void widen(const uint4& v, float* x)
+    __device__ static __forceinline__ void widen(const vec4& v, float* x)
     {
         x[0] = __uint_as_float(v.x << 16); x[1] = __uint_as_float(v.x & 0xFFFF0000u);
         x[2] = __uint_as_float(v.y << 16); x[3] = __uint_as_float(v.y & 0xFFFF0000u);
@@ -66,7 +144,7 @@ template <> struct Lane<kBF16> {
 };
 template <> struct Lane<kF32> {
     static constexpr int EPC = 4;
-    __device__ static __forceinline__ void widen(const uint4& v, float* x)
+    __device__ static __forceinline__ void widen(const vec4& v, float* x)
     {
         x[0] = __uint_as_float(v.x); x[1] = __uint_as_float(v.y);
         x[2] = __uint_as_float(v.z); x[3] = __uint_as_float(v.w);
@@ -75,6 +153,113 @@ template <> struct Lane<kF32> {
 
 // Active iff NOT(|x| <= tau): NaN is active, -0 is not.
 __device__ __forceinline__ bool active(float x, float tau) { return !(fabsf(x) <= tau); }
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two bf16 products summed into an fp32 accumulator (products of bf16 values
+// are exact in fp32).
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c)
+{
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
+}
+
+// Activity thresholds on bf16 magnitude bits. A bf16 value widens to a float
+// whose bits are its 16 bits shifted up, so |x| <= tau exactly when the 15
+// magnitude bits are at most lo = bits(tau) >> 16 (NaN and inf lie above).
+// For the high channel of a dword the low channel's bits ride below it, hence
+// hi = lo << 16 | 0xFFFF.
+struct Thr {
+    uint32_t hi, lo;
+};
+
+__device__ __forceinline__ Thr bf16_thresholds(float tau)
+{
+    const uint32_t lo = __float_as_uint(tau) >> 16;
+    return Thr{(lo << 16) | 0xFFFFu, lo};
+}
+
+constexpr uint32_t kBf16OnePair = 0x3F803F80u;  // (1.0, 1.0) in bf16
+
+// Ballot of (low 16 bits of ax) > lo: one 16-bit compare, no masking step.
+__device__ __forceinline__ uint64_t ballot_lo16_gt(uint32_t ax, uint32_t lo)
+{
+    uint64_t m;
+    asm("v_cmp_gt_u16_e64 %0, %1, %2" : "=s"(m) : "v"(ax), "s"(lo));
+    return m;
+}
+
+// Statistics of one 16-byte chunk: active count (ballot + scalar popcount),
+// L1 and L2 partial sums of this lane.
+template <int DT>
+__device__ __forceinline__ void chunk_stats(const vec4& v, float tau, const Thr& th, uint32_t& act, float& l1,
+                                            float& l2)
+{
+    if constexpr (DT == kBF16) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const uint32_t x = v[w];
+            const uint32_t ax = x & 0x7FFF7FFFu;
+            act += (uint32_t)__popcll(__ballot(ax > th.hi));
+            act += (uint32_t)__popcll(ballot_lo16_gt(ax, th.lo));
+            l1 = dot2(ax, kBf16OnePair, l1);
+            l2 = dot2(x, x, l2);
+        }
+    } else {
+        float x[4];
+        Lane<kF32>::widen(v, x);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            act += (uint32_t)__popcll(__ballot(active(x[e], tau)));
+            l1 += fabsf(x[e]);
+            l2 = fmaf(x[e], x[e], l2);
+        }
+    }
+}
+
+// The same plus the temporal term against the previous frame: prev holds the
+// previous frame's channel values of this lane, pmask its activity ballots
+// (one per channel slot); both are updated to the current frame.
+template <int DT>
+__device__ __forceinline__ void chunk_chain(const vec4& v, float tau, const Thr& th, float* prev, uint64_t* pmask,
+                                            uint32_t& act, uint32_t& d, float& l1, float& l2, float& res)
+{
+    if constexpr (DT == kBF16) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const uint32_t x = v[w];
+            const uint32_t ax = x & 0x7FFF7FFFu;
+            const uint64_t mlo = ballot_lo16_gt(ax, th.lo);
+            const uint64_t mhi = __ballot(ax > th.hi);
+            act += (uint32_t)(__popcll(mlo) + __popcll(mhi));
+            d += (uint32_t)(__popcll(mlo ^ pmask[2 * w]) + __popcll(mhi ^ pmask[2 * w + 1]));
+            pmask[2 * w] = mlo;
+            pmask[2 * w + 1] = mhi;
+            l1 = dot2(ax, kBf16OnePair, l1);
+            l2 = dot2(x, x, l2);
+            const float flo = __uint_as_float(x << 16), fhi = __uint_as_float(x & 0xFFFF0000u);
+            const float dlo = flo - prev[2 * w], dhi = fhi - prev[2 * w + 1];
+            res = fmaf(dlo, dlo, res);
+            res = fmaf(dhi, dhi, res);
+            prev[2 * w] = flo;
+            prev[2 * w + 1] = fhi;
+        }
+    } else {
+        float x[4];
+        Lane<kF32>::widen(v, x);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint64_t m = __ballot(active(x[e], tau));
+            act += (uint32_t)__popcll(m);
+            d += (uint32_t)__popcll(m ^ pmask[e]);
+            pmask[e] = m;
+            l1 += fabsf(x[e]);
+            l2 = fmaf(x[e], x[e], l2);
+            const float df = x[e] - prev[e];
+            res = fmaf(df, df, res);
+            prev[e] = x[e];
+        }
+    }
+}
 
 // Largest s in [0, n) with prefix[s] <= w (prefix[n] is the total, > w).
 __device__ __forceinline__ int find_seg(const int32_t* __restrict__ prefix, int n, int w)
@@ -108,55 +293,82 @@ __device__ __forceinline__ void emit_token(const TokenOut& o, const DevSeg& sg, 
         if (o.info) {
             float red = sg.lam_s * (float)z;
             if (temporal) red += sg.lam_t * (float)((uint32_t)sg.C - s.d);
-            o.info[g] = 1.0f - red / (float)sg.C;
+            o.info[g] = 1.0f - red * __builtin_amdgcn_rcpf((float)sg.C);
         }
     }
     if (o.d) o.d[g] = temporal ? s.d : 0u;
     if (o.res) o.res[g] = temporal ? s.res : 0.0f;
 }
 
-// Rows [r0, r1) of a non-temporal segment whose rows span NU 1-KiB units
-// (64 lanes x 16 B). Several short rows are loaded before any is reduced so
-// that each wavefront keeps about 4 KiB in flight.
+// Statistics of one row held as NU 1-KiB units (64 lanes x 16 B each).
+template <int DT, int NU>
+__device__ __forceinline__ TokStat row_stats(const vec4 (&v)[NU], float tau, const Thr& th)
+{
+    TokStat s{0u, 0u, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int u = 0; u < NU; ++u) chunk_stats<DT>(v[u], tau, th, s.act, s.l1, s.l2);
+    s.l1 = wave_sum(s.l1);
+    s.l2 = wave_sum(s.l2);
+    return s;
+}
+
+// RPI rows starting at r into v; rows at or past r1 read as zero (empty resource).
+template <int NU, int RPI>
+__device__ __forceinline__ void load_rows(vec4 (&v)[RPI][NU], const DevSeg& sg, int r, int r1, int voff)
+{
+    const int rb = sg.nchunk * 16;
+#pragma unroll
+    for (int i = 0; i < RPI; ++i) {
+        const bool ok = r + i < r1;
+        const rsrc_t rs = make_rsrc(sg.data + (int64_t)(ok ? r + i : 0) * sg.stride_bytes, ok ? rb : 0);
+#pragma unroll
+        for (int u = 0; u < NU; ++u) v[i][u] = bload(rs, voff + u * 1024);
+    }
+}
+
+template <int DT, int NU, int RPI>
+__device__ __forceinline__ void rows_batch(const ScoreArgs& a, const DevSeg& sg, const vec4 (&v)[RPI][NU],
+                                           int r, int r1, int lane, uint32_t& nsp)
+{
+#pragma unroll
+    for (int i = 0; i < RPI; ++i) {
+        if (r + i >= r1) break;
+        const TokStat s = row_stats<DT, NU>(v[i], a.t.tau, bf16_thresholds(a.t.tau));
+        emit_token(a.tok, sg, r + i, lane, s, false, kModeScore);
+        nsp += s.act < (uint32_t)sg.A_s;
+    }
+}
+
+// Rows [r0, r1) of a non-temporal segment whose rows span NU units. For
+// rows up to 4 KiB, batches of RPI rows (about 4 KiB) are double-buffered:
+// the next batch is in flight while the current one is reduced. Wider rows
+// already keep NU KiB in flight per wavefront and are single-buffered, which
+// holds the data registers at 32 per lane.
 template <int DT, int NU>
 __device__ __forceinline__ void score_rows(const ScoreArgs& a, const DevSeg& sg, int r0, int r1,
                                            int lane, uint32_t& nsp)
 {
-    using L = Lane<DT>;
-    constexpr int EPC = L::EPC;
     constexpr int RPI = NU >= 4 ? 1 : 4 / NU;
-    const float tau = a.t.tau;
-    for (int r = r0; r < r1; r += RPI) {
-        uint4 v[RPI][NU];
-#pragma unroll
-        for (int i = 0; i < RPI; ++i) {
-            const uint8_t* row = sg.data + (int64_t)(r + i) * sg.stride_bytes;
-#pragma unroll
-            for (int u = 0; u < NU; ++u) {
-                const int c = u * kWave + lane;
-                v[i][u] = make_uint4(0u, 0u, 0u, 0u);
-                if (r + i < r1 && c < sg.nchunk) v[i][u] = ld16(row + (int64_t)c * 16);
-            }
+    const int voff = lane * 16;
+    if constexpr (NU > 4) {
+        for (int r = r0; r < r1; ++r) {
+            vec4 A[1][NU];
+            load_rows<NU, 1>(A, sg, r, r1, voff);
+            rows_batch<DT, NU, 1>(a, sg, A, r, r1, lane, nsp);
         }
-#pragma unroll
-        for (int i = 0; i < RPI; ++i) {
-            if (r + i >= r1) break;
-            TokStat s{0u, 0u, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int u = 0; u < NU; ++u) {
-                float x[EPC];
-                L::widen(v[i][u], x);
-#pragma unroll
-                for (int e = 0; e < EPC; ++e) {
-                    s.act += (uint32_t)__popcll(__ballot(active(x[e], tau)));
-                    s.l1 += fabsf(x[e]);
-                    s.l2 = fmaf(x[e], x[e], s.l2);
-                }
-            }
-            s.l1 = wave_sum(s.l1);
-            s.l2 = wave_sum(s.l2);
-            emit_token(a.tok, sg, r + i, lane, s, false, kModeScore);
-            nsp += s.act < (uint32_t)sg.A_s;
+    } else {
+        vec4 A[RPI][NU], B[RPI][NU];
+        load_rows<NU, RPI>(A, sg, r0, r1, voff);
+        int r = r0;
+        while (true) {
+            if (r + RPI < r1) load_rows<NU, RPI>(B, sg, r + RPI, r1, voff);
+            rows_batch<DT, NU, RPI>(a, sg, A, r, r1, lane, nsp);
+            r += RPI;
+            if (r >= r1) break;
+            if (r + RPI < r1) load_rows<NU, RPI>(A, sg, r + RPI, r1, voff);
+            rows_batch<DT, NU, RPI>(a, sg, B, r, r1, lane, nsp);
+            r += RPI;
+            if (r >= r1) break;
         }
     }
 }
@@ -166,32 +378,19 @@ template <int DT>
 __device__ void score_rows_generic(const ScoreArgs& a, const DevSeg& sg, int r0, int r1, int lane,
                                    uint32_t& nsp)
 {
-    using L = Lane<DT>;
-    constexpr int EPC = L::EPC;
     const float tau = a.t.tau;
+    const Thr th = bf16_thresholds(tau);
     const int nu = (sg.nchunk + kWave - 1) / kWave;
+    const int rb = sg.nchunk * 16;
     for (int r = r0; r < r1; ++r) {
-        const uint8_t* row = sg.data + (int64_t)r * sg.stride_bytes;
+        const rsrc_t rs = make_rsrc(sg.data + (int64_t)r * sg.stride_bytes, rb);
         TokStat s{0u, 0u, 0.0f, 0.0f, 0.0f};
         for (int u0 = 0; u0 < nu; u0 += 4) {
-            uint4 v[4];
+            vec4 v[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int c = (u0 + u) * kWave + lane;
-                v[u] = make_uint4(0u, 0u, 0u, 0u);
-                if (c < sg.nchunk) v[u] = ld16(row + (int64_t)c * 16);
-            }
+            for (int u = 0; u < 4; ++u) v[u] = bload(rs, ((u0 + u) * kWave + lane) * 16);
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                float x[EPC];
-                L::widen(v[u], x);
-#pragma unroll
-                for (int e = 0; e < EPC; ++e) {
-                    s.act += (uint32_t)__popcll(__ballot(active(x[e], tau)));
-                    s.l1 += fabsf(x[e]);
-                    s.l2 = fmaf(x[e], x[e], s.l2);
-                }
-            }
+            for (int u = 0; u < 4; ++u) chunk_stats<DT>(v[u], tau, th, s.act, s.l1, s.l2);
         }
         s.l1 = wave_sum(s.l1);
         s.l2 = wave_sum(s.l2);
@@ -212,18 +411,21 @@ __device__ __forceinline__ void score_chain(const ScoreArgs& a, const DevSeg& sg
     constexpr int EPC = L::EPC;
     constexpr int NE = NU * EPC;
     const float tau = a.t.tau;
+    const Thr th = bf16_thresholds(tau);
     const int64_t fstride = (int64_t)sg.P * sg.stride_bytes;
     const uint8_t* base = sg.data + (int64_t)p * sg.stride_bytes;
+    const int rb = sg.nchunk * 16;
+    const int voff = lane * 16;
+    auto load = [&](vec4 (&v)[NU], int t, bool ok) {
+        const rsrc_t rs = make_rsrc(base + (ok ? (int64_t)t * fstride : 0), ok ? rb : 0);
+#pragma unroll
+        for (int u = 0; u < NU; ++u) v[u] = bload(rs, voff + u * 1024);
+    };
     float prev[NE];
     uint64_t pmask[NE];
     {
-        uint4 v[NU];
-#pragma unroll
-        for (int u = 0; u < NU; ++u) {
-            const int c = u * kWave + lane;
-            v[u] = make_uint4(0u, 0u, 0u, 0u);
-            if (t0 > 0 && c < sg.nchunk) v[u] = ld16(base + (int64_t)(t0 - 1) * fstride + (int64_t)c * 16);
-        }
+        vec4 v[NU];
+        load(v, t0 - 1, t0 > 0);
 #pragma unroll
         for (int u = 0; u < NU; ++u) {
             L::widen(v[u], &prev[u * EPC]);
@@ -231,40 +433,15 @@ __device__ __forceinline__ void score_chain(const ScoreArgs& a, const DevSeg& sg
             for (int e = 0; e < EPC; ++e) pmask[u * EPC + e] = __ballot(active(prev[u * EPC + e], tau));
         }
     }
-    uint4 cur[NU];
-#pragma unroll
-    for (int u = 0; u < NU; ++u) {
-        const int c = u * kWave + lane;
-        cur[u] = make_uint4(0u, 0u, 0u, 0u);
-        if (c < sg.nchunk) cur[u] = ld16(base + (int64_t)t0 * fstride + (int64_t)c * 16);
-    }
+    vec4 cur[NU];
+    load(cur, t0, true);
     for (int t = t0; t < t1; ++t) {
-        uint4 nxt[NU];
-#pragma unroll
-        for (int u = 0; u < NU; ++u) {
-            const int c = u * kWave + lane;
-            nxt[u] = make_uint4(0u, 0u, 0u, 0u);
-            if (t + 1 < t1 && c < sg.nchunk) nxt[u] = ld16(base + (int64_t)(t + 1) * fstride + (int64_t)c * 16);
-        }
+        vec4 nxt[NU];
+        load(nxt, t + 1, t + 1 < t1);
         TokStat s{0u, 0u, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int u = 0; u < NU; ++u) {
-            float x[EPC];
-            L::widen(cur[u], x);
-#pragma unroll
-            for (int e = 0; e < EPC; ++e) {
-                const int k = u * EPC + e;
-                const uint64_t m = __ballot(active(x[e], tau));
-                s.act += (uint32_t)__popcll(m);
-                s.d += (uint32_t)__popcll(m ^ pmask[k]);
-                pmask[k] = m;
-                s.l1 += fabsf(x[e]);
-                s.l2 = fmaf(x[e], x[e], s.l2);
-                const float df = x[e] - prev[k];
-                s.res = fmaf(df, df, s.res);
-                prev[k] = x[e];
-            }
-        }
+        for (int u = 0; u < NU; ++u)
+            chunk_chain<DT>(cur[u], tau, th, &prev[u * EPC], &pmask[u * EPC], s.act, s.d, s.l1, s.l2, s.res);
         s.l1 = wave_sum(s.l1);
         s.l2 = wave_sum(s.l2);
         s.res = wave_sum(s.res);
@@ -288,19 +465,18 @@ __device__ void score_chain_generic(const ScoreArgs& a, const DevSeg& sg, int p,
     const int64_t fstride = (int64_t)sg.P * sg.stride_bytes;
     const uint8_t* base = sg.data + (int64_t)p * sg.stride_bytes;
     const int nu = (sg.nchunk + kWave - 1) / kWave;
+    const int rb = sg.nchunk * 16;
     for (int t = t0; t < t1; ++t) {
+        const rsrc_t rc = make_rsrc(base + (int64_t)t * fstride, rb);
+        const rsrc_t rp = make_rsrc(base + (t > 0 ? (int64_t)(t - 1) * fstride : 0), t > 0 ? rb : 0);
         TokStat s{0u, 0u, 0.0f, 0.0f, 0.0f};
         for (int u0 = 0; u0 < nu; u0 += 2) {
-            uint4 v[2], w[2];
+            vec4 v[2], w[2];
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
-                const int c = (u0 + u) * kWave + lane;
-                v[u] = make_uint4(0u, 0u, 0u, 0u);
-                w[u] = make_uint4(0u, 0u, 0u, 0u);
-                if (c < sg.nchunk) {
-                    v[u] = ld16(base + (int64_t)t * fstride + (int64_t)c * 16);
-                    if (t > 0) w[u] = ld16(base + (int64_t)(t - 1) * fstride + (int64_t)c * 16);
-                }
+                const int off = ((u0 + u) * kWave + lane) * 16;
+                v[u] = bload(rc, off);
+                w[u] = bload(rp, off);
             }
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
@@ -347,17 +523,28 @@ __device__ __forceinline__ void dispatch_rows(const ScoreArgs& a, const DevSeg& 
     }
 }
 
+// Register-resident chains are used while a lane holds at most 16 channels
+// (their activity ballots live in 32 scalar registers); wider rows take the
+// generic path.
 template <int DT>
 __device__ __forceinline__ void dispatch_chain(const ScoreArgs& a, const DevSeg& sg, int p, int t0, int t1,
                                                int lane, uint32_t& nsp, uint64_t& dsum)
 {
     const int nu = (sg.nchunk + kWave - 1) / kWave;
-    switch (nu) {
-    case 1: score_chain<DT, 1>(a, sg, p, t0, t1, lane, nsp, dsum); break;
-    case 2: score_chain<DT, 2>(a, sg, p, t0, t1, lane, nsp, dsum); break;
-    case 3: score_chain<DT, 3>(a, sg, p, t0, t1, lane, nsp, dsum); break;
-    case 4: score_chain<DT, 4>(a, sg, p, t0, t1, lane, nsp, dsum); break;
-    default: score_chain_generic<DT>(a, sg, p, t0, t1, lane, nsp, dsum); break;
+    if constexpr (DT == kBF16) {
+        switch (nu) {
+        case 1: score_chain<DT, 1>(a, sg, p, t0, t1, lane, nsp, dsum); break;
+        case 2: score_chain<DT, 2>(a, sg, p, t0, t1, lane, nsp, dsum); break;
+        default: score_chain_generic<DT>(a, sg, p, t0, t1, lane, nsp, dsum); break;
+        }
+    } else {
+        switch (nu) {
+        case 1: score_chain<DT, 1>(a, sg, p, t0, t1, lane, nsp, dsum); break;
+        case 2: score_chain<DT, 2>(a, sg, p, t0, t1, lane, nsp, dsum); break;
+        case 3: score_chain<DT, 3>(a, sg, p, t0, t1, lane, nsp, dsum); break;
+        case 4: score_chain<DT, 4>(a, sg, p, t0, t1, lane, nsp, dsum); break;
+        default: score_chain_generic<DT>(a, sg, p, t0, t1, lane, nsp, dsum); break;
+        }
     }
 }
 
@@ -403,23 +590,39 @@ __global__ __launch_bounds__(kScoreBlock) void k_score(ScoreArgs a)
 
 // ---------------------------------------------------------------- k_post
 
+constexpr int kPostWaves = kPostBlock / kWave;
+static_assert(kPostWaves == kNumMod, "the request role gives one wavefront to each modality");
+
+constexpr int kRadixBits = 11;
+constexpr int kRadixBins = 1 << kRadixBits;
+constexpr int kBinsPerThread = kRadixBins / kPostBlock;
+
+struct PostShared {
+    uint32_t hist[kRadixBins];
+    uint32_t scan[kPostWaves];
+    uint32_t wcnt[kPostWaves][2];
+    unsigned long long lo, hi, red;
+    uint64_t nsp[kNumMod], dsum[kNumMod], ntok[kNumMod], qbits[kNumMod];
+    uint32_t digit, below;
+};
+
 // Block-wide sum of a 64-bit integer (exact, so the order does not matter).
-__device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, unsigned long long* sh)
+__device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, PostShared& sh)
 {
+    v = wave_sum_u64(v);
     __syncthreads();
-    if (threadIdx.x == 0) *sh = 0ull;
+    if (threadIdx.x == 0) sh.red = 0ull;
     __syncthreads();
-    if (v) atomicAdd(sh, (unsigned long long)v);
+    if ((threadIdx.x & (kWave - 1)) == 0 && v) atomicAdd(&sh.red, (unsigned long long)v);
     __syncthreads();
-    return (uint64_t)*sh;
+    return (uint64_t)sh.red;
 }
 
 // Block-wide exclusive scan of 32-bit counts in thread order; *total gets the sum.
-__device__ __forceinline__ uint32_t block_exscan(uint32_t v, uint32_t* sh, uint32_t* total)
+__device__ __forceinline__ uint32_t block_exscan(uint32_t v, PostShared& sh, uint32_t* total)
 {
     const int lane = threadIdx.x & (kWave - 1);
     const int wid = threadIdx.x >> 6;
-    constexpr int nw = kPostBlock / kWave;
     uint32_t x = v;
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
@@ -427,12 +630,12 @@ __device__ __forceinline__ uint32_t block_exscan(uint32_t v, uint32_t* sh, uint3
         if (lane >= o) x += y;
     }
     __syncthreads();
-    if (lane == kWave - 1) sh[wid] = x;
+    if (lane == kWave - 1) sh.scan[wid] = x;
     __syncthreads();
     uint32_t before = 0, tot = 0;
 #pragma unroll
-    for (int i = 0; i < nw; ++i) {
-        const uint32_t t = sh[i];
+    for (int i = 0; i < kPostWaves; ++i) {
+        const uint32_t t = sh.scan[i];
         if (i < wid) before += t;
         tot += t;
     }
@@ -444,35 +647,40 @@ struct RMAgg {
     uint64_t ntok, nsparse, dsum, qbits;
 };
 
-// Sizes of (request r, modality m) from the segment table (every thread).
-__device__ __forceinline__ void rm_sizes(const Tables& t, int r, int m, uint64_t& ntok, uint64_t& qbits)
+// Eq. 4 and Eq. 5 integer aggregates of request r, all four modalities: each
+// wavefront sums the scoring partials of one modality. Every thread of the
+// block calls this and receives the same values.
+__device__ void rm_aggregate_all(const Tables& t, int r, PostShared& sh, RMAgg g[kNumMod])
 {
-    ntok = 0;
-    qbits = 0;
-    for (int j = t.rm_off[r * kNumMod + m]; j < t.rm_off[r * kNumMod + m + 1]; ++j) {
-        const DevSeg& sg = t.seg[t.rm_seg[j]];
-        ntok += (uint64_t)sg.n_tok;
-        if (sg.temporal) qbits += (uint64_t)(sg.T - 1) * (uint64_t)sg.P * (uint64_t)sg.C;
-    }
-}
-
-// Eq. 4 and Eq. 5 integer aggregates of (r, m): the work items' partials summed.
-__device__ RMAgg rm_aggregate(const Tables& t, int r, int m, unsigned long long* sh)
-{
-    RMAgg g;
-    rm_sizes(t, r, m, g.ntok, g.qbits);
+    const int m = threadIdx.x >> 6;
+    const int lane = threadIdx.x & (kWave - 1);
+    const RmEntry e = t.rm[r * kNumMod + m];
     uint64_t nsp = 0, ds = 0;
-    for (int j = t.rm_off[r * kNumMod + m]; j < t.rm_off[r * kNumMod + m + 1]; ++j) {
-        const int s = t.rm_seg[j];
-        for (int w = t.seg_wi[s] + threadIdx.x; w < t.seg_wi[s + 1]; w += blockDim.x) {
+    for (int j = e.rng_begin; j < e.rng_end; ++j) {
+        const WiRange wr = t.rm_rng[j];
+        for (int w = wr.begin + lane; w < wr.end; w += kWave) {
             const Partial pr = t.partial[w];
             nsp += pr.nsparse;
             ds += pr.dsum;
         }
     }
-    g.nsparse = block_sum_u64(nsp, sh);
-    g.dsum = block_sum_u64(ds, sh + 1);
-    return g;
+    nsp = wave_sum_u64(nsp);
+    ds = wave_sum_u64(ds);
+    __syncthreads();
+    if (lane == 0) {
+        sh.nsp[m] = nsp;
+        sh.dsum[m] = ds;
+        sh.ntok[m] = e.ntok;
+        sh.qbits[m] = e.qbits;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int mm = 0; mm < kNumMod; ++mm) {
+        g[mm].ntok = sh.ntok[mm];
+        g[mm].qbits = sh.qbits[mm];
+        g[mm].nsparse = sh.nsp[mm];
+        g[mm].dsum = sh.dsum[mm];
+    }
 }
 
 // Sec. 4.1.3: softmax of the logits over the modalities present.
@@ -480,11 +688,14 @@ __device__ void modal_softmax(const double al[kNumMod], const bool pres[kNumMod]
 {
 #pragma clang fp contract(off)
     double mx = -INFINITY;
+#pragma unroll
     for (int m = 0; m < kNumMod; ++m)
         if (pres[m] && al[m] > mx) mx = al[m];
     double den = 0.0;
+#pragma unroll
     for (int m = 0; m < kNumMod; ++m)
         if (pres[m]) den += exp(al[m] - mx);
+#pragma unroll
     for (int m = 0; m < kNumMod; ++m) beta[m] = pres[m] ? exp(al[m] - mx) / den : 0.0;
 }
 
@@ -514,42 +725,38 @@ __device__ MasTerms mas_terms(const Tables& t, const RMAgg& g, double beta, int 
     return o;
 }
 
-// MAS of (r, m) as the request role computes it (all threads call; same value).
-__device__ float request_mas(const Tables& t, int r, int m, unsigned long long* sh)
+// MAS of every modality of request r (terms[m] is zero where absent).
+__device__ void request_terms(const Tables& t, int r, const RMAgg g[kNumMod], MasTerms terms[kNumMod],
+                              bool pres[kNumMod])
 {
-    bool pres[kNumMod];
     double al[kNumMod], beta[kNumMod];
-    for (int mm = 0; mm < kNumMod; ++mm) {
-        uint64_t nt, qb;
-        rm_sizes(t, r, mm, nt, qb);
-        pres[mm] = nt > 0;
-        al[mm] = (double)t.alpha[r * kNumMod + mm];
-    }
-    modal_softmax(al, pres, beta);
-    const RMAgg g = rm_aggregate(t, r, m, sh);
-    if (!pres[m]) return 0.0f;
-    return (float)mas_terms(t, g, beta[m], m).mas;
-}
-
-__device__ void role_request(const PostArgs& a, int r, unsigned long long* sh)
-{
-    const Tables& t = a.t;
-    RMAgg g[kNumMod];
-    for (int m = 0; m < kNumMod; ++m) g[m] = rm_aggregate(t, r, m, sh);
-    if (threadIdx.x != 0) return;
-    bool pres[kNumMod];
-    double al[kNumMod], beta[kNumMod];
+#pragma unroll
     for (int m = 0; m < kNumMod; ++m) {
         pres[m] = g[m].ntok > 0;
         al[m] = (double)t.alpha[r * kNumMod + m];
     }
     modal_softmax(al, pres, beta);
+#pragma unroll
+    for (int m = 0; m < kNumMod; ++m) {
+        terms[m] = MasTerms{0.0, 0.0, 0.0, 0.0, false};
+        if (pres[m]) terms[m] = mas_terms(t, g[m], beta[m], m);
+    }
+}
+
+__device__ void role_request(const PostArgs& a, int r, PostShared& sh)
+{
+    const Tables& t = a.t;
+    RMAgg g[kNumMod];
+    rm_aggregate_all(t, r, sh, g);
+    if (threadIdx.x != 0) return;
+    MasTerms o[kNumMod];
+    bool pres[kNumMod];
+    request_terms(t, r, g, o, pres);
+#pragma unroll
     for (int m = 0; m < kNumMod; ++m) {
         const int x = r * kNumMod + m;
-        MasTerms o{0.0, 0.0, 0.0, 0.0, false};
-        if (pres[m]) o = mas_terms(t, g[m], beta[m], m);
         if (a.temporal_only) {
-            if (a.req.temporal) a.req.temporal[x] = (float)o.tterm;
+            if (a.req.temporal) a.req.temporal[x] = (float)o[m].tterm;
             continue;
         }
         if (a.req.agg) {
@@ -558,16 +765,16 @@ __device__ void role_request(const PostArgs& a, int r, unsigned long long* sh)
             a.req.agg[x * 4 + 2] = g[m].dsum;
             a.req.agg[x * 4 + 3] = g[m].qbits;
         }
-        if (a.req.rho) a.req.rho[x] = (float)o.rho;
-        if (a.req.temporal) a.req.temporal[x] = (float)o.tterm;
-        if (a.req.beta) a.req.beta[x] = (float)o.beta;
-        if (a.req.mas) a.req.mas[x] = (float)o.mas;
+        if (a.req.rho) a.req.rho[x] = (float)o[m].rho;
+        if (a.req.temporal) a.req.temporal[x] = (float)o[m].tterm;
+        if (a.req.beta) a.req.beta[x] = (float)o[m].beta;
+        if (a.req.mas) a.req.mas[x] = (float)o[m].mas;
         if (a.req.present) a.req.present[x] = pres[m] ? 1 : 0;
     }
 }
 
 // Eq. 5 for one frame of a temporal segment: D_t = sum of d over its tokens.
-__device__ void role_frame(const PostArgs& a, int f, unsigned long long* sh)
+__device__ void role_frame(const PostArgs& a, int f, PostShared& sh)
 {
     const Tables& t = a.t;
     int lo = 0, hi = t.n_tseg;
@@ -605,41 +812,50 @@ __device__ __forceinline__ uint64_t sel_key(const uint32_t* __restrict__ z, cons
     }
 }
 
-constexpr int kRadixBits = 11;
-constexpr int kRadixBins = 1 << kRadixBits;
-constexpr int kBinsPerThread = kRadixBins / kPostBlock;
-constexpr int kScanItems = 8;
-
-struct SelShared {
-    uint32_t hist[kRadixBins];
-    uint32_t scan[kPostBlock / kWave];
-    unsigned long long red[2];
-    unsigned long long lo, hi;
-    uint32_t digit, below;
-};
+// MAS-guided keep count (Eq. 11 floor): k = min(N, ceil((1 - MAS) * N)) in double.
+__device__ __forceinline__ int guided_keep_count(float mas, int N)
+{
+#pragma clang fp contract(off)
+    double kk = ceil((1.0 - (double)mas) * (double)N);
+    kk = kk > (double)N ? (double)N : kk;
+    kk = kk < 0.0 ? 0.0 : kk;
+    return (int)kk;
+}
 
 // Top-k of one segment: the k smallest (key, index) pairs, kept indices
 // ascending (Sec. 4.1.1 pruning, k from the Eq. 11 floor or a fixed ratio).
-__device__ void role_select(const PostArgs& a, int s, SelShared& sh)
+// Keys are staged in LDS when the segment fits (keys_cap entries), then an
+// MSD radix select finds the key of rank k-1 and each wavefront compacts a
+// contiguous index range with ballot/mbcnt.
+__device__ void role_select(const PostArgs& a, int s, PostShared& sh, uint64_t* keys, int keys_cap)
 {
     const Tables& t = a.t;
     const DevSeg sg = t.seg[s];
     const int N = sg.n_tok;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid >> 6;
     int k = sg.k;
     if (k < 0) {
-#pragma clang fp contract(off)
-        const float mas = a.mas_in ? a.mas_in[sg.request * kNumMod + sg.modality]
-                                   : request_mas(t, sg.request, sg.modality, sh.red);
-        double kk = ceil((1.0 - (double)mas) * (double)N);
-        kk = kk > (double)N ? (double)N : kk;
-        kk = kk < 0.0 ? 0.0 : kk;
-        k = (int)kk;
+        float mas;
+        if (a.mas_in) {
+            mas = a.mas_in[sg.request * kNumMod + sg.modality];
+        } else {
+            RMAgg g[kNumMod];
+            rm_aggregate_all(t, sg.request, sh, g);
+            MasTerms o[kNumMod];
+            bool pres[kNumMod];
+            request_terms(t, sg.request, g, o, pres);
+            mas = 0.0f;
+#pragma unroll
+            for (int m = 0; m < kNumMod; ++m)
+                if (m == sg.modality) mas = (float)o[m].mas;
+        }
+        k = guided_keep_count(mas, N);
     }
-    if (threadIdx.x == 0) a.sel.kept_count[s] = k;
+    if (tid == 0) a.sel.kept_count[s] = k;
     const int off = sg.tok_off;
     if (N == 0) return;
     if (k == 0 || k == N) {
-        for (int i = threadIdx.x; i < N; i += blockDim.x) {
+        for (int i = tid; i < N; i += kPostBlock) {
             if (a.sel.keep) a.sel.keep[off + i] = k == N ? 1 : 0;
             a.sel.kept_idx[off + i] = k == N ? i : -1;
         }
@@ -650,53 +866,60 @@ __device__ void role_select(const PostArgs& a, int s, SelShared& sh)
     const uint32_t C = (uint32_t)sg.C;
     const uint32_t* z = a.z + off;
     const uint32_t* d = a.d ? a.d + off : nullptr;
+    const bool in_lds = N <= keys_cap;
+    auto key_at = [&](int i) -> uint64_t { return in_lds ? keys[i] : sel_key(z, d, i, kind, Ls, Lt, C); };
 
-    // range of the keys
-    if (threadIdx.x == 0) {
+    // keys (staged in LDS) and their range
+    if (tid == 0) {
         sh.lo = ~0ull;
         sh.hi = 0ull;
     }
     __syncthreads();
     {
         uint64_t lo = ~0ull, hi = 0ull;
-        for (int i = threadIdx.x; i < N; i += blockDim.x) {
+        for (int i = tid; i < N; i += kPostBlock) {
             const uint64_t key = sel_key(z, d, i, kind, Ls, Lt, C);
+            if (in_lds) keys[i] = key;
             lo = key < lo ? key : lo;
             hi = key > hi ? key : hi;
         }
-        atomicMin(&sh.lo, (unsigned long long)lo);
-        atomicMax(&sh.hi, (unsigned long long)hi);
+        lo = wave_min_u64(lo);
+        hi = wave_max_u64(hi);
+        if (lane == 0) {
+            atomicMin(&sh.lo, (unsigned long long)lo);
+            atomicMax(&sh.hi, (unsigned long long)hi);
+        }
     }
     __syncthreads();
     const uint64_t lo = sh.lo, hi = sh.hi;
 
     // radix select of the key of rank k-1 among key - lo, most significant digit first
     uint64_t prefix = 0;
-    uint32_t below = 0;            // keys strictly below the current candidate range
+    uint32_t below = 0;            // keys below the current candidate range
     uint32_t rank = (uint32_t)k - 1;
     int bits = hi > lo ? 64 - __clzll((long long)(hi - lo)) : 0;
     while (bits > 0) {
         const int db = bits < kRadixBits ? bits : kRadixBits;
         const int shift = bits - db;
         const uint64_t mask = (1ull << db) - 1ull;
-        for (int b = threadIdx.x; b < kRadixBins; b += blockDim.x) sh.hist[b] = 0u;
+        for (int b = tid; b < kRadixBins; b += kPostBlock) sh.hist[b] = 0u;
         __syncthreads();
-        for (int i = threadIdx.x; i < N; i += blockDim.x) {
-            const uint64_t x = sel_key(z, d, i, kind, Ls, Lt, C) - lo;
-            if ((x >> bits) == prefix) atomicAdd(&sh.hist[(x >> shift) & mask], 1u);
+        for (int i = tid; i < N; i += kPostBlock) {
+            const uint64_t x = key_at(i) - lo;
+            if ((bits >= 64 ? 0ull : (x >> bits)) == prefix) atomicAdd(&sh.hist[(x >> shift) & mask], 1u);
         }
         __syncthreads();
         uint32_t local = 0;
 #pragma unroll
-        for (int j = 0; j < kBinsPerThread; ++j) local += sh.hist[threadIdx.x * kBinsPerThread + j];
+        for (int j = 0; j < kBinsPerThread; ++j) local += sh.hist[tid * kBinsPerThread + j];
         uint32_t tot;
-        const uint32_t ex = block_exscan(local, sh.scan, &tot);
+        const uint32_t ex = block_exscan(local, sh, &tot);
         if (ex <= rank && rank < ex + local) {
             uint32_t cum = ex;
             for (int j = 0; j < kBinsPerThread; ++j) {
-                const uint32_t h = sh.hist[threadIdx.x * kBinsPerThread + j];
+                const uint32_t h = sh.hist[tid * kBinsPerThread + j];
                 if (rank < cum + h) {
-                    sh.digit = (uint32_t)(threadIdx.x * kBinsPerThread + j);
+                    sh.digit = (uint32_t)(tid * kBinsPerThread + j);
                     sh.below = cum;
                     break;
                 }
@@ -711,67 +934,121 @@ __device__ void role_select(const PostArgs& a, int s, SelShared& sh)
         bits = shift;
         __syncthreads();
     }
-    const uint64_t vstar = lo + prefix;      // key of rank k-1
+    const uint64_t vstar = lo + prefix;        // key of rank k-1
     const uint32_t ties = (uint32_t)k - below; // keys equal to vstar that are kept, lowest index first
 
-    // keep flags and ascending kept indices, tile by tile in index order
-    uint32_t eq_carry = 0, kept_carry = 0;
-    for (int base = 0; base < N; base += kPostBlock * kScanItems) {
-        const int i0 = base + threadIdx.x * kScanItems;
-        uint64_t kv[kScanItems];
-        uint32_t nlt = 0, neq = 0;
-#pragma unroll
-        for (int j = 0; j < kScanItems; ++j) {
-            kv[j] = 0;
-            if (i0 + j < N) {
-                kv[j] = sel_key(z, d, i0 + j, kind, Ls, Lt, C);
-                nlt += kv[j] < vstar;
-                neq += kv[j] == vstar;
-            }
-        }
-        uint32_t eq_tot;
-        const uint32_t eq_before = block_exscan(neq, sh.scan, &eq_tot) + eq_carry;
-        const uint32_t take = eq_before >= ties ? 0u : min(neq, ties - eq_before);
-        uint32_t kept_tot;
-        uint32_t pos = block_exscan(nlt + take, sh.scan, &kept_tot) + kept_carry;
-        uint32_t er = eq_before;
-#pragma unroll
-        for (int j = 0; j < kScanItems; ++j) {
-            const int i = i0 + j;
-            if (i < N) {
-                bool kp = kv[j] < vstar;
-                if (kv[j] == vstar) {
-                    kp = er < ties;
-                    ++er;
-                }
-                if (a.sel.keep) a.sel.keep[off + i] = kp ? 1 : 0;
-                if (kp) a.sel.kept_idx[off + (int)pos++] = i;
-            }
-        }
-        eq_carry += eq_tot;
-        kept_carry += kept_tot;
+    // each wavefront compacts one contiguous range of indices
+    const int per = (((N + kPostWaves - 1) / kPostWaves) + kWave - 1) / kWave * kWave;
+    const int b0 = min(N, wid * per), b1 = min(N, b0 + per);
+    uint32_t nlt = 0, neq = 0;
+    for (int base = b0; base < b1; base += kWave) {
+        const int i = base + lane;
+        const bool v = i < b1;
+        const uint64_t key = v ? key_at(i) : 0ull;
+        nlt += (uint32_t)__popcll(__ballot(v && key < vstar));
+        neq += (uint32_t)__popcll(__ballot(v && key == vstar));
     }
-    for (int i = k + threadIdx.x; i < N; i += blockDim.x) a.sel.kept_idx[off + i] = -1;
+    if (lane == 0) {
+        sh.wcnt[wid][0] = nlt;
+        sh.wcnt[wid][1] = neq;
+    }
+    __syncthreads();
+    uint32_t lt_before = 0, eq_before = 0;
+    for (int q = 0; q < wid; ++q) {
+        lt_before += sh.wcnt[q][0];
+        eq_before += sh.wcnt[q][1];
+    }
+    uint32_t eq_run = eq_before;
+    uint32_t kept_run = lt_before + min(eq_before, ties);
+    for (int base = b0; base < b1; base += kWave) {
+        const int i = base + lane;
+        const bool v = i < b1;
+        const uint64_t key = v ? key_at(i) : 0ull;
+        const bool isl = v && key < vstar;
+        const bool ise = v && key == vstar;
+        const uint64_t me = __ballot(ise);
+        const bool kp = isl || (ise && eq_run + lanes_below(me) < ties);
+        const uint64_t mk = __ballot(kp);
+        if (v && a.sel.keep) a.sel.keep[off + i] = kp ? 1 : 0;
+        if (kp) a.sel.kept_idx[off + (int)(kept_run + lanes_below(mk))] = i;
+        eq_run += (uint32_t)__popcll(me);
+        kept_run += (uint32_t)__popcll(mk);
+    }
+    for (int i = k + tid; i < N; i += kPostBlock) a.sel.kept_idx[off + i] = -1;
 }
 
 __global__ __launch_bounds__(kPostBlock) void k_post(PostArgs a)
 {
-    __shared__ SelShared sh;
+    __shared__ PostShared sh;
+    extern __shared__ uint64_t keys[];
     int b = blockIdx.x;
     if (b < a.n_req_blocks) {
-        role_request(a, b, sh.red);
+        role_request(a, b, sh);
         return;
     }
     b -= a.n_req_blocks;
     if (b < a.n_frame_blocks) {
-        role_frame(a, b, sh.red);
+        role_frame(a, b, sh);
         return;
     }
     b -= a.n_frame_blocks;
-    if (b < a.n_sel_blocks) role_select(a, b, sh);
+    if (b < a.n_sel_blocks) role_select(a, b, sh, keys, a.keys_cap);
 }
 
 // ---------------------------------------------------------------- k_gather
+
+// Kept rows [j0, j1) of a segment whose rows span NU units, in batches of
+// about 8 KiB per wavefront; out-of-range lanes are dropped by the store's
+// buffer resource.
+#ifndef MSAO_GATHER_UNITS
+#define MSAO_GATHER_UNITS 8
+#endif
+template <int NU>
+__device__ __forceinline__ void gather_rows(const GatherArgs& a, const DevSeg& sg, int j0, int j1, int lane)
+{
+    constexpr int RB0 = NU >= MSAO_GATHER_UNITS ? 1 : MSAO_GATHER_UNITS / NU;
+    constexpr int RB = RB0 < kGatherRows ? RB0 : kGatherRows;
+    const int rb = sg.nchunk * 16;
+    const int voff = lane * 16;
+    for (int j = j0; j < j1; j += RB) {
+        vec4 v[RB][NU];
+        int src[RB];
+#pragma unroll
+        for (int i = 0; i < RB; ++i) {
+            src[i] = j + i < j1 ? uniform(a.kept_idx[sg.tok_off + j + i]) : -1;
+            const bool ok = src[i] >= 0 && src[i] < sg.n_tok;
+            const rsrc_t rs = make_rsrc(sg.data + (ok ? (int64_t)src[i] * sg.stride_bytes : 0), ok ? rb : 0);
+#pragma unroll
+            for (int u = 0; u < NU; ++u) v[i][u] = bload_gather(rs, voff + u * 1024);
+        }
+#pragma unroll
+        for (int i = 0; i < RB; ++i) {
+            if (src[i] < 0 || src[i] >= sg.n_tok) continue;
+            const rsrc_t rd = make_rsrc(a.out + sg.out_off + (int64_t)(j + i) * rb, rb);
+#pragma unroll
+            for (int u = 0; u < NU; ++u) bstore(v[i][u], rd, voff + u * 1024);
+        }
+    }
+}
+
+__device__ void gather_rows_generic(const GatherArgs& a, const DevSeg& sg, int j0, int j1, int lane)
+{
+    const int rb = sg.nchunk * 16;
+    const int nu = (sg.nchunk + kWave - 1) / kWave;
+    for (int j = j0; j < j1; ++j) {
+        const int src = uniform(a.kept_idx[sg.tok_off + j]);
+        if (src < 0 || src >= sg.n_tok) continue;
+        const rsrc_t rs = make_rsrc(sg.data + (int64_t)src * sg.stride_bytes, rb);
+        const rsrc_t rd = make_rsrc(a.out + sg.out_off + (int64_t)j * rb, rb);
+        for (int u0 = 0; u0 < nu; u0 += 8) {
+            vec4 v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = bload_gather(rs, ((u0 + u) * kWave + lane) * 16);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) bstore(v[u], rd, ((u0 + u) * kWave + lane) * 16);
+        }
+    }
+}
 
 __global__ __launch_bounds__(kGatherBlock) void k_gather(GatherArgs a)
 {
@@ -784,25 +1061,17 @@ __global__ __launch_bounds__(kGatherBlock) void k_gather(GatherArgs a)
     cnt = min(cnt, min(sg.cap, sg.n_tok));
     const int j0 = (w - sg.g_begin) * kGatherRows;
     const int j1 = min(cnt, j0 + kGatherRows);
-    const int64_t row_bytes = (int64_t)sg.nchunk * 16;
-    for (int j = j0; j < j1; ++j) {
-        const int src = uniform(a.kept_idx[sg.tok_off + j]);
-        if (src < 0 || src >= sg.n_tok) continue;
-        const uint8_t* in = sg.data + (int64_t)src * sg.stride_bytes;
-        uint8_t* o = a.out + sg.out_off + (int64_t)j * row_bytes;
-        for (int c0 = 0; c0 < sg.nchunk; c0 += 4 * kWave) {
-            uint4 v[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int c = c0 + u * kWave + lane;
-                if (c < sg.nchunk) v[u] = ld16(in + (int64_t)c * 16);
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int c = c0 + u * kWave + lane;
-                if (c < sg.nchunk) *reinterpret_cast<uint4*>(o + (int64_t)c * 16) = v[u];
-            }
-        }
+    if (j0 >= j1) return;
+    switch ((sg.nchunk + kWave - 1) / kWave) {
+    case 1: gather_rows<1>(a, sg, j0, j1, lane); break;
+    case 2: gather_rows<2>(a, sg, j0, j1, lane); break;
+    case 3: gather_rows<3>(a, sg, j0, j1, lane); break;
+    case 4: gather_rows<4>(a, sg, j0, j1, lane); break;
+    case 5: gather_rows<5>(a, sg, j0, j1, lane); break;
+    case 6: gather_rows<6>(a, sg, j0, j1, lane); break;
+    case 7: gather_rows<7>(a, sg, j0, j1, lane); break;
+    case 8: gather_rows<8>(a, sg, j0, j1, lane); break;
+    default: gather_rows_generic(a, sg, j0, j1, lane); break;
     }
 }
 
@@ -821,7 +1090,12 @@ int launch_post(const PostArgs& a, void* stream)
 {
     const int blocks = a.n_req_blocks + a.n_frame_blocks + a.n_sel_blocks;
     if (blocks <= 0) return 0;
-    hipLaunchKernelGGL(k_post, dim3((unsigned)blocks), dim3(kPostBlock), 0, (hipStream_t)stream, a);
+    const size_t lds = (size_t)a.keys_cap * sizeof(uint64_t);
+    if (lds > 65536) {
+        const hipError_t e = hipFuncSetAttribute((const void*)k_post, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return (int)e;
+    }
+    hipLaunchKernelGGL(k_post, dim3((unsigned)blocks), dim3(kPostBlock), lds, (hipStream_t)stream, a);
     return (int)hipGetLastError();
 }
 

@@ -374,3 +374,35 @@ def test_launch_shapes_same_results(row_bytes, chain, dev, monkeypatch):
     ctx = B.Context(0)
     run_and_compare(segs, R, default_params(), dev, ctx=ctx)
     ctx.close()
+
+
+def test_plan_runs_match_oracle(dev):
+    """msao_plan_create once, msao_plan_run several times (data rewritten in
+    place between runs): every run matches the oracle on that run's data."""
+    segs = make_workload(4, n_requests=2).segments + ADV["video"][:3] + ADV["guided"][:2]
+    R = 3
+    p = default_params()
+    log("[parity] plan API, three runs with rewritten inputs")
+    dsegs = to_device(segs, dev)
+    out = msao.Outputs(dsegs, R)
+    plan = msao.Plan(dsegs, R, out, p)
+    rng = np.random.default_rng(77)
+    for run in range(3):
+        if run:
+            # new data in the same buffers: permute each segment's rows
+            for s, ds in zip(segs, dsegs):
+                perm = rng.permutation(s.n_tokens)
+                s.data = np.ascontiguousarray(s.data[perm])
+                src = torch.from_numpy(s.data.view(np.int16 if s.dtype == "bf16" else np.float32)).to(dev)
+                ds.data.copy_(src.view(torch.bfloat16) if s.dtype == "bf16" else src)
+        plan()
+        torch.cuda.synchronize()
+        got = out.results(R, len(segs))
+        ref = oracle.run(segs, R, p)
+        compare_scores(segs, R, got, ref)
+        compare_frames(got, ref)
+        compare_requests(got, ref)
+        compare_selection(segs, R, got, ref, p, gpu_mas=host(got["mas"]))
+        kc = host(got["kept_count"])
+        compare_compaction(dsegs, segs, out, oracle.compact_rows(segs, kc, host(got["kept_idx"])), kc)
+    plan.close()
