@@ -35,6 +35,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU time budget of the oracle baseline")
     ap.add_argument("--no-compact", action="store_true", help="time score+select only (no compaction)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (calibrates HBM byte counters)")
+    ap.add_argument("--streams", type=int, default=2,
+                    help="batches in flight: consecutive steps alternate over this many HIP streams")
     return ap.parse_args()
 
 
@@ -78,6 +82,21 @@ def algorithmic_bytes(w, kept_rows_bytes, kept_total):
     return score, select, kept_rows_bytes
 
 
+def committed_traffic(config):
+    """HBM bytes per k_score launch from the committed rocprofv3 counter summary,
+    or None when there is none for this workload or the kernel sources changed
+    since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "k_score_trimodal_traffic.json")
+    if config != 4 or not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    h = hashlib.sha256()
+    for f in ("msao_kernels.hip", "msao_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2604_02945_amd", "csrc", f), "rb").read())
+    return rec["traffic_bytes_per_launch"] if rec.get("kernel_source_sha256") == h.hexdigest() else None
+
+
 def cpu_baseline(w, budget_s):
     import oracle
 
@@ -105,6 +124,16 @@ def main():
     import numpy as np
     import torch
 
+    if args.copy_calibration:
+        nbytes = args.copy_calibration << 20
+        src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": nbytes, "copies": args.steps}), flush=True)
+        return
+
     import paper_2604_02945_amd as msao
     from workloads import CONFIG_NAMES, make_workload
 
@@ -115,47 +144,75 @@ def main():
     R, n = w.n_requests, len(w.segments)
     has_video = any(s.modality == 2 and s.n_frames >= 2 for s in w.segments)
     fields = ("z", "l1", "l2", "info", "d", "res") if has_video else ("z", "l1", "l2", "info")
-    ctx = msao.Context(0)
-    stream = torch.cuda.current_stream()
-    # one plan per input replica (tables uploaded once); every replica writes the same outputs
-    out = msao.Outputs(reps[0], R, token_fields=fields, compact=not args.no_compact)
-    outs = [out] + [msao.Outputs(reps[0], R, token_fields=fields, compact=False) for _ in reps[1:]]
-    for o in outs[1:]:  # share the output buffers, keep a workspace per plan
-        o.tok, o.frm, o.req, o.sel = out.tok, out.frm, out.req, out.sel
-        o.out, o.out_off, o.out_bytes = out.out, out.out_off, getattr(out, "out_bytes", 0)
+    compact = not args.no_compact
+    n_str = max(1, args.streams)
+    n_rep = -(-n_rep // n_str) * n_str  # a whole number of replicas per stream
+    while len(reps) < n_rep:
+        extra, _ = pack_replicas(w, 1, dev)
+        reps += extra
+    main = torch.cuda.current_stream()
+    streams = [main] + [torch.cuda.Stream() for _ in range(n_str - 1)]
+    ctxs = [msao.Context(0) for _ in range(n_str)]  # one context per stream
+    # every stream writes its own outputs; every plan (one per replica) has its own workspace
+    base_out = [msao.Outputs(reps[0], R, token_fields=fields, compact=compact) for _ in range(n_str)]
+    plans = []
+    for r, segs in enumerate(reps):
+        k = r % n_str
+        o = msao.Outputs(reps[0], R, token_fields=fields, compact=False)
+        b = base_out[k]
+        o.tok, o.frm, o.req, o.sel = b.tok, b.frm, b.req, b.sel
+        o.out, o.out_off, o.out_bytes = b.out, b.out_off, getattr(b, "out_bytes", 0)
         o._structs()
-    calls = [msao.Plan(segs, R, o, w.params, ctx=ctx, compact=not args.no_compact, stream=stream)
-             for segs, o in zip(reps, outs)]
+        plans.append((k, msao.Plan(segs, R, o, w.params, ctx=ctxs[k], compact=compact, stream=main)))
     torch.cuda.synchronize()
 
-    for i in range(args.warmup):
-        calls[i % n_rep](stream)
+    def run_steps(count, nstreams):
+        """Enqueue `count` steps; step i runs plan i % n_rep on its stream."""
+        start = torch.cuda.Event()
+        start.record(main)
+        for st in streams[1:nstreams]:
+            st.wait_event(start)
+        used = set()
+        for i in range(count):
+            k, plan = plans[i % n_rep] if nstreams > 1 else (0, plans[(i * n_str) % n_rep][1])
+            plan(streams[k])
+            used.add(k)
+        for k in used:
+            if k:
+                ev = torch.cuda.Event()
+                ev.record(streams[k])
+                main.wait_event(ev)
+
+    def timed(count, nstreams):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        e0.record(main)
+        run_steps(count, nstreams)
+        e1.record(main)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / count, time.perf_counter() - t
+
+    run_steps(args.warmup, n_str)
     torch.cuda.synchronize()
+    out = base_out[0]
     kept_count = out.sel["kept_count"][:n].cpu().numpy()
     kept_total = int(kept_count.sum())
     kept_rows_bytes = int(sum(int(k) * s.hidden * (4 if s.dtype == "f32" else 2)
-                              for k, s in zip(kept_count, w.segments)))
-    if args.no_compact:
-        kept_rows_bytes = 0
+                              for k, s in zip(kept_count, w.segments))) if compact else 0
 
-    # timed region: K whole steps, replicas rotated
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    e0.record(stream)
-    for i in range(args.steps):
-        calls[i % n_rep](stream)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_wall
-    ms_step = e0.elapsed_time(e1) / args.steps
+    # timed region: K whole steps over rotated replicas, n_str batches in flight
+    ms_step, wall = timed(args.steps, n_str)
+    # the same steps one after another on one stream: per-batch latency
+    ms_step_serial, _ = timed(args.steps, 1)
 
-    # per-kernel durations: HIP events recorded by the library around each launch on this stream
-    ctx.set_profiling(True)
+    # per-kernel durations: HIP events recorded by the library around each launch,
+    # on the stream the kernel is launched on (one stream, so kernels do not overlap)
+    ctxs[0].set_profiling(True)
     for i in range(args.steps):
-        calls[i % n_rep](stream)
-    k_ms = np.array(ctx.kernel_times())
-    ctx.set_profiling(False)
+        plans[(i * n_str) % n_rep][1](main)
+    k_ms = np.array(ctxs[0].kernel_times())
+    ctxs[0].set_profiling(False)
 
     b_score, b_select, b_compact = algorithmic_bytes(w, kept_rows_bytes, kept_total)
     b_step = b_score + b_select + b_compact
@@ -177,19 +234,23 @@ def main():
             "workload": f"{CONFIG_NAMES[args.config]} (config {args.config})",
             "requests": R, "segments": n, "tokens": w.n_tokens, "input_dtype": sorted({s.dtype for s in w.segments}),
             "input_bytes": w.input_bytes, "kept_tokens": kept_total, "replicas_rotated": n_rep,
-            "compaction": not args.no_compact,
+            "compaction": compact, "batches_in_flight": n_str,
         },
+        "ms_per_step_one_stream": ms_step_serial,
         "hbm_gbps_step": b_step / (ms_step * 1e-3) / 1e9,
         "hbm_frac_step": b_step / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS,
         "algorithmic_bytes": {"score": b_score, "select": b_select, "compact_write": b_compact},
         "kernel_ms": {"score": k_ms[0], "post": k_ms[1], "gather": k_ms[2]},
         "roofline": {"bound": "hbm", "kernel": "k_score", "achieved": score_gbs, "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": score_gbs / PEAK_HBM_GBS, "traffic": None},
+                     "unit": "GB/s", "frac": score_gbs / PEAK_HBM_GBS, "traffic": committed_traffic(args.config)},
         "wall_s_timed": wall,
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
-    ctx.close()
+    for _, plan in plans:
+        plan.close()
+    for c in ctxs:
+        c.close()
     print(json.dumps(line), flush=True)
 
 

@@ -32,7 +32,7 @@ struct msao_ctx {
     std::vector<hipEvent_t> pool;                       // free events
     std::vector<std::pair<hipEvent_t, hipEvent_t>> rec[MSAO_NUM_KERNELS];
     // tuning
-    int row_item_bytes = 16384;
+    int row_item_bytes = 8192;
     int chain_frames = 0;       // frames per temporal work item; 0 = automatic
 };
 
@@ -120,7 +120,8 @@ msao_status validate_impl(const msao_segment* segs, int n, int R, const msao_par
 // Per-call tables, built on the host and uploaded into the workspace.
 struct Plan {
     std::vector<DevSeg> seg;
-    std::vector<int32_t> seg_wi, seg_gi, tseg;
+    std::vector<int32_t> seg_wi, seg_gi, tseg;   // seg_wi, seg_gi: per-segment prefixes (host only)
+    std::vector<int32_t> wi_seg, gi_seg;         // segment of every work item
     std::vector<RmEntry> rm;
     std::vector<WiRange> rm_rng;
     std::vector<float> alpha;
@@ -132,7 +133,7 @@ struct Plan {
     size_t table_bytes = 0, off_partial = 0, total_bytes = 0;
 };
 
-size_t table_layout(Plan& pl, int n, int R)
+size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi)
 {
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -141,8 +142,8 @@ size_t table_layout(Plan& pl, int n, int R)
         return at;
     };
     pl.off_seg = take(sizeof(DevSeg) * (size_t)std::max(n, 1));
-    pl.off_wi = take(sizeof(int32_t) * (size_t)(n + 1));
-    pl.off_gi = take(sizeof(int32_t) * (size_t)(n + 1));
+    pl.off_wi = take(sizeof(int32_t) * (size_t)std::max<int64_t>(n_wi, 1));
+    pl.off_gi = take(sizeof(int32_t) * (size_t)std::max<int64_t>(n_gwi, 1));
     pl.off_rmoff = take(sizeof(RmEntry) * (size_t)std::max(R * kNumMod, 1));
     pl.off_rmseg = take(sizeof(WiRange) * (size_t)std::max(n, 1));
     pl.off_tseg = take(sizeof(int32_t) * (size_t)std::max(n, 1));
@@ -151,11 +152,12 @@ size_t table_layout(Plan& pl, int n, int R)
     return o;
 }
 
-// Workspace bound that does not depend on tuning: one Partial per token at most.
+// Workspace bound that does not depend on tuning: work items and gather items
+// never outnumber tokens, so one Partial and two table entries per token.
 size_t workspace_bytes_for(int n, int R, int64_t ntok)
 {
     Plan pl;
-    const size_t tb = table_layout(pl, n, R);
+    const size_t tb = table_layout(pl, n, R, ntok + n, ntok + n);
     return align_up(tb, kWsAlign) + sizeof(Partial) * (size_t)std::max<int64_t>(ntok + n, 1);
 }
 
@@ -212,7 +214,7 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
             pl.tseg.push_back(i);
             pl.any_temporal = true;
         } else if (N > 0) {
-            const int rb = (int)std::max<int64_t>(1, (ctx ? ctx->row_item_bytes : 16384) / ((int64_t)s.hidden * es));
+            const int rb = (int)std::max<int64_t>(1, (ctx ? ctx->row_item_bytes : 8192) / ((int64_t)s.hidden * es));
             d.per_item = rb;
             items = (int)((N + rb - 1) / rb);
         } else {
@@ -251,10 +253,16 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         if (d.temporal) e.qbits += (uint64_t)(d.T - 1) * (uint64_t)d.P * (uint64_t)d.C;
         pl.rm_rng[(size_t)count[(size_t)(s.request * kNumMod + s.modality)]++] = WiRange{pl.seg_wi[(size_t)i], pl.seg_wi[(size_t)i + 1]};
     }
+    pl.wi_seg.resize((size_t)pl.n_wi);
+    pl.gi_seg.resize((size_t)pl.n_gwi);
+    for (int i = 0; i < n; ++i) {
+        std::fill(pl.wi_seg.begin() + pl.seg_wi[(size_t)i], pl.wi_seg.begin() + pl.seg_wi[(size_t)i + 1], i);
+        std::fill(pl.gi_seg.begin() + pl.seg_gi[(size_t)i], pl.gi_seg.begin() + pl.seg_gi[(size_t)i + 1], i);
+    }
     pl.alpha.assign((size_t)std::max(R * kNumMod, 1), 0.0f);
     if (alpha)
         for (int x = 0; x < R * kNumMod; ++x) pl.alpha[(size_t)x] = alpha[x];
-    table_layout(pl, n, R);
+    table_layout(pl, n, R, pl.n_wi, pl.n_gwi);
     pl.off_partial = align_up(pl.table_bytes, kWsAlign);
     pl.total_bytes = pl.off_partial + sizeof(Partial) * (size_t)std::max(pl.n_wi, 1);
 }
@@ -302,8 +310,8 @@ msao_status upload(msao_ctx* ctx, const Plan& pl, void* ws, hipStream_t stream)
         if (bytes) std::memcpy(h + off, src, bytes);
     };
     put(pl.off_seg, pl.seg.data(), sizeof(DevSeg) * pl.seg.size());
-    put(pl.off_wi, pl.seg_wi.data(), sizeof(int32_t) * pl.seg_wi.size());
-    put(pl.off_gi, pl.seg_gi.data(), sizeof(int32_t) * pl.seg_gi.size());
+    put(pl.off_wi, pl.wi_seg.data(), sizeof(int32_t) * pl.wi_seg.size());
+    put(pl.off_gi, pl.gi_seg.data(), sizeof(int32_t) * pl.gi_seg.size());
     put(pl.off_rmoff, pl.rm.data(), sizeof(RmEntry) * pl.rm.size());
     put(pl.off_rmseg, pl.rm_rng.data(), sizeof(WiRange) * pl.rm_rng.size());
     put(pl.off_tseg, pl.tseg.data(), sizeof(int32_t) * pl.tseg.size());
@@ -320,8 +328,8 @@ Tables device_tables(const Plan& pl, void* ws, int n, int R, const msao_params* 
     uint8_t* b = (uint8_t*)ws;
     Tables t;
     t.seg = (const DevSeg*)(b + pl.off_seg);
-    t.seg_wi = (const int32_t*)(b + pl.off_wi);
-    t.seg_gi = (const int32_t*)(b + pl.off_gi);
+    t.wi_seg = (const int32_t*)(b + pl.off_wi);
+    t.gi_seg = (const int32_t*)(b + pl.off_gi);
     t.rm = (const RmEntry*)(b + pl.off_rmoff);
     t.rm_rng = (const WiRange*)(b + pl.off_rmseg);
     t.tseg = (const int32_t*)(b + pl.off_tseg);

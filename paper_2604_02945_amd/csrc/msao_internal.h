@@ -60,8 +60,8 @@ struct WiRange {
 // Device pointers into the workspace, plus scalars, passed by value.
 struct Tables {
     const DevSeg* seg;
-    const int32_t* seg_wi;   // [n+1] prefix of scoring work items
-    const int32_t* seg_gi;   // [n+1] prefix of gather work items
+    const int32_t* wi_seg;   // [n_wi] segment of each scoring work item
+    const int32_t* gi_seg;   // [n_gwi] segment of each gather work item
     const RmEntry* rm;       // [R*4]
     const WiRange* rm_rng;   // [n] work-item ranges grouped by (request, modality)
     const int32_t* tseg;     // [n_tseg] temporal segment ids in table order
@@ -95,9 +95,9 @@ struct PostArgs {
     const uint32_t* z;    // selection inputs
     const uint32_t* d;
     const float* mas_in;  // MAS from the caller (selection only); NULL: recompute
-    int32_t n_req_blocks; // blocks [0, n_req_blocks): one per request
-    int32_t n_frame_blocks;
-    int32_t n_sel_blocks; // one per segment
+    int32_t n_sel_blocks; // blocks [0, n_sel_blocks): one per segment
+    int32_t n_req_blocks; // then one per request
+    int32_t n_frame_blocks;// then one per temporal frame
     int32_t temporal_only;// request role writes only the temporal term
     int32_t keys_cap;     // selection keys staged in LDS per block (larger segments re-read z, d)
 };

@@ -261,17 +261,6 @@ __device__ __forceinline__ void chunk_chain(const vec4& v, float tau, const Thr&
     }
 }
 
-// Largest s in [0, n) with prefix[s] <= w (prefix[n] is the total, > w).
-__device__ __forceinline__ int find_seg(const int32_t* __restrict__ prefix, int n, int w)
-{
-    int lo = 0, hi = n;
-    while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (prefix[mid] <= w) lo = mid; else hi = mid;
-    }
-    return lo;
-}
-
 // ---------------------------------------------------------------- k_score
 
 struct TokStat {
@@ -339,6 +328,10 @@ __device__ __forceinline__ void rows_batch(const ScoreArgs& a, const DevSeg& sg,
     }
 }
 
+#ifndef MSAO_ROW_BATCH_UNITS
+#define MSAO_ROW_BATCH_UNITS 8  // 1-KiB units per row batch (double-buffered)
+#endif
+
 // Rows [r0, r1) of a non-temporal segment whose rows span NU units. For
 // rows up to 4 KiB, batches of RPI rows (about 4 KiB) are double-buffered:
 // the next batch is in flight while the current one is reduced. Wider rows
@@ -348,7 +341,7 @@ template <int DT, int NU>
 __device__ __forceinline__ void score_rows(const ScoreArgs& a, const DevSeg& sg, int r0, int r1,
                                            int lane, uint32_t& nsp)
 {
-    constexpr int RPI = NU >= 4 ? 1 : 4 / NU;
+    constexpr int RPI = NU >= MSAO_ROW_BATCH_UNITS ? 1 : MSAO_ROW_BATCH_UNITS / NU;
     const int voff = lane * 16;
     if constexpr (NU > 4) {
         for (int r = r0; r < r1; ++r) {
@@ -553,7 +546,7 @@ __global__ __launch_bounds__(kScoreBlock) void k_score(ScoreArgs a)
     const int lane = threadIdx.x & (kWave - 1);
     const int w = uniform(blockIdx.x * (kScoreBlock / kWave) + (threadIdx.x >> 6));
     if (w >= a.t.n_wi) return;
-    const int s = find_seg(a.t.seg_wi, a.t.n, w);
+    const int s = uniform(a.t.wi_seg[w]);
     const DevSeg sg = a.t.seg[s];
     const int q = w - sg.wi_begin;
     uint32_t nsp = 0;
@@ -981,41 +974,46 @@ __global__ __launch_bounds__(kPostBlock) void k_post(PostArgs a)
 {
     __shared__ PostShared sh;
     extern __shared__ uint64_t keys[];
+    // selection blocks first: they are the longest and are dispatched first
     int b = blockIdx.x;
+    if (b < a.n_sel_blocks) {
+        role_select(a, b, sh, keys, a.keys_cap);
+        return;
+    }
+    b -= a.n_sel_blocks;
     if (b < a.n_req_blocks) {
         role_request(a, b, sh);
         return;
     }
     b -= a.n_req_blocks;
-    if (b < a.n_frame_blocks) {
-        role_frame(a, b, sh);
-        return;
-    }
-    b -= a.n_frame_blocks;
-    if (b < a.n_sel_blocks) role_select(a, b, sh, keys, a.keys_cap);
+    if (b < a.n_frame_blocks) role_frame(a, b, sh);
 }
 
 // ---------------------------------------------------------------- k_gather
 
-// Kept rows [j0, j1) of a segment whose rows span NU units, in batches of
-// about 8 KiB per wavefront; out-of-range lanes are dropped by the store's
-// buffer resource.
 #ifndef MSAO_GATHER_UNITS
-#define MSAO_GATHER_UNITS 8
+#define MSAO_GATHER_UNITS 8  // 16-byte units per lane in flight per gather batch
 #endif
+
+// Kept rows [j0, j0 + kGatherRows) of a segment whose rows span NU units.
+// The kept indices arrive in one vector load (lane i holds row j0 + i) and are
+// read out per row, so every row's load is issued without waiting on another;
+// out-of-range lanes are dropped by the store's buffer resource.
 template <int NU>
-__device__ __forceinline__ void gather_rows(const GatherArgs& a, const DevSeg& sg, int j0, int j1, int lane)
+__device__ __forceinline__ void gather_rows(const GatherArgs& a, const DevSeg& sg, int j0, int cnt, int lane)
 {
     constexpr int RB0 = NU >= MSAO_GATHER_UNITS ? 1 : MSAO_GATHER_UNITS / NU;
     constexpr int RB = RB0 < kGatherRows ? RB0 : kGatherRows;
     const int rb = sg.nchunk * 16;
     const int voff = lane * 16;
-    for (int j = j0; j < j1; j += RB) {
+    const int nrows = min(kGatherRows, cnt - j0);
+    const int mine = lane < nrows ? a.kept_idx[sg.tok_off + j0 + lane] : -1;
+    for (int i0 = 0; i0 < nrows; i0 += RB) {
         vec4 v[RB][NU];
         int src[RB];
 #pragma unroll
         for (int i = 0; i < RB; ++i) {
-            src[i] = j + i < j1 ? uniform(a.kept_idx[sg.tok_off + j + i]) : -1;
+            src[i] = i0 + i < nrows ? __builtin_amdgcn_readlane(mine, i0 + i) : -1;
             const bool ok = src[i] >= 0 && src[i] < sg.n_tok;
             const rsrc_t rs = make_rsrc(sg.data + (ok ? (int64_t)src[i] * sg.stride_bytes : 0), ok ? rb : 0);
 #pragma unroll
@@ -1024,17 +1022,18 @@ __device__ __forceinline__ void gather_rows(const GatherArgs& a, const DevSeg& s
 #pragma unroll
         for (int i = 0; i < RB; ++i) {
             if (src[i] < 0 || src[i] >= sg.n_tok) continue;
-            const rsrc_t rd = make_rsrc(a.out + sg.out_off + (int64_t)(j + i) * rb, rb);
+            const rsrc_t rd = make_rsrc(a.out + sg.out_off + (int64_t)(j0 + i0 + i) * rb, rb);
 #pragma unroll
             for (int u = 0; u < NU; ++u) bstore(v[i][u], rd, voff + u * 1024);
         }
     }
 }
 
-__device__ void gather_rows_generic(const GatherArgs& a, const DevSeg& sg, int j0, int j1, int lane)
+__device__ void gather_rows_generic(const GatherArgs& a, const DevSeg& sg, int j0, int cnt, int lane)
 {
     const int rb = sg.nchunk * 16;
     const int nu = (sg.nchunk + kWave - 1) / kWave;
+    const int j1 = min(cnt, j0 + kGatherRows);
     for (int j = j0; j < j1; ++j) {
         const int src = uniform(a.kept_idx[sg.tok_off + j]);
         if (src < 0 || src >= sg.n_tok) continue;
@@ -1055,23 +1054,22 @@ __global__ __launch_bounds__(kGatherBlock) void k_gather(GatherArgs a)
     const int lane = threadIdx.x & (kWave - 1);
     const int w = uniform(blockIdx.x * (kGatherBlock / kWave) + (threadIdx.x >> 6));
     if (w >= a.t.n_gwi) return;
-    const int s = find_seg(a.t.seg_gi, a.t.n, w);
+    const int s = uniform(a.t.gi_seg[w]);
     const DevSeg sg = a.t.seg[s];
     int cnt = uniform(a.kept_count[s]);
     cnt = min(cnt, min(sg.cap, sg.n_tok));
     const int j0 = (w - sg.g_begin) * kGatherRows;
-    const int j1 = min(cnt, j0 + kGatherRows);
-    if (j0 >= j1) return;
+    if (j0 >= cnt) return;
     switch ((sg.nchunk + kWave - 1) / kWave) {
-    case 1: gather_rows<1>(a, sg, j0, j1, lane); break;
-    case 2: gather_rows<2>(a, sg, j0, j1, lane); break;
-    case 3: gather_rows<3>(a, sg, j0, j1, lane); break;
-    case 4: gather_rows<4>(a, sg, j0, j1, lane); break;
-    case 5: gather_rows<5>(a, sg, j0, j1, lane); break;
-    case 6: gather_rows<6>(a, sg, j0, j1, lane); break;
-    case 7: gather_rows<7>(a, sg, j0, j1, lane); break;
-    case 8: gather_rows<8>(a, sg, j0, j1, lane); break;
-    default: gather_rows_generic(a, sg, j0, j1, lane); break;
+    case 1: gather_rows<1>(a, sg, j0, cnt, lane); break;
+    case 2: gather_rows<2>(a, sg, j0, cnt, lane); break;
+    case 3: gather_rows<3>(a, sg, j0, cnt, lane); break;
+    case 4: gather_rows<4>(a, sg, j0, cnt, lane); break;
+    case 5: gather_rows<5>(a, sg, j0, cnt, lane); break;
+    case 6: gather_rows<6>(a, sg, j0, cnt, lane); break;
+    case 7: gather_rows<7>(a, sg, j0, cnt, lane); break;
+    case 8: gather_rows<8>(a, sg, j0, cnt, lane); break;
+    default: gather_rows_generic(a, sg, j0, cnt, lane); break;
     }
 }
 
