@@ -37,7 +37,7 @@ def parse():
     ap.add_argument("--no-compact", action="store_true", help="time score+select only (no compaction)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (calibrates HBM byte counters)")
-    ap.add_argument("--streams", type=int, default=2,
+    ap.add_argument("--streams", type=int, default=3,
                     help="batches in flight: consecutive steps alternate over this many HIP streams")
     return ap.parse_args()
 
@@ -71,15 +71,27 @@ def pack_replicas(w, n_rep, dev):
     return reps, total
 
 
-def algorithmic_bytes(w, kept_rows_bytes, kept_total):
-    """Bytes the method must move (see the design notes): input rows read once,
-    16 B/token of statistics (z, l1, l2, info), 8 B/token more for video tokens
-    (d, res), 1 B/token keep flag, 4 B per kept index, and the kept rows written."""
+def algorithmic_bytes(w, kept_count, compact):
+    """Bytes the method must move (see the design notes), split by kernel.
+
+    k_score: input rows read once, 16 B/token of statistics (z, l1, l2, info),
+    8 B/token more for video tokens (d, res), plus, with compaction, the rows of
+    segments that keep every token (written by the scoring pass).
+    k_post: 1 B/token keep flag and 4 B per kept index.
+    k_gather: the other kept rows, written once."""
     ntok = w.n_tokens
     nvid = sum(s.n_tokens for s in w.segments if s.modality == 2 and s.n_frames >= 2)
     score = w.input_bytes + 16 * ntok + 8 * nvid
-    select = ntok * 1 + 4 * kept_total
-    return score, select, kept_rows_bytes
+    select = ntok * 1 + 4 * int(sum(kept_count))
+    fused = gather = 0
+    if compact:
+        for k, s in zip(kept_count, w.segments):
+            rows = int(k) * s.hidden * (4 if s.dtype == "f32" else 2)
+            if int(k) == s.n_tokens and s.n_tokens > 0:
+                fused += rows
+            else:
+                gather += rows
+    return score + fused, select, gather
 
 
 def committed_traffic(config):
@@ -151,18 +163,17 @@ def main():
         extra, _ = pack_replicas(w, 1, dev)
         reps += extra
     main = torch.cuda.current_stream()
-    streams = [main] + [torch.cuda.Stream() for _ in range(n_str - 1)]
+    # steps run on streams of their own (not the default stream, which would
+    # serialize with them); the timing events are on the default stream
+    streams = [torch.cuda.Stream() for _ in range(n_str)]
     ctxs = [msao.Context(0) for _ in range(n_str)]  # one context per stream
-    # every stream writes its own outputs; every plan (one per replica) has its own workspace
-    base_out = [msao.Outputs(reps[0], R, token_fields=fields, compact=compact) for _ in range(n_str)]
-    plans = []
+    # every replica has its own outputs and plan workspace, so that neither the
+    # inputs nor the outputs of a step are still in the Infinity Cache
+    plans, outs = [], []
     for r, segs in enumerate(reps):
         k = r % n_str
-        o = msao.Outputs(reps[0], R, token_fields=fields, compact=False)
-        b = base_out[k]
-        o.tok, o.frm, o.req, o.sel = b.tok, b.frm, b.req, b.sel
-        o.out, o.out_off, o.out_bytes = b.out, b.out_off, getattr(b, "out_bytes", 0)
-        o._structs()
+        o = msao.Outputs(segs, R, token_fields=fields, compact=compact)
+        outs.append(o)
         plans.append((k, msao.Plan(segs, R, o, w.params, ctx=ctxs[k], compact=compact, stream=main)))
     torch.cuda.synchronize()
 
@@ -170,18 +181,18 @@ def main():
         """Enqueue `count` steps; step i runs plan i % n_rep on its stream."""
         start = torch.cuda.Event()
         start.record(main)
-        for st in streams[1:nstreams]:
+        for st in streams[:nstreams]:
             st.wait_event(start)
         used = set()
         for i in range(count):
-            k, plan = plans[i % n_rep] if nstreams > 1 else (0, plans[(i * n_str) % n_rep][1])
+            k, plan = plans[i % n_rep]
+            k = k if nstreams > 1 else 0
             plan(streams[k])
             used.add(k)
         for k in used:
-            if k:
-                ev = torch.cuda.Event()
-                ev.record(streams[k])
-                main.wait_event(ev)
+            ev = torch.cuda.Event()
+            ev.record(streams[k])
+            main.wait_event(ev)
 
     def timed(count, nstreams):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -195,11 +206,9 @@ def main():
 
     run_steps(args.warmup, n_str)
     torch.cuda.synchronize()
-    out = base_out[0]
+    out = outs[0]
     kept_count = out.sel["kept_count"][:n].cpu().numpy()
     kept_total = int(kept_count.sum())
-    kept_rows_bytes = int(sum(int(k) * s.hidden * (4 if s.dtype == "f32" else 2)
-                              for k, s in zip(kept_count, w.segments))) if compact else 0
 
     # timed region: K whole steps over rotated replicas, n_str batches in flight
     ms_step, wall = timed(args.steps, n_str)
@@ -208,13 +217,15 @@ def main():
 
     # per-kernel durations: HIP events recorded by the library around each launch,
     # on the stream the kernel is launched on (one stream, so kernels do not overlap)
-    ctxs[0].set_profiling(True)
+    for c in ctxs:
+        c.set_profiling(True)
     for i in range(args.steps):
-        plans[(i * n_str) % n_rep][1](main)
-    k_ms = np.array(ctxs[0].kernel_times())
-    ctxs[0].set_profiling(False)
+        plans[i % n_rep][1](streams[0])
+    k_ms = np.mean([np.array(c.kernel_times()) for c in ctxs], axis=0)
+    for c in ctxs:
+        c.set_profiling(False)
 
-    b_score, b_select, b_compact = algorithmic_bytes(w, kept_rows_bytes, kept_total)
+    b_score, b_select, b_compact = algorithmic_bytes(w, kept_count, compact)
     b_step = b_score + b_select + b_compact
     score_gbs = b_score / (k_ms[0] * 1e-3) / 1e9
     line = {
@@ -239,7 +250,7 @@ def main():
         "ms_per_step_one_stream": ms_step_serial,
         "hbm_gbps_step": b_step / (ms_step * 1e-3) / 1e9,
         "hbm_frac_step": b_step / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS,
-        "algorithmic_bytes": {"score": b_score, "select": b_select, "compact_write": b_compact},
+        "algorithmic_bytes": {"score": b_score, "select": b_select, "gather_write": b_compact},
         "kernel_ms": {"score": k_ms[0], "post": k_ms[1], "gather": k_ms[2]},
         "roofline": {"bound": "hbm", "kernel": "k_score", "achieved": score_gbs, "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": score_gbs / PEAK_HBM_GBS, "traffic": committed_traffic(args.config)},

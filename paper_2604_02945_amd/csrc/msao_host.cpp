@@ -161,8 +161,10 @@ size_t workspace_bytes_for(int n, int R, int64_t ntok)
     return align_up(tb, kWsAlign) + sizeof(Partial) * (size_t)std::max<int64_t>(ntok + n, 1);
 }
 
+// fuse_copy: a full run with compaction, where segments that keep every row
+// are copied by the scoring pass (they get no gather items).
 void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* p,
-                const float* alpha, const int64_t* out_off, Plan& pl)
+                const float* alpha, const int64_t* out_off, Plan& pl, bool fuse_copy = false)
 {
     pl.seg.resize((size_t)n);
     pl.seg_wi.assign((size_t)n + 1, 0);
@@ -200,6 +202,7 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         d.lam_t = p->lambda_t[s.modality];
         d.k = s.keep_ratio < 0.0f ? -1 : (int32_t)keep_count(s.keep_ratio, N);
         d.cap = d.k < 0 ? (int32_t)N : d.k;
+        d.copy_in_score = (fuse_copy && out_off && N > 0 && d.k == (int32_t)N) ? 1 : 0;
         // scoring work items, one wavefront each
         int items = 0;
         if (d.temporal) {
@@ -224,7 +227,7 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         wi += items;
         pl.seg_wi[(size_t)i + 1] = wi;
         d.g_begin = gi;
-        gi += (d.cap + kGatherRows - 1) / kGatherRows;
+        if (!d.copy_in_score) gi += (d.cap + kGatherRows - 1) / kGatherRows;
         pl.seg_gi[(size_t)i + 1] = gi;
         if (d.k < 0) pl.any_guided = true;
         pl.max_n = std::max(pl.max_n, (int)N);
@@ -385,29 +388,25 @@ hipEvent_t pooled_event(msao_ctx* ctx)
     return hipEventCreate(&e) == hipSuccess ? e : nullptr;
 }
 
-// Launch with optional profiling events around it.
-msao_status launched(msao_ctx* ctx, int kernel, hipStream_t stream, int (*fn)(const void*, void*), const void* args)
+// Launch, with profiling events recorded at the kernel's start and end.
+msao_status launched(msao_ctx* ctx, int kernel, hipStream_t stream, int (*fn)(const void*, void*, void*, void*),
+                     const void* args)
 {
-    hipError_t e;
     hipEvent_t e0 = nullptr, e1 = nullptr;
     if (ctx->profiling) {
         e0 = pooled_event(ctx);
         e1 = pooled_event(ctx);
         if (!e0 || !e1) return fail(&ctx->err, MSAO_ERR_HIP, "hipEventCreate failed");
-        if ((e = hipEventRecord(e0, stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
     }
-    const int rc = fn(args, stream);
+    const int rc = fn(args, stream, e0, e1);
     if (rc != 0) return hip_fail(ctx, (hipError_t)rc, "kernel launch");
-    if (ctx->profiling) {
-        if ((e = hipEventRecord(e1, stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
-        ctx->rec[kernel].push_back({e0, e1});
-    }
+    if (ctx->profiling) ctx->rec[kernel].push_back({e0, e1});
     return MSAO_OK;
 }
 
-int run_score(const void* a, void* s) { return launch_score(*(const ScoreArgs*)a, s); }
-int run_post(const void* a, void* s) { return launch_post(*(const PostArgs*)a, s); }
-int run_gather(const void* a, void* s) { return launch_gather(*(const GatherArgs*)a, s); }
+int run_score(const void* a, void* s, void* e0, void* e1) { return launch_score(*(const ScoreArgs*)a, s, e0, e1); }
+int run_post(const void* a, void* s, void* e0, void* e1) { return launch_post(*(const PostArgs*)a, s, e0, e1); }
+int run_gather(const void* a, void* s, void* e0, void* e1) { return launch_gather(*(const GatherArgs*)a, s, e0, e1); }
 
 #define MSAO_TRY(x)                                                                                                   \
     do {                                                                                                              \
@@ -620,6 +619,7 @@ msao_status msao_mas_score(msao_ctx* ctx, const msao_segment* segs, int n, int R
     ScoreArgs sa;
     sa.t = device_tables(pl, ws, n, R, params);
     sa.tok = token_out(tok);
+    sa.out = nullptr;
     sa.mode = kModeScore;
     MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
     PostArgs pa;
@@ -759,6 +759,7 @@ msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const ms
     ScoreArgs sa;
     sa.t = t;
     sa.tok = token_out(tok);
+    sa.out = (uint8_t*)out;
     sa.mode = kModeScore;
     MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
     PostArgs pa;
@@ -777,7 +778,7 @@ msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const ms
     pa.n_sel_blocks = t.n;
     pa.keys_cap = std::min(pl.max_n, kMaxLdsKeys);
     MSAO_TRY(launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa));
-    if (!out) return MSAO_OK;
+    if (!out || t.n_gwi == 0) return MSAO_OK;
     GatherArgs ga;
     ga.t = t;
     ga.kept_idx = sel->kept_idx;
@@ -808,7 +809,7 @@ msao_status msao_run(msao_ctx* ctx, const msao_segment* segs, int n, int R, cons
     if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
     MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
     Plan pl;
-    build_plan(ctx, segs, n, R, params, alpha, out_byte_off, pl);
+    build_plan(ctx, segs, n, R, params, alpha, out_byte_off, pl, out != nullptr);
     MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
     const std::vector<msao_segment> sv(segs, segs + n);
     MSAO_TRY(check_run_outputs(ctx, pl, sv, tok, frm, req, sel, out, out_byte_off, out_bytes));
@@ -831,7 +832,7 @@ msao_status msao_plan_create(msao_ctx* ctx, const msao_segment* segs, int n, int
     p->segs.assign(segs, segs + n);
     if (out_byte_off) p->out_off.assign(out_byte_off, out_byte_off + n);
     p->params = *params;
-    build_plan(ctx, segs, n, R, params, alpha, out_byte_off, p->pl);
+    build_plan(ctx, segs, n, R, params, alpha, out_byte_off, p->pl, out_byte_off != nullptr);
     msao_status st = check_ws(ctx, p->pl, ws, ws_bytes);
     if (st == MSAO_OK) {
         DeviceGuard guard(ctx->device);

@@ -34,7 +34,7 @@ struct DevSeg {
     int32_t k;             // fixed keep count, or -1 when MAS-guided
     int32_t cap;           // compaction capacity in rows
     int32_t g_begin;       // first gather work item
-    int32_t pad_;
+    int32_t copy_in_score; // every row is kept: the scoring pass writes the compacted rows itself
 };
 
 // Integer partial sums of one scoring work item (no atomics, no zeroing).
@@ -105,6 +105,7 @@ struct PostArgs {
 struct ScoreArgs {
     Tables t;
     TokenOut tok;
+    uint8_t* out;         // compaction output for copy_in_score segments (NULL: none)
     int32_t mode;
 };
 
@@ -116,10 +117,11 @@ struct GatherArgs {
     int64_t out_bytes;
 };
 
-// Launchers (msao_kernels.hip). Return the HIP error code of the launch.
-int launch_score(const ScoreArgs& a, void* stream);
-int launch_post(const PostArgs& a, void* stream);
-int launch_gather(const GatherArgs& a, void* stream);
+// Launchers (msao_kernels.hip). Return the HIP error code of the launch. ev0 and
+// ev1 (hipEvent_t, may be NULL) are recorded at the kernel's start and end.
+int launch_score(const ScoreArgs& a, void* stream, void* ev0, void* ev1);
+int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1);
+int launch_gather(const GatherArgs& a, void* stream, void* ev0, void* ev1);
 
 constexpr int kScoreBlock = 256;   // 4 wavefronts, one work item each
 constexpr int kPostBlock = 256;

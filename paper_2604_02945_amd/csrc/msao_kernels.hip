@@ -15,6 +15,7 @@
 //            per frame), one per segment (top-k by LDS radix select over
 //            exact integer keys, ties by index, block-scan compaction).
 //   k_gather one wavefront per few kept rows: packed bitwise copy.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -65,7 +66,7 @@ constexpr int kRsrcWord3 = 0x00020000;
 #define MSAO_LOAD_AUX 2  // nontemporal: every input row is read once
 #endif
 #ifndef MSAO_STORE_AUX
-#define MSAO_STORE_AUX 0
+#define MSAO_STORE_AUX 2  // nontemporal: compacted rows are written once and not re-read here
 #endif
 #ifndef MSAO_GATHER_LOAD_AUX
 #define MSAO_GATHER_LOAD_AUX 0  // kept rows may still be cached from the scoring pass
@@ -289,6 +290,19 @@ __device__ __forceinline__ void emit_token(const TokenOut& o, const DevSeg& sg, 
     if (o.res) o.res[g] = temporal ? s.res : 0.0f;
 }
 
+// A segment that keeps every row is compacted by the scoring pass itself: the
+// row just read is written to its packed slot (row i of the segment goes to
+// out + out_off + i * row bytes), so the gather never re-reads it.
+template <int NU>
+__device__ __forceinline__ void copy_row_out(const ScoreArgs& a, const DevSeg& sg, int row, const vec4 (&v)[NU],
+                                             int voff)
+{
+    const int rb = sg.nchunk * 16;
+    const rsrc_t rd = make_rsrc(a.out + sg.out_off + (int64_t)row * rb, rb);
+#pragma unroll
+    for (int u = 0; u < NU; ++u) bstore(v[u], rd, voff + u * 1024);
+}
+
 // Statistics of one row held as NU 1-KiB units (64 lanes x 16 B each).
 template <int DT, int NU>
 __device__ __forceinline__ TokStat row_stats(const vec4 (&v)[NU], float tau, const Thr& th)
@@ -319,9 +333,11 @@ template <int DT, int NU, int RPI>
 __device__ __forceinline__ void rows_batch(const ScoreArgs& a, const DevSeg& sg, const vec4 (&v)[RPI][NU],
                                            int r, int r1, int lane, uint32_t& nsp)
 {
+    const bool copy = a.out && sg.copy_in_score;
 #pragma unroll
     for (int i = 0; i < RPI; ++i) {
         if (r + i >= r1) break;
+        if (copy) copy_row_out<NU>(a, sg, r + i, v[i], lane * 16);
         const TokStat s = row_stats<DT, NU>(v[i], a.t.tau, bf16_thresholds(a.t.tau));
         emit_token(a.tok, sg, r + i, lane, s, false, kModeScore);
         nsp += s.act < (uint32_t)sg.A_s;
@@ -375,13 +391,19 @@ __device__ void score_rows_generic(const ScoreArgs& a, const DevSeg& sg, int r0,
     const Thr th = bf16_thresholds(tau);
     const int nu = (sg.nchunk + kWave - 1) / kWave;
     const int rb = sg.nchunk * 16;
+    const bool copy = a.out && sg.copy_in_score;
     for (int r = r0; r < r1; ++r) {
         const rsrc_t rs = make_rsrc(sg.data + (int64_t)r * sg.stride_bytes, rb);
+        const rsrc_t rd = make_rsrc(a.out + sg.out_off + (int64_t)r * rb, copy ? rb : 0);
         TokStat s{0u, 0u, 0.0f, 0.0f, 0.0f};
         for (int u0 = 0; u0 < nu; u0 += 4) {
             vec4 v[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) v[u] = bload(rs, ((u0 + u) * kWave + lane) * 16);
+            if (copy) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) bstore(v[u], rd, ((u0 + u) * kWave + lane) * 16);
+            }
 #pragma unroll
             for (int u = 0; u < 4; ++u) chunk_stats<DT>(v[u], tau, th, s.act, s.l1, s.l2);
         }
@@ -431,6 +453,7 @@ __device__ __forceinline__ void score_chain(const ScoreArgs& a, const DevSeg& sg
     for (int t = t0; t < t1; ++t) {
         vec4 nxt[NU];
         load(nxt, t + 1, t + 1 < t1);
+        if (a.out && sg.copy_in_score) copy_row_out<NU>(a, sg, t * sg.P + p, cur, voff);
         TokStat s{0u, 0u, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int u = 0; u < NU; ++u)
@@ -459,9 +482,11 @@ __device__ void score_chain_generic(const ScoreArgs& a, const DevSeg& sg, int p,
     const uint8_t* base = sg.data + (int64_t)p * sg.stride_bytes;
     const int nu = (sg.nchunk + kWave - 1) / kWave;
     const int rb = sg.nchunk * 16;
+    const bool copy = a.out && sg.copy_in_score;
     for (int t = t0; t < t1; ++t) {
         const rsrc_t rc = make_rsrc(base + (int64_t)t * fstride, rb);
         const rsrc_t rp = make_rsrc(base + (t > 0 ? (int64_t)(t - 1) * fstride : 0), t > 0 ? rb : 0);
+        const rsrc_t rd = make_rsrc(a.out + sg.out_off + (int64_t)(t * sg.P + p) * rb, copy ? rb : 0);
         TokStat s{0u, 0u, 0.0f, 0.0f, 0.0f};
         for (int u0 = 0; u0 < nu; u0 += 2) {
             vec4 v[2], w[2];
@@ -470,6 +495,10 @@ __device__ void score_chain_generic(const ScoreArgs& a, const DevSeg& sg, int p,
                 const int off = ((u0 + u) * kWave + lane) * 16;
                 v[u] = bload(rc, off);
                 w[u] = bload(rp, off);
+            }
+            if (copy) {
+#pragma unroll
+                for (int u = 0; u < 2; ++u) bstore(v[u], rd, ((u0 + u) * kWave + lane) * 16);
             }
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
@@ -1075,16 +1104,28 @@ __global__ __launch_bounds__(kGatherBlock) void k_gather(GatherArgs a)
 
 }  // namespace
 
-int launch_score(const ScoreArgs& a, void* stream)
+// With ev0/ev1 (profiling), the launch records them at the kernel's own start
+// and end, so their span is the kernel's execution time.
+template <typename Args>
+static int launch(void (*kernel)(Args), dim3 grid, dim3 block, size_t lds, void* stream, const Args& a,
+                  void* ev0, void* ev1)
+{
+    if (ev0 && ev1)
+        hipExtLaunchKernelGGL(kernel, grid, block, lds, (hipStream_t)stream, (hipEvent_t)ev0, (hipEvent_t)ev1, 0, a);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, lds, (hipStream_t)stream, a);
+    return (int)hipGetLastError();
+}
+
+int launch_score(const ScoreArgs& a, void* stream, void* ev0, void* ev1)
 {
     if (a.t.n_wi <= 0) return 0;
     const int waves = kScoreBlock / kWave;
     const unsigned grid = (unsigned)((a.t.n_wi + waves - 1) / waves);
-    hipLaunchKernelGGL(k_score, dim3(grid), dim3(kScoreBlock), 0, (hipStream_t)stream, a);
-    return (int)hipGetLastError();
+    return launch(k_score, dim3(grid), dim3(kScoreBlock), 0, stream, a, ev0, ev1);
 }
 
-int launch_post(const PostArgs& a, void* stream)
+int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1)
 {
     const int blocks = a.n_req_blocks + a.n_frame_blocks + a.n_sel_blocks;
     if (blocks <= 0) return 0;
@@ -1093,17 +1134,15 @@ int launch_post(const PostArgs& a, void* stream)
         const hipError_t e = hipFuncSetAttribute((const void*)k_post, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return (int)e;
     }
-    hipLaunchKernelGGL(k_post, dim3((unsigned)blocks), dim3(kPostBlock), lds, (hipStream_t)stream, a);
-    return (int)hipGetLastError();
+    return launch(k_post, dim3((unsigned)blocks), dim3(kPostBlock), lds, stream, a, ev0, ev1);
 }
 
-int launch_gather(const GatherArgs& a, void* stream)
+int launch_gather(const GatherArgs& a, void* stream, void* ev0, void* ev1)
 {
     if (a.t.n_gwi <= 0) return 0;
     const int waves = kGatherBlock / kWave;
     const unsigned grid = (unsigned)((a.t.n_gwi + waves - 1) / waves);
-    hipLaunchKernelGGL(k_gather, dim3(grid), dim3(kGatherBlock), 0, (hipStream_t)stream, a);
-    return (int)hipGetLastError();
+    return launch(k_gather, dim3(grid), dim3(kGatherBlock), 0, stream, a, ev0, ev1);
 }
 
 }  // namespace msao
