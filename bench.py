@@ -35,6 +35,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU time budget of the oracle baseline")
     ap.add_argument("--no-compact", action="store_true", help="time score+select only (no compaction)")
+    ap.add_argument("--no-score-select", action="store_true",
+                    help="skip the extra score+select-only timing that follows a run with compaction")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (calibrates HBM byte counters)")
     ap.add_argument("--streams", type=int, default=3,
@@ -167,17 +169,20 @@ def main():
     # serialize with them); the timing events are on the default stream
     streams = [torch.cuda.Stream() for _ in range(n_str)]
     ctxs = [msao.Context(0) for _ in range(n_str)]  # one context per stream
-    # every replica has its own outputs and plan workspace, so that neither the
-    # inputs nor the outputs of a step are still in the Infinity Cache
-    plans, outs = [], []
-    for r, segs in enumerate(reps):
-        k = r % n_str
-        o = msao.Outputs(segs, R, token_fields=fields, compact=compact)
-        outs.append(o)
-        plans.append((k, msao.Plan(segs, R, o, w.params, ctx=ctxs[k], compact=compact, stream=main)))
-    torch.cuda.synchronize()
 
-    def run_steps(count, nstreams):
+    def make_plans(with_compaction):
+        """One plan per replica, each with its own outputs and workspace, so that
+        neither the inputs nor the outputs of a step are still in the Infinity Cache."""
+        plans, outs = [], []
+        for r, segs in enumerate(reps):
+            k = r % n_str
+            o = msao.Outputs(segs, R, token_fields=fields, compact=with_compaction)
+            outs.append(o)
+            plans.append((k, msao.Plan(segs, R, o, w.params, ctx=ctxs[k], compact=with_compaction, stream=main)))
+        torch.cuda.synchronize()
+        return plans, outs
+
+    def run_steps(plans, count, nstreams):
         """Enqueue `count` steps; step i runs plan i % n_rep on its stream."""
         start = torch.cuda.Event()
         start.record(main)
@@ -194,26 +199,27 @@ def main():
             ev.record(streams[k])
             main.wait_event(ev)
 
-    def timed(count, nstreams):
+    def timed(plans, count, nstreams):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t = time.perf_counter()
         e0.record(main)
-        run_steps(count, nstreams)
+        run_steps(plans, count, nstreams)
         e1.record(main)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / count, time.perf_counter() - t
 
-    run_steps(args.warmup, n_str)
+    plans, outs = make_plans(compact)
+    run_steps(plans, args.warmup, n_str)
     torch.cuda.synchronize()
     out = outs[0]
     kept_count = out.sel["kept_count"][:n].cpu().numpy()
     kept_total = int(kept_count.sum())
 
     # timed region: K whole steps over rotated replicas, n_str batches in flight
-    ms_step, wall = timed(args.steps, n_str)
+    ms_step, wall = timed(plans, args.steps, n_str)
     # the same steps one after another on one stream: per-batch latency
-    ms_step_serial, _ = timed(args.steps, 1)
+    ms_step_serial, _ = timed(plans, args.steps, 1)
 
     # per-kernel durations: HIP events recorded by the library around each launch,
     # on the stream the kernel is launched on (one stream, so kernels do not overlap)
@@ -227,6 +233,24 @@ def main():
 
     b_score, b_select, b_compact = algorithmic_bytes(w, kept_count, compact)
     b_step = b_score + b_select + b_compact
+
+    # scoring and selection alone (no compaction), same replicas and streams
+    score_select = None
+    if compact and not args.no_score_select:
+        torch.cuda.synchronize()
+        for _, plan in plans:
+            plan.close()
+        del plans, outs
+        plans_ss, _ = make_plans(False)
+        run_steps(plans_ss, args.warmup, n_str)
+        ms_ss, _ = timed(plans_ss, args.steps, n_str)
+        ms_ss_serial, _ = timed(plans_ss, args.steps, 1)
+        b_s, b_sel, _ = algorithmic_bytes(w, kept_count, False)
+        score_select = {"ms_per_step": ms_ss, "ms_per_step_one_stream": ms_ss_serial,
+                        "tokens_per_s": w.n_tokens / (ms_ss * 1e-3), "algorithmic_bytes": b_s + b_sel,
+                        "hbm_gbps": (b_s + b_sel) / (ms_ss * 1e-3) / 1e9,
+                        "hbm_frac": (b_s + b_sel) / (ms_ss * 1e-3) / 1e9 / PEAK_HBM_GBS}
+        plans = plans_ss
     score_gbs = b_score / (k_ms[0] * 1e-3) / 1e9
     line = {
         "metric": METRIC,
@@ -255,6 +279,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "k_score", "achieved": score_gbs, "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": score_gbs / PEAK_HBM_GBS, "traffic": committed_traffic(args.config)},
         "wall_s_timed": wall,
+        "score_select": score_select,
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

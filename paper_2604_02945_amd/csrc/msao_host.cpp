@@ -34,6 +34,7 @@ struct msao_ctx {
     // tuning
     int row_item_bytes = 8192;
     int chain_frames = 0;       // frames per temporal work item; 0 = automatic
+    int xcd_order = -1;         // scoring block order: -1 automatic, 0 dispatch order, 1 one range per XCD
 };
 
 namespace {
@@ -129,6 +130,7 @@ struct Plan {
     int n_wi = 0, n_gwi = 0;
     int max_n = 0;                 // largest segment (LDS key staging)
     bool any_temporal = false, any_guided = false;
+    bool any_copy = false;         // some segment is compacted by the scoring pass
     size_t off_seg = 0, off_wi = 0, off_gi = 0, off_rmoff = 0, off_rmseg = 0, off_tseg = 0, off_alpha = 0;
     size_t table_bytes = 0, off_partial = 0, total_bytes = 0;
 };
@@ -230,6 +232,7 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         if (!d.copy_in_score) gi += (d.cap + kGatherRows - 1) / kGatherRows;
         pl.seg_gi[(size_t)i + 1] = gi;
         if (d.k < 0) pl.any_guided = true;
+        if (d.copy_in_score) pl.any_copy = true;
         pl.max_n = std::max(pl.max_n, (int)N);
         tok += N;
         if (d.temporal) frame += s.n_frames;
@@ -414,6 +417,16 @@ int run_gather(const void* a, void* s, void* e0, void* e1) { return launch_gathe
         if (st_ != MSAO_OK) return st_;                                                                               \
     } while (0)
 
+// Scoring block order. The order with one contiguous range of work items per
+// XCD makes the per-token statistic stores cheaper, but was measured slower
+// when the scoring pass also writes compacted rows, so it is used only for
+// launches that copy no rows (unless MSAO_XCD_ORDER forces either order).
+int32_t xcd_order_for(const msao_ctx* ctx, bool copies_rows)
+{
+    if (ctx->xcd_order >= 0) return ctx->xcd_order ? 1 : 0;
+    return copies_rows ? 0 : 1;
+}
+
 TokenOut token_out(const msao_token_out* t)
 {
     TokenOut o{};
@@ -544,6 +557,7 @@ msao_status msao_create(msao_ctx** out, int device)
     }
     if (const char* v = std::getenv("MSAO_ROW_ITEM_BYTES")) c->row_item_bytes = std::max(1, std::atoi(v));
     if (const char* v = std::getenv("MSAO_CHAIN_FRAMES")) c->chain_frames = std::max(0, std::atoi(v));
+    if (const char* v = std::getenv("MSAO_XCD_ORDER")) c->xcd_order = std::atoi(v) < 0 ? -1 : (std::atoi(v) ? 1 : 0);
     *out = c;
     return MSAO_OK;
 }
@@ -621,6 +635,7 @@ msao_status msao_mas_score(msao_ctx* ctx, const msao_segment* segs, int n, int R
     sa.tok = token_out(tok);
     sa.out = nullptr;
     sa.mode = kModeScore;
+    sa.xcd_order = xcd_order_for(ctx, false);
     MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
     PostArgs pa;
     std::memset(&pa, 0, sizeof pa);
@@ -658,6 +673,7 @@ msao_status msao_temporal_redundancy(msao_ctx* ctx, const msao_segment* segs, in
     sa.tok.d = d;
     sa.tok.res = res;
     sa.mode = kModeTemporal;
+    sa.xcd_order = xcd_order_for(ctx, false);
     MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
     PostArgs pa;
     std::memset(&pa, 0, sizeof pa);
@@ -761,6 +777,7 @@ msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const ms
     sa.tok = token_out(tok);
     sa.out = (uint8_t*)out;
     sa.mode = kModeScore;
+    sa.xcd_order = xcd_order_for(ctx, out && pl.any_copy);
     MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
     PostArgs pa;
     std::memset(&pa, 0, sizeof pa);

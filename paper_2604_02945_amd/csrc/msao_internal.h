@@ -107,6 +107,7 @@ struct ScoreArgs {
     TokenOut tok;
     uint8_t* out;         // compaction output for copy_in_score segments (NULL: none)
     int32_t mode;
+    int32_t xcd_order;    // 1: each XCD takes one contiguous range of workgroups
 };
 
 struct GatherArgs {
@@ -124,7 +125,10 @@ int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1);
 int launch_gather(const GatherArgs& a, void* stream, void* ev0, void* ev1);
 
 constexpr int kScoreBlock = 256;   // 4 wavefronts, one work item each
-constexpr int kPostBlock = 256;
+#ifndef MSAO_POST_BLOCK
+#define MSAO_POST_BLOCK 256
+#endif
+constexpr int kPostBlock = MSAO_POST_BLOCK;  // threads per post-scoring block
 #ifndef MSAO_GATHER_BLOCK
 #define MSAO_GATHER_BLOCK 64
 #endif

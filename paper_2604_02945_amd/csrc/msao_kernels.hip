@@ -270,24 +270,46 @@ struct TokStat {
     float l1, l2, res;
 };
 
-__device__ __forceinline__ void emit_token(const TokenOut& o, const DevSeg& sg, int row, int lane,
-                                           const TokStat& s, bool temporal, int mode)
+// Statistics of up to 64 tokens of one wavefront: lane j holds the j-th token
+// of the current run, so that each output array is written with one store
+// instruction per run instead of one per token.
+struct TokBuf {
+    uint32_t act, d;
+    float l1, l2, res;
+};
+
+__device__ __forceinline__ void tokbuf_put(TokBuf& b, int slot, int lane, const TokStat& s)
 {
-    if (lane != 0) return;
-    const int g = sg.tok_off + row;
-    const uint32_t z = (uint32_t)sg.C - s.act;
+    if (lane == slot) {
+        b.act = s.act;
+        b.d = s.d;
+        b.l1 = s.l1;
+        b.l2 = s.l2;
+        b.res = s.res;
+    }
+}
+
+// Writes tokens first_row + j * row_step (j < count) of the segment from
+// lanes j: z = C - active count, L1, L2, info = 1 - (lambda_s z + lambda_t e)/C
+// with e = C - d for temporal tokens, and d, res (zero outside temporal segments).
+__device__ __forceinline__ void tokbuf_flush(const TokenOut& o, const DevSeg& sg, const TokBuf& b, int first_row,
+                                             int row_step, int count, int lane, bool temporal, int mode)
+{
+    if (lane >= count) return;
+    const int g = sg.tok_off + first_row + lane * row_step;
+    const uint32_t z = (uint32_t)sg.C - b.act;
     if (mode == kModeScore) {
         if (o.z) o.z[g] = z;
-        if (o.l1) o.l1[g] = s.l1;
-        if (o.l2) o.l2[g] = s.l2;
+        if (o.l1) o.l1[g] = b.l1;
+        if (o.l2) o.l2[g] = b.l2;
         if (o.info) {
             float red = sg.lam_s * (float)z;
-            if (temporal) red += sg.lam_t * (float)((uint32_t)sg.C - s.d);
+            if (temporal) red += sg.lam_t * (float)((uint32_t)sg.C - b.d);
             o.info[g] = 1.0f - red * __builtin_amdgcn_rcpf((float)sg.C);
         }
     }
-    if (o.d) o.d[g] = temporal ? s.d : 0u;
-    if (o.res) o.res[g] = temporal ? s.res : 0.0f;
+    if (o.d) o.d[g] = temporal ? b.d : 0u;
+    if (o.res) o.res[g] = temporal ? b.res : 0.0f;
 }
 
 // A segment that keeps every row is compacted by the scoring pass itself: the
@@ -329,18 +351,28 @@ __device__ __forceinline__ void load_rows(vec4 (&v)[RPI][NU], const DevSeg& sg, 
     }
 }
 
+// Rows [r, r + RPI) clipped to r1 of the item that starts at row r0. Row
+// statistics go to slot (row - r0) & 63 of the token buffer, which is written
+// out when it holds 64 rows or the item ends (RPI divides 64, so a batch
+// never straddles a flush).
 template <int DT, int NU, int RPI>
 __device__ __forceinline__ void rows_batch(const ScoreArgs& a, const DevSeg& sg, const vec4 (&v)[RPI][NU],
-                                           int r, int r1, int lane, uint32_t& nsp)
+                                           int r0, int r, int r1, int lane, uint32_t& nsp, TokBuf& tb)
 {
+    static_assert(64 % RPI == 0, "a row batch must divide the token buffer");
     const bool copy = a.out && sg.copy_in_score;
 #pragma unroll
     for (int i = 0; i < RPI; ++i) {
         if (r + i >= r1) break;
         if (copy) copy_row_out<NU>(a, sg, r + i, v[i], lane * 16);
         const TokStat s = row_stats<DT, NU>(v[i], a.t.tau, bf16_thresholds(a.t.tau));
-        emit_token(a.tok, sg, r + i, lane, s, false, kModeScore);
+        tokbuf_put(tb, (r + i - r0) & 63, lane, s);
         nsp += s.act < (uint32_t)sg.A_s;
+    }
+    const int done = min(r + RPI, r1);
+    if (((done - r0) & 63) == 0 || done == r1) {
+        const int first = (done - 1) - ((done - 1 - r0) & 63);
+        tokbuf_flush(a.tok, sg, tb, first, 1, done - first, lane, false, kModeScore);
     }
 }
 
@@ -359,11 +391,12 @@ __device__ __forceinline__ void score_rows(const ScoreArgs& a, const DevSeg& sg,
 {
     constexpr int RPI = NU >= MSAO_ROW_BATCH_UNITS ? 1 : MSAO_ROW_BATCH_UNITS / NU;
     const int voff = lane * 16;
+    TokBuf tb{};
     if constexpr (NU > 4) {
         for (int r = r0; r < r1; ++r) {
             vec4 A[1][NU];
             load_rows<NU, 1>(A, sg, r, r1, voff);
-            rows_batch<DT, NU, 1>(a, sg, A, r, r1, lane, nsp);
+            rows_batch<DT, NU, 1>(a, sg, A, r0, r, r1, lane, nsp, tb);
         }
     } else {
         vec4 A[RPI][NU], B[RPI][NU];
@@ -371,11 +404,11 @@ __device__ __forceinline__ void score_rows(const ScoreArgs& a, const DevSeg& sg,
         int r = r0;
         while (true) {
             if (r + RPI < r1) load_rows<NU, RPI>(B, sg, r + RPI, r1, voff);
-            rows_batch<DT, NU, RPI>(a, sg, A, r, r1, lane, nsp);
+            rows_batch<DT, NU, RPI>(a, sg, A, r0, r, r1, lane, nsp, tb);
             r += RPI;
             if (r >= r1) break;
             if (r + RPI < r1) load_rows<NU, RPI>(A, sg, r + RPI, r1, voff);
-            rows_batch<DT, NU, RPI>(a, sg, B, r, r1, lane, nsp);
+            rows_batch<DT, NU, RPI>(a, sg, B, r0, r, r1, lane, nsp, tb);
             r += RPI;
             if (r >= r1) break;
         }
@@ -392,6 +425,7 @@ __device__ void score_rows_generic(const ScoreArgs& a, const DevSeg& sg, int r0,
     const int nu = (sg.nchunk + kWave - 1) / kWave;
     const int rb = sg.nchunk * 16;
     const bool copy = a.out && sg.copy_in_score;
+    TokBuf tb{};
     for (int r = r0; r < r1; ++r) {
         const rsrc_t rs = make_rsrc(sg.data + (int64_t)r * sg.stride_bytes, rb);
         const rsrc_t rd = make_rsrc(a.out + sg.out_off + (int64_t)r * rb, copy ? rb : 0);
@@ -409,7 +443,9 @@ __device__ void score_rows_generic(const ScoreArgs& a, const DevSeg& sg, int r0,
         }
         s.l1 = wave_sum(s.l1);
         s.l2 = wave_sum(s.l2);
-        emit_token(a.tok, sg, r, lane, s, false, kModeScore);
+        const int slot = (r - r0) & 63;
+        tokbuf_put(tb, slot, lane, s);
+        if (slot == 63 || r == r1 - 1) tokbuf_flush(a.tok, sg, tb, r - slot, 1, slot + 1, lane, false, kModeScore);
         nsp += s.act < (uint32_t)sg.A_s;
     }
 }
@@ -450,6 +486,7 @@ __device__ __forceinline__ void score_chain(const ScoreArgs& a, const DevSeg& sg
     }
     vec4 cur[NU];
     load(cur, t0, true);
+    TokBuf tb{};
     for (int t = t0; t < t1; ++t) {
         vec4 nxt[NU];
         load(nxt, t + 1, t + 1 < t1);
@@ -461,7 +498,10 @@ __device__ __forceinline__ void score_chain(const ScoreArgs& a, const DevSeg& sg
         s.l1 = wave_sum(s.l1);
         s.l2 = wave_sum(s.l2);
         s.res = wave_sum(s.res);
-        emit_token(a.tok, sg, t * sg.P + p, lane, s, true, a.mode);
+        const int slot = (t - t0) & 63;
+        tokbuf_put(tb, slot, lane, s);
+        if (slot == 63 || t == t1 - 1)
+            tokbuf_flush(a.tok, sg, tb, (t - slot) * sg.P + p, sg.P, slot + 1, lane, true, a.mode);
         nsp += s.act < (uint32_t)sg.A_s;
         if (t >= 1) dsum += s.d;
 #pragma unroll
@@ -483,6 +523,7 @@ __device__ void score_chain_generic(const ScoreArgs& a, const DevSeg& sg, int p,
     const int nu = (sg.nchunk + kWave - 1) / kWave;
     const int rb = sg.nchunk * 16;
     const bool copy = a.out && sg.copy_in_score;
+    TokBuf tb{};
     for (int t = t0; t < t1; ++t) {
         const rsrc_t rc = make_rsrc(base + (int64_t)t * fstride, rb);
         const rsrc_t rp = make_rsrc(base + (t > 0 ? (int64_t)(t - 1) * fstride : 0), t > 0 ? rb : 0);
@@ -521,7 +562,10 @@ __device__ void score_chain_generic(const ScoreArgs& a, const DevSeg& sg, int p,
         s.l1 = wave_sum(s.l1);
         s.l2 = wave_sum(s.l2);
         s.res = wave_sum(s.res);
-        emit_token(a.tok, sg, t * sg.P + p, lane, s, true, a.mode);
+        const int slot = (t - t0) & 63;
+        tokbuf_put(tb, slot, lane, s);
+        if (slot == 63 || t == t1 - 1)
+            tokbuf_flush(a.tok, sg, tb, (t - slot) * sg.P + p, sg.P, slot + 1, lane, true, a.mode);
         nsp += s.act < (uint32_t)sg.A_s;
         if (t >= 1) dsum += s.d;
     }
@@ -570,10 +614,22 @@ __device__ __forceinline__ void dispatch_chain(const ScoreArgs& a, const DevSeg&
     }
 }
 
+// Workgroups are dispatched to the eight XCDs in turn (block b to XCD b % 8).
+// With xcd_order set, blocks are renumbered so that each XCD takes one
+// contiguous range of work items: the per-token statistics its wavefronts
+// write then share cache lines only within that XCD's L2.
+__device__ __forceinline__ int score_block(const ScoreArgs& a)
+{
+    const int b = blockIdx.x;
+    if (!a.xcd_order) return b;
+    const int nb = gridDim.x, x = b & 7, per = nb >> 3, rem = nb & 7;
+    return x * per + min(x, rem) + (b >> 3);
+}
+
 __global__ __launch_bounds__(kScoreBlock) void k_score(ScoreArgs a)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int w = uniform(blockIdx.x * (kScoreBlock / kWave) + (threadIdx.x >> 6));
+    const int w = uniform(score_block(a) * (kScoreBlock / kWave) + (threadIdx.x >> 6));
     if (w >= a.t.n_wi) return;
     const int s = uniform(a.t.wi_seg[w]);
     const DevSeg sg = a.t.seg[s];
@@ -613,7 +669,7 @@ __global__ __launch_bounds__(kScoreBlock) void k_score(ScoreArgs a)
 // ---------------------------------------------------------------- k_post
 
 constexpr int kPostWaves = kPostBlock / kWave;
-static_assert(kPostWaves == kNumMod, "the request role gives one wavefront to each modality");
+static_assert(kPostWaves % kNumMod == 0, "the request role splits the wavefronts evenly over the modalities");
 
 constexpr int kRadixBits = 11;
 constexpr int kRadixBins = 1 << kRadixBits;
@@ -624,7 +680,7 @@ struct PostShared {
     uint32_t scan[kPostWaves];
     uint32_t wcnt[kPostWaves][2];
     unsigned long long lo, hi, red;
-    uint64_t nsp[kNumMod], dsum[kNumMod], ntok[kNumMod], qbits[kNumMod];
+    uint64_t nsp[kPostWaves], dsum[kPostWaves], ntok[kNumMod], qbits[kNumMod];
     uint32_t digit, below;
 };
 
@@ -669,18 +725,21 @@ struct RMAgg {
     uint64_t ntok, nsparse, dsum, qbits;
 };
 
-// Eq. 4 and Eq. 5 integer aggregates of request r, all four modalities: each
-// wavefront sums the scoring partials of one modality. Every thread of the
-// block calls this and receives the same values.
+// Eq. 4 and Eq. 5 integer aggregates of request r, all four modalities:
+// wavefront w sums every kParts-th 64-item stripe of the scoring partials of
+// modality w % 4. Every thread of the block calls this and receives the same
+// values.
 __device__ void rm_aggregate_all(const Tables& t, int r, PostShared& sh, RMAgg g[kNumMod])
 {
-    const int m = threadIdx.x >> 6;
+    constexpr int kParts = kPostWaves / kNumMod;
+    const int wid = threadIdx.x >> 6;
+    const int m = wid % kNumMod, part = wid / kNumMod;
     const int lane = threadIdx.x & (kWave - 1);
     const RmEntry e = t.rm[r * kNumMod + m];
     uint64_t nsp = 0, ds = 0;
     for (int j = e.rng_begin; j < e.rng_end; ++j) {
         const WiRange wr = t.rm_rng[j];
-        for (int w = wr.begin + lane; w < wr.end; w += kWave) {
+        for (int w = wr.begin + part * kWave + lane; w < wr.end; w += kParts * kWave) {
             const Partial pr = t.partial[w];
             nsp += pr.nsparse;
             ds += pr.dsum;
@@ -690,18 +749,26 @@ __device__ void rm_aggregate_all(const Tables& t, int r, PostShared& sh, RMAgg g
     ds = wave_sum_u64(ds);
     __syncthreads();
     if (lane == 0) {
-        sh.nsp[m] = nsp;
-        sh.dsum[m] = ds;
-        sh.ntok[m] = e.ntok;
-        sh.qbits[m] = e.qbits;
+        sh.nsp[wid] = nsp;
+        sh.dsum[wid] = ds;
+        if (part == 0) {
+            sh.ntok[m] = e.ntok;
+            sh.qbits[m] = e.qbits;
+        }
     }
     __syncthreads();
 #pragma unroll
     for (int mm = 0; mm < kNumMod; ++mm) {
         g[mm].ntok = sh.ntok[mm];
         g[mm].qbits = sh.qbits[mm];
-        g[mm].nsparse = sh.nsp[mm];
-        g[mm].dsum = sh.dsum[mm];
+        uint64_t a = 0, b = 0;
+#pragma unroll
+        for (int q = 0; q < kParts; ++q) {
+            a += sh.nsp[q * kNumMod + mm];
+            b += sh.dsum[q * kNumMod + mm];
+        }
+        g[mm].nsparse = a;
+        g[mm].dsum = b;
     }
 }
 
@@ -834,6 +901,34 @@ __device__ __forceinline__ uint64_t sel_key(const uint32_t* __restrict__ z, cons
     }
 }
 
+// Keys of tokens [0, N) of a segment staged into LDS (when in_lds) and their
+// range. U tokens per thread are loaded before any is used, so that the
+// global loads of one thread overlap.
+template <int KIND>
+__device__ __forceinline__ void stage_keys(const uint32_t* __restrict__ z, const uint32_t* __restrict__ d, int N,
+                                           uint64_t Ls, uint64_t Lt, uint32_t C, bool in_lds, uint64_t* keys,
+                                           uint64_t& lo, uint64_t& hi)
+{
+    constexpr int U = 4;
+    for (int i0 = threadIdx.x; i0 < N; i0 += U * kPostBlock) {
+        uint64_t kk[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * kPostBlock;
+            kk[u] = i < N ? sel_key(z, d, i, KIND, Ls, Lt, C) : 0ull;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * kPostBlock;
+            if (i < N) {
+                if (in_lds) keys[i] = kk[u];
+                lo = kk[u] < lo ? kk[u] : lo;
+                hi = kk[u] > hi ? kk[u] : hi;
+            }
+        }
+    }
+}
+
 // MAS-guided keep count (Eq. 11 floor): k = min(N, ceil((1 - MAS) * N)) in double.
 __device__ __forceinline__ int guided_keep_count(float mas, int N)
 {
@@ -899,11 +994,11 @@ __device__ void role_select(const PostArgs& a, int s, PostShared& sh, uint64_t* 
     __syncthreads();
     {
         uint64_t lo = ~0ull, hi = 0ull;
-        for (int i = tid; i < N; i += kPostBlock) {
-            const uint64_t key = sel_key(z, d, i, kind, Ls, Lt, C);
-            if (in_lds) keys[i] = key;
-            lo = key < lo ? key : lo;
-            hi = key > hi ? key : hi;
+        switch (kind) {
+        case kKeyZ: stage_keys<kKeyZ>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
+        case kKeyE: stage_keys<kKeyE>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
+        case kKeyFull: stage_keys<kKeyFull>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
+        default: stage_keys<kKeyZero>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
         }
         lo = wave_min_u64(lo);
         hi = wave_max_u64(hi);

@@ -362,17 +362,30 @@ def test_repeat_runs_bitwise_identical(dev):
                 assert np.array_equal(first[k].view(np.uint8), snap[k].view(np.uint8)), (i, k)
 
 
-@pytest.mark.parametrize("row_bytes,chain", [("2048", "4"), ("65536", "32"), ("1", "1")])
-def test_launch_shapes_same_results(row_bytes, chain, dev, monkeypatch):
-    """Different work-item sizes (rows per wavefront, frames per video run)
-    give bit-identical outputs."""
-    segs = make_workload(4, n_requests=2).segments + ADV["video"][:3]
+def _long_runs():
+    """Work items longer than the 64-token store buffer of a wavefront: 16-byte
+    rows (512 rows per 8 KiB item) and a 130-frame clip run as one chain."""
+    rng = np.random.default_rng(99)
+    return [_rand_seg(rng, 0, IMAGE, 1, 300, 8, "bf16", 0.3, "relu_bg"),
+            _rand_seg(rng, 0, TEXT, 1, 200, 24, "f32", 0.5),
+            _rand_seg(rng, 0, VIDEO, 130, 3, 64, "bf16", 0.4, "static_video"),
+            _rand_seg(rng, 1, VIDEO, 70, 2, 4104, "bf16", 0.4)]   # generic chain path
+
+
+@pytest.mark.parametrize("row_bytes,chain,xcd", [("2048", "4", "1"), ("65536", "32", "0"), ("1", "1", "1"),
+                                                 ("8192", "200", "0"), ("8192", "200", "1")])
+def test_launch_shapes_same_results(row_bytes, chain, xcd, dev, monkeypatch):
+    """Different work-item sizes (rows per wavefront, frames per video run) and
+    workgroup orders give the oracle's outputs."""
+    segs = make_workload(4, n_requests=2).segments + ADV["video"][:3] + _long_runs()
     R = 3
-    log(f"[parity] launch shape rows={row_bytes}B chain={chain}")
+    log(f"[parity] launch shape rows={row_bytes}B chain={chain} xcd_order={xcd}")
     monkeypatch.setenv("MSAO_ROW_ITEM_BYTES", row_bytes)
     monkeypatch.setenv("MSAO_CHAIN_FRAMES", chain)
+    monkeypatch.setenv("MSAO_XCD_ORDER", xcd)
     ctx = B.Context(0)
     run_and_compare(segs, R, default_params(), dev, ctx=ctx)
+    run_and_compare(segs, R, default_params(), dev, ctx=ctx, compact=False)
     ctx.close()
 
 
