@@ -129,6 +129,10 @@ constexpr int kScoreBlock = 256;   // 4 wavefronts, one work item each
 #define MSAO_POST_BLOCK 256
 #endif
 constexpr int kPostBlock = MSAO_POST_BLOCK;  // threads per post-scoring block
+#ifndef MSAO_POST_BIG_SEGMENT
+#define MSAO_POST_BIG_SEGMENT 4096
+#endif
+constexpr int kPostBigSegment = MSAO_POST_BIG_SEGMENT;  // larger selections use 1024-thread blocks
 #ifndef MSAO_GATHER_BLOCK
 #define MSAO_GATHER_BLOCK 64
 #endif

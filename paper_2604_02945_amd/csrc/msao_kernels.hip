@@ -668,24 +668,32 @@ __global__ __launch_bounds__(kScoreBlock) void k_score(ScoreArgs a)
 
 // ---------------------------------------------------------------- k_post
 
-constexpr int kPostWaves = kPostBlock / kWave;
-static_assert(kPostWaves % kNumMod == 0, "the request role splits the wavefronts evenly over the modalities");
 
 constexpr int kRadixBits = 11;
 constexpr int kRadixBins = 1 << kRadixBits;
-constexpr int kBinsPerThread = kRadixBins / kPostBlock;
 
+// Shared state of a post-scoring block of NT threads.
+template <int NT>
 struct PostShared {
+    static constexpr int kWaves = NT / kWave;
+    static_assert(kWaves % kNumMod == 0, "the request role splits the wavefronts evenly over the modalities");
+    static_assert(kRadixBins % NT == 0, "every thread owns the same number of radix bins");
     uint32_t hist[kRadixBins];
-    uint32_t scan[kPostWaves];
-    uint32_t wcnt[kPostWaves][2];
+    uint32_t scan[kWaves];
+    uint32_t wcnt[kWaves][2];
     unsigned long long lo, hi, red;
-    uint64_t nsp[kPostWaves], dsum[kPostWaves], ntok[kNumMod], qbits[kNumMod];
-    uint32_t digit, below;
+    uint64_t nsp[kWaves], dsum[kWaves], ntok[kNumMod], qbits[kNumMod];
+    uint32_t digit, below, in_bin, ncand;
 };
 
+// Radix candidates copied out of the staged keys once few remain (LDS entries
+// after the keys).
+constexpr int kMaxCand = 2048;
+__device__ __host__ __forceinline__ int cand_cap_for(int keys_cap) { return keys_cap < kMaxCand ? keys_cap : kMaxCand; }
+
 // Block-wide sum of a 64-bit integer (exact, so the order does not matter).
-__device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, PostShared& sh)
+template <int NT>
+__device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, PostShared<NT>& sh)
 {
     v = wave_sum_u64(v);
     __syncthreads();
@@ -697,7 +705,8 @@ __device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, PostShared& sh)
 }
 
 // Block-wide exclusive scan of 32-bit counts in thread order; *total gets the sum.
-__device__ __forceinline__ uint32_t block_exscan(uint32_t v, PostShared& sh, uint32_t* total)
+template <int NT>
+__device__ __forceinline__ uint32_t block_exscan(uint32_t v, PostShared<NT>& sh, uint32_t* total)
 {
     const int lane = threadIdx.x & (kWave - 1);
     const int wid = threadIdx.x >> 6;
@@ -712,7 +721,7 @@ __device__ __forceinline__ uint32_t block_exscan(uint32_t v, PostShared& sh, uin
     __syncthreads();
     uint32_t before = 0, tot = 0;
 #pragma unroll
-    for (int i = 0; i < kPostWaves; ++i) {
+    for (int i = 0; i < (NT / kWave); ++i) {
         const uint32_t t = sh.scan[i];
         if (i < wid) before += t;
         tot += t;
@@ -729,9 +738,10 @@ struct RMAgg {
 // wavefront w sums every kParts-th 64-item stripe of the scoring partials of
 // modality w % 4. Every thread of the block calls this and receives the same
 // values.
-__device__ void rm_aggregate_all(const Tables& t, int r, PostShared& sh, RMAgg g[kNumMod])
+template <int NT>
+__device__ void rm_aggregate_all(const Tables& t, int r, PostShared<NT>& sh, RMAgg g[kNumMod])
 {
-    constexpr int kParts = kPostWaves / kNumMod;
+    constexpr int kParts = (NT / kWave) / kNumMod;
     const int wid = threadIdx.x >> 6;
     const int m = wid % kNumMod, part = wid / kNumMod;
     const int lane = threadIdx.x & (kWave - 1);
@@ -832,7 +842,8 @@ __device__ void request_terms(const Tables& t, int r, const RMAgg g[kNumMod], Ma
     }
 }
 
-__device__ void role_request(const PostArgs& a, int r, PostShared& sh)
+template <int NT>
+__device__ void role_request(const PostArgs& a, int r, PostShared<NT>& sh)
 {
     const Tables& t = a.t;
     RMAgg g[kNumMod];
@@ -863,7 +874,8 @@ __device__ void role_request(const PostArgs& a, int r, PostShared& sh)
 }
 
 // Eq. 5 for one frame of a temporal segment: D_t = sum of d over its tokens.
-__device__ void role_frame(const PostArgs& a, int f, PostShared& sh)
+template <int NT>
+__device__ void role_frame(const PostArgs& a, int f, PostShared<NT>& sh)
 {
     const Tables& t = a.t;
     int lo = 0, hi = t.n_tseg;
@@ -903,23 +915,21 @@ __device__ __forceinline__ uint64_t sel_key(const uint32_t* __restrict__ z, cons
 
 // Keys of tokens [0, N) of a segment staged into LDS (when in_lds) and their
 // range. U tokens per thread are loaded before any is used, so that the
-// global loads of one thread overlap.
-template <int KIND>
+// global loads of one thread overlap; indices past N are clamped (and their
+// keys dropped) so that no load sits behind a branch.
+template <int NT, int KIND>
 __device__ __forceinline__ void stage_keys(const uint32_t* __restrict__ z, const uint32_t* __restrict__ d, int N,
                                            uint64_t Ls, uint64_t Lt, uint32_t C, bool in_lds, uint64_t* keys,
                                            uint64_t& lo, uint64_t& hi)
 {
-    constexpr int U = 4;
-    for (int i0 = threadIdx.x; i0 < N; i0 += U * kPostBlock) {
+    constexpr int U = 8;
+    for (int i0 = threadIdx.x; i0 < N; i0 += U * NT) {
         uint64_t kk[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int i = i0 + u * kPostBlock;
-            kk[u] = i < N ? sel_key(z, d, i, KIND, Ls, Lt, C) : 0ull;
-        }
+        for (int u = 0; u < U; ++u) kk[u] = sel_key(z, d, min(i0 + u * NT, N - 1), KIND, Ls, Lt, C);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int i = i0 + u * kPostBlock;
+            const int i = i0 + u * NT;
             if (i < N) {
                 if (in_lds) keys[i] = kk[u];
                 lo = kk[u] < lo ? kk[u] : lo;
@@ -939,12 +949,167 @@ __device__ __forceinline__ int guided_keep_count(float mas, int N)
     return (int)kk;
 }
 
+// Where the selection keys are read from: staged in LDS, or recomputed from
+// z and d for segments larger than the LDS staging area.
+struct KeySrc {
+    const uint64_t* keys;
+    const uint32_t* z;
+    const uint32_t* d;
+    int kind;
+    uint64_t Ls, Lt;
+    uint32_t C;
+    template <bool IN_LDS>
+    __device__ __forceinline__ uint64_t at(int i) const
+    {
+        if constexpr (IN_LDS) return keys[i];
+        else return sel_key(z, d, i, kind, Ls, Lt, C);
+    }
+};
+
+// Rank k-1 of the segment's keys (range [lo, hi]) by MSD radix select, then
+// keep flags and ascending kept indices. IN_LDS: every key is staged in LDS.
+template <int NT, bool IN_LDS>
+__device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const KeySrc& src, uint64_t* cand,
+                                   int cand_cap, int N, int k, int off, uint64_t lo, uint64_t hi)
+{
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid >> 6;
+    auto key_at = [&](int i) -> uint64_t { return src.at<IN_LDS>(i); };
+    // radix select of the key of rank k-1 among key - lo, most significant digit
+    // first. Once the candidate range holds at most cand_cap keys, the next
+    // pass also copies them to cand[] and later passes read only those.
+    int ncand = -1;                // -1: passes read every key
+    uint32_t in_range = (uint32_t)N;
+    uint64_t prefix = 0;
+    uint32_t below = 0;            // keys below the current candidate range
+    uint32_t rank = (uint32_t)k - 1;
+    int bits = hi > lo ? 64 - __clzll((long long)(hi - lo)) : 0;
+    while (bits > 0) {
+        const int db = bits < kRadixBits ? bits : kRadixBits;
+        const int shift = bits - db;
+        const uint64_t mask = (1ull << db) - 1ull;
+        // copy out the candidates once they are few (and fewer than half the keys)
+        const bool collect = ncand < 0 && in_range <= (uint32_t)cand_cap && 2 * in_range < (uint32_t)N;
+        for (int b = tid; b < kRadixBins; b += NT) sh.hist[b] = 0u;
+        if (tid == 0) sh.ncand = 0u;
+        __syncthreads();
+        // wave-uniform loop over the keys (or candidates), U x 64 per step
+        constexpr int U = 4;
+        const int nscan = ncand >= 0 ? ncand : N;
+        for (int base = wid * kWave; base < nscan; base += U * NT) {
+            uint64_t x[U];
+            // clamped indices: every load is issued before any is used
+            if (ncand >= 0) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) x[u] = cand[min(base + u * NT + lane, nscan - 1)];
+            } else {
+#pragma unroll
+                for (int u = 0; u < U; ++u) x[u] = key_at(min(base + u * NT + lane, N - 1)) - lo;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const bool match = base + u * NT + lane < nscan &&
+                                   (bits >= 64 ? 0ull : (x[u] >> bits)) == prefix;
+                if (match) atomicAdd(&sh.hist[(x[u] >> shift) & mask], 1u);
+                if (collect) {
+                    const uint64_t m = __ballot(match);
+                    if (m) {
+                        uint32_t at = 0;
+                        if (lane == 0) at = atomicAdd(&sh.ncand, (uint32_t)__popcll(m));
+                        at = (uint32_t)__shfl((int)at, 0);
+                        if (match) cand[at + lanes_below(m)] = x[u];
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        if (collect) ncand = (int)sh.ncand;
+        uint32_t local = 0;
+#pragma unroll
+        for (int j = 0; j < (kRadixBins / NT); ++j) local += sh.hist[tid * (kRadixBins / NT) + j];
+        uint32_t tot;
+        const uint32_t ex = block_exscan(local, sh, &tot);
+        if (ex <= rank && rank < ex + local) {
+            uint32_t cum = ex;
+            for (int j = 0; j < (kRadixBins / NT); ++j) {
+                const uint32_t h = sh.hist[tid * (kRadixBins / NT) + j];
+                if (rank < cum + h) {
+                    sh.digit = (uint32_t)(tid * (kRadixBins / NT) + j);
+                    sh.below = cum;
+                    sh.in_bin = h;
+                    break;
+                }
+                cum += h;
+            }
+        }
+        __syncthreads();
+        const uint32_t dg = sh.digit, bl = sh.below;
+        in_range = sh.in_bin;
+        below += bl;
+        rank -= bl;
+        prefix = (prefix << db) | dg;
+        bits = shift;
+        __syncthreads();
+    }
+    const uint64_t vstar = lo + prefix;        // key of rank k-1
+    const uint32_t ties = (uint32_t)k - below; // keys equal to vstar that are kept, lowest index first
+
+    // each wavefront compacts one contiguous range of indices, 4 x 64 at a time
+    constexpr int U = 4;
+    const int per = (((N + (NT / kWave) - 1) / (NT / kWave)) + kWave - 1) / kWave * kWave;
+    const int b0 = min(N, wid * per), b1 = min(N, b0 + per);
+    uint32_t nlt = 0, neq = 0;
+    for (int base = b0; base < b1; base += U * kWave) {
+        uint64_t kv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) kv[u] = key_at(min(base + u * kWave + lane, b1 - 1));
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const bool v = base + u * kWave + lane < b1;
+            nlt += (uint32_t)__popcll(__ballot(v && kv[u] < vstar));
+            neq += (uint32_t)__popcll(__ballot(v && kv[u] == vstar));
+        }
+    }
+    if (lane == 0) {
+        sh.wcnt[wid][0] = nlt;
+        sh.wcnt[wid][1] = neq;
+    }
+    __syncthreads();
+    uint32_t lt_before = 0, eq_before = 0;
+    for (int q = 0; q < wid; ++q) {
+        lt_before += sh.wcnt[q][0];
+        eq_before += sh.wcnt[q][1];
+    }
+    uint32_t eq_run = eq_before;
+    uint32_t kept_run = lt_before + min(eq_before, ties);
+    for (int base = b0; base < b1; base += U * kWave) {
+        uint64_t kv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) kv[u] = key_at(min(base + u * kWave + lane, b1 - 1));
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = base + u * kWave + lane;
+            const bool v = i < b1;
+            const bool isl = v && kv[u] < vstar;
+            const bool ise = v && kv[u] == vstar;
+            const uint64_t me = __ballot(ise);
+            const bool kp = isl || (ise && eq_run + lanes_below(me) < ties);
+            const uint64_t mk = __ballot(kp);
+            if (v && a.sel.keep) a.sel.keep[off + i] = kp ? 1 : 0;
+            if (kp) a.sel.kept_idx[off + (int)(kept_run + lanes_below(mk))] = i;
+            eq_run += (uint32_t)__popcll(me);
+            kept_run += (uint32_t)__popcll(mk);
+        }
+    }
+    for (int i = k + tid; i < N; i += NT) a.sel.kept_idx[off + i] = -1;
+}
+
 // Top-k of one segment: the k smallest (key, index) pairs, kept indices
 // ascending (Sec. 4.1.1 pruning, k from the Eq. 11 floor or a fixed ratio).
 // Keys are staged in LDS when the segment fits (keys_cap entries), then an
 // MSD radix select finds the key of rank k-1 and each wavefront compacts a
 // contiguous index range with ballot/mbcnt.
-__device__ void role_select(const PostArgs& a, int s, PostShared& sh, uint64_t* keys, int keys_cap)
+template <int NT>
+__device__ void role_select(const PostArgs& a, int s, PostShared<NT>& sh, uint64_t* keys, int keys_cap)
 {
     const Tables& t = a.t;
     const DevSeg sg = t.seg[s];
@@ -972,7 +1137,7 @@ __device__ void role_select(const PostArgs& a, int s, PostShared& sh, uint64_t* 
     const int off = sg.tok_off;
     if (N == 0) return;
     if (k == 0 || k == N) {
-        for (int i = tid; i < N; i += kPostBlock) {
+        for (int i = tid; i < N; i += NT) {
             if (a.sel.keep) a.sel.keep[off + i] = k == N ? 1 : 0;
             a.sel.kept_idx[off + i] = k == N ? i : -1;
         }
@@ -984,7 +1149,6 @@ __device__ void role_select(const PostArgs& a, int s, PostShared& sh, uint64_t* 
     const uint32_t* z = a.z + off;
     const uint32_t* d = a.d ? a.d + off : nullptr;
     const bool in_lds = N <= keys_cap;
-    auto key_at = [&](int i) -> uint64_t { return in_lds ? keys[i] : sel_key(z, d, i, kind, Ls, Lt, C); };
 
     // keys (staged in LDS) and their range
     if (tid == 0) {
@@ -995,10 +1159,10 @@ __device__ void role_select(const PostArgs& a, int s, PostShared& sh, uint64_t* 
     {
         uint64_t lo = ~0ull, hi = 0ull;
         switch (kind) {
-        case kKeyZ: stage_keys<kKeyZ>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
-        case kKeyE: stage_keys<kKeyE>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
-        case kKeyFull: stage_keys<kKeyFull>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
-        default: stage_keys<kKeyZero>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
+        case kKeyZ: stage_keys<NT, kKeyZ>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
+        case kKeyE: stage_keys<NT, kKeyE>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
+        case kKeyFull: stage_keys<NT, kKeyFull>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
+        default: stage_keys<NT, kKeyZero>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
         }
         lo = wave_min_u64(lo);
         hi = wave_max_u64(hi);
@@ -1010,93 +1174,16 @@ __device__ void role_select(const PostArgs& a, int s, PostShared& sh, uint64_t* 
     __syncthreads();
     const uint64_t lo = sh.lo, hi = sh.hi;
 
-    // radix select of the key of rank k-1 among key - lo, most significant digit first
-    uint64_t prefix = 0;
-    uint32_t below = 0;            // keys below the current candidate range
-    uint32_t rank = (uint32_t)k - 1;
-    int bits = hi > lo ? 64 - __clzll((long long)(hi - lo)) : 0;
-    while (bits > 0) {
-        const int db = bits < kRadixBits ? bits : kRadixBits;
-        const int shift = bits - db;
-        const uint64_t mask = (1ull << db) - 1ull;
-        for (int b = tid; b < kRadixBins; b += kPostBlock) sh.hist[b] = 0u;
-        __syncthreads();
-        for (int i = tid; i < N; i += kPostBlock) {
-            const uint64_t x = key_at(i) - lo;
-            if ((bits >= 64 ? 0ull : (x >> bits)) == prefix) atomicAdd(&sh.hist[(x >> shift) & mask], 1u);
-        }
-        __syncthreads();
-        uint32_t local = 0;
-#pragma unroll
-        for (int j = 0; j < kBinsPerThread; ++j) local += sh.hist[tid * kBinsPerThread + j];
-        uint32_t tot;
-        const uint32_t ex = block_exscan(local, sh, &tot);
-        if (ex <= rank && rank < ex + local) {
-            uint32_t cum = ex;
-            for (int j = 0; j < kBinsPerThread; ++j) {
-                const uint32_t h = sh.hist[tid * kBinsPerThread + j];
-                if (rank < cum + h) {
-                    sh.digit = (uint32_t)(tid * kBinsPerThread + j);
-                    sh.below = cum;
-                    break;
-                }
-                cum += h;
-            }
-        }
-        __syncthreads();
-        const uint32_t dg = sh.digit, bl = sh.below;
-        below += bl;
-        rank -= bl;
-        prefix = (prefix << db) | dg;
-        bits = shift;
-        __syncthreads();
-    }
-    const uint64_t vstar = lo + prefix;        // key of rank k-1
-    const uint32_t ties = (uint32_t)k - below; // keys equal to vstar that are kept, lowest index first
-
-    // each wavefront compacts one contiguous range of indices
-    const int per = (((N + kPostWaves - 1) / kPostWaves) + kWave - 1) / kWave * kWave;
-    const int b0 = min(N, wid * per), b1 = min(N, b0 + per);
-    uint32_t nlt = 0, neq = 0;
-    for (int base = b0; base < b1; base += kWave) {
-        const int i = base + lane;
-        const bool v = i < b1;
-        const uint64_t key = v ? key_at(i) : 0ull;
-        nlt += (uint32_t)__popcll(__ballot(v && key < vstar));
-        neq += (uint32_t)__popcll(__ballot(v && key == vstar));
-    }
-    if (lane == 0) {
-        sh.wcnt[wid][0] = nlt;
-        sh.wcnt[wid][1] = neq;
-    }
-    __syncthreads();
-    uint32_t lt_before = 0, eq_before = 0;
-    for (int q = 0; q < wid; ++q) {
-        lt_before += sh.wcnt[q][0];
-        eq_before += sh.wcnt[q][1];
-    }
-    uint32_t eq_run = eq_before;
-    uint32_t kept_run = lt_before + min(eq_before, ties);
-    for (int base = b0; base < b1; base += kWave) {
-        const int i = base + lane;
-        const bool v = i < b1;
-        const uint64_t key = v ? key_at(i) : 0ull;
-        const bool isl = v && key < vstar;
-        const bool ise = v && key == vstar;
-        const uint64_t me = __ballot(ise);
-        const bool kp = isl || (ise && eq_run + lanes_below(me) < ties);
-        const uint64_t mk = __ballot(kp);
-        if (v && a.sel.keep) a.sel.keep[off + i] = kp ? 1 : 0;
-        if (kp) a.sel.kept_idx[off + (int)(kept_run + lanes_below(mk))] = i;
-        eq_run += (uint32_t)__popcll(me);
-        kept_run += (uint32_t)__popcll(mk);
-    }
-    for (int i = k + tid; i < N; i += kPostBlock) a.sel.kept_idx[off + i] = -1;
+    const KeySrc src{keys, z, d, kind, Ls, Lt, C};
+    uint64_t* cand = keys + keys_cap;
+    if (in_lds) select_and_compact<NT, true>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, lo, hi);
+    else select_and_compact<NT, false>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, lo, hi);
 }
 
-__global__ __launch_bounds__(kPostBlock) void k_post(PostArgs a)
+template <int NT>
+__global__ __launch_bounds__(NT) void k_post(PostArgs a)
 {
-    __shared__ PostShared sh;
+    __shared__ PostShared<NT> sh;
     extern __shared__ uint64_t keys[];
     // selection blocks first: they are the longest and are dispatched first
     int b = blockIdx.x;
@@ -1220,16 +1307,27 @@ int launch_score(const ScoreArgs& a, void* stream, void* ev0, void* ev1)
     return launch(k_score, dim3(grid), dim3(kScoreBlock), 0, stream, a, ev0, ev1);
 }
 
+template <int NT>
+static int launch_post_nt(const PostArgs& a, int blocks, size_t lds, void* stream, void* ev0, void* ev1)
+{
+    if (lds > 65536) {
+        const hipError_t e = hipFuncSetAttribute((const void*)k_post<NT>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return (int)e;
+    }
+    return launch(k_post<NT>, dim3((unsigned)blocks), dim3(NT), lds, stream, a, ev0, ev1);
+}
+
+// Segments of kPostBigSegment tokens or more are selected by 1024-thread
+// blocks (their loops are latency-bound with one wavefront per SIMD);
+// otherwise kPostBlock threads, which leave room for the scoring of other
+// batches in flight.
 int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1)
 {
     const int blocks = a.n_req_blocks + a.n_frame_blocks + a.n_sel_blocks;
     if (blocks <= 0) return 0;
-    const size_t lds = (size_t)a.keys_cap * sizeof(uint64_t);
-    if (lds > 65536) {
-        const hipError_t e = hipFuncSetAttribute((const void*)k_post, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return (int)e;
-    }
-    return launch(k_post, dim3((unsigned)blocks), dim3(kPostBlock), lds, stream, a, ev0, ev1);
+    const size_t lds = (size_t)(a.keys_cap + cand_cap_for(a.keys_cap)) * sizeof(uint64_t);
+    if (a.n_sel_blocks > 0 && a.keys_cap >= kPostBigSegment) return launch_post_nt<1024>(a, blocks, lds, stream, ev0, ev1);
+    return launch_post_nt<kPostBlock>(a, blocks, lds, stream, ev0, ev1);
 }
 
 int launch_gather(const GatherArgs& a, void* stream, void* ev0, void* ev1)

@@ -389,6 +389,18 @@ def test_launch_shapes_same_results(row_bytes, chain, xcd, dev, monkeypatch):
     ctx.close()
 
 
+def test_selection_beyond_lds_staging(dev):
+    """Segments of more than 16,384 tokens: their selection keys do not fit the
+    LDS staging area and are recomputed from z and d on every pass."""
+    rng = np.random.default_rng(123)
+    segs = [_rand_seg(rng, 0, IMAGE, 1, 20000, 16, "bf16", 0.3, "relu_bg"),
+            _rand_seg(rng, 0, VIDEO, 80, 300, 64, "bf16", 0.4, "static_video"),
+            _rand_seg(rng, 1, AUDIO, 1, 17000, 8, "bf16", -1.0, "relu_bg"),
+            _rand_seg(rng, 1, TEXT, 1, 300, 64, "f32", 0.5)]
+    log("[parity] selection of segments larger than the LDS key staging")
+    run_and_compare(segs, 2, default_params(), dev)
+
+
 def test_plan_runs_match_oracle(dev):
     """msao_plan_create once, msao_plan_run several times (data rewritten in
     place between runs): every run matches the oracle on that run's data."""
