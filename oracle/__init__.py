@@ -1,4 +1,6 @@
-"""ctypes wrapper of the plain CPU oracle (msao_oracle.c).
+"""ctypes wrapper of the plain CPU oracle (msao_oracle.c: the sparsity
+analysis of Sec. 4.1 and the selection it drives; msao_oracle_decode.c: the
+decoding-side quantities of Sec. 4.2 and Algorithm 1).
 
 TEST INFRASTRUCTURE ONLY: the oracle is the reference the GPU path is checked
 against. Only the test suite, the smoke check and the benchmark's CPU-baseline
@@ -18,6 +20,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "msao_oracle.c")
+_SRC_DECODE = os.path.join(_HERE, "msao_oracle_decode.c")
 _LIB = os.path.join(_HERE, "libmsao_oracle.so")
 
 NMOD = 4
@@ -30,7 +33,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + f".tmp{os.getpid()}"
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-ffp-contract=off",
-                               "-fPIC", "-shared", "-o", tmp, _SRC, "-lm"])
+                               "-fPIC", "-shared", "-o", tmp, _SRC, _SRC_DECODE, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -86,6 +89,29 @@ def lib():
         L.orc_keep_count.restype = ctypes.c_int64
         L.orc_q24.argtypes = [ctypes.c_float]
         L.orc_q24.restype = ctypes.c_uint64
+        D, I64, I = ctypes.c_double, ctypes.c_int64, ctypes.c_int
+        L.orc_entropy_rows.argtypes = [_P, I64, I64, I64, I, _P, _P]
+        L.orc_entropy_rows.restype = None
+        L.orc_entropy_normalized.argtypes = [D, I64]
+        L.orc_entropy_normalized.restype = D
+        L.orc_speculate.argtypes = [D, D]
+        L.orc_speculate.restype = I
+        L.orc_comm_latency.argtypes = [D, D, D]
+        L.orc_comm_latency.restype = D
+        L.orc_p_conf.argtypes = [_P, I64, D]
+        L.orc_p_conf.restype = D
+        L.orc_expected_spec.argtypes = [D]
+        L.orc_expected_spec.restype = D
+        L.orc_expected_e2e.argtypes = [D, D, D, D, I, D, D, D]
+        L.orc_expected_e2e.restype = D
+        L.orc_entropy_quantile.argtypes = [_P, I64, D]
+        L.orc_entropy_quantile.restype = D
+        L.orc_n_draft.argtypes = [D, D, I]
+        L.orc_n_draft.restype = I
+        L.orc_retention.argtypes = [_P, I, _P]
+        L.orc_retention.restype = None
+        L.orc_sched_run.argtypes = [_P, I64, D, I, D, D, D, _P, _P, _P]
+        L.orc_sched_run.restype = None
         _lib = L
     return _lib
 
@@ -255,3 +281,74 @@ def keep_count(kappa: float, N: int) -> int:
 
 def q24(lam: float) -> int:
     return int(lib().orc_q24(lam))
+
+
+# ---- Sec. 4.2: draft confidence and Algorithm 1 -------------------------------
+
+HOLD, SEND, OFFLOAD = 0, 1, 2
+
+
+def entropy_rows(logits: np.ndarray, dtype: str = "f32", vocab: Optional[int] = None):
+    """Eq. 9 per row of a [rows, row_stride] array (float32, or bf16 bit
+    patterns as uint16): entropy in nats (float64) and the arg max."""
+    a = np.ascontiguousarray(logits)
+    rows, stride = a.shape
+    V = stride if vocab is None else vocab
+    H = np.zeros(rows, np.float64)
+    am = np.zeros(rows, np.int32)
+    lib().orc_entropy_rows(_ptr(a), rows, V, stride, F32 if dtype == "f32" else BF16, _ptr(H), _ptr(am))
+    return H, am
+
+
+def entropy_normalized(H: float, vocab: int) -> float:
+    return lib().orc_entropy_normalized(H, vocab)
+
+
+def speculate(h_norm: float, theta: float) -> bool:
+    return bool(lib().orc_speculate(h_norm, theta))
+
+
+def comm_latency(data_bytes: float, bandwidth_bytes_per_s: float, rtt_s: float) -> float:
+    return lib().orc_comm_latency(data_bytes, bandwidth_bytes_per_s, rtt_s)
+
+
+def p_conf(h: np.ndarray, theta: float) -> float:
+    a = np.ascontiguousarray(h, dtype=np.float64)
+    return lib().orc_p_conf(_ptr(a), a.size, theta)
+
+
+def expected_spec(p: float) -> float:
+    return lib().orc_expected_spec(p)
+
+
+def expected_e2e(prefill_edge, prefill_cloud, comm_offloaded, p, n_draft, t_draft, t_verify, t_offload) -> float:
+    return lib().orc_expected_e2e(prefill_edge, prefill_cloud, comm_offloaded, p, int(n_draft), t_draft,
+                                  t_verify, t_offload)
+
+
+def entropy_quantile(h: np.ndarray, q: float) -> float:
+    a = np.ascontiguousarray(h, dtype=np.float64)
+    return lib().orc_entropy_quantile(_ptr(a), a.size, q)
+
+
+def n_draft(p: float, p_target: float, n_max: int) -> int:
+    return int(lib().orc_n_draft(p, p_target, n_max))
+
+
+def retention(mas: Sequence[float]) -> np.ndarray:
+    a = np.ascontiguousarray(mas, dtype=np.float64)
+    b = np.zeros_like(a)
+    lib().orc_retention(_ptr(a), a.size, _ptr(b))
+    return b
+
+
+def sched_run(h_norm: np.ndarray, theta0: float, n_draft: int, delta: float, theta_min: float, alpha: float):
+    """Algorithm 1, per-step loop: decisions (HOLD/SEND/OFFLOAD), threshold
+    after every step, and counts (held, sends, offloads, tokens sent)."""
+    h = np.ascontiguousarray(h_norm, dtype=np.float64)
+    dec = np.zeros(h.size, np.int8)
+    th = np.zeros(h.size, np.float64)
+    cnt = np.zeros(4, np.int64)
+    lib().orc_sched_run(_ptr(h), h.size, theta0, int(n_draft), delta, theta_min, alpha, _ptr(dec), _ptr(th),
+                        _ptr(cnt))
+    return dec, th, cnt
