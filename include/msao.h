@@ -240,13 +240,114 @@ msao_status msao_plan_run(msao_plan* plan, const msao_token_out* tok, const msao
 /* Free a plan (NULL is ignored); the caller must have synchronised its runs. */
 void msao_plan_destroy(msao_plan* plan);
 
+/* ---- Sec. 4.2: the draft model's confidence ------------------------------- */
+
+/* Outputs of msao_draft_entropy, each [rows] device memory or NULL (not
+ * written). entropy: Eq. 9 in nats, H = -sum_v p_v ln p_v with p the softmax
+ * of the row's logits. entropy_norm: H / ln(vocab), in [0, 1] (the scale of
+ * the confidence threshold). draft_token: the greedy draft token, the index
+ * of the largest logit (the first of equal maxima). speculate: Eq. 10,
+ * 1 if entropy_norm <= theta else 0. */
+typedef struct {
+    float* entropy;
+    float* entropy_norm;
+    int32_t* draft_token;
+    uint8_t* speculate;
+} msao_entropy_out;
+
+/* Eq. 9-10 for `rows` rows of draft-model logits (Sec. 4.2.1: confidence of
+ * the draft model at each generation step). logits: device, row r starts at
+ * element r * row_stride, `vocab` logits per row, dtype MSAO_F32 or
+ * MSAO_BF16; 16-byte aligned, row_stride * element size a multiple of 16,
+ * row_stride >= vocab, 2 <= vocab, vocab * element size < 2^31 - 2^20,
+ * rows < 2^31. Logits may be -inf (probability 0); a row with a NaN or +inf
+ * logit, or with no finite one, gets a NaN entropy. theta: the confidence
+ * threshold on entropy_norm (finite). Errors: MSAO_ERR_INVALID_ARG,
+ * MSAO_ERR_ALIGNMENT, MSAO_ERR_HIP; nothing is written on a validation error.
+ * Enqueued on `stream`; outputs are valid after the caller synchronises. */
+msao_status msao_draft_entropy(msao_ctx* ctx, const void* logits, int64_t rows, int64_t vocab, int64_t row_stride,
+                               int dtype, float theta, const msao_entropy_out* out, void* stream);
+
+/* ---- Sec. 4.2.2: Algorithm 1 on the host ----------------------------------- */
+
+/* Parameters of Algorithm 1 (defaults from Sec. 5.1: P_target 0.8, N_max 5,
+ * the 70th percentile of the calibration entropies as the initial threshold,
+ * decay delta 0.95; theta_min and the EMA weight alpha are not given by the
+ * paper: 0.05 and 0.1). */
+typedef struct {
+    double p_target;   /* target acceptance probability (line 3) */
+    int32_t n_max;     /* longest draft (line 3) */
+    double quantile;   /* quantile of the calibration entropies giving theta (line 2) */
+    double delta;      /* threshold decay on an offload (line 11) */
+    double theta_min;  /* floor of the decayed threshold (line 11) */
+    double alpha;      /* EMA weight of a verified cache's mean entropy (line 8) */
+} msao_sched_params;
+
+/* Per-request state of the per-step loop. */
+typedef struct {
+    double theta;        /* confidence threshold on normalised entropy */
+    double p_conf;       /* Eq. 12 of the calibration set at the initial threshold */
+    int32_t n_draft;     /* draft length from line 3 */
+    int32_t cache;       /* drafted tokens held on the edge, not yet sent */
+    double cache_h;      /* sum of their normalised entropies */
+    int64_t steps, held, sends, offloads, tokens_sent;
+} msao_sched_state;
+
+#define MSAO_DECIDE_HOLD 0     /* confident: the draft token joins the cache */
+#define MSAO_DECIDE_SEND 1     /* confident and the cache reached n_draft: send it for verification */
+#define MSAO_DECIDE_OFFLOAD 2  /* not confident: offload the intermediate state */
+
+msao_sched_params msao_sched_default_params(void);
+/* Lines 2-3: theta = lower empirical quantile sorted[ceil(q n) - 1] of the
+ * host calibration entropies (normalised, [n], n >= 1, finite); p_conf = Eq.
+ * 12 at that theta; n_draft = min(floor(log(1 - P_target) / log p_conf),
+ * N_max), at least 1 (N_max when p_conf = 1). Resets the per-step state.
+ * MSAO_ERR_INVALID_ARG on NULL pointers, n < 1, non-finite entropies or
+ * parameters outside their ranges (0 < p_target < 1, n_max >= 1, 0 <= q <= 1,
+ * 0 < delta <= 1, theta_min >= 0, 0 <= alpha <= 1). */
+msao_status msao_sched_init(const float* calib_h_norm, int64_t n, const msao_sched_params* params,
+                            msao_sched_state* state);
+/* Lines 5-11 for one step with normalised entropy h_norm (from
+ * msao_draft_entropy): h_norm <= theta adds the token to the cache, and once
+ * the cache holds n_draft tokens they are sent (decision SEND) and theta
+ * moves to (1 - alpha) theta + alpha * (their mean entropy); otherwise
+ * (HOLD). h_norm > theta (or NaN) offloads: the cache travels with the
+ * offloaded state and theta = max(theta * delta, theta_min). */
+msao_status msao_sched_step(msao_sched_state* state, const msao_sched_params* params, float h_norm,
+                            int32_t* decision);
+/* msao_sched_step over `steps` host entropies; decisions and theta_after
+ * ([steps], host) may be NULL. */
+msao_status msao_sched_run(msao_sched_state* state, const msao_sched_params* params, const float* h_norm,
+                           int64_t steps, int8_t* decisions, double* theta_after);
+/* Line 1 at the floor of Eq. 11: beta_m = 1 - MAS_m (host arrays [n]). */
+msao_status msao_retention_floor(const float* mas, int n, float* beta);
+/* Eq. 8: data_bytes / bandwidth + rtt (seconds; bandwidth in bytes/s). */
+double msao_comm_latency(double data_bytes, double bandwidth_bytes_per_s, double rtt_s);
+/* Eq. 12: fraction of the n host entropies that are <= theta (0 if n < 1). */
+double msao_p_conf(const float* h_norm, int64_t n, double theta);
+/* Eq. 13: 1 / (1 - p_conf), +inf at p_conf >= 1. */
+double msao_expected_spec_tokens(double p_conf);
+
+/* Terms of Eq. 14 (seconds). comm_offloaded: sum of Eq. 8 over the
+ * offloaded modalities. */
+typedef struct {
+    double prefill_edge, prefill_cloud, comm_offloaded;
+    double p_conf;
+    int32_t n_draft;
+    double t_draft, t_verify, t_offload;  /* per draft token, per verified token, per offload */
+} msao_latency_model;
+/* Eq. 14: max(prefill_edge, prefill_cloud + comm_offloaded)
+ *   + E[N_spec] (n_draft t_draft + p_conf n_draft t_verify) + (1 - p_conf) t_offload. */
+double msao_expected_e2e_latency(const msao_latency_model* m);
+
 /* ---- profiling ----------------------------------------------------------- */
 
-/* Kernels of the hot path, for msao_kernel_times. */
+/* Kernels of the library, for msao_kernel_times. */
 #define MSAO_KERNEL_SCORE 0   /* per-token statistics and temporal term */
 #define MSAO_KERNEL_POST 1    /* aggregation, MAS, per-frame terms, selection */
 #define MSAO_KERNEL_GATHER 2  /* compaction */
-#define MSAO_NUM_KERNELS 3
+#define MSAO_KERNEL_ENTROPY 3 /* draft confidence */
+#define MSAO_NUM_KERNELS 4
 
 /* When enabled, every launch is bracketed by a pair of HIP events recorded on
  * the caller's stream. */

@@ -21,7 +21,8 @@ NMOD = 4
 TEXT, IMAGE, VIDEO, AUDIO = 0, 1, 2, 3
 F32, BF16 = 0, 1
 FLAG_TEMPORAL_LITERAL = 1
-KERNEL_SCORE, KERNEL_POST, KERNEL_GATHER, NUM_KERNELS = 0, 1, 2, 3
+KERNEL_SCORE, KERNEL_POST, KERNEL_GATHER, KERNEL_ENTROPY, NUM_KERNELS = 0, 1, 2, 3, 4
+DECIDE_HOLD, DECIDE_SEND, DECIDE_OFFLOAD = 0, 1, 2
 
 STATUS = {0: "MSAO_OK", 1: "MSAO_ERR_INVALID_ARG", 2: "MSAO_ERR_ALIGNMENT", 3: "MSAO_ERR_WORKSPACE",
           4: "MSAO_ERR_UNSUPPORTED", 5: "MSAO_ERR_HIP"}
@@ -56,6 +57,28 @@ class MsaoReqOut(ctypes.Structure):
 
 class MsaoSelectOut(ctypes.Structure):
     _fields_ = [(n, _P) for n in ("keep", "kept_idx", "kept_count")]
+
+
+class MsaoEntropyOut(ctypes.Structure):
+    _fields_ = [(n, _P) for n in ("entropy", "entropy_norm", "draft_token", "speculate")]
+
+
+class MsaoSchedParams(ctypes.Structure):
+    _fields_ = [("p_target", ctypes.c_double), ("n_max", ctypes.c_int32), ("quantile", ctypes.c_double),
+                ("delta", ctypes.c_double), ("theta_min", ctypes.c_double), ("alpha", ctypes.c_double)]
+
+
+class MsaoSchedState(ctypes.Structure):
+    _fields_ = [("theta", ctypes.c_double), ("p_conf", ctypes.c_double), ("n_draft", ctypes.c_int32),
+                ("cache", ctypes.c_int32), ("cache_h", ctypes.c_double), ("steps", ctypes.c_int64),
+                ("held", ctypes.c_int64), ("sends", ctypes.c_int64), ("offloads", ctypes.c_int64),
+                ("tokens_sent", ctypes.c_int64)]
+
+
+class MsaoLatencyModel(ctypes.Structure):
+    _fields_ = [("prefill_edge", ctypes.c_double), ("prefill_cloud", ctypes.c_double),
+                ("comm_offloaded", ctypes.c_double), ("p_conf", ctypes.c_double), ("n_draft", ctypes.c_int32),
+                ("t_draft", ctypes.c_double), ("t_verify", ctypes.c_double), ("t_offload", ctypes.c_double)]
 
 
 class MsaoError(RuntimeError):
@@ -94,6 +117,17 @@ SIGNATURES = [
     ("msao_plan_destroy", None, [_P]),
     ("msao_set_profiling", ctypes.c_int, [_P, ctypes.c_int]),
     ("msao_kernel_times", ctypes.c_int, [_P, _P]),
+    ("msao_draft_entropy", ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                          ctypes.c_float, _P, _P]),
+    ("msao_sched_default_params", MsaoSchedParams, []),
+    ("msao_sched_init", ctypes.c_int, [_P, ctypes.c_int64, _P, _P]),
+    ("msao_sched_step", ctypes.c_int, [_P, _P, ctypes.c_float, _P]),
+    ("msao_sched_run", ctypes.c_int, [_P, _P, _P, ctypes.c_int64, _P, _P]),
+    ("msao_retention_floor", ctypes.c_int, [_P, ctypes.c_int, _P]),
+    ("msao_comm_latency", ctypes.c_double, [ctypes.c_double, ctypes.c_double, ctypes.c_double]),
+    ("msao_p_conf", ctypes.c_double, [_P, ctypes.c_int64, ctypes.c_double]),
+    ("msao_expected_spec_tokens", ctypes.c_double, [ctypes.c_double]),
+    ("msao_expected_e2e_latency", ctypes.c_double, [_P]),
 ]
 
 
@@ -462,3 +496,92 @@ def compacted_rows(segments: Sequence[DeviceSegment], outputs: Outputs, kept_cou
         view = outputs.out[off:off + nb]
         rows.append(view.view(s.data.dtype).view(int(k), s.data.shape[1]))
     return rows
+
+
+# ---- Sec. 4.2: draft confidence (GPU) and Algorithm 1 (host) ------------------
+
+def msao_draft_entropy(logits: torch.Tensor, theta: float, vocab: Optional[int] = None, ctx: Optional[Context] = None,
+                       stream=None, outputs: Optional[Dict[str, torch.Tensor]] = None) -> Dict[str, torch.Tensor]:
+    """Eq. 9-10 per row of a [rows, row_stride] float32/bfloat16 device tensor
+    (the first `vocab` columns are the logits). Returns device tensors
+    entropy (nats), entropy_norm, draft_token and speculate."""
+    if logits.dim() != 2 or logits.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("logits must be a 2-D float32 or bfloat16 tensor")
+    if logits.numel() and logits.stride(1) != 1:
+        raise ValueError("rows must be contiguous")
+    rows = int(logits.shape[0])
+    V = int(logits.shape[1]) if vocab is None else int(vocab)
+    stride = int(logits.stride(0)) if rows > 1 else int(logits.shape[1])
+    dev = logits.device
+    if ctx is None:
+        ctx = default_context(dev.index if dev.index is not None else torch.cuda.current_device())
+    o = outputs or {"entropy": torch.empty(rows, dtype=torch.float32, device=dev),
+                    "entropy_norm": torch.empty(rows, dtype=torch.float32, device=dev),
+                    "draft_token": torch.empty(rows, dtype=torch.int32, device=dev),
+                    "speculate": torch.empty(rows, dtype=torch.uint8, device=dev)}
+    out = MsaoEntropyOut(*[_ptr(o.get(k)) for k in ("entropy", "entropy_norm", "draft_token", "speculate")])
+    st = stream if stream is not None else torch.cuda.current_stream(dev)
+    dt = F32 if logits.dtype == torch.float32 else BF16
+    _check(lib().msao_draft_entropy(ctx.handle, _ptr(logits) if logits.numel() else None, rows, V, stride, dt,
+                                    float(theta), _addr(out), ctypes.c_void_p(st.cuda_stream)), ctx)
+    return o
+
+
+def sched_default_params() -> MsaoSchedParams:
+    return lib().msao_sched_default_params()
+
+
+def _host_f32(x):
+    import numpy as np
+    return np.ascontiguousarray(x, dtype=np.float32)
+
+
+class Scheduler:
+    """Algorithm 1 for one request: line 2-3 from calibration entropies, then
+    the per-step hold / send / offload loop (host code in libmsao.so)."""
+
+    def __init__(self, calib_h_norm, params: Optional[MsaoSchedParams] = None):
+        self.params = params if params is not None else sched_default_params()
+        self.state = MsaoSchedState()
+        h = _host_f32(calib_h_norm)
+        _check(lib().msao_sched_init(h.ctypes.data, h.size, _addr(self.params), _addr(self.state)))
+
+    def step(self, h_norm: float) -> int:
+        d = ctypes.c_int32()
+        _check(lib().msao_sched_step(_addr(self.state), _addr(self.params), float(h_norm), ctypes.byref(d)))
+        return d.value
+
+    def run(self, h_norm):
+        import numpy as np
+        h = _host_f32(h_norm)
+        dec = np.zeros(h.size, np.int8)
+        th = np.zeros(h.size, np.float64)
+        _check(lib().msao_sched_run(_addr(self.state), _addr(self.params), h.ctypes.data, h.size,
+                                    dec.ctypes.data, th.ctypes.data))
+        return dec, th
+
+
+def retention_floor(mas):
+    import numpy as np
+    m = _host_f32(mas)
+    b = np.zeros_like(m)
+    _check(lib().msao_retention_floor(m.ctypes.data, m.size, b.ctypes.data))
+    return b
+
+
+def comm_latency(data_bytes: float, bandwidth_bytes_per_s: float, rtt_s: float) -> float:
+    return lib().msao_comm_latency(data_bytes, bandwidth_bytes_per_s, rtt_s)
+
+
+def p_conf(h_norm, theta: float) -> float:
+    h = _host_f32(h_norm)
+    return lib().msao_p_conf(h.ctypes.data, h.size, theta)
+
+
+def expected_spec_tokens(p: float) -> float:
+    return lib().msao_expected_spec_tokens(p)
+
+
+def expected_e2e_latency(**terms) -> float:
+    m = MsaoLatencyModel(**terms)
+    return lib().msao_expected_e2e_latency(_addr(m))

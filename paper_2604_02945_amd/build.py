@@ -8,7 +8,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libmsao.so")
-SOURCES = [os.path.join(HERE, "csrc", "msao_host.cpp"), os.path.join(HERE, "csrc", "msao_kernels.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in
+           ("msao_host.cpp", "msao_sched.cpp", "msao_kernels.hip", "msao_entropy.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -1,0 +1,222 @@
+// msao_entropy.hip -- gfx950 (CDNA4) kernel for the draft model's confidence
+// in MSAO's speculative decoding (Sec. 4.2): per row of draft logits, the
+// entropy of its softmax (Eq. 9), the greedy draft token (arg max) and the
+// speculation test against the confidence threshold (Eq. 10).
+//
+// HBM-bound streaming reduction, one pass over the logits: one workgroup per
+// row, each lane reading 16-byte chunks with nontemporal buffer loads. A lane
+// keeps a running maximum m, s = sum exp(x - m) and t = sum exp(x - m)(x - m)
+// over its chunks, so that H = ln s - t / s needs no second pass and no
+// cancellation against m. Per batch of chunks the batch maximum is taken
+// first; only when it exceeds m are s and t rescaled (and the arg max
+// searched), which after the first batches is rare. Lane states merge by
+// shuffles, then across the block's wavefronts through LDS.
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "msao_internal.h"
+
+namespace msao {
+namespace {
+
+constexpr int kEntWave = 64;
+constexpr float kLog2e = 1.4426950408889634f;
+// exp(-200) is far below the smallest normal float: clamping the difference
+// that multiplies exp(x - m) in t only matters for x = -inf, whose term is
+// then 0 * -200 = 0 instead of 0 * -inf = NaN. A NaN logit still makes s NaN.
+constexpr float kMinDiff = -200.0f;
+
+typedef unsigned int ent_vec4 __attribute__((ext_vector_type(4)));
+typedef __amdgpu_buffer_rsrc_t ent_rsrc_t;
+
+__device__ __forceinline__ ent_rsrc_t ent_rsrc(const void* base, int bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+}
+
+// nontemporal: every logit is read once
+__device__ __forceinline__ ent_vec4 ent_load(ent_rsrc_t r, int off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2);
+}
+
+__device__ __forceinline__ float ent_exp(float d) { return __builtin_amdgcn_exp2f(d * kLog2e); }
+
+// Softmax statistics of a set of logits: maximum m (first index idx), and
+// s, t relative to m.
+struct Acc {
+    float m, s, t;
+    int idx;
+};
+
+// Merge b into a: the larger maximum wins (the lower index on equal maxima)
+// and the other side's sums are rescaled to it. Only an empty side (s == 0)
+// is skipped, so a NaN sum still reaches the result.
+__device__ __forceinline__ Acc acc_merge(Acc a, Acc b)
+{
+    if (b.m > a.m || (b.m == a.m && b.idx < a.idx)) {
+        const Acc c = a;
+        a = b;
+        b = c;
+    }
+    if (b.s != 0.0f) {
+        const float dm = b.m - a.m;
+        const float sc = ent_exp(dm);
+        a.t += (b.t + dm * b.s) * sc;
+        a.s += b.s * sc;
+    }
+    return a;
+}
+
+__device__ __forceinline__ Acc acc_shfl_xor(const Acc& a, int o)
+{
+    Acc r;
+    r.m = __shfl_xor(a.m, o);
+    r.s = __shfl_xor(a.s, o);
+    r.t = __shfl_xor(a.t, o);
+    r.idx = __shfl_xor(a.idx, o);
+    return r;
+}
+
+template <int DT> struct EntLane;
+template <> struct EntLane<kBF16> {
+    static constexpr int EPC = 8;  // elements per 16-byte chunk
+    __device__ static __forceinline__ void widen(const ent_vec4& v, float* x)
+    {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            x[2 * w] = __uint_as_float(v[w] << 16);
+            x[2 * w + 1] = __uint_as_float(v[w] & 0xFFFF0000u);
+        }
+    }
+    __device__ static __forceinline__ float element(const uint8_t* row, int64_t i)
+    {
+        return __uint_as_float((uint32_t)((const uint16_t*)row)[i] << 16);
+    }
+};
+template <> struct EntLane<kF32> {
+    static constexpr int EPC = 4;
+    __device__ static __forceinline__ void widen(const ent_vec4& v, float* x)
+    {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) x[w] = __uint_as_float(v[w]);
+    }
+    __device__ static __forceinline__ float element(const uint8_t* row, int64_t i)
+    {
+        return ((const float*)row)[i];
+    }
+};
+
+// Add n values x (element indices first, first + 1, ...) to the lane state.
+template <int N>
+__device__ __forceinline__ void acc_add(Acc& a, const float (&x)[N], const int (&first)[N])
+{
+    float cm = x[0];
+#pragma unroll
+    for (int j = 1; j < N; ++j) cm = fmaxf(cm, x[j]);
+    if (cm > a.m) {
+        int at = first[0];
+#pragma unroll
+        for (int j = N - 1; j >= 0; --j)
+            if (x[j] == cm) at = first[j];
+        if (a.s > 0.0f) {
+            const float dm = a.m - cm;
+            const float sc = ent_exp(dm);
+            a.t = (a.t + dm * a.s) * sc;
+            a.s *= sc;
+        }
+        a.m = cm;
+        a.idx = at;
+    }
+    // While nothing finite has been seen (m = -inf) the values are -inf (they
+    // contribute 0) or NaN (which must reach s): take differences against 0,
+    // since -inf - (-inf) would turn every -inf into NaN.
+    const float mref = a.m == -INFINITY ? 0.0f : a.m;
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+        const float d = x[j] - mref;
+        const float e = ent_exp(d);
+        a.s += e;
+        a.t = fmaf(e, fmaxf(d, kMinDiff), a.t);
+    }
+}
+
+template <int DT, int U>
+__global__ __launch_bounds__(kEntBlock) void k_entropy(EntArgs a)
+{
+    using L = EntLane<DT>;
+    constexpr int EPC = L::EPC;
+    const int row = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & (kEntWave - 1), wid = tid >> 6;
+    const uint8_t* base = a.logits + (int64_t)row * a.row_bytes;
+    const int nfull = a.vocab / EPC;  // whole 16-byte chunks
+    const ent_rsrc_t rs = ent_rsrc(base, nfull * 16);
+    Acc acc{-INFINITY, 0.0f, 0.0f, 0};
+    for (int c0 = 0; c0 < nfull; c0 += U * kEntBlock) {
+        ent_vec4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = ent_load(rs, (c0 + u * kEntBlock + tid) * 16);
+        float x[U * EPC];
+        int first[U * EPC];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            L::widen(v[u], &x[u * EPC]);
+            const int c = c0 + u * kEntBlock + tid;
+#pragma unroll
+            for (int j = 0; j < EPC; ++j) first[u * EPC + j] = c * EPC + j;
+            if (c0 + U * kEntBlock > nfull && c >= nfull) {  // chunks past the row read as -inf
+#pragma unroll
+                for (int j = 0; j < EPC; ++j) x[u * EPC + j] = -INFINITY;
+            }
+        }
+        acc_add<U * EPC>(acc, x, first);
+    }
+    // the elements past the last whole chunk, one per thread
+    const int tail = a.vocab - nfull * EPC;
+    if (tid < tail) {
+        float x1[1] = {L::element(base, (int64_t)nfull * EPC + tid)};
+        const int f1[1] = {nfull * EPC + tid};
+        acc_add<1>(acc, x1, f1);
+    }
+#pragma unroll
+    for (int o = 1; o < kEntWave; o <<= 1) acc = acc_merge(acc, acc_shfl_xor(acc, o));
+    __shared__ Acc part[kEntBlock / kEntWave];
+    if (lane == 0) part[wid] = acc;
+    __syncthreads();
+    if (tid != 0) return;
+    Acc r = part[0];
+#pragma unroll
+    for (int w = 1; w < kEntBlock / kEntWave; ++w) r = acc_merge(r, part[w]);
+    // Eq. 9: H = -sum p log p = ln s - t / s with p = exp(x - m) / s
+    const float H = __logf(r.s) - r.t / r.s;
+    const float Hn = H * a.inv_log_vocab;
+    if (a.entropy) a.entropy[row] = H;
+    if (a.entropy_norm) a.entropy_norm[row] = Hn;
+    if (a.draft_token) a.draft_token[row] = r.idx;
+    if (a.speculate) a.speculate[row] = Hn <= a.theta ? 1 : 0;  // Eq. 10
+}
+
+}  // namespace
+
+int launch_entropy(const EntArgs& a, void* stream, void* ev0, void* ev1)
+{
+    if (a.rows <= 0) return 0;
+    const dim3 grid((unsigned)a.rows), block(kEntBlock);
+    if (a.dtype == kBF16) {
+        if (ev0 && ev1)
+            hipExtLaunchKernelGGL((k_entropy<kBF16, 4>), grid, block, 0, (hipStream_t)stream, (hipEvent_t)ev0,
+                                  (hipEvent_t)ev1, 0, a);
+        else
+            hipLaunchKernelGGL((k_entropy<kBF16, 4>), grid, block, 0, (hipStream_t)stream, a);
+    } else {
+        if (ev0 && ev1)
+            hipExtLaunchKernelGGL((k_entropy<kF32, 4>), grid, block, 0, (hipStream_t)stream, (hipEvent_t)ev0,
+                                  (hipEvent_t)ev1, 0, a);
+        else
+            hipLaunchKernelGGL((k_entropy<kF32, 4>), grid, block, 0, (hipStream_t)stream, a);
+    }
+    return (int)hipGetLastError();
+}
+
+}  // namespace msao

@@ -410,6 +410,7 @@ msao_status launched(msao_ctx* ctx, int kernel, hipStream_t stream, int (*fn)(co
 int run_score(const void* a, void* s, void* e0, void* e1) { return launch_score(*(const ScoreArgs*)a, s, e0, e1); }
 int run_post(const void* a, void* s, void* e0, void* e1) { return launch_post(*(const PostArgs*)a, s, e0, e1); }
 int run_gather(const void* a, void* s, void* e0, void* e1) { return launch_gather(*(const GatherArgs*)a, s, e0, e1); }
+int run_entropy(const void* a, void* s, void* e0, void* e1) { return launch_entropy(*(const EntArgs*)a, s, e0, e1); }
 
 #define MSAO_TRY(x)                                                                                                   \
     do {                                                                                                              \
@@ -743,6 +744,40 @@ msao_status msao_compact(msao_ctx* ctx, const msao_segment* segs, int n, const i
     ga.out = (uint8_t*)out;
     ga.out_bytes = out_bytes;
     return launched(ctx, MSAO_KERNEL_GATHER, st, run_gather, &ga);
+}
+
+msao_status msao_draft_entropy(msao_ctx* ctx, const void* logits, int64_t rows, int64_t vocab, int64_t row_stride,
+                               int dtype, float theta, const msao_entropy_out* out, void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    if (!out) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "out is NULL");
+    if (dtype != MSAO_F32 && dtype != MSAO_BF16) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "unknown dtype");
+    const int64_t es = elt_size(dtype);
+    if (rows < 0 || rows > INT32_MAX) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "rows out of range");
+    if (vocab < 2 || vocab * es >= ((int64_t)1 << 31) - ((int64_t)1 << 20))
+        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "vocab out of range");
+    if (row_stride < vocab) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "row_stride < vocab");
+    if (std::isnan(theta) || std::isinf(theta)) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "theta is not finite");
+    if (rows > 0 && !logits) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "logits is NULL");
+    if (((uintptr_t)logits) % 16 != 0) return fail(&ctx->err, MSAO_ERR_ALIGNMENT, "logits are not 16-byte aligned");
+    if ((row_stride * es) % 16 != 0) return fail(&ctx->err, MSAO_ERR_ALIGNMENT, "row pitch is not a multiple of 16 bytes");
+    MSAO_TRY(check_out_alignment(ctx, {{out->entropy, 4}, {out->entropy_norm, 4}, {out->draft_token, 4}}));
+    if (rows == 0) return MSAO_OK;
+    DeviceGuard guard(ctx->device);
+    EntArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.logits = (const uint8_t*)logits;
+    a.row_bytes = row_stride * es;
+    a.rows = (int32_t)rows;
+    a.vocab = (int32_t)vocab;
+    a.dtype = dtype;
+    a.theta = theta;
+    a.inv_log_vocab = (float)(1.0 / std::log((double)vocab));
+    a.entropy = out->entropy;
+    a.entropy_norm = out->entropy_norm;
+    a.draft_token = out->draft_token;
+    a.speculate = out->speculate;
+    return launched(ctx, MSAO_KERNEL_ENTROPY, (hipStream_t)stream, run_entropy, &a);
 }
 
 }  // extern "C"

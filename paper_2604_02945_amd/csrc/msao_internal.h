@@ -118,6 +118,21 @@ struct GatherArgs {
     int64_t out_bytes;
 };
 
+// Draft-model confidence (msao_entropy.hip): one row of logits per workgroup.
+struct EntArgs {
+    const uint8_t* logits;   // row r starts at logits + r * row_bytes
+    int64_t row_bytes;
+    int32_t rows, vocab, dtype;
+    float theta;             // Eq. 10 threshold on the normalised entropy
+    float inv_log_vocab;     // 1 / ln(vocab)
+    float* entropy;          // [rows] nats (NULL: not written)
+    float* entropy_norm;     // [rows] entropy / ln(vocab)
+    int32_t* draft_token;    // [rows] arg max, first of equal maxima
+    uint8_t* speculate;      // [rows] entropy_norm <= theta
+};
+constexpr int kEntBlock = 256;
+int launch_entropy(const EntArgs& a, void* stream, void* ev0, void* ev1);
+
 // Launchers (msao_kernels.hip). Return the HIP error code of the launch. ev0 and
 // ev1 (hipEvent_t, may be NULL) are recorded at the kernel's start and end.
 int launch_score(const ScoreArgs& a, void* stream, void* ev0, void* ev1);

@@ -16,7 +16,7 @@ OK, INVALID, ALIGN, WS, UNSUP, HIP = range(6)
 def _declared_functions():
     src = open(os.path.join(ROOT, "include", "msao.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(msao_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(msao_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_every_declared_symbol_is_exported():

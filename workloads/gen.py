@@ -279,3 +279,45 @@ def make_workload(config: int, seed: int = 0, n_requests: Optional[int] = None) 
     n = full if n_requests is None else min(int(n_requests), full)
     segs = _BUILDERS[config](seed, n)
     return Workload(CONFIG_NAMES[config], config, n, segs, default_params(), None)
+
+
+# ---- draft-model logits (Sec. 4.2) --------------------------------------------
+
+DRAFT_VOCAB = 151936          # the Qwen2-VL output vocabulary (embedding rows, padded)
+DRAFT_ROWS = 1280             # 256 requests x N_max = 5 draft tokens per speculative round
+
+
+def draft_logits(rows: int = DRAFT_ROWS, vocab: int = DRAFT_VOCAB, seed: int = 0, dtype: str = "bf16",
+                 row_stride: Optional[int] = None) -> np.ndarray:
+    """Synthetic logits of a draft model, [rows, row_stride] (float32, or bf16
+    bit patterns), standing in for the per-step output distributions of the
+    paper's Qwen2-VL-2B draft model (Sec. 5.1), which is not available.
+
+    Recipe per row r (PCG64 seeded with SeedSequence([seed, 6, rows, vocab])):
+    background logits N(0, sigma_r^2) with sigma_r ~ U(0.5, 2.5); one peak
+    token at a uniform index raised by b_r ~ U(0, 30); three runner-up tokens
+    (fewer when the vocabulary is smaller) raised by b_r - U(1, 8). Small b_r gives a flat, unconfident row (normalised
+    entropy near 1), large b_r a confident one (near 0), so the rows span the
+    whole threshold range of Algorithm 1. Columns past `vocab` (when
+    row_stride > vocab) are filled with NaN so that reading them would show."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 6, rows, vocab])))
+    stride = vocab if row_stride is None else row_stride
+    sigma = rng.uniform(0.5, 2.5, rows).astype(np.float32)
+    boost = rng.uniform(0.0, 30.0, rows).astype(np.float32)
+    k = min(4, vocab)                          # boosted tokens per row (the peak and its runners-up)
+    if vocab <= 64:
+        idx = np.stack([rng.permutation(vocab)[:k] for _ in range(rows)]) if rows else np.zeros((0, k), np.int64)
+    else:
+        idx = rng.integers(0, vocab, (rows, k))
+        for r in range(rows):                  # distinct tokens; collisions are rare for a large vocabulary
+            while len(set(idx[r].tolist())) < k:
+                idx[r] = rng.integers(0, vocab, k)
+    runner = rng.uniform(1.0, 8.0, (rows, k - 1)).astype(np.float32)
+    x = np.full((rows, stride), np.nan, np.float32)
+    x[:, :vocab] = rng.standard_normal((rows, vocab), dtype=np.float32)
+    x[:, :vocab] *= sigma[:, None]
+    r_ix = np.arange(rows)
+    x[r_ix, idx[:, 0]] += boost
+    if k > 1:
+        x[r_ix[:, None], idx[:, 1:]] += boost[:, None] - runner
+    return x if dtype == "f32" else f32_to_bf16_bits(x)
