@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--no-compact", action="store_true", help="time score+select only (no compaction)")
     ap.add_argument("--no-score-select", action="store_true",
                     help="skip the extra score+select-only timing that follows a run with compaction")
+    ap.add_argument("--no-entropy", action="store_true",
+                    help="skip the draft-confidence kernel and Algorithm 1 measurements")
+    ap.add_argument("--entropy-steps", type=int, default=100, help="timed launches of the draft-confidence kernel")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (calibrates HBM byte counters)")
     ap.add_argument("--streams", type=int, default=3,
@@ -109,6 +112,87 @@ def committed_traffic(config):
     for f in ("msao_kernels.hip", "msao_internal.h"):
         h.update(open(os.path.join(ROOT, "paper_2604_02945_amd", "csrc", f), "rb").read())
     return rec["traffic_bytes_per_launch"] if rec.get("kernel_source_sha256") == h.hexdigest() else None
+
+
+def committed_entropy_traffic():
+    """HBM bytes per k_entropy launch from the committed counter summary (None
+    if absent or if the kernel sources changed since)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "k_entropy_draft_logits_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    h = hashlib.sha256()
+    for f in ("msao_entropy.hip", "msao_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2604_02945_amd", "csrc", f), "rb").read())
+    return rec["traffic_bytes_per_launch"] if rec.get("kernel_source_sha256") == h.hexdigest() else None
+
+
+def entropy_bench(args, dev, ctx):
+    """Draft confidence (Eq. 9-10) on 1,280 rows x 151,936 bf16 logits (256
+    requests x 5 draft tokens over the Qwen2-VL vocabulary), three rotated
+    replicas (1.17 GB, so the Infinity Cache is cold), then Algorithm 1's
+    per-step loop on the host over the resulting normalised entropies."""
+    import numpy as np
+    import torch
+
+    import paper_2604_02945_amd as msao
+    from workloads import DRAFT_ROWS, DRAFT_VOCAB, draft_logits
+
+    x = draft_logits(DRAFT_ROWS, DRAFT_VOCAB, seed=0, dtype="bf16")
+    first = torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+    reps = [first] + [first.clone() for _ in range(2)]
+    rows, V = DRAFT_ROWS, DRAFT_VOCAB
+    outs = [{"entropy": torch.empty(rows, device=dev), "entropy_norm": torch.empty(rows, device=dev),
+             "draft_token": torch.empty(rows, dtype=torch.int32, device=dev),
+             "speculate": torch.empty(rows, dtype=torch.uint8, device=dev)} for _ in reps]
+    theta = 0.5
+    for i in range(6):
+        msao.msao_draft_entropy(reps[i % 3], theta, ctx=ctx, outputs=outs[i % 3])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.entropy_steps):
+        msao.msao_draft_entropy(reps[i % 3], theta, ctx=ctx, outputs=outs[i % 3])
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.entropy_steps
+    ctx.set_profiling(True)
+    for i in range(args.entropy_steps):
+        msao.msao_draft_entropy(reps[i % 3], theta, ctx=ctx, outputs=outs[i % 3])
+    k_ms = ctx.kernel_times()[msao.binding.KERNEL_ENTROPY]
+    ctx.set_profiling(False)
+    b = rows * V * 2 + rows * (4 + 4 + 4 + 1)
+    gbs = b / (k_ms * 1e-3) / 1e9
+    hn = outs[0]["entropy_norm"].cpu().numpy()
+    # Algorithm 1 on the host: lines 2-3 from the first 500 rows (the paper's
+    # calibration-set size), then the per-step loop over the kernel's entropies
+    sched = msao.Scheduler(hn[:500])
+    theta0, n_draft, p_conf = sched.state.theta, sched.state.n_draft, sched.state.p_conf
+    trace = np.tile(hn, 200)
+    t0 = time.perf_counter()
+    dec, _ = sched.run(trace)
+    ns = (time.perf_counter() - t0) / trace.size * 1e9
+    res = {
+        "workload": f"draft logits {rows} x {V} bf16 (256 requests x 5 draft tokens), 3 rotated replicas",
+        "ms_per_launch": ms, "rows_per_s": rows / (ms * 1e-3), "kernel_ms": k_ms,
+        "algorithmic_bytes": b, "hbm_gbps": gbs,
+        "roofline": {"bound": "hbm", "kernel": "k_entropy", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": gbs / PEAK_HBM_GBS, "traffic": committed_entropy_traffic()},
+        "speculating_rows": int(outs[0]["speculate"].sum().item()),
+        "sched": {"theta0": theta0, "n_draft": n_draft, "p_conf": p_conf, "steps": int(trace.size),
+                  "ns_per_step": ns, "sends": int((dec == msao.DECIDE_SEND).sum()),
+                  "offloads": int((dec == msao.DECIDE_OFFLOAD).sum())},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        t0 = time.perf_counter()
+        oracle.entropy_rows(x[:64], "bf16")
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": 64 / dt, "unit": "rows/s", "cores": 1, "kind": "oracle",
+                               "sample": f"64 rows x {V} of the same logits, single-threaded C oracle (fp64), {dt:.2f} s"}
+    del reps, first
+    return res
 
 
 def cpu_baseline(w, budget_s):
@@ -283,6 +367,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    if not args.no_entropy:
+        line["entropy"] = entropy_bench(args, dev, ctxs[0])
     for _, plan in plans:
         plan.close()
     for c in ctxs:

@@ -3,7 +3,10 @@
  * fine-grained sparsity analysis: per-token activation-sparsity statistics,
  * the temporal-redundancy term between consecutive video frames, per-modality
  * aggregation into MAS (Modal Activation Sparsity), and the MAS-guided
- * selection and compaction of the tokens that are kept.
+ * selection and compaction of the tokens that are kept. Also the decoding
+ * side of its speculative offloading (Sec. 4.2): the draft model's
+ * confidence per generation step on the GPU (Eq. 9-10), and on the host the
+ * latency model (Eq. 8, 12-14) and Algorithm 1's threshold logic.
  *
  * Paper: "MSAO" (arXiv 2604.02945). Sec. 4.1 defines the probing module:
  * spatial sparsity (Sec. 4.1.1, Eq. 3-4), temporal sparsity (Sec. 4.1.2,

@@ -4,13 +4,14 @@
 // speculation test against the confidence threshold (Eq. 10).
 //
 // HBM-bound streaming reduction, one pass over the logits: one workgroup per
-// row, each lane reading 16-byte chunks with nontemporal buffer loads. A lane
-// keeps a running maximum m, s = sum exp(x - m) and t = sum exp(x - m)(x - m)
-// over its chunks, so that H = ln s - t / s needs no second pass and no
-// cancellation against m. Per batch of chunks the batch maximum is taken
-// first; only when it exceeds m are s and t rescaled (and the arg max
-// searched), which after the first batches is rare. Lane states merge by
-// shuffles, then across the block's wavefronts through LDS.
+// row, each lane reading 16-byte chunks with nontemporal buffer loads, the
+// next batch in flight while the current one is reduced. A lane keeps a
+// running maximum m, s = sum exp(x - m) and t = sum exp(x - m)(x - m) over its
+// chunks, so that H = ln s - t / s needs no second pass and no cancellation
+// against m. Per batch of chunks the batch maximum is taken first; only when
+// it exceeds m are s and t rescaled (and the arg max searched), which after
+// the first batches is rare. Lane states merge by shuffles, then across the
+// block's wavefronts through LDS.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -41,12 +42,12 @@ __device__ __forceinline__ ent_vec4 ent_load(ent_rsrc_t r, int off)
     return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2);
 }
 
-__device__ __forceinline__ float ent_exp(float d) { return __builtin_amdgcn_exp2f(d * kLog2e); }
-
-// Softmax statistics of a set of logits: maximum m (first index idx), and
-// s, t relative to m.
+// Softmax statistics of a set of logits: maximum m (first index idx),
+// s = sum 2^(L (x - m)) = sum exp(x - m) and u = sum 2^(L (x - m)) L (x - m)
+// with L = log2(e), i.e. u = L t for t = sum exp(x - m) (x - m). Keeping u in
+// log2 units lets one fma give the exponent: L x - L m.
 struct Acc {
-    float m, s, t;
+    float m, s, u;
     int idx;
 };
 
@@ -61,9 +62,9 @@ __device__ __forceinline__ Acc acc_merge(Acc a, Acc b)
         b = c;
     }
     if (b.s != 0.0f) {
-        const float dm = b.m - a.m;
-        const float sc = ent_exp(dm);
-        a.t += (b.t + dm * b.s) * sc;
+        const float dm = (b.m - a.m) * kLog2e;
+        const float sc = __builtin_amdgcn_exp2f(dm);
+        a.u += (b.u + dm * b.s) * sc;
         a.s += b.s * sc;
     }
     return a;
@@ -74,7 +75,7 @@ __device__ __forceinline__ Acc acc_shfl_xor(const Acc& a, int o)
     Acc r;
     r.m = __shfl_xor(a.m, o);
     r.s = __shfl_xor(a.s, o);
-    r.t = __shfl_xor(a.t, o);
+    r.u = __shfl_xor(a.u, o);
     r.idx = __shfl_xor(a.idx, o);
     return r;
 }
@@ -108,37 +109,38 @@ template <> struct EntLane<kF32> {
     }
 };
 
-// Add n values x (element indices first, first + 1, ...) to the lane state.
-template <int N>
-__device__ __forceinline__ void acc_add(Acc& a, const float (&x)[N], const int (&first)[N])
+// Add the N values x to the lane state; x[j] is element first + stride_of(j)
+// (index(j) gives it), used only when the maximum moves.
+template <int N, typename IndexOf>
+__device__ __forceinline__ void acc_add(Acc& a, const float (&x)[N], IndexOf index)
 {
     float cm = x[0];
 #pragma unroll
     for (int j = 1; j < N; ++j) cm = fmaxf(cm, x[j]);
     if (cm > a.m) {
-        int at = first[0];
+        int at = index(0);
 #pragma unroll
         for (int j = N - 1; j >= 0; --j)
-            if (x[j] == cm) at = first[j];
+            if (x[j] == cm) at = index(j);
         if (a.s > 0.0f) {
-            const float dm = a.m - cm;
-            const float sc = ent_exp(dm);
-            a.t = (a.t + dm * a.s) * sc;
+            const float dm = (a.m - cm) * kLog2e;
+            const float sc = __builtin_amdgcn_exp2f(dm);
+            a.u = (a.u + dm * a.s) * sc;
             a.s *= sc;
         }
         a.m = cm;
         a.idx = at;
     }
     // While nothing finite has been seen (m = -inf) the values are -inf (they
-    // contribute 0) or NaN (which must reach s): take differences against 0,
+    // contribute 0) or NaN (which must reach s): take the exponent against 0,
     // since -inf - (-inf) would turn every -inf into NaN.
-    const float mref = a.m == -INFINITY ? 0.0f : a.m;
+    const float nml = a.m == -INFINITY ? 0.0f : -a.m * kLog2e;
 #pragma unroll
     for (int j = 0; j < N; ++j) {
-        const float d = x[j] - mref;
-        const float e = ent_exp(d);
+        const float d = fmaf(x[j], kLog2e, nml);  // L (x - m)
+        const float e = __builtin_amdgcn_exp2f(d);
         a.s += e;
-        a.t = fmaf(e, fmaxf(d, kMinDiff), a.t);
+        a.u = fmaf(e, fmaxf(d, kMinDiff * kLog2e), a.u);
     }
 }
 
@@ -147,37 +149,52 @@ __global__ __launch_bounds__(kEntBlock) void k_entropy(EntArgs a)
 {
     using L = EntLane<DT>;
     constexpr int EPC = L::EPC;
+    constexpr int STEP = U * kEntBlock;  // chunks per batch of the block
     const int row = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & (kEntWave - 1), wid = tid >> 6;
     const uint8_t* base = a.logits + (int64_t)row * a.row_bytes;
-    const int nfull = a.vocab / EPC;  // whole 16-byte chunks
+    const int nfull = a.vocab / EPC;         // whole 16-byte chunks
+    const int nmain = nfull / STEP * STEP;   // chunks of whole batches
     const ent_rsrc_t rs = ent_rsrc(base, nfull * 16);
     Acc acc{-INFINITY, 0.0f, 0.0f, 0};
-    for (int c0 = 0; c0 < nfull; c0 += U * kEntBlock) {
-        ent_vec4 v[U];
+    float x[U * EPC];
+    // whole batches, the next one loading while the current one is reduced
+    ent_vec4 cur[U];
+    if (nmain > 0) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = ent_load(rs, (c0 + u * kEntBlock + tid) * 16);
-        float x[U * EPC];
-        int first[U * EPC];
+        for (int u = 0; u < U; ++u) cur[u] = ent_load(rs, (u * kEntBlock + tid) * 16);
+    }
+    for (int c0 = 0; c0 < nmain; c0 += STEP) {
+        ent_vec4 nxt[U];
+        if (c0 + STEP < nmain) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) nxt[u] = ent_load(rs, (c0 + STEP + u * kEntBlock + tid) * 16);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) L::widen(cur[u], &x[u * EPC]);
+        acc_add<U * EPC>(acc, x, [&](int j) { return (c0 + (j / EPC) * kEntBlock + tid) * EPC + j % EPC; });
+#pragma unroll
+        for (int u = 0; u < U; ++u) cur[u] = nxt[u];
+    }
+    // the last, partial batch: chunks past the row read as -inf
+    if (nmain < nfull) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            L::widen(v[u], &x[u * EPC]);
-            const int c = c0 + u * kEntBlock + tid;
-#pragma unroll
-            for (int j = 0; j < EPC; ++j) first[u * EPC + j] = c * EPC + j;
-            if (c0 + U * kEntBlock > nfull && c >= nfull) {  // chunks past the row read as -inf
+            const int c = nmain + u * kEntBlock + tid;
+            L::widen(ent_load(rs, c * 16), &x[u * EPC]);
+            if (c >= nfull) {
 #pragma unroll
                 for (int j = 0; j < EPC; ++j) x[u * EPC + j] = -INFINITY;
             }
         }
-        acc_add<U * EPC>(acc, x, first);
+        acc_add<U * EPC>(acc, x, [&](int j) { return (nmain + (j / EPC) * kEntBlock + tid) * EPC + j % EPC; });
     }
     // the elements past the last whole chunk, one per thread
     const int tail = a.vocab - nfull * EPC;
     if (tid < tail) {
-        float x1[1] = {L::element(base, (int64_t)nfull * EPC + tid)};
-        const int f1[1] = {nfull * EPC + tid};
-        acc_add<1>(acc, x1, f1);
+        const int i = nfull * EPC + tid;
+        float x1[1] = {L::element(base, i)};
+        acc_add<1>(acc, x1, [&](int) { return i; });
     }
 #pragma unroll
     for (int o = 1; o < kEntWave; o <<= 1) acc = acc_merge(acc, acc_shfl_xor(acc, o));
@@ -188,8 +205,8 @@ __global__ __launch_bounds__(kEntBlock) void k_entropy(EntArgs a)
     Acc r = part[0];
 #pragma unroll
     for (int w = 1; w < kEntBlock / kEntWave; ++w) r = acc_merge(r, part[w]);
-    // Eq. 9: H = -sum p log p = ln s - t / s with p = exp(x - m) / s
-    const float H = __logf(r.s) - r.t / r.s;
+    // Eq. 9: H = -sum p ln p = ln s - t / s with p = exp(x - m) / s and t = u / L
+    const float H = __logf(r.s) - (r.u * 0.6931471805599453f) / r.s;
     const float Hn = H * a.inv_log_vocab;
     if (a.entropy) a.entropy[row] = H;
     if (a.entropy_norm) a.entropy_norm[row] = Hn;
@@ -205,16 +222,16 @@ int launch_entropy(const EntArgs& a, void* stream, void* ev0, void* ev1)
     const dim3 grid((unsigned)a.rows), block(kEntBlock);
     if (a.dtype == kBF16) {
         if (ev0 && ev1)
-            hipExtLaunchKernelGGL((k_entropy<kBF16, 4>), grid, block, 0, (hipStream_t)stream, (hipEvent_t)ev0,
+            hipExtLaunchKernelGGL((k_entropy<kBF16, kEntUnits>), grid, block, 0, (hipStream_t)stream, (hipEvent_t)ev0,
                                   (hipEvent_t)ev1, 0, a);
         else
-            hipLaunchKernelGGL((k_entropy<kBF16, 4>), grid, block, 0, (hipStream_t)stream, a);
+            hipLaunchKernelGGL((k_entropy<kBF16, kEntUnits>), grid, block, 0, (hipStream_t)stream, a);
     } else {
         if (ev0 && ev1)
-            hipExtLaunchKernelGGL((k_entropy<kF32, 4>), grid, block, 0, (hipStream_t)stream, (hipEvent_t)ev0,
+            hipExtLaunchKernelGGL((k_entropy<kF32, kEntUnits>), grid, block, 0, (hipStream_t)stream, (hipEvent_t)ev0,
                                   (hipEvent_t)ev1, 0, a);
         else
-            hipLaunchKernelGGL((k_entropy<kF32, 4>), grid, block, 0, (hipStream_t)stream, a);
+            hipLaunchKernelGGL((k_entropy<kF32, kEntUnits>), grid, block, 0, (hipStream_t)stream, a);
     }
     return (int)hipGetLastError();
 }

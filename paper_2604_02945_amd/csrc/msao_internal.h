@@ -130,7 +130,14 @@ struct EntArgs {
     int32_t* draft_token;    // [rows] arg max, first of equal maxima
     uint8_t* speculate;      // [rows] entropy_norm <= theta
 };
-constexpr int kEntBlock = 256;
+#ifndef MSAO_ENT_BLOCK
+#define MSAO_ENT_BLOCK 256
+#endif
+#ifndef MSAO_ENT_UNITS
+#define MSAO_ENT_UNITS 4
+#endif
+constexpr int kEntBlock = MSAO_ENT_BLOCK;  // threads per row of logits
+constexpr int kEntUnits = MSAO_ENT_UNITS;  // 16-byte chunks per thread per batch
 int launch_entropy(const EntArgs& a, void* stream, void* ev0, void* ev1);
 
 // Launchers (msao_kernels.hip). Return the HIP error code of the launch. ev0 and
