@@ -87,6 +87,9 @@ def lib():
         L.orc_mas_value.restype = ctypes.c_double
         L.orc_keep_count.argtypes = [ctypes.c_double, ctypes.c_int64]
         L.orc_keep_count.restype = ctypes.c_int64
+        L.orc_run_learned.argtypes = [ctypes.POINTER(_Segment), ctypes.c_int, ctypes.c_int, ctypes.POINTER(_Params),
+                                      _P, _P, ctypes.POINTER(_Outputs), _P, _P, _P]
+        L.orc_run_learned.restype = ctypes.c_int
         L.orc_q24.argtypes = [ctypes.c_float]
         L.orc_q24.restype = ctypes.c_uint64
         D, I64, I = ctypes.c_double, ctypes.c_int64, ctypes.c_int
@@ -194,6 +197,76 @@ def run(segments: Sequence, n_requests: int, params: dict, alpha: Optional[np.nd
     o["k"] = o["k"][:n]
     if compact:
         o["compact"] = compact_rows(segments, o["k"], o["kept_idx"])
+    return o
+
+
+DESC = 8  # entries of the modality descriptor of Eq. 6
+
+
+class _Head(ctypes.Structure):
+    _fields_ = [("weight", _P), ("bias", ctypes.c_float), ("grid_w", ctypes.c_int32), ("pool", ctypes.c_int32)]
+
+
+class _Mlp(ctypes.Structure):
+    _fields_ = [("w1", _P), ("b1", _P), ("w2", _P), ("b2", ctypes.c_float), ("hidden", ctypes.c_int32),
+                ("prompt_dim", ctypes.c_int32), ("prompt", _P)]
+
+
+def run_learned(segments: Sequence, n_requests: int, params: dict, heads: Optional[Sequence] = None,
+                mlp: Optional[dict] = None) -> dict:
+    """The analysis with learned probe heads (Eq. 3) and the relevance MLP
+    (Eq. 6). heads[s] is None or a dict(weight=[hidden] array in the
+    segment's encoding, bias, grid_w, pool); mlp is None or a dict(w1=[hidden,
+    prompt_dim + 8], b1, w2, b2, prompt=[n_requests, prompt_dim]) of float32.
+    Returns the outputs of run() (rho, beta, mas, agg updated) plus
+    importance (per token), alpha and desc (per request and modality)."""
+    L = lib()
+    n = len(segments)
+    ntok = sum(s.n_frames * s.tokens_per_frame for s in segments)
+    nframe = sum(s.n_frames for s in segments if _is_temporal(s))
+    R = n_requests
+    o = {
+        "z": np.zeros(ntok, np.uint32), "l1": np.zeros(ntok, np.float32),
+        "l2": np.zeros(ntok, np.float32), "info": np.zeros(ntok, np.float32),
+        "d": np.zeros(ntok, np.uint32), "res": np.zeros(ntok, np.float32),
+        "dframe": np.zeros(nframe, np.uint64), "sim": np.zeros(nframe, np.float32),
+        "gamma": np.zeros(nframe, np.float32),
+        "agg": np.zeros(R * NMOD * 4, np.uint64), "rho": np.zeros(R * NMOD, np.float32),
+        "temporal": np.zeros(R * NMOD, np.float32), "beta": np.zeros(R * NMOD, np.float32),
+        "mas": np.zeros(R * NMOD, np.float32), "present": np.zeros(R * NMOD, np.uint8),
+        "k": np.zeros(max(n, 1), np.int32), "keep": np.zeros(ntok, np.uint8),
+        "kept_idx": np.zeros(ntok, np.int32),
+    }
+    outs = _Outputs(**{k: _ptr(v) for k, v in o.items()})
+    keep_alive = []
+    harr = None
+    if heads is not None:
+        harr = (_Head * max(1, n))()
+        for i, h in enumerate(heads):
+            if h is None:
+                continue
+            w = np.ascontiguousarray(h["weight"])
+            keep_alive.append(w)
+            harr[i] = _Head(w.ctypes.data, h.get("bias", 0.0), h.get("grid_w", 0), h.get("pool", 1))
+    m = None
+    if mlp is not None:
+        arrs = {k: np.ascontiguousarray(mlp[k], dtype=np.float32) for k in ("w1", "b1", "w2", "prompt")}
+        keep_alive += list(arrs.values())
+        m = _Mlp(arrs["w1"].ctypes.data, arrs["b1"].ctypes.data, arrs["w2"].ctypes.data, float(mlp.get("b2", 0.0)),
+                 arrs["b1"].size, arrs["prompt"].shape[1], arrs["prompt"].ctypes.data)
+    imp = np.zeros(max(ntok, 1), np.float64)
+    alpha = np.zeros(max(R * NMOD, 1), np.float64)
+    desc = np.zeros(max(R * NMOD * DESC, 1), np.float64)
+    rc = L.orc_run_learned(_segment_table(segments), n, R, ctypes.byref(_params(params)),
+                           ctypes.cast(harr, _P) if harr is not None else None,
+                           ctypes.byref(m) if m is not None else None, ctypes.byref(outs),
+                           _ptr(imp), _ptr(alpha), _ptr(desc))
+    if rc != 0:
+        raise RuntimeError(f"orc_run_learned failed ({rc})")
+    o["importance"] = imp[:ntok]
+    o["alpha"] = alpha[:R * NMOD]
+    o["desc"] = desc[:R * NMOD * DESC].reshape(R * NMOD, DESC)
+    o["k"] = o["k"][:n]
     return o
 
 

@@ -428,3 +428,178 @@ double orc_mas_value(double beta, double lam_s, double rho, double lam_t, double
 int64_t orc_keep_count(double kappa, int64_t N) { return keep_count(kappa, N); }
 
 uint64_t orc_q24(float lambda) { return q24(lambda); }
+
+/* ==================================================================
+ * Learned probe heads with caller weights (Sec. 4.1.1 Eq. 3 and
+ * Sec. 4.1.3 Eq. 6), in place of the parameter-free stand-ins.
+ * ================================================================ */
+
+typedef struct {
+    const void* weight; /* [hidden], segment dtype: the 1x1 convolution to one logit; NULL: no head */
+    float bias;
+    int32_t grid_w;     /* patches per grid row of a frame; grid (P / grid_w) x grid_w; 0: one row */
+    int32_t pool;       /* odd AvgPool window; 1: none */
+} orc_head;
+
+#define ORC_DESC 8      /* entries of the modality descriptor z_m */
+
+typedef struct {
+    const float* w1;    /* [hidden][prompt_dim + ORC_DESC], row-major */
+    const float* b1;    /* [hidden] */
+    const float* w2;    /* [hidden] */
+    float b2;
+    int32_t hidden, prompt_dim;
+    const float* prompt; /* [R][prompt_dim]: the prompt embedding p of each request */
+} orc_mlp;
+
+static double sigmoid(double v) { return 1.0 / (1.0 + exp(-v)); }
+
+/* Eq. 3 for one frame of a segment with a head (P tokens from token t0, on
+ * an H x W grid, token q at row q / W, column q % W):
+ *     M = sigmoid(Conv1x1(AvgPool(F))),  Conv1x1(f) = w . f + b.
+ * The window of a patch is the pool x pool square around it, cut to the grid;
+ * its average is over the patches inside. The convolution is linear, so the
+ * average of the projections w . f over the window equals the projection of
+ * the averaged features. */
+static void head_frame(const orc_segment* s, const orc_head* h, int64_t t0, double* M)
+{
+    const int64_t P = s->tokens_per_frame, C = s->hidden;
+    const int64_t W = h->grid_w > 0 ? h->grid_w : P, H = P / W, r = (h->pool - 1) / 2;
+    double* y = (double*)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1));
+    for (int64_t q = 0; q < P; ++q) {
+        const void* row = row_ptr(s, t0 + q);
+        double acc = 0.0;
+        for (int64_t c = 0; c < C; ++c)
+            acc += (double)widen(h->weight, s->dtype, (int)c) * (double)widen(row, s->dtype, (int)c);
+        y[q] = acc;
+    }
+    for (int64_t q = 0; q < P; ++q) {
+        const int64_t i = q / W, j = q % W;
+        double sum = 0.0;
+        int64_t cnt = 0;
+        for (int64_t ii = i - r; ii <= i + r; ++ii)
+            for (int64_t jj = j - r; jj <= j + r; ++jj)
+                if (ii >= 0 && ii < H && jj >= 0 && jj < W) {
+                    sum += y[ii * W + jj];
+                    cnt += 1;
+                }
+        M[q] = sigmoid(sum / (double)cnt + (double)h->bias);
+    }
+    free(y);
+}
+
+/* The analysis of orc_run with learned heads:
+ *  - importance[g] of every token: Eq. 3 where the segment has a head, its
+ *    activity density a / C otherwise;
+ *  - Nsparse of Eq. 4 counts importance < tau_s (the density test of orc_run
+ *    where there is no head);
+ *  - per (request, modality) the descriptor z_m (desc[x * 8 + 0..7]):
+ *    1, rho (Eq. 4), sum a / sum C, sum L1 / sum C, sqrt(sum L2 / sum C),
+ *    the temporal term of Eq. 7 (0 if none), 1 if that term exists,
+ *    ln(1 + Ntok) / 16, the sums over the modality's tokens (L1, L2 as the
+ *    per-token float values);
+ *  - Eq. 6: alpha = w2 . relu(W1 [p; z_m] + b1) + b2 (alpha = 0 without an
+ *    MLP), then the softmax over the modalities present and Eq. 7.
+ * heads may be NULL (no head anywhere), heads[s].weight NULL for no head on
+ * segment s. o receives the token, frame and request outputs of orc_run with
+ * agg[.][1], rho, beta and mas replaced; its selection outputs are those of
+ * the plain run and are not meaningful here. */
+int orc_run_learned(const orc_segment* segs, int n, int R, const orc_params* p, const orc_head* heads,
+                    const orc_mlp* mlp, orc_outputs* o, double* importance, double* alpha_out, double* desc)
+{
+    int rc = orc_run(segs, n, R, p, NULL, o);
+    if (rc) return rc;
+    const int X = R * ORC_NMOD;
+    double* A = (double*)calloc((size_t)(X > 0 ? X : 1), sizeof(double));
+    double* CC = (double*)calloc((size_t)(X > 0 ? X : 1), sizeof(double));
+    double* L1 = (double*)calloc((size_t)(X > 0 ? X : 1), sizeof(double));
+    double* L2 = (double*)calloc((size_t)(X > 0 ? X : 1), sizeof(double));
+    for (int x = 0; x < X; ++x) o->agg[x * 4 + 1] = 0;
+    int64_t tok = 0;
+    for (int s = 0; s < n; ++s) {
+        const orc_segment* sg = &segs[s];
+        const int64_t T = sg->n_frames, P = sg->tokens_per_frame, C = sg->hidden, N = T * P;
+        const int x = sg->request * ORC_NMOD + sg->modality;
+        const orc_head* h = heads && heads[s].weight ? &heads[s] : NULL;
+        double* M = (double*)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1));
+        for (int64_t t = 0; t < T; ++t) {
+            if (h) head_frame(sg, h, t * P, M);
+            for (int64_t q = 0; q < P; ++q) {
+                const int64_t g = tok + t * P + q;
+                const uint32_t a = (uint32_t)C - o->z[g];
+                if (h) {
+                    importance[g] = M[q];
+                    o->agg[x * 4 + 1] += M[q] < (double)p->tau_s;
+                } else {
+                    importance[g] = (double)a / (double)C;
+                    o->agg[x * 4 + 1] += (uint64_t)is_sparse(a, (int)C, p->tau_s);
+                }
+                A[x] += (double)a;
+                CC[x] += (double)C;
+                L1[x] += (double)o->l1[g];
+                L2[x] += (double)o->l2[g];
+            }
+        }
+        free(M);
+        tok += N;
+    }
+    for (int r = 0; r < R; ++r) {
+        int present[ORC_NMOD];
+        double al[ORC_NMOD], beta[ORC_NMOD], rho[ORC_NMOD], tterm[ORC_NMOD];
+        int has_t[ORC_NMOD];
+        for (int m = 0; m < ORC_NMOD; ++m) {
+            const int x = r * ORC_NMOD + m;
+            const uint64_t* ag = &o->agg[x * 4];
+            present[m] = ag[0] > 0;
+            rho[m] = present[m] ? (double)ag[1] / (double)ag[0] : 0.0;
+            has_t[m] = ag[3] > 0;
+            tterm[m] = 0.0;
+            if (has_t[m]) {
+                const double gamma_avg = (double)ag[2] / (double)ag[3];
+                tterm[m] = (p->flags & ORC_FLAG_TEMPORAL_LITERAL) ? gamma_avg : 1.0 - gamma_avg;
+            }
+            double* z = &desc[x * ORC_DESC];
+            for (int k = 0; k < ORC_DESC; ++k) z[k] = 0.0;
+            if (present[m]) {
+                z[0] = 1.0;
+                z[1] = rho[m];
+                z[2] = A[x] / CC[x];
+                z[3] = L1[x] / CC[x];
+                z[4] = sqrt(L2[x] / CC[x]);
+                z[5] = tterm[m];
+                z[6] = has_t[m] ? 1.0 : 0.0;
+                z[7] = log(1.0 + (double)ag[0]) / 16.0;
+            }
+            al[m] = 0.0;
+            if (mlp && present[m]) {
+                const int in = mlp->prompt_dim + ORC_DESC;
+                double out = (double)mlp->b2;
+                for (int j = 0; j < mlp->hidden; ++j) {
+                    double hsum = (double)mlp->b1[j];
+                    for (int k = 0; k < in; ++k) {
+                        const double v = k < mlp->prompt_dim ? (double)mlp->prompt[r * mlp->prompt_dim + k]
+                                                             : z[k - mlp->prompt_dim];
+                        hsum += (double)mlp->w1[j * in + k] * v;
+                    }
+                    out += (double)mlp->w2[j] * (hsum > 0.0 ? hsum : 0.0);
+                }
+                al[m] = out;
+            }
+            alpha_out[x] = al[m];
+        }
+        modal_softmax(al, present, beta);
+        for (int m = 0; m < ORC_NMOD; ++m) {
+            const int x = r * ORC_NMOD + m;
+            if (!present[m]) continue;
+            o->rho[x] = (float)rho[m];
+            o->beta[x] = (float)beta[m];
+            o->mas[x] = (float)mas_value(beta[m], (double)p->lambda_s[m], rho[m], (double)p->lambda_t[m], tterm[m],
+                                         has_t[m]);
+        }
+    }
+    free(A);
+    free(CC);
+    free(L1);
+    free(L2);
+    return 0;
+}
