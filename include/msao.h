@@ -243,6 +243,62 @@ msao_status msao_plan_run(msao_plan* plan, const msao_token_out* tok, const msao
 /* Free a plan (NULL is ignored); the caller must have synchronised its runs. */
 void msao_plan_destroy(msao_plan* plan);
 
+/* ---- Sec. 4.1.1 Eq. 3 and Sec. 4.1.3 Eq. 6 with caller weights ------------ */
+
+/* A learned spatial probing head for one segment (Eq. 3):
+ *     M = sigmoid(Conv1x1(AvgPool(F)))
+ * with the 1x1 convolution w . f + bias to one importance logit. AvgPool
+ * averages over the pool x pool square around each patch of a frame's grid
+ * (grid_w patches per row, tokens_per_frame / grid_w rows), cut to the grid.
+ * A token is sparse (Eq. 4) iff M < tau_s. weight: device [hidden] in the
+ * segment's dtype, 16-byte aligned; NULL means no head (the density
+ * importance a / C is used). pool: odd, 1..15. grid_w: 0 (one row) or a
+ * divisor of tokens_per_frame; tokens_per_frame <= 16384 with a head. */
+typedef struct {
+    const void* weight;
+    float bias;
+    int32_t grid_w;
+    int32_t pool;
+} msao_spatial_head;
+
+/* Entries of the modality descriptor z_m fed to the relevance MLP: 1, rho
+ * (Eq. 4), sum a / sum C (active fraction), sum L1 / sum C, sqrt(sum L2 /
+ * sum C), the temporal term of Eq. 7 (0 if none), 1 if that term exists,
+ * ln(1 + Ntok) / 16, all over the modality's tokens in the request. */
+#define MSAO_MODAL_DESC 8
+
+/* The relevance MLP of Eq. 6, shared by the modalities:
+ *     alpha_m = w2 . relu(W1 [p; z_m] + b1) + b2
+ * with p the request's prompt embedding. All pointers device, fp32, 4-byte
+ * aligned: w1 [hidden][prompt_dim + MSAO_MODAL_DESC] row-major, b1 and w2
+ * [hidden], prompt [n_requests][prompt_dim] (may be NULL when prompt_dim is
+ * 0). 1 <= hidden <= 4096, 0 <= prompt_dim <= 16384. */
+typedef struct {
+    const float* w1;
+    const float* b1;
+    const float* w2;
+    float b2;
+    int32_t hidden;
+    int32_t prompt_dim;
+    const float* prompt;
+} msao_modal_mlp;
+
+/* Sec. 4.1.1-4.1.4 with learned heads: msao_mas_score's outputs, where a
+ * segment with a head (heads[s].weight non-NULL; heads may be NULL) counts
+ * Eq. 4 on its Eq. 3 importance, and beta is the softmax of the MLP's alpha
+ * (of the host logits alpha, or 0, when mlp is NULL). importance (device
+ * [total tokens] or NULL): M for tokens of segments with a head, a / C for
+ * the others. alpha_out (device [n_requests*4]) and desc (device
+ * [n_requests*4*MSAO_MODAL_DESC]) may be NULL; absent modalities get 0.
+ * The workspace is the one msao_workspace_size gives. Errors as
+ * msao_mas_score, plus MSAO_ERR_INVALID_ARG / MSAO_ERR_ALIGNMENT for the
+ * head and MLP rules above. */
+msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int n, int n_requests,
+                                   const msao_params* params, const msao_spatial_head* heads,
+                                   const msao_modal_mlp* mlp, const float* alpha, const msao_token_out* tok,
+                                   float* importance, const msao_frame_out* frm, const msao_req_out* req,
+                                   float* alpha_out, float* desc, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- Sec. 4.2: the draft model's confidence ------------------------------- */
 
 /* Outputs of msao_draft_entropy, each [rows] device memory or NULL (not
@@ -350,7 +406,8 @@ double msao_expected_e2e_latency(const msao_latency_model* m);
 #define MSAO_KERNEL_POST 1    /* aggregation, MAS, per-frame terms, selection */
 #define MSAO_KERNEL_GATHER 2  /* compaction */
 #define MSAO_KERNEL_ENTROPY 3 /* draft confidence */
-#define MSAO_NUM_KERNELS 4
+#define MSAO_KERNEL_HEAD 4    /* learned spatial head: pooling, sigmoid, Eq. 4 counts */
+#define MSAO_NUM_KERNELS 5
 
 /* When enabled, every launch is bracketed by a pair of HIP events recorded on
  * the caller's stream. */

@@ -21,7 +21,8 @@ NMOD = 4
 TEXT, IMAGE, VIDEO, AUDIO = 0, 1, 2, 3
 F32, BF16 = 0, 1
 FLAG_TEMPORAL_LITERAL = 1
-KERNEL_SCORE, KERNEL_POST, KERNEL_GATHER, KERNEL_ENTROPY, NUM_KERNELS = 0, 1, 2, 3, 4
+KERNEL_SCORE, KERNEL_POST, KERNEL_GATHER, KERNEL_ENTROPY, KERNEL_HEAD, NUM_KERNELS = 0, 1, 2, 3, 4, 5
+MODAL_DESC = 8
 DECIDE_HOLD, DECIDE_SEND, DECIDE_OFFLOAD = 0, 1, 2
 
 STATUS = {0: "MSAO_OK", 1: "MSAO_ERR_INVALID_ARG", 2: "MSAO_ERR_ALIGNMENT", 3: "MSAO_ERR_WORKSPACE",
@@ -57,6 +58,15 @@ class MsaoReqOut(ctypes.Structure):
 
 class MsaoSelectOut(ctypes.Structure):
     _fields_ = [(n, _P) for n in ("keep", "kept_idx", "kept_count")]
+
+
+class MsaoSpatialHead(ctypes.Structure):
+    _fields_ = [("weight", _P), ("bias", ctypes.c_float), ("grid_w", ctypes.c_int32), ("pool", ctypes.c_int32)]
+
+
+class MsaoModalMlp(ctypes.Structure):
+    _fields_ = [("w1", _P), ("b1", _P), ("w2", _P), ("b2", ctypes.c_float), ("hidden", ctypes.c_int32),
+                ("prompt_dim", ctypes.c_int32), ("prompt", _P)]
 
 
 class MsaoEntropyOut(ctypes.Structure):
@@ -117,6 +127,8 @@ SIGNATURES = [
     ("msao_plan_destroy", None, [_P]),
     ("msao_set_profiling", ctypes.c_int, [_P, ctypes.c_int]),
     ("msao_kernel_times", ctypes.c_int, [_P, _P]),
+    ("msao_mas_score_learned", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P,
+                                              _P, _P, _P, ctypes.c_size_t, _P]),
     ("msao_draft_entropy", ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
                                           ctypes.c_float, _P, _P]),
     ("msao_sched_default_params", MsaoSchedParams, []),
@@ -585,3 +597,56 @@ def expected_spec_tokens(p: float) -> float:
 def expected_e2e_latency(**terms) -> float:
     m = MsaoLatencyModel(**terms)
     return lib().msao_expected_e2e_latency(_addr(m))
+
+
+# ---- Sec. 4.1.1 Eq. 3 and Sec. 4.1.3 Eq. 6 with caller weights ----------------
+
+def msao_mas_score_learned(segments, n_requests, params=None, heads=None, mlp=None, alpha=None, ctx=None,
+                           outputs=None, stream=None):
+    """msao_mas_score with learned probe heads: heads[s] is None or a dict
+    (weight=[hidden] device tensor in the segment's dtype, bias, grid_w, pool);
+    mlp is None or a dict of device float32 tensors (w1 [hidden, prompt_dim +
+    8], b1, w2, prompt [n_requests, prompt_dim]) and b2. Returns
+    (outputs, extra) with extra = importance, alpha and desc device tensors."""
+    device = _device_of(segments)
+    ctx = ctx or default_context(device.index if device.index is not None else torch.cuda.current_device())
+    o = outputs or Outputs(segments, n_requests, compact=False)
+    segt = segment_table(segments)
+    prm = params_struct(params)
+    n, R = len(segments), n_requests
+    keep = [segt, prm]
+    harr = None
+    if heads is not None:
+        harr = (MsaoSpatialHead * max(1, n))()
+        for i, h in enumerate(heads):
+            if h is None:
+                continue
+            w = h["weight"]
+            keep.append(w)
+            harr[i] = MsaoSpatialHead(w.data_ptr(), float(h.get("bias", 0.0)), int(h.get("grid_w", 0)),
+                                      int(h.get("pool", 1)))
+        keep.append(harr)
+    m = None
+    if mlp is not None:
+        m = MsaoModalMlp(mlp["w1"].data_ptr(), mlp["b1"].data_ptr(), mlp["w2"].data_ptr(), float(mlp.get("b2", 0.0)),
+                         int(mlp["b1"].numel()), int(mlp["prompt"].shape[1]) if mlp.get("prompt") is not None else 0,
+                         mlp["prompt"].data_ptr() if mlp.get("prompt") is not None else None)
+        keep.append(m)
+    al = None
+    if alpha is not None:
+        vals = list(alpha)
+        al = (ctypes.c_float * len(vals))(*vals)
+        keep.append(al)
+    extra = {"importance": torch.empty(max(o.ntok, 1), dtype=torch.float32, device=device)[:o.ntok],
+             "alpha": torch.empty(R * NMOD, dtype=torch.float32, device=device),
+             "desc": torch.empty(R * NMOD * MODAL_DESC, dtype=torch.float32, device=device)}
+    st = stream if stream is not None else torch.cuda.current_stream(device)
+    _check(lib().msao_mas_score_learned(ctx.handle, segt, n, R, _addr(prm),
+                                        ctypes.cast(harr, _P) if harr is not None else None,
+                                        _addr(m) if m is not None else None, al, _addr(o.c_tok),
+                                        _ptr(extra["importance"]) if o.ntok else None, _addr(o.c_frm),
+                                        _addr(o.c_req), _ptr(extra["alpha"]), _ptr(extra["desc"]),
+                                        _ptr(o.workspace), ctypes.c_size_t(o.ws_bytes), ctypes.c_void_p(st.cuda_stream)),
+           ctx)
+    extra["_keep"] = keep
+    return o, extra

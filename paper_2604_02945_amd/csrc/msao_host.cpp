@@ -131,11 +131,16 @@ struct Plan {
     int max_n = 0;                 // largest segment (LDS key staging)
     bool any_temporal = false, any_guided = false;
     bool any_copy = false;         // some segment is compacted by the scoring pass
+    // learned calls (Eq. 3 heads, Eq. 6 descriptors)
+    bool learned = false;
+    std::vector<int32_t> hb_seg;   // segment of each head block (one per frame of a segment with a head)
+    int max_head_p = 0;            // largest frame among segments with a head
+    size_t off_hbseg = 0, off_partial_x = 0, off_proj = 0, off_head_count = 0;
     size_t off_seg = 0, off_wi = 0, off_gi = 0, off_rmoff = 0, off_rmseg = 0, off_tseg = 0, off_alpha = 0;
     size_t table_bytes = 0, off_partial = 0, total_bytes = 0;
 };
 
-size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi)
+size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t n_hb = 0)
 {
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -150,24 +155,35 @@ size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi)
     pl.off_rmseg = take(sizeof(WiRange) * (size_t)std::max(n, 1));
     pl.off_tseg = take(sizeof(int32_t) * (size_t)std::max(n, 1));
     pl.off_alpha = take(sizeof(float) * (size_t)std::max(R * kNumMod, 1));
+    pl.off_hbseg = take(sizeof(int32_t) * (size_t)std::max<int64_t>(n_hb, 1));
     pl.table_bytes = o;
     return o;
 }
 
-// Workspace bound that does not depend on tuning: work items and gather items
-// never outnumber tokens, so one Partial and two table entries per token.
+// Workspace bound that does not depend on tuning: work items, gather items
+// and head blocks never outnumber tokens, so one Partial and table entries
+// per token, plus what a learned call adds (a PartialX per work item, one
+// projection and one head count per token).
 size_t workspace_bytes_for(int n, int R, int64_t ntok)
 {
     Plan pl;
-    const size_t tb = table_layout(pl, n, R, ntok + n, ntok + n);
-    return align_up(tb, kWsAlign) + sizeof(Partial) * (size_t)std::max<int64_t>(ntok + n, 1);
+    const int64_t items = ntok + n;
+    const size_t tb = table_layout(pl, n, R, items, items, items);
+    return align_up(tb, kWsAlign) + align_up(sizeof(Partial) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
+           align_up(sizeof(PartialX) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
+           align_up(sizeof(float) * (size_t)std::max<int64_t>(ntok, 1), kWsAlign) +
+           align_up(sizeof(uint32_t) * (size_t)std::max<int64_t>(items, 1), kWsAlign);
 }
 
 // fuse_copy: a full run with compaction, where segments that keep every row
 // are copied by the scoring pass (they get no gather items).
 void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* p,
-                const float* alpha, const int64_t* out_off, Plan& pl, bool fuse_copy = false)
+                const float* alpha, const int64_t* out_off, Plan& pl, bool fuse_copy = false,
+                const msao_spatial_head* heads = nullptr, bool learned = false)
 {
+    pl.learned = learned;
+    pl.hb_seg.clear();
+    pl.max_head_p = 0;
     pl.seg.resize((size_t)n);
     pl.seg_wi.assign((size_t)n + 1, 0);
     pl.seg_gi.assign((size_t)n + 1, 0);
@@ -205,6 +221,15 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         d.k = s.keep_ratio < 0.0f ? -1 : (int32_t)keep_count(s.keep_ratio, N);
         d.cap = d.k < 0 ? (int32_t)N : d.k;
         d.copy_in_score = (fuse_copy && out_off && N > 0 && d.k == (int32_t)N) ? 1 : 0;
+        if (learned && heads && heads[i].weight && N > 0) {
+            d.head_w = (const uint8_t*)heads[i].weight;
+            d.head_b = heads[i].bias;
+            d.grid_w = heads[i].grid_w > 0 ? heads[i].grid_w : s.tokens_per_frame;
+            d.pool = heads[i].pool;
+            d.hb_begin = (int32_t)pl.hb_seg.size();
+            for (int f = 0; f < s.n_frames; ++f) pl.hb_seg.push_back(i);
+            pl.max_head_p = std::max(pl.max_head_p, s.tokens_per_frame);
+        }
         // scoring work items, one wavefront each
         int items = 0;
         if (d.temporal) {
@@ -250,14 +275,15 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         pl.rm[(size_t)x].rng_begin = count[(size_t)x];
         pl.rm[(size_t)x].rng_end = count[(size_t)x + 1];
     }
-    pl.rm_rng.assign((size_t)std::max(n, 1), WiRange{0, 0});
+    pl.rm_rng.assign((size_t)std::max(n, 1), WiRange{0, 0, 0, 0});
     for (int i = 0; i < n; ++i) {
         const msao_segment& s = segs[i];
         const DevSeg& d = pl.seg[(size_t)i];
         RmEntry& e = pl.rm[(size_t)(s.request * kNumMod + s.modality)];
         e.ntok += (uint64_t)d.n_tok;
         if (d.temporal) e.qbits += (uint64_t)(d.T - 1) * (uint64_t)d.P * (uint64_t)d.C;
-        pl.rm_rng[(size_t)count[(size_t)(s.request * kNumMod + s.modality)]++] = WiRange{pl.seg_wi[(size_t)i], pl.seg_wi[(size_t)i + 1]};
+        pl.rm_rng[(size_t)count[(size_t)(s.request * kNumMod + s.modality)]++] =
+            WiRange{pl.seg_wi[(size_t)i], pl.seg_wi[(size_t)i + 1], i, 0};
     }
     pl.wi_seg.resize((size_t)pl.n_wi);
     pl.gi_seg.resize((size_t)pl.n_gwi);
@@ -268,9 +294,15 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
     pl.alpha.assign((size_t)std::max(R * kNumMod, 1), 0.0f);
     if (alpha)
         for (int x = 0; x < R * kNumMod; ++x) pl.alpha[(size_t)x] = alpha[x];
-    table_layout(pl, n, R, pl.n_wi, pl.n_gwi);
+    table_layout(pl, n, R, pl.n_wi, pl.n_gwi, (int64_t)pl.hb_seg.size());
     pl.off_partial = align_up(pl.table_bytes, kWsAlign);
     pl.total_bytes = pl.off_partial + sizeof(Partial) * (size_t)std::max(pl.n_wi, 1);
+    if (learned) {
+        pl.off_partial_x = align_up(pl.total_bytes, kWsAlign);
+        pl.off_proj = align_up(pl.off_partial_x + sizeof(PartialX) * (size_t)std::max(pl.n_wi, 1), kWsAlign);
+        pl.off_head_count = align_up(pl.off_proj + sizeof(float) * (size_t)std::max<int64_t>(pl.ntok, 1), kWsAlign);
+        pl.total_bytes = pl.off_head_count + sizeof(uint32_t) * std::max<size_t>(pl.hb_seg.size(), 1);
+    }
 }
 
 msao_status hip_fail(msao_ctx* ctx, hipError_t e, const char* what)
@@ -322,6 +354,7 @@ msao_status upload(msao_ctx* ctx, const Plan& pl, void* ws, hipStream_t stream)
     put(pl.off_rmseg, pl.rm_rng.data(), sizeof(WiRange) * pl.rm_rng.size());
     put(pl.off_tseg, pl.tseg.data(), sizeof(int32_t) * pl.tseg.size());
     put(pl.off_alpha, pl.alpha.data(), sizeof(float) * pl.alpha.size());
+    put(pl.off_hbseg, pl.hb_seg.data(), sizeof(int32_t) * pl.hb_seg.size());
     if ((e = hipMemcpyAsync(ws, h, pl.table_bytes, hipMemcpyHostToDevice, stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipMemcpyAsync");
     if ((e = hipEventRecord(ctx->stage_ev[slot], stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
@@ -341,6 +374,11 @@ Tables device_tables(const Plan& pl, void* ws, int n, int R, const msao_params* 
     t.tseg = (const int32_t*)(b + pl.off_tseg);
     t.alpha = (const float*)(b + pl.off_alpha);
     t.partial = (Partial*)(b + pl.off_partial);
+    t.partial_x = pl.learned ? (PartialX*)(b + pl.off_partial_x) : nullptr;
+    t.proj = pl.learned ? (float*)(b + pl.off_proj) : nullptr;
+    t.head_count = pl.learned ? (uint32_t*)(b + pl.off_head_count) : nullptr;
+    t.hb_seg = (const int32_t*)(b + pl.off_hbseg);
+    t.n_hb = (int32_t)pl.hb_seg.size();
     t.n = n;
     t.R = R;
     t.n_wi = pl.n_wi;
@@ -411,6 +449,7 @@ int run_score(const void* a, void* s, void* e0, void* e1) { return launch_score(
 int run_post(const void* a, void* s, void* e0, void* e1) { return launch_post(*(const PostArgs*)a, s, e0, e1); }
 int run_gather(const void* a, void* s, void* e0, void* e1) { return launch_gather(*(const GatherArgs*)a, s, e0, e1); }
 int run_entropy(const void* a, void* s, void* e0, void* e1) { return launch_entropy(*(const EntArgs*)a, s, e0, e1); }
+int run_head(const void* a, void* s, void* e0, void* e1) { return launch_head(*(const HeadArgs*)a, s, e0, e1); }
 
 #define MSAO_TRY(x)                                                                                                   \
     do {                                                                                                              \
@@ -632,6 +671,7 @@ msao_status msao_mas_score(msao_ctx* ctx, const msao_segment* segs, int n, int R
     hipStream_t st = (hipStream_t)stream;
     MSAO_TRY(upload(ctx, pl, ws, st));
     ScoreArgs sa;
+    std::memset(&sa, 0, sizeof sa);
     sa.t = device_tables(pl, ws, n, R, params);
     sa.tok = token_out(tok);
     sa.out = nullptr;
@@ -738,12 +778,95 @@ msao_status msao_compact(msao_ctx* ctx, const msao_segment* segs, int n, const i
     hipStream_t st = (hipStream_t)stream;
     MSAO_TRY(upload(ctx, pl, ws, st));
     GatherArgs ga;
+    std::memset(&ga, 0, sizeof ga);
     ga.t = device_tables(pl, ws, n, R, &p);
     ga.kept_idx = kept_idx;
     ga.kept_count = kept_count;
     ga.out = (uint8_t*)out;
     ga.out_bytes = out_bytes;
     return launched(ctx, MSAO_KERNEL_GATHER, st, run_gather, &ga);
+}
+
+msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
+                                   const msao_spatial_head* heads, const msao_modal_mlp* mlp, const float* alpha,
+                                   const msao_token_out* tok, float* importance, const msao_frame_out* frm,
+                                   const msao_req_out* req, float* alpha_out, float* desc, void* ws, size_t ws_bytes,
+                                   void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
+    char buf[160];
+    for (int i = 0; heads && i < n; ++i) {
+        const msao_spatial_head& h = heads[i];
+        if (!h.weight) continue;
+        auto bad = [&](msao_status st, const char* what) {
+            std::snprintf(buf, sizeof buf, "head of segment %d: %s", i, what);
+            return fail(&ctx->err, st, buf);
+        };
+        if (((uintptr_t)h.weight) % 16 != 0) return bad(MSAO_ERR_ALIGNMENT, "weight is not 16-byte aligned");
+        if (!std::isfinite(h.bias)) return bad(MSAO_ERR_INVALID_ARG, "bias is not finite");
+        if (h.pool < 1 || h.pool > kMaxPool || h.pool % 2 == 0) return bad(MSAO_ERR_INVALID_ARG, "pool must be odd, 1..15");
+        const int P = segs[i].tokens_per_frame;
+        if (P > kMaxHeadFrame) return bad(MSAO_ERR_UNSUPPORTED, "more than 16384 tokens per frame");
+        if (h.grid_w < 0 || (h.grid_w > 0 && P % h.grid_w != 0))
+            return bad(MSAO_ERR_INVALID_ARG, "grid_w must be 0 or divide tokens_per_frame");
+    }
+    if (mlp) {
+        if (!mlp->w1 || !mlp->b1 || !mlp->w2) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "MLP weights are NULL");
+        if (mlp->hidden < 1 || mlp->hidden > 4096) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "MLP hidden out of range");
+        if (mlp->prompt_dim < 0 || mlp->prompt_dim > 16384)
+            return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "MLP prompt_dim out of range");
+        if (mlp->prompt_dim > 0 && !mlp->prompt) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "prompt is NULL");
+        if (!std::isfinite(mlp->b2)) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "b2 is not finite");
+        MSAO_TRY(check_out_alignment(ctx, {{mlp->w1, 4}, {mlp->b1, 4}, {mlp->w2, 4}, {mlp->prompt, 4}}));
+    }
+    Plan pl;
+    build_plan(ctx, segs, n, R, params, alpha, nullptr, pl, false, heads, true);
+    MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
+    const bool want_frames = frm && (frm->dframe || frm->sim || frm->gamma) && pl.nframes > 0;
+    if (want_frames && !(tok && tok->d))
+        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "per-frame outputs need tok->d");
+    if (tok) MSAO_TRY(check_out_alignment(ctx, {{tok->z, 4}, {tok->l1, 4}, {tok->l2, 4}, {tok->info, 4}, {tok->d, 4}, {tok->res, 4}}));
+    if (frm) MSAO_TRY(check_out_alignment(ctx, {{frm->dframe, 8}, {frm->sim, 4}, {frm->gamma, 4}}));
+    if (req) MSAO_TRY(check_out_alignment(ctx, {{req->agg, 8}, {req->rho, 4}, {req->temporal, 4}, {req->beta, 4}, {req->mas, 4}}));
+    MSAO_TRY(check_out_alignment(ctx, {{importance, 4}, {alpha_out, 4}, {desc, 4}}));
+    DeviceGuard guard(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    MSAO_TRY(upload(ctx, pl, ws, st));
+    ScoreArgs sa;
+    std::memset(&sa, 0, sizeof sa);
+    sa.t = device_tables(pl, ws, n, R, params);
+    sa.tok = token_out(tok);
+    sa.mode = kModeScore;
+    sa.xcd_order = xcd_order_for(ctx, false);
+    sa.learned = 1;
+    sa.importance = importance;
+    MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
+    if (!pl.hb_seg.empty()) {
+        HeadArgs ha;
+        std::memset(&ha, 0, sizeof ha);
+        ha.t = sa.t;
+        ha.importance = importance;
+        ha.max_p = pl.max_head_p;
+        MSAO_TRY(launched(ctx, MSAO_KERNEL_HEAD, st, run_head, &ha));
+    }
+    PostArgs pa;
+    std::memset(&pa, 0, sizeof pa);
+    pa.t = sa.t;
+    if (req) pa.req = ReqOut{req->agg, req->rho, req->temporal, req->beta, req->mas, req->present};
+    if (frm) pa.frm = FrameOut{frm->dframe, frm->sim, frm->gamma};
+    pa.d = tok ? tok->d : nullptr;
+    pa.learned = 1;
+    if (mlp) {
+        pa.use_mlp = 1;
+        pa.mlp = ModalMlp{mlp->w1, mlp->b1, mlp->w2, mlp->b2, mlp->hidden, mlp->prompt_dim, mlp->prompt};
+        pa.keys_cap = (mlp->prompt_dim + kDesc + 1) / 2;  // LDS for [p; z] as floats
+    }
+    pa.alpha_out = alpha_out;
+    pa.desc_out = desc;
+    pa.n_req_blocks = R;
+    pa.n_frame_blocks = want_frames ? (int)pl.nframes : 0;
+    return launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa);
 }
 
 msao_status msao_draft_entropy(msao_ctx* ctx, const void* logits, int64_t rows, int64_t vocab, int64_t row_stride,
@@ -808,6 +931,7 @@ msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const ms
                         int64_t out_bytes, hipStream_t st)
 {
     ScoreArgs sa;
+    std::memset(&sa, 0, sizeof sa);
     sa.t = t;
     sa.tok = token_out(tok);
     sa.out = (uint8_t*)out;
@@ -832,6 +956,7 @@ msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const ms
     MSAO_TRY(launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa));
     if (!out || t.n_gwi == 0) return MSAO_OK;
     GatherArgs ga;
+    std::memset(&ga, 0, sizeof ga);
     ga.t = t;
     ga.kept_idx = sel->kept_idx;
     ga.kept_count = sel->kept_count;

@@ -35,6 +35,12 @@ struct DevSeg {
     int32_t cap;           // compaction capacity in rows
     int32_t g_begin;       // first gather work item
     int32_t copy_in_score; // every row is kept: the scoring pass writes the compacted rows itself
+    // learned spatial head (Eq. 3), set only by learned calls
+    const uint8_t* head_w; // [C] in the segment's dtype; NULL: no head
+    float head_b;
+    int32_t grid_w;        // patches per row of a frame's grid
+    int32_t pool;          // odd AvgPool window
+    int32_t hb_begin;      // first head block (one per frame)
 };
 
 // Integer partial sums of one scoring work item (no atomics, no zeroing).
@@ -55,6 +61,15 @@ struct RmEntry {
 
 struct WiRange {
     int32_t begin, end;    // scoring work items of one segment
+    int32_t seg, pad_;     // that segment
+};
+
+// More sums of one scoring work item, for the modality descriptor of Eq. 6
+// (learned calls only).
+struct PartialX {
+    uint32_t asum;         // active channels over the item's tokens
+    float l1, l2;          // sums of the tokens' L1 and L2
+    uint32_t pad_;
 };
 
 // Device pointers into the workspace, plus scalars, passed by value.
@@ -67,6 +82,12 @@ struct Tables {
     const int32_t* tseg;     // [n_tseg] temporal segment ids in table order
     const float* alpha;      // [R*4] relevance logits
     Partial* partial;        // [n_wi]
+    // learned calls only
+    PartialX* partial_x;     // [n_wi]
+    float* proj;             // [Ntot] w . x of tokens of segments with a head
+    uint32_t* head_count;    // [n_hb] tokens with importance < tau_s, per head block
+    const int32_t* hb_seg;   // [n_hb] segment of each head block
+    int32_t n_hb;
     int32_t n, R, n_wi, n_gwi, n_tseg, n_frames;
     float tau, tau_s;
     float lam_s[kNumMod], lam_t[kNumMod];
@@ -86,6 +107,17 @@ struct SelOut {
     uint8_t* keep; int32_t* kept_idx; int32_t* kept_count;
 };
 
+// The relevance MLP of Eq. 6 (device pointers).
+struct ModalMlp {
+    const float* w1;       // [hidden][prompt_dim + kDesc]
+    const float* b1;       // [hidden]
+    const float* w2;       // [hidden]
+    float b2;
+    int32_t hidden, prompt_dim;
+    const float* prompt;   // [R][prompt_dim]
+};
+constexpr int kDesc = 8;   // entries of the modality descriptor z_m
+
 // Roles of the post-scoring launch.
 struct PostArgs {
     Tables t;
@@ -100,6 +132,12 @@ struct PostArgs {
     int32_t n_frame_blocks;// then one per temporal frame
     int32_t temporal_only;// request role writes only the temporal term
     int32_t keys_cap;     // selection keys staged in LDS per block (larger segments re-read z, d)
+    // learned calls: head counts and descriptors feed Eq. 4, Eq. 6 gives alpha
+    int32_t learned;
+    int32_t use_mlp;
+    ModalMlp mlp;
+    float* alpha_out;     // [R*4] (NULL: not written)
+    float* desc_out;      // [R*4*kDesc]
 };
 
 struct ScoreArgs {
@@ -108,7 +146,20 @@ struct ScoreArgs {
     uint8_t* out;         // compaction output for copy_in_score segments (NULL: none)
     int32_t mode;
     int32_t xcd_order;    // 1: each XCD takes one contiguous range of workgroups
+    int32_t learned;      // learned call: projections, importance of head-less tokens, PartialX
+    float* importance;    // [Ntot] (learned calls; NULL: not written)
 };
+
+// Pooling, sigmoid and the Eq. 4 test of the learned spatial head: one
+// block per frame of a segment with a head.
+struct HeadArgs {
+    Tables t;
+    float* importance;    // [Ntot] (NULL: not written)
+    int32_t max_p;        // largest frame among segments with a head (LDS staging)
+};
+constexpr int kHeadBlock = 256;
+constexpr int kMaxHeadFrame = 16384;  // tokens per frame of a segment with a head (LDS)
+constexpr int kMaxPool = 15;
 
 struct GatherArgs {
     Tables t;
@@ -145,6 +196,7 @@ int launch_entropy(const EntArgs& a, void* stream, void* ev0, void* ev1);
 int launch_score(const ScoreArgs& a, void* stream, void* ev0, void* ev1);
 int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1);
 int launch_gather(const GatherArgs& a, void* stream, void* ev0, void* ev1);
+int launch_head(const HeadArgs& a, void* stream, void* ev0, void* ev1);
 
 constexpr int kScoreBlock = 256;   // 4 wavefronts, one work item each
 #ifndef MSAO_POST_BLOCK

@@ -276,9 +276,10 @@ struct TokStat {
 struct TokBuf {
     uint32_t act, d;
     float l1, l2, res;
+    float y;        // learned calls: the head's projection w . x
 };
 
-__device__ __forceinline__ void tokbuf_put(TokBuf& b, int slot, int lane, const TokStat& s)
+__device__ __forceinline__ void tokbuf_put(TokBuf& b, int slot, int lane, const TokStat& s, float y = 0.0f)
 {
     if (lane == slot) {
         b.act = s.act;
@@ -286,17 +287,65 @@ __device__ __forceinline__ void tokbuf_put(TokBuf& b, int slot, int lane, const 
         b.l1 = s.l1;
         b.l2 = s.l2;
         b.res = s.res;
+        b.y = y;
     }
+}
+
+// Per-lane state of a learned call's work item: sums of the item's tokens for
+// the modality descriptor of Eq. 6 (wave-uniform values).
+struct Lrn {
+    uint32_t asum;
+    float l1, l2;
+};
+
+__device__ __forceinline__ void lrn_add(Lrn& l, const TokStat& s)
+{
+    l.asum += s.act;
+    l.l1 += s.l1;
+    l.l2 += s.l2;
+}
+
+// Partial dot product of a 16-byte chunk of a row with the same chunk of the
+// head's weights (Eq. 3's 1x1 convolution), products exact in fp32 for bf16.
+template <int DT>
+__device__ __forceinline__ float dot_chunk(const vec4& x, const vec4& w, float acc)
+{
+    if constexpr (DT == kBF16) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc = dot2(x[k], w[k], acc);
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc = fmaf(__uint_as_float(x[k]), __uint_as_float(w[k]), acc);
+    }
+    return acc;
+}
+
+// The head's weights as NU 1-KiB units of this lane (zero without a head;
+// the resource cuts the ragged last unit).
+template <int NU>
+__device__ __forceinline__ void load_head(vec4 (&wv)[NU], const DevSeg& sg, int voff)
+{
+    const rsrc_t rw = make_rsrc(sg.head_w, sg.head_w ? sg.nchunk * 16 : 0);
+#pragma unroll
+    for (int u = 0; u < NU; ++u) wv[u] = bload_gather(rw, voff + u * 1024);
 }
 
 // Writes tokens first_row + j * row_step (j < count) of the segment from
 // lanes j: z = C - active count, L1, L2, info = 1 - (lambda_s z + lambda_t e)/C
 // with e = C - d for temporal tokens, and d, res (zero outside temporal segments).
-__device__ __forceinline__ void tokbuf_flush(const TokenOut& o, const DevSeg& sg, const TokBuf& b, int first_row,
+// Learned calls also write the projection of tokens of segments with a head,
+// and the density importance a / C of the other tokens.
+template <bool LR>
+__device__ __forceinline__ void tokbuf_flush(const ScoreArgs& a, const DevSeg& sg, const TokBuf& b, int first_row,
                                              int row_step, int count, int lane, bool temporal, int mode)
 {
     if (lane >= count) return;
+    const TokenOut& o = a.tok;
     const int g = sg.tok_off + first_row + lane * row_step;
+    if constexpr (LR) {
+        if (sg.head_w) a.t.proj[g] = b.y;
+        else if (a.importance) a.importance[g] = (float)b.act / (float)sg.C;
+    }
     const uint32_t z = (uint32_t)sg.C - b.act;
     if (mode == kModeScore) {
         if (o.z) o.z[g] = z;
@@ -355,9 +404,10 @@ __device__ __forceinline__ void load_rows(vec4 (&v)[RPI][NU], const DevSeg& sg, 
 // statistics go to slot (row - r0) & 63 of the token buffer, which is written
 // out when it holds 64 rows or the item ends (RPI divides 64, so a batch
 // never straddles a flush).
-template <int DT, int NU, int RPI>
+template <int DT, int NU, int RPI, bool LR>
 __device__ __forceinline__ void rows_batch(const ScoreArgs& a, const DevSeg& sg, const vec4 (&v)[RPI][NU],
-                                           int r0, int r, int r1, int lane, uint32_t& nsp, TokBuf& tb)
+                                           int r0, int r, int r1, int lane, uint32_t& nsp, TokBuf& tb,
+                                           const vec4 (&wv)[NU], Lrn& lr)
 {
     static_assert(64 % RPI == 0, "a row batch must divide the token buffer");
     const bool copy = a.out && sg.copy_in_score;
@@ -366,13 +416,23 @@ __device__ __forceinline__ void rows_batch(const ScoreArgs& a, const DevSeg& sg,
         if (r + i >= r1) break;
         if (copy) copy_row_out<NU>(a, sg, r + i, v[i], lane * 16);
         const TokStat s = row_stats<DT, NU>(v[i], a.t.tau, bf16_thresholds(a.t.tau));
-        tokbuf_put(tb, (r + i - r0) & 63, lane, s);
+        float y = 0.0f;
+        if constexpr (LR) {
+            if (sg.head_w) {
+                float acc = 0.0f;
+#pragma unroll
+                for (int u = 0; u < NU; ++u) acc = dot_chunk<DT>(v[i][u], wv[u], acc);
+                y = wave_sum(acc);
+            }
+            lrn_add(lr, s);
+        }
+        tokbuf_put(tb, (r + i - r0) & 63, lane, s, y);
         nsp += s.act < (uint32_t)sg.A_s;
     }
     const int done = min(r + RPI, r1);
     if (((done - r0) & 63) == 0 || done == r1) {
         const int first = (done - 1) - ((done - 1 - r0) & 63);
-        tokbuf_flush(a.tok, sg, tb, first, 1, done - first, lane, false, kModeScore);
+        tokbuf_flush<LR>(a, sg, tb, first, 1, done - first, lane, false, kModeScore);
     }
 }
 
@@ -385,18 +445,20 @@ __device__ __forceinline__ void rows_batch(const ScoreArgs& a, const DevSeg& sg,
 // the next batch is in flight while the current one is reduced. Wider rows
 // already keep NU KiB in flight per wavefront and are single-buffered, which
 // holds the data registers at 32 per lane.
-template <int DT, int NU>
+template <int DT, int NU, bool LR>
 __device__ __forceinline__ void score_rows(const ScoreArgs& a, const DevSeg& sg, int r0, int r1,
-                                           int lane, uint32_t& nsp)
+                                           int lane, uint32_t& nsp, Lrn& lr)
 {
     constexpr int RPI = NU >= MSAO_ROW_BATCH_UNITS ? 1 : MSAO_ROW_BATCH_UNITS / NU;
     const int voff = lane * 16;
     TokBuf tb{};
+    vec4 wv[NU];
+    if constexpr (LR) load_head<NU>(wv, sg, voff);
     if constexpr (NU > 4) {
         for (int r = r0; r < r1; ++r) {
             vec4 A[1][NU];
             load_rows<NU, 1>(A, sg, r, r1, voff);
-            rows_batch<DT, NU, 1>(a, sg, A, r0, r, r1, lane, nsp, tb);
+            rows_batch<DT, NU, 1, LR>(a, sg, A, r0, r, r1, lane, nsp, tb, wv, lr);
         }
     } else {
         vec4 A[RPI][NU], B[RPI][NU];
@@ -404,11 +466,11 @@ __device__ __forceinline__ void score_rows(const ScoreArgs& a, const DevSeg& sg,
         int r = r0;
         while (true) {
             if (r + RPI < r1) load_rows<NU, RPI>(B, sg, r + RPI, r1, voff);
-            rows_batch<DT, NU, RPI>(a, sg, A, r0, r, r1, lane, nsp, tb);
+            rows_batch<DT, NU, RPI, LR>(a, sg, A, r0, r, r1, lane, nsp, tb, wv, lr);
             r += RPI;
             if (r >= r1) break;
             if (r + RPI < r1) load_rows<NU, RPI>(A, sg, r + RPI, r1, voff);
-            rows_batch<DT, NU, RPI>(a, sg, B, r0, r, r1, lane, nsp, tb);
+            rows_batch<DT, NU, RPI, LR>(a, sg, B, r0, r, r1, lane, nsp, tb, wv, lr);
             r += RPI;
             if (r >= r1) break;
         }
@@ -416,20 +478,22 @@ __device__ __forceinline__ void score_rows(const ScoreArgs& a, const DevSeg& sg,
 }
 
 // Any row width: units processed in blocks of 4.
-template <int DT>
+template <int DT, bool LR>
 __device__ void score_rows_generic(const ScoreArgs& a, const DevSeg& sg, int r0, int r1, int lane,
-                                   uint32_t& nsp)
+                                   uint32_t& nsp, Lrn& lr)
 {
     const float tau = a.t.tau;
     const Thr th = bf16_thresholds(tau);
     const int nu = (sg.nchunk + kWave - 1) / kWave;
     const int rb = sg.nchunk * 16;
     const bool copy = a.out && sg.copy_in_score;
+    const rsrc_t rw = make_rsrc(sg.head_w, LR && sg.head_w ? rb : 0);
     TokBuf tb{};
     for (int r = r0; r < r1; ++r) {
         const rsrc_t rs = make_rsrc(sg.data + (int64_t)r * sg.stride_bytes, rb);
         const rsrc_t rd = make_rsrc(a.out + sg.out_off + (int64_t)r * rb, copy ? rb : 0);
         TokStat s{0u, 0u, 0.0f, 0.0f, 0.0f};
+        float yacc = 0.0f;
         for (int u0 = 0; u0 < nu; u0 += 4) {
             vec4 v[4];
 #pragma unroll
@@ -440,12 +504,24 @@ __device__ void score_rows_generic(const ScoreArgs& a, const DevSeg& sg, int r0,
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u) chunk_stats<DT>(v[u], tau, th, s.act, s.l1, s.l2);
+            if constexpr (LR) {
+                if (sg.head_w) {
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        yacc = dot_chunk<DT>(v[u], bload_gather(rw, ((u0 + u) * kWave + lane) * 16), yacc);
+                }
+            }
         }
         s.l1 = wave_sum(s.l1);
         s.l2 = wave_sum(s.l2);
+        float y = 0.0f;
+        if constexpr (LR) {
+            if (sg.head_w) y = wave_sum(yacc);
+            lrn_add(lr, s);
+        }
         const int slot = (r - r0) & 63;
-        tokbuf_put(tb, slot, lane, s);
-        if (slot == 63 || r == r1 - 1) tokbuf_flush(a.tok, sg, tb, r - slot, 1, slot + 1, lane, false, kModeScore);
+        tokbuf_put(tb, slot, lane, s, y);
+        if (slot == 63 || r == r1 - 1) tokbuf_flush<LR>(a, sg, tb, r - slot, 1, slot + 1, lane, false, kModeScore);
         nsp += s.act < (uint32_t)sg.A_s;
     }
 }
@@ -454,9 +530,9 @@ __device__ void score_rows_generic(const ScoreArgs& a, const DevSeg& sg, int r0,
 // previous frame's values and activity ballots stay in registers; frame t+1
 // is loaded before frame t is reduced. A run that starts after frame 0 first
 // loads frame t0-1 (its halo).
-template <int DT, int NU>
+template <int DT, int NU, bool LR>
 __device__ __forceinline__ void score_chain(const ScoreArgs& a, const DevSeg& sg, int p, int t0, int t1,
-                                            int lane, uint32_t& nsp, uint64_t& dsum)
+                                            int lane, uint32_t& nsp, uint64_t& dsum, Lrn& lr)
 {
     using L = Lane<DT>;
     constexpr int EPC = L::EPC;
@@ -486,22 +562,36 @@ __device__ __forceinline__ void score_chain(const ScoreArgs& a, const DevSeg& sg
     }
     vec4 cur[NU];
     load(cur, t0, true);
+    vec4 wv[NU];
+    if constexpr (LR) load_head<NU>(wv, sg, voff);
     TokBuf tb{};
     for (int t = t0; t < t1; ++t) {
         vec4 nxt[NU];
         load(nxt, t + 1, t + 1 < t1);
         if (a.out && sg.copy_in_score) copy_row_out<NU>(a, sg, t * sg.P + p, cur, voff);
         TokStat s{0u, 0u, 0.0f, 0.0f, 0.0f};
+        float yacc = 0.0f;
+        if constexpr (LR) {
+            if (sg.head_w) {
+#pragma unroll
+                for (int u = 0; u < NU; ++u) yacc = dot_chunk<DT>(cur[u], wv[u], yacc);
+            }
+        }
 #pragma unroll
         for (int u = 0; u < NU; ++u)
             chunk_chain<DT>(cur[u], tau, th, &prev[u * EPC], &pmask[u * EPC], s.act, s.d, s.l1, s.l2, s.res);
         s.l1 = wave_sum(s.l1);
         s.l2 = wave_sum(s.l2);
         s.res = wave_sum(s.res);
+        float y = 0.0f;
+        if constexpr (LR) {
+            if (sg.head_w) y = wave_sum(yacc);
+            lrn_add(lr, s);
+        }
         const int slot = (t - t0) & 63;
-        tokbuf_put(tb, slot, lane, s);
+        tokbuf_put(tb, slot, lane, s, y);
         if (slot == 63 || t == t1 - 1)
-            tokbuf_flush(a.tok, sg, tb, (t - slot) * sg.P + p, sg.P, slot + 1, lane, true, a.mode);
+            tokbuf_flush<LR>(a, sg, tb, (t - slot) * sg.P + p, sg.P, slot + 1, lane, true, a.mode);
         nsp += s.act < (uint32_t)sg.A_s;
         if (t >= 1) dsum += s.d;
 #pragma unroll
@@ -511,9 +601,9 @@ __device__ __forceinline__ void score_chain(const ScoreArgs& a, const DevSeg& sg
 
 // Any row width: the previous frame's row is re-read (it was just read by
 // this wavefront, so it is normally served by the L2).
-template <int DT>
+template <int DT, bool LR>
 __device__ void score_chain_generic(const ScoreArgs& a, const DevSeg& sg, int p, int t0, int t1, int lane,
-                                    uint32_t& nsp, uint64_t& dsum)
+                                    uint32_t& nsp, uint64_t& dsum, Lrn& lr)
 {
     using L = Lane<DT>;
     constexpr int EPC = L::EPC;
@@ -523,12 +613,14 @@ __device__ void score_chain_generic(const ScoreArgs& a, const DevSeg& sg, int p,
     const int nu = (sg.nchunk + kWave - 1) / kWave;
     const int rb = sg.nchunk * 16;
     const bool copy = a.out && sg.copy_in_score;
+    const rsrc_t rw = make_rsrc(sg.head_w, LR && sg.head_w ? rb : 0);
     TokBuf tb{};
     for (int t = t0; t < t1; ++t) {
         const rsrc_t rc = make_rsrc(base + (int64_t)t * fstride, rb);
         const rsrc_t rp = make_rsrc(base + (t > 0 ? (int64_t)(t - 1) * fstride : 0), t > 0 ? rb : 0);
         const rsrc_t rd = make_rsrc(a.out + sg.out_off + (int64_t)(t * sg.P + p) * rb, copy ? rb : 0);
         TokStat s{0u, 0u, 0.0f, 0.0f, 0.0f};
+        float yacc = 0.0f;
         for (int u0 = 0; u0 < nu; u0 += 2) {
             vec4 v[2], w[2];
 #pragma unroll
@@ -540,6 +632,13 @@ __device__ void score_chain_generic(const ScoreArgs& a, const DevSeg& sg, int p,
             if (copy) {
 #pragma unroll
                 for (int u = 0; u < 2; ++u) bstore(v[u], rd, ((u0 + u) * kWave + lane) * 16);
+            }
+            if constexpr (LR) {
+                if (sg.head_w) {
+#pragma unroll
+                    for (int u = 0; u < 2; ++u)
+                        yacc = dot_chunk<DT>(v[u], bload_gather(rw, ((u0 + u) * kWave + lane) * 16), yacc);
+                }
             }
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
@@ -562,54 +661,59 @@ __device__ void score_chain_generic(const ScoreArgs& a, const DevSeg& sg, int p,
         s.l1 = wave_sum(s.l1);
         s.l2 = wave_sum(s.l2);
         s.res = wave_sum(s.res);
+        float yv = 0.0f;
+        if constexpr (LR) {
+            if (sg.head_w) yv = wave_sum(yacc);
+            lrn_add(lr, s);
+        }
         const int slot = (t - t0) & 63;
-        tokbuf_put(tb, slot, lane, s);
+        tokbuf_put(tb, slot, lane, s, yv);
         if (slot == 63 || t == t1 - 1)
-            tokbuf_flush(a.tok, sg, tb, (t - slot) * sg.P + p, sg.P, slot + 1, lane, true, a.mode);
+            tokbuf_flush<LR>(a, sg, tb, (t - slot) * sg.P + p, sg.P, slot + 1, lane, true, a.mode);
         nsp += s.act < (uint32_t)sg.A_s;
         if (t >= 1) dsum += s.d;
     }
 }
 
-template <int DT>
+template <int DT, bool LR>
 __device__ __forceinline__ void dispatch_rows(const ScoreArgs& a, const DevSeg& sg, int r0, int r1, int lane,
-                                              uint32_t& nsp)
+                                              uint32_t& nsp, Lrn& lr)
 {
     const int nu = (sg.nchunk + kWave - 1) / kWave;
     switch (nu) {
-    case 1: score_rows<DT, 1>(a, sg, r0, r1, lane, nsp); break;
-    case 2: score_rows<DT, 2>(a, sg, r0, r1, lane, nsp); break;
-    case 3: score_rows<DT, 3>(a, sg, r0, r1, lane, nsp); break;
-    case 4: score_rows<DT, 4>(a, sg, r0, r1, lane, nsp); break;
-    case 5: score_rows<DT, 5>(a, sg, r0, r1, lane, nsp); break;
-    case 6: score_rows<DT, 6>(a, sg, r0, r1, lane, nsp); break;
-    case 7: score_rows<DT, 7>(a, sg, r0, r1, lane, nsp); break;
-    case 8: score_rows<DT, 8>(a, sg, r0, r1, lane, nsp); break;
-    default: score_rows_generic<DT>(a, sg, r0, r1, lane, nsp); break;
+    case 1: score_rows<DT, 1, LR>(a, sg, r0, r1, lane, nsp, lr); break;
+    case 2: score_rows<DT, 2, LR>(a, sg, r0, r1, lane, nsp, lr); break;
+    case 3: score_rows<DT, 3, LR>(a, sg, r0, r1, lane, nsp, lr); break;
+    case 4: score_rows<DT, 4, LR>(a, sg, r0, r1, lane, nsp, lr); break;
+    case 5: score_rows<DT, 5, LR>(a, sg, r0, r1, lane, nsp, lr); break;
+    case 6: score_rows<DT, 6, LR>(a, sg, r0, r1, lane, nsp, lr); break;
+    case 7: score_rows<DT, 7, LR>(a, sg, r0, r1, lane, nsp, lr); break;
+    case 8: score_rows<DT, 8, LR>(a, sg, r0, r1, lane, nsp, lr); break;
+    default: score_rows_generic<DT, LR>(a, sg, r0, r1, lane, nsp, lr); break;
     }
 }
 
 // Register-resident chains are used while a lane holds at most 16 channels
 // (their activity ballots live in 32 scalar registers); wider rows take the
 // generic path.
-template <int DT>
+template <int DT, bool LR>
 __device__ __forceinline__ void dispatch_chain(const ScoreArgs& a, const DevSeg& sg, int p, int t0, int t1,
-                                               int lane, uint32_t& nsp, uint64_t& dsum)
+                                               int lane, uint32_t& nsp, uint64_t& dsum, Lrn& lr)
 {
     const int nu = (sg.nchunk + kWave - 1) / kWave;
     if constexpr (DT == kBF16) {
         switch (nu) {
-        case 1: score_chain<DT, 1>(a, sg, p, t0, t1, lane, nsp, dsum); break;
-        case 2: score_chain<DT, 2>(a, sg, p, t0, t1, lane, nsp, dsum); break;
-        default: score_chain_generic<DT>(a, sg, p, t0, t1, lane, nsp, dsum); break;
+        case 1: score_chain<DT, 1, LR>(a, sg, p, t0, t1, lane, nsp, dsum, lr); break;
+        case 2: score_chain<DT, 2, LR>(a, sg, p, t0, t1, lane, nsp, dsum, lr); break;
+        default: score_chain_generic<DT, LR>(a, sg, p, t0, t1, lane, nsp, dsum, lr); break;
         }
     } else {
         switch (nu) {
-        case 1: score_chain<DT, 1>(a, sg, p, t0, t1, lane, nsp, dsum); break;
-        case 2: score_chain<DT, 2>(a, sg, p, t0, t1, lane, nsp, dsum); break;
-        case 3: score_chain<DT, 3>(a, sg, p, t0, t1, lane, nsp, dsum); break;
-        case 4: score_chain<DT, 4>(a, sg, p, t0, t1, lane, nsp, dsum); break;
-        default: score_chain_generic<DT>(a, sg, p, t0, t1, lane, nsp, dsum); break;
+        case 1: score_chain<DT, 1, LR>(a, sg, p, t0, t1, lane, nsp, dsum, lr); break;
+        case 2: score_chain<DT, 2, LR>(a, sg, p, t0, t1, lane, nsp, dsum, lr); break;
+        case 3: score_chain<DT, 3, LR>(a, sg, p, t0, t1, lane, nsp, dsum, lr); break;
+        case 4: score_chain<DT, 4, LR>(a, sg, p, t0, t1, lane, nsp, dsum, lr); break;
+        default: score_chain_generic<DT, LR>(a, sg, p, t0, t1, lane, nsp, dsum, lr); break;
         }
     }
 }
@@ -626,6 +730,10 @@ __device__ __forceinline__ int score_block(const ScoreArgs& a)
     return x * per + min(x, rem) + (b >> 3);
 }
 
+// LR: a learned call (Eq. 3 head projections, density importance of tokens
+// without a head, and the descriptor sums of Eq. 6); a separate instance, so
+// that the plain kernel keeps its registers.
+template <bool LR>
 __global__ __launch_bounds__(kScoreBlock) void k_score(ScoreArgs a)
 {
     const int lane = threadIdx.x & (kWave - 1);
@@ -636,12 +744,13 @@ __global__ __launch_bounds__(kScoreBlock) void k_score(ScoreArgs a)
     const int q = w - sg.wi_begin;
     uint32_t nsp = 0;
     uint64_t dsum = 0;
+    Lrn lr{0u, 0.0f, 0.0f};
     if (sg.temporal) {
         const int p = q % sg.P;
         const int t0 = (q / sg.P) * sg.per_item;
         const int t1 = min(sg.T, t0 + sg.per_item);
-        if (sg.dtype == kBF16) dispatch_chain<kBF16>(a, sg, p, t0, t1, lane, nsp, dsum);
-        else dispatch_chain<kF32>(a, sg, p, t0, t1, lane, nsp, dsum);
+        if (sg.dtype == kBF16) dispatch_chain<kBF16, LR>(a, sg, p, t0, t1, lane, nsp, dsum, lr);
+        else dispatch_chain<kF32, LR>(a, sg, p, t0, t1, lane, nsp, dsum, lr);
     } else {
         const int r0 = q * sg.per_item;
         const int r1 = min(sg.n_tok, r0 + sg.per_item);
@@ -652,9 +761,9 @@ __global__ __launch_bounds__(kScoreBlock) void k_score(ScoreArgs a)
                 if (a.tok.res) a.tok.res[sg.tok_off + r] = 0.0f;
             }
         } else if (sg.dtype == kBF16) {
-            dispatch_rows<kBF16>(a, sg, r0, r1, lane, nsp);
+            dispatch_rows<kBF16, LR>(a, sg, r0, r1, lane, nsp, lr);
         } else {
-            dispatch_rows<kF32>(a, sg, r0, r1, lane, nsp);
+            dispatch_rows<kF32, LR>(a, sg, r0, r1, lane, nsp, lr);
         }
     }
     if (lane == 0) {
@@ -663,6 +772,7 @@ __global__ __launch_bounds__(kScoreBlock) void k_score(ScoreArgs a)
         pr.pad_ = 0u;
         pr.dsum = dsum;
         a.t.partial[w] = pr;
+        if constexpr (LR) a.t.partial_x[w] = PartialX{lr.asum, lr.l1, lr.l2, 0u};
     }
 }
 
@@ -684,6 +794,11 @@ struct PostShared {
     unsigned long long lo, hi, red;
     uint64_t nsp[kWaves], dsum[kWaves], ntok[kNumMod], qbits[kNumMod];
     uint32_t digit, below, in_bin, ncand;
+    // learned calls
+    uint64_t asum[kWaves], csum[kWaves];
+    double l1[kWaves], l2[kWaves];
+    float fred[kWaves];
+    float alpha[kNumMod];
 };
 
 // Radix candidates copied out of the staged keys once few remain (LDS entries
@@ -870,6 +985,165 @@ __device__ void role_request(const PostArgs& a, int r, PostShared<NT>& sh)
         if (a.req.beta) a.req.beta[x] = (float)o[m].beta;
         if (a.req.mas) a.req.mas[x] = (float)o[m].mas;
         if (a.req.present) a.req.present[x] = pres[m] ? 1 : 0;
+    }
+}
+
+// The modality descriptor z_m of Eq. 6 (zero for an absent modality).
+__device__ __forceinline__ void modality_descriptor(bool pres, const MasTerms& pre, uint64_t asum, uint64_t csum,
+                                                    double l1, double l2, uint64_t ntok, double* z)
+{
+#pragma clang fp contract(off)
+    z[0] = pres ? 1.0 : 0.0;
+    z[1] = pre.rho;
+    z[2] = pres ? (double)asum / (double)csum : 0.0;
+    z[3] = pres ? l1 / (double)csum : 0.0;
+    z[4] = pres ? sqrt(l2 / (double)csum) : 0.0;
+    z[5] = pre.tterm;
+    z[6] = pre.has_t ? 1.0 : 0.0;
+    z[7] = pres ? log(1.0 + (double)ntok) / 16.0 : 0.0;
+}
+
+__device__ __forceinline__ double wave_sum_f64(double v)
+{
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// Block-wide float sum in a fixed order (wavefront DPP sums, then the
+// wavefronts in order), the same value in every thread.
+template <int NT>
+__device__ __forceinline__ float block_sum_f32(float v, PostShared<NT>& sh)
+{
+    v = wave_sum(v);
+    __syncthreads();
+    if ((threadIdx.x & (kWave - 1)) == 0) sh.fred[threadIdx.x >> 6] = v;
+    __syncthreads();
+    float s = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NT / kWave; ++w) s += sh.fred[w];
+    return s;
+}
+
+// A learned call's request role: Eq. 4 counts from the heads' per-frame
+// counts (from the density test where a segment has no head), the
+// descriptor z_m of every modality, Eq. 6 on [p; z_m] when an MLP is given
+// (alpha from the table otherwise), then the softmax and Eq. 7.
+// The descriptor: 1, rho, sum a / sum C, sum L1 / sum C, sqrt(sum L2 / sum C),
+// the temporal term (0 if none), 1 if it exists, ln(1 + Ntok) / 16.
+template <int NT>
+__device__ void role_request_learned(const PostArgs& a, int r, PostShared<NT>& sh, float* vin)
+{
+    const Tables& t = a.t;
+    constexpr int kParts = (NT / kWave) / kNumMod;
+    const int wid = threadIdx.x >> 6, m = wid % kNumMod, part = wid / kNumMod;
+    const int lane = threadIdx.x & (kWave - 1);
+    const RmEntry e = t.rm[r * kNumMod + m];
+    uint64_t nsp = 0, ds = 0, as = 0, cs = 0;
+    double l1 = 0.0, l2 = 0.0;
+    for (int j = e.rng_begin; j < e.rng_end; ++j) {
+        const WiRange wr = t.rm_rng[j];
+        const DevSeg& sg = t.seg[wr.seg];
+        const bool head = sg.head_w != nullptr;
+        if (part == 0 && lane == 0) cs += (uint64_t)sg.n_tok * (uint64_t)sg.C;
+        for (int w = wr.begin + part * kWave + lane; w < wr.end; w += kParts * kWave) {
+            const Partial pr = t.partial[w];
+            const PartialX px = t.partial_x[w];
+            if (!head) nsp += pr.nsparse;
+            ds += pr.dsum;
+            as += px.asum;
+            l1 += (double)px.l1;
+            l2 += (double)px.l2;
+        }
+        if (head)
+            for (int h = sg.hb_begin + part * kWave + lane; h < sg.hb_begin + sg.T; h += kParts * kWave)
+                nsp += t.head_count[h];
+    }
+    nsp = wave_sum_u64(nsp);
+    ds = wave_sum_u64(ds);
+    as = wave_sum_u64(as);
+    cs = wave_sum_u64(cs);
+    l1 = wave_sum_f64(l1);
+    l2 = wave_sum_f64(l2);
+    __syncthreads();
+    if (lane == 0) {
+        sh.nsp[wid] = nsp;
+        sh.dsum[wid] = ds;
+        sh.asum[wid] = as;
+        sh.csum[wid] = cs;
+        sh.l1[wid] = l1;
+        sh.l2[wid] = l2;
+        if (part == 0) {
+            sh.ntok[m] = e.ntok;
+            sh.qbits[m] = e.qbits;
+        }
+    }
+    __syncthreads();
+    RMAgg g[kNumMod];
+    double z[kNumMod][kDesc];
+    bool pres[kNumMod];
+    MasTerms pre[kNumMod];
+#pragma unroll
+    for (int mm = 0; mm < kNumMod; ++mm) {
+        uint64_t n1 = 0, d1 = 0, a1 = 0, c1 = 0;
+        double s1 = 0.0, s2 = 0.0;
+#pragma unroll
+        for (int q = 0; q < kParts; ++q) {
+            const int w = q * kNumMod + mm;
+            n1 += sh.nsp[w];
+            d1 += sh.dsum[w];
+            a1 += sh.asum[w];
+            c1 += sh.csum[w];
+            s1 += sh.l1[w];
+            s2 += sh.l2[w];
+        }
+        g[mm] = RMAgg{sh.ntok[mm], n1, d1, sh.qbits[mm]};
+        pres[mm] = g[mm].ntok > 0;
+        pre[mm] = MasTerms{0.0, 0.0, 0.0, 0.0, false};
+        if (pres[mm]) pre[mm] = mas_terms(t, g[mm], 1.0, mm);  // rho and the temporal term
+        modality_descriptor(pres[mm], pre[mm], a1, c1, s1, s2, g[mm].ntok, z[mm]);
+    }
+    // Eq. 6: alpha = w2 . relu(W1 [p; z] + b1) + b2, one modality at a time
+    double al[kNumMod];
+    const int P = a.mlp.prompt_dim, IN = P + kDesc;
+#pragma unroll
+    for (int mm = 0; mm < kNumMod; ++mm) {
+        al[mm] = (double)t.alpha[r * kNumMod + mm];
+        if (!a.use_mlp || !pres[mm]) continue;
+        __syncthreads();
+        for (int k = threadIdx.x; k < IN; k += NT)
+            vin[k] = k < P ? a.mlp.prompt[(int64_t)r * P + k] : (float)z[mm][k - P];
+        __syncthreads();
+        float part_sum = 0.0f;
+        for (int j = threadIdx.x; j < a.mlp.hidden; j += NT) {
+            const float* row = a.mlp.w1 + (int64_t)j * IN;
+            float h = a.mlp.b1[j];
+            for (int k = 0; k < IN; ++k) h = fmaf(row[k], vin[k], h);
+            part_sum = fmaf(a.mlp.w2[j], fmaxf(h, 0.0f), part_sum);
+        }
+        al[mm] = (double)(a.mlp.b2 + block_sum_f32<NT>(part_sum, sh));
+    }
+    if (threadIdx.x != 0) return;
+    double beta[kNumMod];
+    modal_softmax(al, pres, beta);
+#pragma unroll
+    for (int mm = 0; mm < kNumMod; ++mm) {
+        const int x = r * kNumMod + mm;
+        const MasTerms o = pres[mm] ? mas_terms(t, g[mm], beta[mm], mm) : MasTerms{0.0, 0.0, 0.0, 0.0, false};
+        if (a.req.agg) {
+            a.req.agg[x * 4 + 0] = g[mm].ntok;
+            a.req.agg[x * 4 + 1] = g[mm].nsparse;
+            a.req.agg[x * 4 + 2] = g[mm].dsum;
+            a.req.agg[x * 4 + 3] = g[mm].qbits;
+        }
+        if (a.req.rho) a.req.rho[x] = (float)o.rho;
+        if (a.req.temporal) a.req.temporal[x] = (float)o.tterm;
+        if (a.req.beta) a.req.beta[x] = (float)o.beta;
+        if (a.req.mas) a.req.mas[x] = (float)o.mas;
+        if (a.req.present) a.req.present[x] = pres[mm] ? 1 : 0;
+        if (a.alpha_out) a.alpha_out[x] = pres[mm] ? (float)al[mm] : 0.0f;
+        if (a.desc_out)
+            for (int k = 0; k < kDesc; ++k) a.desc_out[x * kDesc + k] = (float)z[mm][k];
     }
 }
 
@@ -1180,20 +1454,26 @@ __device__ void role_select(const PostArgs& a, int s, PostShared<NT>& sh, uint64
     else select_and_compact<NT, false>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, lo, hi);
 }
 
-template <int NT>
+// LR: a learned call (request role with head counts, descriptors and the
+// relevance MLP; no selection); a separate instance, so that the plain
+// kernel keeps its registers.
+template <int NT, bool LR>
 __global__ __launch_bounds__(NT) void k_post(PostArgs a)
 {
     __shared__ PostShared<NT> sh;
     extern __shared__ uint64_t keys[];
     // selection blocks first: they are the longest and are dispatched first
     int b = blockIdx.x;
-    if (b < a.n_sel_blocks) {
-        role_select(a, b, sh, keys, a.keys_cap);
-        return;
+    if constexpr (!LR) {
+        if (b < a.n_sel_blocks) {
+            role_select(a, b, sh, keys, a.keys_cap);
+            return;
+        }
+        b -= a.n_sel_blocks;
     }
-    b -= a.n_sel_blocks;
     if (b < a.n_req_blocks) {
-        role_request(a, b, sh);
+        if constexpr (LR) role_request_learned<NT>(a, b, sh, reinterpret_cast<float*>(keys));
+        else role_request(a, b, sh);
         return;
     }
     b -= a.n_req_blocks;
@@ -1288,6 +1568,48 @@ __global__ __launch_bounds__(kGatherBlock) void k_gather(GatherArgs a)
 
 // With ev0/ev1 (profiling), the launch records them at the kernel's own start
 // and end, so their span is the kernel's execution time.
+// ---------------------------------------------------------------- k_head
+
+// Eq. 3 with a learned head for one frame of a segment (P tokens on an
+// H x W grid, token q at row q / W, column q % W): importance
+// M = sigmoid(mean of the projections over the pool x pool window cut to the
+// grid + b), which is Conv1x1(AvgPool(F)) since the 1x1 convolution is
+// linear; then the number of tokens with M < tau_s (Eq. 4).
+__global__ __launch_bounds__(kHeadBlock) void k_head(HeadArgs a)
+{
+    extern __shared__ float ys[];
+    __shared__ uint64_t cnt[kHeadBlock / kWave];
+    const Tables& t = a.t;
+    const int hb = blockIdx.x;
+    const DevSeg sg = t.seg[t.hb_seg[hb]];
+    const int P = sg.P;
+    const int base = sg.tok_off + (hb - sg.hb_begin) * P;
+    for (int q = threadIdx.x; q < P; q += kHeadBlock) ys[q] = t.proj[base + q];
+    __syncthreads();
+    const int W = sg.grid_w > 0 ? sg.grid_w : P, H = P / W, r = (sg.pool - 1) / 2;
+    uint64_t c = 0;
+    for (int q = threadIdx.x; q < P; q += kHeadBlock) {
+        const int i = q / W, j = q % W;
+        const int i0 = max(0, i - r), i1 = min(H - 1, i + r), j0 = max(0, j - r), j1 = min(W - 1, j + r);
+        float sum = 0.0f;
+        for (int ii = i0; ii <= i1; ++ii)
+            for (int jj = j0; jj <= j1; ++jj) sum += ys[ii * W + jj];
+        const float v = sum / (float)((i1 - i0 + 1) * (j1 - j0 + 1)) + sg.head_b;
+        const float M = 1.0f / (1.0f + expf(-v));
+        if (a.importance) a.importance[base + q] = M;
+        c += M < t.tau_s ? 1u : 0u;
+    }
+    c = wave_sum_u64(c);
+    if ((threadIdx.x & (kWave - 1)) == 0) cnt[threadIdx.x >> 6] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t total = 0;
+#pragma unroll
+        for (int w = 0; w < kHeadBlock / kWave; ++w) total += cnt[w];
+        t.head_count[hb] = (uint32_t)total;
+    }
+}
+
 template <typename Args>
 static int launch(void (*kernel)(Args), dim3 grid, dim3 block, size_t lds, void* stream, const Args& a,
                   void* ev0, void* ev1)
@@ -1304,17 +1626,22 @@ int launch_score(const ScoreArgs& a, void* stream, void* ev0, void* ev1)
     if (a.t.n_wi <= 0) return 0;
     const int waves = kScoreBlock / kWave;
     const unsigned grid = (unsigned)((a.t.n_wi + waves - 1) / waves);
-    return launch(k_score, dim3(grid), dim3(kScoreBlock), 0, stream, a, ev0, ev1);
+    if (a.learned) {
+        if (!a.t.partial_x || !a.t.proj) return (int)hipErrorInvalidValue;  // a learned plan's tables
+        return launch(k_score<true>, dim3(grid), dim3(kScoreBlock), 0, stream, a, ev0, ev1);
+    }
+    return launch(k_score<false>, dim3(grid), dim3(kScoreBlock), 0, stream, a, ev0, ev1);
 }
 
-template <int NT>
+template <int NT, bool LR>
 static int launch_post_nt(const PostArgs& a, int blocks, size_t lds, void* stream, void* ev0, void* ev1)
 {
     if (lds > 65536) {
-        const hipError_t e = hipFuncSetAttribute((const void*)k_post<NT>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        const hipError_t e =
+            hipFuncSetAttribute((const void*)k_post<NT, LR>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return (int)e;
     }
-    return launch(k_post<NT>, dim3((unsigned)blocks), dim3(NT), lds, stream, a, ev0, ev1);
+    return launch(k_post<NT, LR>, dim3((unsigned)blocks), dim3(NT), lds, stream, a, ev0, ev1);
 }
 
 // Segments of kPostBigSegment tokens or more are selected by 1024-thread
@@ -1326,8 +1653,23 @@ int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1)
     const int blocks = a.n_req_blocks + a.n_frame_blocks + a.n_sel_blocks;
     if (blocks <= 0) return 0;
     const size_t lds = (size_t)(a.keys_cap + cand_cap_for(a.keys_cap)) * sizeof(uint64_t);
-    if (a.n_sel_blocks > 0 && a.keys_cap >= kPostBigSegment) return launch_post_nt<1024>(a, blocks, lds, stream, ev0, ev1);
-    return launch_post_nt<kPostBlock>(a, blocks, lds, stream, ev0, ev1);
+    if (a.learned && (!a.t.partial_x || !a.t.head_count)) return (int)hipErrorInvalidValue;
+    if (a.learned) return launch_post_nt<kPostBlock, true>(a, a.n_req_blocks + a.n_frame_blocks, lds, stream, ev0, ev1);
+    if (a.n_sel_blocks > 0 && a.keys_cap >= kPostBigSegment)
+        return launch_post_nt<1024, false>(a, blocks, lds, stream, ev0, ev1);
+    return launch_post_nt<kPostBlock, false>(a, blocks, lds, stream, ev0, ev1);
+}
+
+int launch_head(const HeadArgs& a, void* stream, void* ev0, void* ev1)
+{
+    if (a.t.n_hb <= 0) return 0;
+    if (!a.t.proj || !a.t.head_count || a.max_p < 1 || a.max_p > kMaxHeadFrame) return (int)hipErrorInvalidValue;
+    const size_t lds = (size_t)a.max_p * sizeof(float);
+    if (lds > 65536) {
+        const hipError_t e = hipFuncSetAttribute((const void*)k_head, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return (int)e;
+    }
+    return launch(k_head, dim3((unsigned)a.t.n_hb), dim3(kHeadBlock), lds, stream, a, ev0, ev1);
 }
 
 int launch_gather(const GatherArgs& a, void* stream, void* ev0, void* ev1)

@@ -32,6 +32,8 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(B.MsaoSegment) == 48
     assert ctypes.sizeof(B.MsaoParams) == 44
     assert ctypes.sizeof(B.MsaoTokenOut) == 48
+    assert ctypes.sizeof(B.MsaoSpatialHead) == 24
+    assert ctypes.sizeof(B.MsaoModalMlp) == 48
 
 
 def test_default_params_are_the_papers():
