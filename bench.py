@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--no-entropy", action="store_true",
                     help="skip the draft-confidence kernel and Algorithm 1 measurements")
     ap.add_argument("--entropy-steps", type=int, default=100, help="timed launches of the draft-confidence kernel")
+    ap.add_argument("--no-learned", action="store_true",
+                    help="skip the learned-head variant (Eq. 3 heads and the Eq. 6 MLP) of the scoring pass")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (calibrates HBM byte counters)")
     ap.add_argument("--streams", type=int, default=3,
@@ -99,33 +101,37 @@ def algorithmic_bytes(w, kept_count, compact):
     return score + fused, select, gather
 
 
-def committed_traffic(config):
-    """HBM bytes per k_score launch from the committed rocprofv3 counter summary,
-    or None when there is none for this workload or the kernel sources changed
-    since the counters were taken."""
+def _committed(profile, sources):
+    """traffic_bytes_per_launch of a committed rocprofv3 counter summary, or
+    None when it is absent or the kernel sources changed since it was taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "k_score_trimodal_traffic.json")
-    if config != 4 or not os.path.exists(path):
-        return None
-    rec = json.load(open(path))
-    h = hashlib.sha256()
-    for f in ("msao_kernels.hip", "msao_internal.h"):
-        h.update(open(os.path.join(ROOT, "paper_2604_02945_amd", "csrc", f), "rb").read())
-    return rec["traffic_bytes_per_launch"] if rec.get("kernel_source_sha256") == h.hexdigest() else None
-
-
-def committed_entropy_traffic():
-    """HBM bytes per k_entropy launch from the committed counter summary (None
-    if absent or if the kernel sources changed since)."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", "k_entropy_draft_logits_traffic.json")
+    path = os.path.join(ROOT, "profiles", profile)
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
     h = hashlib.sha256()
-    for f in ("msao_entropy.hip", "msao_internal.h"):
+    for f in sources:
         h.update(open(os.path.join(ROOT, "paper_2604_02945_amd", "csrc", f), "rb").read())
     return rec["traffic_bytes_per_launch"] if rec.get("kernel_source_sha256") == h.hexdigest() else None
+
+
+def committed_traffic(config):
+    """HBM bytes per k_score launch on the tri-modal workload (committed counters)."""
+    if config != 4:
+        return None
+    return _committed("k_score_trimodal_traffic.json", ("msao_kernels.hip", "msao_internal.h"))
+
+
+def committed_learned_traffic(config):
+    """HBM bytes per learned k_score launch on the tri-modal workload (committed counters)."""
+    if config != 4:
+        return None
+    return _committed("k_score_learned_trimodal_traffic.json", ("msao_kernels.hip", "msao_internal.h"))
+
+
+def committed_entropy_traffic():
+    """HBM bytes per k_entropy launch (committed counters)."""
+    return _committed("k_entropy_draft_logits_traffic.json", ("msao_entropy.hip", "msao_internal.h"))
 
 
 def entropy_bench(args, dev, ctx):
@@ -193,6 +199,72 @@ def entropy_bench(args, dev, ctx):
                                "sample": f"64 rows x {V} of the same logits, single-threaded C oracle (fp64), {dt:.2f} s"}
     del reps, first
     return res
+
+
+def learned_bench(args, dev, ctx, w, reps, fields):
+    """The scoring pass with learned probe heads (Eq. 3: weights on the image
+    and audio segments, 3x3 and 1x5 AvgPool) and the Eq. 6 relevance MLP (256
+    hidden units over a 1,536-wide prompt embedding plus the 8-entry
+    descriptor), over the same rotated replicas, beside the plain scoring pass.
+    Random weights: the cost does not depend on their values."""
+    import numpy as np
+    import torch
+
+    import paper_2604_02945_amd as msao
+    from workloads import AUDIO, IMAGE
+
+    rng = np.random.default_rng(5)
+    R, n = w.n_requests, len(w.segments)
+    heads = []
+    for s in w.segments:
+        if s.modality in (IMAGE, AUDIO):
+            wt = torch.from_numpy((rng.standard_normal(s.hidden) * 1.5 / np.sqrt(s.hidden)).astype(np.float32))
+            wt = wt.to(dev).to(torch.bfloat16 if s.dtype == "bf16" else torch.float32)
+            heads.append(dict(weight=wt, bias=-0.8 if s.modality == IMAGE else -0.2,
+                              grid_w=24 if s.modality == IMAGE else 0, pool=3 if s.modality == IMAGE else 5))
+        else:
+            heads.append(None)
+    pd, hid = 1536, 256
+    mlp = {"w1": torch.from_numpy((rng.standard_normal((hid, pd + 8)) * 0.05).astype(np.float32)).to(dev),
+           "b1": torch.from_numpy((rng.standard_normal(hid) * 0.1).astype(np.float32)).to(dev),
+           "w2": torch.from_numpy((rng.standard_normal(hid) * 0.1).astype(np.float32)).to(dev), "b2": 0.0,
+           "prompt": torch.from_numpy(rng.standard_normal((R, pd)).astype(np.float32)).to(dev)}
+    outs = [msao.Outputs(segs, R, token_fields=fields, compact=False) for segs in reps]
+    steps = max(1, min(args.steps, 100))
+
+    def kernels(fn):
+        for i in range(len(reps)):
+            fn(i)
+        torch.cuda.synchronize()
+        ctx.set_profiling(True)
+        for i in range(steps):
+            fn(i % len(reps))
+        torch.cuda.synchronize()
+        k = ctx.kernel_times()
+        ctx.set_profiling(False)
+        return k
+
+    k_plain = kernels(lambda i: msao.msao_mas_score(reps[i], R, w.params, ctx=ctx, outputs=outs[i]))
+    k_lrn = kernels(lambda i: msao.msao_mas_score_learned(reps[i], R, w.params, heads=heads, mlp=mlp, ctx=ctx,
+                                                          outputs=outs[i]))
+    ntok = w.n_tokens
+    b_plain = w.input_bytes + 4 * len(fields) * ntok
+    b_lrn = b_plain + 4 * ntok          # + the projection or the density importance of every token
+    gbs = b_lrn / (k_lrn[msao.binding.KERNEL_SCORE] * 1e-3) / 1e9
+    total = k_lrn[msao.binding.KERNEL_SCORE] + k_lrn[msao.binding.KERNEL_HEAD] + k_lrn[msao.binding.KERNEL_POST]
+    return {
+        "workload": f"{w.name}: heads on image (24x24 grid, pool 3) and audio (1500 frames, pool 5), "
+                    f"MLP {hid} x ({pd} + 8)",
+        "kernel_ms": {"score_learned": k_lrn[msao.binding.KERNEL_SCORE], "head": k_lrn[msao.binding.KERNEL_HEAD],
+                      "post_learned": k_lrn[msao.binding.KERNEL_POST], "score_plain": k_plain[msao.binding.KERNEL_SCORE],
+                      "post_plain": k_plain[msao.binding.KERNEL_POST]},
+        "gpu_ms_per_call": total,
+        "tokens_per_s": ntok / (total * 1e-3),
+        "score_overhead": k_lrn[msao.binding.KERNEL_SCORE] / k_plain[msao.binding.KERNEL_SCORE] - 1.0,
+        "algorithmic_bytes_score": b_lrn,
+        "roofline": {"bound": "hbm", "kernel": "k_score<true>", "achieved": gbs, "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "traffic": committed_learned_traffic(w.config)},
+    }
 
 
 def cpu_baseline(w, budget_s):
@@ -367,6 +439,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    if not args.no_learned:
+        line["learned"] = learned_bench(args, dev, ctxs[0], w, reps, fields)
     if not args.no_entropy:
         line["entropy"] = entropy_bench(args, dev, ctxs[0])
     for _, plan in plans:

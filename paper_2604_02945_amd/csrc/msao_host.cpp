@@ -135,7 +135,8 @@ struct Plan {
     bool learned = false;
     std::vector<int32_t> hb_seg;   // segment of each head block (one per frame of a segment with a head)
     int max_head_p = 0;            // largest frame among segments with a head
-    size_t off_hbseg = 0, off_partial_x = 0, off_proj = 0, off_head_count = 0;
+    int mlp_hidden = 0;            // > 0: the relevance MLP's u = W1[:, :P] p + b1 per request
+    size_t off_hbseg = 0, off_partial_x = 0, off_proj = 0, off_head_count = 0, off_mlp_u = 0;
     size_t off_seg = 0, off_wi = 0, off_gi = 0, off_rmoff = 0, off_rmseg = 0, off_tseg = 0, off_alpha = 0;
     size_t table_bytes = 0, off_partial = 0, total_bytes = 0;
 };
@@ -163,7 +164,8 @@ size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t
 // Workspace bound that does not depend on tuning: work items, gather items
 // and head blocks never outnumber tokens, so one Partial and table entries
 // per token, plus what a learned call adds (a PartialX per work item, one
-// projection and one head count per token).
+// projection and one head count per token, kMaxMlpHidden floats of the MLP's
+// prompt product per request).
 size_t workspace_bytes_for(int n, int R, int64_t ntok)
 {
     Plan pl;
@@ -172,16 +174,18 @@ size_t workspace_bytes_for(int n, int R, int64_t ntok)
     return align_up(tb, kWsAlign) + align_up(sizeof(Partial) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
            align_up(sizeof(PartialX) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
            align_up(sizeof(float) * (size_t)std::max<int64_t>(ntok, 1), kWsAlign) +
-           align_up(sizeof(uint32_t) * (size_t)std::max<int64_t>(items, 1), kWsAlign);
+           align_up(sizeof(uint32_t) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
+           align_up(sizeof(float) * (size_t)kMaxMlpHidden * (size_t)std::max(R, 1), kWsAlign);
 }
 
 // fuse_copy: a full run with compaction, where segments that keep every row
 // are copied by the scoring pass (they get no gather items).
 void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* p,
                 const float* alpha, const int64_t* out_off, Plan& pl, bool fuse_copy = false,
-                const msao_spatial_head* heads = nullptr, bool learned = false)
+                const msao_spatial_head* heads = nullptr, bool learned = false, int mlp_hidden = 0)
 {
     pl.learned = learned;
+    pl.mlp_hidden = learned ? mlp_hidden : 0;
     pl.hb_seg.clear();
     pl.max_head_p = 0;
     pl.seg.resize((size_t)n);
@@ -302,6 +306,10 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         pl.off_proj = align_up(pl.off_partial_x + sizeof(PartialX) * (size_t)std::max(pl.n_wi, 1), kWsAlign);
         pl.off_head_count = align_up(pl.off_proj + sizeof(float) * (size_t)std::max<int64_t>(pl.ntok, 1), kWsAlign);
         pl.total_bytes = pl.off_head_count + sizeof(uint32_t) * std::max<size_t>(pl.hb_seg.size(), 1);
+        if (pl.mlp_hidden > 0) {
+            pl.off_mlp_u = align_up(pl.total_bytes, kWsAlign);
+            pl.total_bytes = pl.off_mlp_u + sizeof(float) * (size_t)pl.mlp_hidden * (size_t)std::max(R, 1);
+        }
     }
 }
 
@@ -813,7 +821,8 @@ msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int 
     }
     if (mlp) {
         if (!mlp->w1 || !mlp->b1 || !mlp->w2) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "MLP weights are NULL");
-        if (mlp->hidden < 1 || mlp->hidden > 4096) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "MLP hidden out of range");
+        if (mlp->hidden < 1 || mlp->hidden > kMaxMlpHidden)
+            return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "MLP hidden out of range");
         if (mlp->prompt_dim < 0 || mlp->prompt_dim > 16384)
             return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "MLP prompt_dim out of range");
         if (mlp->prompt_dim > 0 && !mlp->prompt) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "prompt is NULL");
@@ -821,7 +830,7 @@ msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int 
         MSAO_TRY(check_out_alignment(ctx, {{mlp->w1, 4}, {mlp->b1, 4}, {mlp->w2, 4}, {mlp->prompt, 4}}));
     }
     Plan pl;
-    build_plan(ctx, segs, n, R, params, alpha, nullptr, pl, false, heads, true);
+    build_plan(ctx, segs, n, R, params, alpha, nullptr, pl, false, heads, true, mlp ? mlp->hidden : 0);
     MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
     const bool want_frames = frm && (frm->dframe || frm->sim || frm->gamma) && pl.nframes > 0;
     if (want_frames && !(tok && tok->d))
@@ -842,12 +851,19 @@ msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int 
     sa.learned = 1;
     sa.importance = importance;
     MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
-    if (!pl.hb_seg.empty()) {
+    float* mlp_u = mlp ? (float*)((uint8_t*)ws + pl.off_mlp_u) : nullptr;
+    if (!pl.hb_seg.empty() || mlp) {
         HeadArgs ha;
         std::memset(&ha, 0, sizeof ha);
         ha.t = sa.t;
         ha.importance = importance;
         ha.max_p = pl.max_head_p;
+        if (mlp) {
+            ha.mlp = ModalMlp{mlp->w1, mlp->b1, mlp->w2, mlp->b2, mlp->hidden, mlp->prompt_dim, mlp->prompt};
+            ha.u = mlp_u;
+            const int64_t waves = (int64_t)mlp->hidden * ((R + kMlpGroup - 1) / kMlpGroup);
+            ha.n_mlp_blocks = (int32_t)((waves + kHeadBlock / 64 - 1) / (kHeadBlock / 64));
+        }
         MSAO_TRY(launched(ctx, MSAO_KERNEL_HEAD, st, run_head, &ha));
     }
     PostArgs pa;
@@ -860,7 +876,7 @@ msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int 
     if (mlp) {
         pa.use_mlp = 1;
         pa.mlp = ModalMlp{mlp->w1, mlp->b1, mlp->w2, mlp->b2, mlp->hidden, mlp->prompt_dim, mlp->prompt};
-        pa.keys_cap = (mlp->prompt_dim + kDesc + 1) / 2;  // LDS for [p; z] as floats
+        pa.mlp_u = mlp_u;
     }
     pa.alpha_out = alpha_out;
     pa.desc_out = desc;

@@ -138,6 +138,7 @@ struct PostArgs {
     ModalMlp mlp;
     float* alpha_out;     // [R*4] (NULL: not written)
     float* desc_out;      // [R*4*kDesc]
+    const float* mlp_u;   // [R][hidden] prompt half of the MLP's first layer plus b1
 };
 
 struct ScoreArgs {
@@ -151,15 +152,22 @@ struct ScoreArgs {
 };
 
 // Pooling, sigmoid and the Eq. 4 test of the learned spatial head: one
-// block per frame of a segment with a head.
+// block per frame of a segment with a head; then, when an MLP is given,
+// n_mlp_blocks blocks computing u = W1[:, :prompt_dim] p + b1 per request
+// (the part of Eq. 6's first layer that all modalities share).
 struct HeadArgs {
     Tables t;
     float* importance;    // [Ntot] (NULL: not written)
     int32_t max_p;        // largest frame among segments with a head (LDS staging)
+    int32_t n_mlp_blocks;
+    ModalMlp mlp;
+    float* u;             // [R][hidden]
 };
 constexpr int kHeadBlock = 256;
 constexpr int kMaxHeadFrame = 16384;  // tokens per frame of a segment with a head (LDS)
 constexpr int kMaxPool = 15;
+constexpr int kMaxMlpHidden = 4096;
+constexpr int kMlpGroup = 8;          // requests per wavefront in the prompt product
 
 struct GatherArgs {
     Tables t;

@@ -421,7 +421,13 @@ __device__ __forceinline__ void rows_batch(const ScoreArgs& a, const DevSeg& sg,
             if (sg.head_w) {
                 float acc = 0.0f;
 #pragma unroll
-                for (int u = 0; u < NU; ++u) acc = dot_chunk<DT>(v[i][u], wv[u], acc);
+                for (int u = 0; u < NU; ++u) {
+                    // rows over 3 KiB re-read the weights (L1 hits) instead of holding
+                    // them: the registers go to the double-buffered rows
+                    const vec4 w = NU > 3 ? bload_gather(make_rsrc(sg.head_w, sg.nchunk * 16), lane * 16 + u * 1024)
+                                          : wv[u];
+                    acc = dot_chunk<DT>(v[i][u], w, acc);
+                }
                 y = wave_sum(acc);
             }
             lrn_add(lr, s);
@@ -453,7 +459,7 @@ __device__ __forceinline__ void score_rows(const ScoreArgs& a, const DevSeg& sg,
     const int voff = lane * 16;
     TokBuf tb{};
     vec4 wv[NU];
-    if constexpr (LR) load_head<NU>(wv, sg, voff);
+    if constexpr (LR && NU <= 3) load_head<NU>(wv, sg, voff);
     if constexpr (NU > 4) {
         for (int r = r0; r < r1; ++r) {
             vec4 A[1][NU];
@@ -563,7 +569,7 @@ __device__ __forceinline__ void score_chain(const ScoreArgs& a, const DevSeg& sg
     vec4 cur[NU];
     load(cur, t0, true);
     vec4 wv[NU];
-    if constexpr (LR) load_head<NU>(wv, sg, voff);
+    if constexpr (LR && NU <= 2) load_head<NU>(wv, sg, voff);
     TokBuf tb{};
     for (int t = t0; t < t1; ++t) {
         vec4 nxt[NU];
@@ -574,7 +580,11 @@ __device__ __forceinline__ void score_chain(const ScoreArgs& a, const DevSeg& sg
         if constexpr (LR) {
             if (sg.head_w) {
 #pragma unroll
-                for (int u = 0; u < NU; ++u) yacc = dot_chunk<DT>(cur[u], wv[u], yacc);
+                for (int u = 0; u < NU; ++u) {
+                    // the chain already holds the previous frame: re-read (L1 hits) beyond 2 units
+                    const vec4 w = NU > 2 ? bload_gather(make_rsrc(sg.head_w, sg.nchunk * 16), voff + u * 1024) : wv[u];
+                    yacc = dot_chunk<DT>(cur[u], w, yacc);
+                }
             }
         }
 #pragma unroll
@@ -732,9 +742,12 @@ __device__ __forceinline__ int score_block(const ScoreArgs& a)
 
 // LR: a learned call (Eq. 3 head projections, density importance of tokens
 // without a head, and the descriptor sums of Eq. 6); a separate instance, so
-// that the plain kernel keeps its registers.
+// that the plain kernel keeps its registers. Both are held to 96 VGPRs (five
+// wavefronts per SIMD, the loads in flight this HBM-bound pass needs): the
+// plain instance needs 83; the learned one, which also holds the head's
+// weights of rows up to 3 KiB, takes 96 without spilling.
 template <bool LR>
-__global__ __launch_bounds__(kScoreBlock) void k_score(ScoreArgs a)
+__global__ __launch_bounds__(kScoreBlock) __attribute__((amdgpu_waves_per_eu(5, 8))) void k_score(ScoreArgs a)
 {
     const int lane = threadIdx.x & (kWave - 1);
     const int w = uniform(score_block(a) * (kScoreBlock / kWave) + (threadIdx.x >> 6));
@@ -1032,7 +1045,7 @@ __device__ __forceinline__ float block_sum_f32(float v, PostShared<NT>& sh)
 // The descriptor: 1, rho, sum a / sum C, sum L1 / sum C, sqrt(sum L2 / sum C),
 // the temporal term (0 if none), 1 if it exists, ln(1 + Ntok) / 16.
 template <int NT>
-__device__ void role_request_learned(const PostArgs& a, int r, PostShared<NT>& sh, float* vin)
+__device__ void role_request_learned(const PostArgs& a, int r, PostShared<NT>& sh)
 {
     const Tables& t = a.t;
     constexpr int kParts = (NT / kWave) / kNumMod;
@@ -1103,22 +1116,23 @@ __device__ void role_request_learned(const PostArgs& a, int r, PostShared<NT>& s
         if (pres[mm]) pre[mm] = mas_terms(t, g[mm], 1.0, mm);  // rho and the temporal term
         modality_descriptor(pres[mm], pre[mm], a1, c1, s1, s2, g[mm].ntok, z[mm]);
     }
-    // Eq. 6: alpha = w2 . relu(W1 [p; z] + b1) + b2, one modality at a time
+    // Eq. 6: alpha = w2 . relu(W1 [p; z] + b1) + b2, one modality at a time,
+    // with u = W1[:, :P] p + b1 from the head launch
     double al[kNumMod];
-    const int P = a.mlp.prompt_dim, IN = P + kDesc;
+    const int P = a.mlp.prompt_dim, IN = P + kDesc, H = a.mlp.hidden;
 #pragma unroll
     for (int mm = 0; mm < kNumMod; ++mm) {
         al[mm] = (double)t.alpha[r * kNumMod + mm];
         if (!a.use_mlp || !pres[mm]) continue;
-        __syncthreads();
-        for (int k = threadIdx.x; k < IN; k += NT)
-            vin[k] = k < P ? a.mlp.prompt[(int64_t)r * P + k] : (float)z[mm][k - P];
-        __syncthreads();
+        float zf[kDesc];
+#pragma unroll
+        for (int k = 0; k < kDesc; ++k) zf[k] = (float)z[mm][k];
         float part_sum = 0.0f;
-        for (int j = threadIdx.x; j < a.mlp.hidden; j += NT) {
-            const float* row = a.mlp.w1 + (int64_t)j * IN;
-            float h = a.mlp.b1[j];
-            for (int k = 0; k < IN; ++k) h = fmaf(row[k], vin[k], h);
+        for (int j = threadIdx.x; j < H; j += NT) {
+            const float* row = a.mlp.w1 + (int64_t)j * IN + P;
+            float h = a.mlp_u[(int64_t)r * H + j];
+#pragma unroll
+            for (int k = 0; k < kDesc; ++k) h = fmaf(row[k], zf[k], h);
             part_sum = fmaf(a.mlp.w2[j], fmaxf(h, 0.0f), part_sum);
         }
         al[mm] = (double)(a.mlp.b2 + block_sum_f32<NT>(part_sum, sh));
@@ -1472,7 +1486,7 @@ __global__ __launch_bounds__(NT) void k_post(PostArgs a)
         b -= a.n_sel_blocks;
     }
     if (b < a.n_req_blocks) {
-        if constexpr (LR) role_request_learned<NT>(a, b, sh, reinterpret_cast<float*>(keys));
+        if constexpr (LR) role_request_learned<NT>(a, b, sh);
         else role_request(a, b, sh);
         return;
     }
@@ -1570,17 +1584,62 @@ __global__ __launch_bounds__(kGatherBlock) void k_gather(GatherArgs a)
 // and end, so their span is the kernel's execution time.
 // ---------------------------------------------------------------- k_head
 
+// u[r][j] = b1[j] + W1[j][:prompt_dim] . p_r for kMlpGroup requests per
+// wavefront: the lanes stride over the row (coalesced loads of W1 and of
+// the prompts, 8 strides issued before they are used, since each load is
+// an L2 round trip), then one wavefront sum per request.
+__device__ __forceinline__ void prompt_product(const HeadArgs& a, int blk)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int g = blk * (kHeadBlock / kWave) + (threadIdx.x >> 6);
+    const int R = a.t.R, H = a.mlp.hidden, P = a.mlp.prompt_dim;
+    const int ngr = (R + kMlpGroup - 1) / kMlpGroup;
+    if (g >= H * ngr) return;  // wave-uniform
+    const int j = g / ngr, r0 = (g % ngr) * kMlpGroup, nr = min(kMlpGroup, R - r0);
+    const float* wrow = a.mlp.w1 + (int64_t)j * (P + kDesc);
+    float acc[kMlpGroup];
+#pragma unroll
+    for (int q = 0; q < kMlpGroup; ++q) acc[q] = 0.0f;
+    constexpr int U = 8;
+    for (int k0 = lane; k0 < P; k0 += kWave * U) {
+        float wk[U], pv[U][kMlpGroup];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int k = k0 + u * kWave;
+            wk[u] = k < P ? wrow[k] : 0.0f;
+#pragma unroll
+            for (int q = 0; q < kMlpGroup; ++q)
+                pv[u][q] = (k < P && q < nr) ? a.mlp.prompt[(int64_t)(r0 + q) * P + k] : 0.0f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int q = 0; q < kMlpGroup; ++q) acc[q] = fmaf(wk[u], pv[u][q], acc[q]);
+    }
+    const float b = a.mlp.b1[j];
+#pragma unroll
+    for (int q = 0; q < kMlpGroup; ++q) {
+        const float s = wave_sum(acc[q]);
+        if (lane == 0 && q < nr) a.u[(int64_t)(r0 + q) * H + j] = s + b;
+    }
+}
+
 // Eq. 3 with a learned head for one frame of a segment (P tokens on an
 // H x W grid, token q at row q / W, column q % W): importance
 // M = sigmoid(mean of the projections over the pool x pool window cut to the
 // grid + b), which is Conv1x1(AvgPool(F)) since the 1x1 convolution is
 // linear; then the number of tokens with M < tau_s (Eq. 4).
+// Blocks past the head blocks compute the MLP's prompt product.
 __global__ __launch_bounds__(kHeadBlock) void k_head(HeadArgs a)
 {
     extern __shared__ float ys[];
     __shared__ uint64_t cnt[kHeadBlock / kWave];
     const Tables& t = a.t;
     const int hb = blockIdx.x;
+    if (hb >= t.n_hb) {
+        prompt_product(a, hb - t.n_hb);
+        return;
+    }
     const DevSeg sg = t.seg[t.hb_seg[hb]];
     const int P = sg.P;
     const int base = sg.tok_off + (hb - sg.hb_begin) * P;
@@ -1653,7 +1712,7 @@ int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1)
     const int blocks = a.n_req_blocks + a.n_frame_blocks + a.n_sel_blocks;
     if (blocks <= 0) return 0;
     const size_t lds = (size_t)(a.keys_cap + cand_cap_for(a.keys_cap)) * sizeof(uint64_t);
-    if (a.learned && (!a.t.partial_x || !a.t.head_count)) return (int)hipErrorInvalidValue;
+    if (a.learned && (!a.t.partial_x || !a.t.head_count || (a.use_mlp && !a.mlp_u))) return (int)hipErrorInvalidValue;
     if (a.learned) return launch_post_nt<kPostBlock, true>(a, a.n_req_blocks + a.n_frame_blocks, lds, stream, ev0, ev1);
     if (a.n_sel_blocks > 0 && a.keys_cap >= kPostBigSegment)
         return launch_post_nt<1024, false>(a, blocks, lds, stream, ev0, ev1);
@@ -1662,14 +1721,19 @@ int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1)
 
 int launch_head(const HeadArgs& a, void* stream, void* ev0, void* ev1)
 {
-    if (a.t.n_hb <= 0) return 0;
-    if (!a.t.proj || !a.t.head_count || a.max_p < 1 || a.max_p > kMaxHeadFrame) return (int)hipErrorInvalidValue;
-    const size_t lds = (size_t)a.max_p * sizeof(float);
+    const int blocks = a.t.n_hb + a.n_mlp_blocks;
+    if (blocks <= 0) return 0;
+    if (a.t.n_hb > 0 && (!a.t.proj || !a.t.head_count || a.max_p < 1 || a.max_p > kMaxHeadFrame))
+        return (int)hipErrorInvalidValue;
+    if (a.n_mlp_blocks > 0 && (!a.u || !a.mlp.w1 || !a.mlp.b1 || a.mlp.hidden < 1 || a.mlp.hidden > kMaxMlpHidden ||
+                               (a.mlp.prompt_dim > 0 && !a.mlp.prompt)))
+        return (int)hipErrorInvalidValue;
+    const size_t lds = a.t.n_hb > 0 ? (size_t)a.max_p * sizeof(float) : 0;
     if (lds > 65536) {
         const hipError_t e = hipFuncSetAttribute((const void*)k_head, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return (int)e;
     }
-    return launch(k_head, dim3((unsigned)a.t.n_hb), dim3(kHeadBlock), lds, stream, a, ev0, ev1);
+    return launch(k_head, dim3((unsigned)blocks), dim3(kHeadBlock), lds, stream, a, ev0, ev1);
 }
 
 int launch_gather(const GatherArgs& a, void* stream, void* ev0, void* ev1)

@@ -226,6 +226,17 @@ def test_heads_on_video_and_odd_widths(dev):
     compare(segs, 3, heads, g, ref, mlp)
 
 
+def test_mlp_without_heads_many_requests(dev):
+    # the head launch runs only prompt-product blocks; 10 requests make a
+    # ragged group of the 8 requests one wavefront serves
+    w = make_workload(4, n_requests=10)
+    rng = np.random.default_rng(13)
+    mlp = mlp_for(10, 200, 96, rng)
+    log("[learned] MLP 96 x (200 + 8), no heads, 10 requests")
+    g, ref = run_case(w.segments, 10, None, mlp, dev)
+    assert compare(w.segments, 10, None, g, ref, mlp)
+
+
 def test_without_heads_or_mlp_it_is_mas_score(dev):
     w = make_workload(4, n_requests=2)
     alpha = [0.5, -0.25, 0.0, 1.0, 0.0, 0.0, 0.0, 0.0]
