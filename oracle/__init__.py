@@ -26,6 +26,7 @@ _LIB = os.path.join(_HERE, "libmsao_oracle.so")
 NMOD = 4
 F32, BF16 = 0, 1
 FLAG_TEMPORAL_LITERAL = 1
+FLAG_SELECT_PER_FRAME = 2
 
 
 def build(force: bool = True) -> str:
@@ -90,6 +91,9 @@ def lib():
         L.orc_run_learned.argtypes = [ctypes.POINTER(_Segment), ctypes.c_int, ctypes.c_int, ctypes.POINTER(_Params),
                                       _P, _P, ctypes.POINTER(_Outputs), _P, _P, _P]
         L.orc_run_learned.restype = ctypes.c_int
+        L.orc_temporal_simhash.argtypes = [ctypes.POINTER(_Segment), ctypes.c_int, ctypes.c_int,
+                                           ctypes.POINTER(_Params), _P, _P, _P, _P, _P, _P, _P, _P]
+        L.orc_temporal_simhash.restype = ctypes.c_int
         L.orc_q24.argtypes = [ctypes.c_float]
         L.orc_q24.restype = ctypes.c_uint64
         D, I64, I = ctypes.c_double, ctypes.c_int64, ctypes.c_int
@@ -268,6 +272,44 @@ def run_learned(segments: Sequence, n_requests: int, params: dict, heads: Option
     o["desc"] = desc[:R * NMOD * DESC].reshape(R * NMOD, DESC)
     o["k"] = o["k"][:n]
     return o
+
+
+class _SimHash(ctypes.Structure):
+    _fields_ = [("planes", _P), ("bits", ctypes.c_int32)]
+
+
+def temporal_simhash(segments: Sequence, n_requests: int, params: dict, hashes: Sequence) -> dict:
+    """The SimHash variant of Eq. 5: hashes[s] = dict(planes=[bits, hidden]
+    array in the segment's encoding, bits=K) for every temporal segment (None
+    elsewhere). Returns sig, d per token, dframe, sim, gamma per temporal
+    frame, dsum, qbits and temporal per (request, modality)."""
+    L = lib()
+    n = len(segments)
+    ntok = sum(s.n_frames * s.tokens_per_frame for s in segments)
+    nframe = sum(s.n_frames for s in segments if _is_temporal(s))
+    R = n_requests
+    o = {"sig": np.zeros(max(ntok, 1), np.uint64), "d": np.zeros(max(ntok, 1), np.uint32),
+         "dframe": np.zeros(max(nframe, 1), np.uint64), "sim": np.zeros(max(nframe, 1), np.float32),
+         "gamma": np.zeros(max(nframe, 1), np.float32), "dq": np.zeros(max(R * NMOD * 2, 1), np.uint64),
+         "temporal": np.zeros(max(R * NMOD, 1), np.float32)}
+    harr = (_SimHash * max(1, n))()
+    keep = []
+    for i, h in enumerate(hashes):
+        if h is None:
+            continue
+        a = np.ascontiguousarray(h["planes"])
+        keep.append(a)
+        harr[i] = _SimHash(a.ctypes.data, int(h["bits"]))
+    rc = L.orc_temporal_simhash(_segment_table(segments), n, R, ctypes.byref(_params(params)),
+                                ctypes.cast(harr, _P), *[_ptr(o[k]) for k in ("sig", "d", "dframe", "sim", "gamma",
+                                                                              "dq", "temporal")])
+    if rc != 0:
+        raise RuntimeError(f"orc_temporal_simhash failed ({rc})")
+    dq = o.pop("dq")[:R * NMOD * 2].reshape(-1, 2)
+    out = {k: v[:ntok] for k, v in o.items() if k in ("sig", "d")}
+    out.update({k: o[k][:nframe] for k in ("dframe", "sim", "gamma")})
+    out.update(dsum=dq[:, 0].copy(), qbits=dq[:, 1].copy(), temporal=o["temporal"][:R * NMOD])
+    return out
 
 
 def select(segments: Sequence, n_requests: int, params: dict, z: np.ndarray,

@@ -30,7 +30,12 @@
  *  - a token's selection key is the exact integer
  *        Ls*z + Lt*(C - d)   with Ls = rne(lambda_s * 2^24), Lt likewise,
  *    the keep count is k = min(N, ceil(kappa * N)) and the k smallest
- *    (key, index) pairs of each segment are kept, ties by ascending index.
+ *    (key, index) pairs of each segment are kept, ties by ascending index;
+ *    with the per-frame scope flag each frame of P tokens is its own
+ *    selection, k_f = min(P, ceil(kappa * P)) tokens per frame;
+ *  - the SimHash variant of Eq. 5 hashes each token with K caller
+ *    hyperplanes r_k: bit k is 1 iff r_k . f >= 0 (Charikar's hash); frame
+ *    0 is compared with the all-zero frame, whose bits are all 1.
  *
  * Parity pins for every function below live in the CPU test suite.
  */
@@ -42,7 +47,7 @@
 
 enum { ORC_TEXT = 0, ORC_IMAGE = 1, ORC_VIDEO = 2, ORC_AUDIO = 3, ORC_NMOD = 4 };
 enum { ORC_F32 = 0, ORC_BF16 = 1 };
-enum { ORC_FLAG_TEMPORAL_LITERAL = 1 };
+enum { ORC_FLAG_TEMPORAL_LITERAL = 1, ORC_FLAG_SELECT_PER_FRAME = 2 };
 
 typedef struct {
     const void* data;          /* row (t*P + p) starts at data + (t*P+p)*row_stride elements */
@@ -223,32 +228,52 @@ static int pair_cmp(const void* a, const void* b)
     return 0;
 }
 
-/* Selection of one segment: sort (key, index) ascending, keep the first k. */
-static int select_segment(const orc_segment* s, const orc_params* p, const uint32_t* z,
-                          const uint32_t* d, int64_t k, uint8_t* keep, int32_t* kept_idx)
+/* Selection among tokens [i0, i0 + n) of a segment: sort (key, index)
+ * ascending, keep the first k (keep flags set for the range only). */
+static int select_range(const orc_segment* s, const orc_params* p, const uint32_t* z,
+                        const uint32_t* d, int64_t i0, int64_t n, int64_t k, uint8_t* keep)
 {
-    int64_t N = (int64_t)s->n_frames * s->tokens_per_frame;
     int64_t C = s->hidden;
     uint64_t Ls = q24(p->lambda_s[s->modality]);
     uint64_t Lt = q24(p->lambda_t[s->modality]);
     int temporal = is_temporal(s);
-    orc_pair* pairs = (orc_pair*)malloc(sizeof(orc_pair) * (size_t)(N > 0 ? N : 1));
+    orc_pair* pairs = (orc_pair*)malloc(sizeof(orc_pair) * (size_t)(n > 0 ? n : 1));
     if (!pairs) return -1;
-    for (int64_t i = 0; i < N; ++i) {
+    for (int64_t j = 0; j < n; ++j) {
+        int64_t i = i0 + j;
         uint64_t key = Ls * (uint64_t)z[i];
         if (temporal) key += Lt * (uint64_t)(C - (int64_t)d[i]);
-        pairs[i].key = key;
-        pairs[i].idx = i;
+        pairs[j].key = key;
+        pairs[j].idx = i;
     }
-    qsort(pairs, (size_t)N, sizeof(orc_pair), pair_cmp);
-    for (int64_t i = 0; i < N; ++i) keep[i] = 0;
+    qsort(pairs, (size_t)n, sizeof(orc_pair), pair_cmp);
+    for (int64_t j = 0; j < n; ++j) keep[i0 + j] = 0;
     for (int64_t j = 0; j < k; ++j) keep[pairs[j].idx] = 1;
+    free(pairs);
+    return 0;
+}
+
+/* Selection of one segment with keep ratio kappa: the whole segment, or
+ * (per-frame scope) each of its T frames of P tokens on its own. Kept
+ * indices ascending, then -1. Returns the keep count. */
+static int64_t select_segment(const orc_segment* s, const orc_params* p, const uint32_t* z,
+                              const uint32_t* d, double kappa, uint8_t* keep, int32_t* kept_idx)
+{
+    int64_t T = s->n_frames, P = s->tokens_per_frame, N = T * P, k = 0;
+    if (p->flags & ORC_FLAG_SELECT_PER_FRAME) {
+        int64_t kf = keep_count(kappa, P);
+        for (int64_t t = 0; t < T; ++t)
+            if (select_range(s, p, z, d, t * P, P, kf, keep)) return -1;
+        k = kf * T;
+    } else {
+        k = keep_count(kappa, N);
+        if (select_range(s, p, z, d, 0, N, k, keep)) return -1;
+    }
     int64_t w = 0;
     for (int64_t i = 0; i < N; ++i)
         if (keep[i]) kept_idx[w++] = (int32_t)i;
     for (; w < N; ++w) kept_idx[w] = -1;
-    free(pairs);
-    return 0;
+    return k;
 }
 
 /* Selection over all segments from given per-token z, d and per-(request,
@@ -268,10 +293,9 @@ int orc_select(const orc_segment* segs, int n, int R, const orc_params* p,
         } else {
             kappa = (double)sg->keep_ratio;
         }
-        int64_t k = keep_count(kappa, N);
+        int64_t k = select_segment(sg, p, z + off, d ? d + off : NULL, kappa, keep + off, kept_idx + off);
+        if (k < 0) return -1;
         k_out[s] = (int32_t)k;
-        if (select_segment(sg, p, z + off, d ? d + off : NULL, k, keep + off, kept_idx + off))
-            return -1;
         off += N;
     }
     return 0;
@@ -601,5 +625,95 @@ int orc_run_learned(const orc_segment* segs, int n, int R, const orc_params* p, 
     free(CC);
     free(L1);
     free(L2);
+    return 0;
+}
+
+/* ==================================================================
+ * SimHash variant of Eq. 5 (Sec. 4.1.2): Charikar's random-hyperplane
+ * hash in place of bit sampling over the activity bits.
+ * ================================================================ */
+
+typedef struct {
+    const void* planes; /* [bits][hidden] in the segment's dtype: hyperplane r_k is row k */
+    int32_t bits;       /* K hash functions per token, 1..64 */
+} orc_simhash;
+
+/* Signature of one token: bit k is 1 iff r_k . f >= 0, the dot product
+ * summed in double over the channels in order (NaN compares false: 0). */
+static uint64_t simhash_token(const void* row, const void* planes, int dtype, int C, int K)
+{
+    uint64_t sig = 0;
+    for (int k = 0; k < K; ++k) {
+        const void* r = (const char*)planes + (size_t)k * (size_t)C * elt_size(dtype);
+        double y = 0.0;
+        for (int c = 0; c < C; ++c) y += (double)widen(r, dtype, c) * (double)widen(row, dtype, c);
+        if (y >= 0.0) sig |= (uint64_t)1 << k;
+    }
+    return sig;
+}
+
+static uint32_t popcount64(uint64_t v)
+{
+    uint32_t n = 0;
+    for (; v; v &= v - 1) ++n;
+    return n;
+}
+
+/* Eq. 5 with K hyperplanes per token (K P hash functions per frame):
+ *   sig[g]  the token's signature (0 outside temporal segments);
+ *   d[g]    the number of its K bits that differ from the same patch in the
+ *           previous frame (frame 0: from the all-zero frame, all bits 1);
+ *   D_t = sum_p d, sim_t = 1 - D_t / (P K), gamma_t = 1 - sim_t;
+ *   per (request, modality) x: dq[2x] = sum of D_t over frames 1..T-1,
+ *   dq[2x+1] = (T - 1) P K, and the temporal term of Eq. 7 (1 - Dsum/Qbits,
+ *   or Dsum/Qbits with the literal flag; 0 where there is none).
+ * Every temporal segment needs planes (else -1). */
+int orc_temporal_simhash(const orc_segment* segs, int n, int R, const orc_params* p, const orc_simhash* h,
+                         uint64_t* sig, uint32_t* d, uint64_t* dframe, float* sim, float* gamma, uint64_t* dq,
+                         float* temporal)
+{
+    for (int i = 0; i < R * ORC_NMOD * 2; ++i) dq[i] = 0;
+    int64_t tok = 0, frame = 0;
+    for (int s = 0; s < n; ++s) {
+        const orc_segment* sg = &segs[s];
+        int64_t T = sg->n_frames, P = sg->tokens_per_frame, N = T * P;
+        if (!is_temporal(sg)) {
+            for (int64_t i = 0; i < N; ++i) {
+                sig[tok + i] = 0;
+                d[tok + i] = 0;
+            }
+            tok += N;
+            continue;
+        }
+        if (!h || !h[s].planes || h[s].bits < 1 || h[s].bits > 64) return -1;
+        const int K = h[s].bits;
+        const uint64_t all = K == 64 ? ~(uint64_t)0 : (((uint64_t)1 << K) - 1);
+        for (int64_t i = 0; i < N; ++i)
+            sig[tok + i] = simhash_token(row_ptr(sg, i), h[s].planes, sg->dtype, sg->hidden, K);
+        uint64_t* x = &dq[(sg->request * ORC_NMOD + sg->modality) * 2];
+        for (int64_t t = 0; t < T; ++t) {
+            uint64_t D = 0;
+            for (int64_t q = 0; q < P; ++q) {
+                const int64_t g = tok + t * P + q;
+                const uint64_t prev = t > 0 ? sig[g - P] : all;
+                d[g] = popcount64(sig[g] ^ prev);
+                D += d[g];
+            }
+            const double sm = 1.0 - (double)D / (double)(P * K);
+            dframe[frame + t] = D;
+            sim[frame + t] = (float)sm;
+            gamma[frame + t] = (float)(1.0 - sm);
+            if (t >= 1) x[0] += D;
+        }
+        x[1] += (uint64_t)((T - 1) * P * K);
+        frame += T;
+        tok += N;
+    }
+    for (int x = 0; x < R * ORC_NMOD; ++x) {
+        temporal[x] = 0.0f;
+        if (dq[2 * x + 1] == 0) continue;
+        const double gamma_avg = (double)dq[2 * x] / (double)dq[2 * x + 1];
+        temporal[x] = (float)((p->flags & ORC_FLAG_TEMPORAL_LITERAL) ? gamma_avg : 1.0 - gamma_avg);
+    }
     return 0;
 }

@@ -7,5 +7,5 @@ arithmetic: no activity test, no statistic, no score, no selection.
 from .gen import (  # noqa: F401
     TEXT, IMAGE, VIDEO, AUDIO, MODALITY_NAMES,
     Segment, Workload, default_params, make_workload, f32_to_bf16_bits,
-    bf16_bits_to_f32, CONFIG_NAMES, DRAFT_ROWS, DRAFT_VOCAB, draft_logits,
+    bf16_bits_to_f32, CONFIG_NAMES, DRAFT_ROWS, DRAFT_VOCAB, draft_logits, simhash_planes,
 )

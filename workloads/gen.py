@@ -321,3 +321,12 @@ def draft_logits(rows: int = DRAFT_ROWS, vocab: int = DRAFT_VOCAB, seed: int = 0
     if k > 1:
         x[r_ix[:, None], idx[:, 1:]] += boost[:, None] - runner
     return x if dtype == "f32" else f32_to_bf16_bits(x)
+
+
+# ---- SimHash hyperplanes (Sec. 4.1.2 variant) -----------------------------------
+
+def simhash_planes(bits: int, hidden: int, seed: int = 0, dtype: str = "bf16") -> np.ndarray:
+    """[bits, hidden] random hyperplanes with N(0, 1) entries drawn in float32,
+    encoded like segment data (float32, or bf16 bit patterns)."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 7, bits, hidden])))
+    return _encode(rng.standard_normal((bits, hidden), dtype=np.float32), dtype)
