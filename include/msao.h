@@ -84,6 +84,13 @@ typedef enum { MSAO_F32 = 0, MSAO_BF16 = 1 } msao_dtype;
 
 /* Eq. 7 takes gamma_avg itself as the temporal term (default: 1 - gamma_avg). */
 #define MSAO_FLAG_TEMPORAL_LITERAL 1u
+/* Per-frame selection scope (the alternative to one selection per segment
+ * that Sec. 4.1.1's pruning leaves open): every frame of a segment with
+ * T >= 2 keeps its own k_f = min(P, ceil(kappa P)) tokens, the k_f smallest
+ * (key, index) pairs of the frame (a MAS-guided kappa = 1 - MAS of the
+ * segment's request and modality for every frame); kept_count = T k_f and
+ * the kept indices stay ascending over the segment. */
+#define MSAO_FLAG_SELECT_PER_FRAME 2u
 
 typedef struct msao_ctx msao_ctx;
 
@@ -171,8 +178,9 @@ msao_status msao_count(const msao_segment* segs, int n, int64_t* n_tokens, int64
 msao_status msao_workspace_size(const msao_segment* segs, int n, int n_requests, size_t* bytes);
 /* Default packed compaction layout (host only): out_byte_off[s] (host, [n]) is
  * where segment s's kept rows start; a segment with a fixed keep ratio gets
- * room for exactly its k rows, a MAS-guided one for all N rows; offsets are
- * 256-byte aligned. *total_bytes receives the buffer size needed. */
+ * room for its kept rows under either selection scope (max(ceil(kappa N),
+ * T ceil(kappa P))), a MAS-guided one for all N rows; offsets are 256-byte
+ * aligned. *total_bytes receives the buffer size needed. */
 msao_status msao_compact_layout(const msao_segment* segs, int n, int64_t* out_byte_off, int64_t* total_bytes);
 
 /* ---- entry points (enqueue on `stream`) ---------------------------------- */
@@ -299,6 +307,42 @@ msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int 
                                    float* importance, const msao_frame_out* frm, const msao_req_out* req,
                                    float* alpha_out, float* desc, void* ws, size_t ws_bytes, void* stream);
 
+/* ---- the SimHash variant of Eq. 5 ----------------------------------------- */
+
+/* Random hyperplanes of one segment for Charikar's hash (Sec. 4.1.2 Eq. 5
+ * with h_k(f) = 1 iff r_k . f >= 0). planes: device [bits][hidden] in the
+ * segment's dtype (row k is r_k), 16-byte aligned; bits: 16, 32, 48 or 64.
+ * The caller draws the hyperplanes (e.g. N(0, 1) entries). */
+typedef struct {
+    const void* planes;
+    int32_t bits;
+} msao_simhash;
+
+/* Sec. 4.1.2 Eq. 5 with SimHash instead of bit sampling. hashes (host, [n]):
+ * the entry of every temporal segment (VIDEO, n_frames >= 2,
+ * tokens_per_frame > 0) is required, the others are ignored.
+ *   sig (device [total tokens] u64, required): the token's K-bit signature
+ *     (bit k for r_k; 0 outside temporal segments);
+ *   d (device [total tokens], required): the number of its K bits that
+ *     differ from the same patch in the previous frame; frame 0 is compared
+ *     with the all-zero frame, whose bits are all 1; 0 outside temporal
+ *     segments;
+ *   frm: D_t = sum of d over the frame, sim = 1 - D_t/(P K), gamma = 1 - sim;
+ *   temporal (device [n_requests*4] or NULL): the temporal term of Eq. 7
+ *     from frames 1..T-1 (1 - gamma_avg, or gamma_avg under
+ *     MSAO_FLAG_TEMPORAL_LITERAL).
+ * The projections are fp32 sums of exact bf16 products (fp32 products for
+ * fp32 data) on the matrix cores, so a bit whose projection is within
+ * rounding of 0 may differ from an exact evaluation. Workspace from
+ * msao_workspace_size. Errors: those of msao_temporal_redundancy, plus
+ * MSAO_ERR_INVALID_ARG for a missing hash entry or bits not in {16, 32, 48,
+ * 64}, MSAO_ERR_ALIGNMENT for planes, sig or d, MSAO_ERR_UNSUPPORTED for a
+ * row pitch of 64 MiB or more. */
+msao_status msao_temporal_simhash(msao_ctx* ctx, const msao_segment* segs, int n, int n_requests,
+                                  const msao_params* params, const msao_simhash* hashes, uint64_t* sig,
+                                  uint32_t* d, const msao_frame_out* frm, float* temporal, void* ws,
+                                  size_t ws_bytes, void* stream);
+
 /* ---- Sec. 4.2: the draft model's confidence ------------------------------- */
 
 /* Outputs of msao_draft_entropy, each [rows] device memory or NULL (not
@@ -407,7 +451,8 @@ double msao_expected_e2e_latency(const msao_latency_model* m);
 #define MSAO_KERNEL_GATHER 2  /* compaction */
 #define MSAO_KERNEL_ENTROPY 3 /* draft confidence */
 #define MSAO_KERNEL_HEAD 4    /* learned spatial head: pooling, sigmoid, Eq. 4 counts */
-#define MSAO_NUM_KERNELS 5
+#define MSAO_KERNEL_SIMHASH 5 /* SimHash signatures (the k_hash_post launch counts as POST) */
+#define MSAO_NUM_KERNELS 6
 
 /* When enabled, every launch is bracketed by a pair of HIP events recorded on
  * the caller's stream. */

@@ -21,7 +21,8 @@ NMOD = 4
 TEXT, IMAGE, VIDEO, AUDIO = 0, 1, 2, 3
 F32, BF16 = 0, 1
 FLAG_TEMPORAL_LITERAL = 1
-KERNEL_SCORE, KERNEL_POST, KERNEL_GATHER, KERNEL_ENTROPY, KERNEL_HEAD, NUM_KERNELS = 0, 1, 2, 3, 4, 5
+FLAG_SELECT_PER_FRAME = 2
+KERNEL_SCORE, KERNEL_POST, KERNEL_GATHER, KERNEL_ENTROPY, KERNEL_HEAD, KERNEL_SIMHASH, NUM_KERNELS = 0, 1, 2, 3, 4, 5, 6
 MODAL_DESC = 8
 DECIDE_HOLD, DECIDE_SEND, DECIDE_OFFLOAD = 0, 1, 2
 
@@ -67,6 +68,10 @@ class MsaoSpatialHead(ctypes.Structure):
 class MsaoModalMlp(ctypes.Structure):
     _fields_ = [("w1", _P), ("b1", _P), ("w2", _P), ("b2", ctypes.c_float), ("hidden", ctypes.c_int32),
                 ("prompt_dim", ctypes.c_int32), ("prompt", _P)]
+
+
+class MsaoSimHash(ctypes.Structure):
+    _fields_ = [("planes", _P), ("bits", ctypes.c_int32)]
 
 
 class MsaoEntropyOut(ctypes.Structure):
@@ -129,6 +134,8 @@ SIGNATURES = [
     ("msao_kernel_times", ctypes.c_int, [_P, _P]),
     ("msao_mas_score_learned", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P,
                                               _P, _P, _P, ctypes.c_size_t, _P]),
+    ("msao_temporal_simhash", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P,
+                                             ctypes.c_size_t, _P]),
     ("msao_draft_entropy", ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
                                           ctypes.c_float, _P, _P]),
     ("msao_sched_default_params", MsaoSchedParams, []),
@@ -477,6 +484,34 @@ def msao_temporal_redundancy(segments, n_requests, params=None, ctx=None, output
     """Eq. 5 terms only: d, res, per-frame D/sim/gamma, temporal term per (request, modality)."""
     return _one_shot("msao_temporal_redundancy", segments, n_requests, params, None, ctx, outputs, stream,
                      compact=False)
+
+
+def msao_temporal_simhash(segments, n_requests, hashes, params=None, ctx=None, outputs=None, stream=None, sig=None):
+    """Eq. 5 with SimHash: hashes[s] = dict(planes=[bits, hidden] device
+    tensor in the segment's dtype, bits) for temporal segments (None
+    elsewhere). Fills outputs.tok["d"], outputs.frm and outputs.req["temporal"];
+    returns (outputs, sig) with sig the [total tokens] int64 signatures."""
+    device = _device_of(segments)
+    ctx = ctx or default_context(device.index if device.index is not None else torch.cuda.current_device())
+    o = outputs or Outputs(segments, n_requests, compact=False)
+    segt = segment_table(segments)
+    prm = params_struct(params)
+    n = len(segments)
+    harr = (MsaoSimHash * max(1, n))()
+    keep = [segt, prm, harr]
+    for i, h in enumerate(hashes):
+        if h is None:
+            continue
+        keep.append(h["planes"])
+        harr[i] = MsaoSimHash(h["planes"].data_ptr(), int(h["bits"]))
+    if sig is None:
+        sig = torch.empty(max(o.ntok, 1), dtype=torch.int64, device=device)[:o.ntok]
+    st = stream if stream is not None else torch.cuda.current_stream(device)
+    _check(lib().msao_temporal_simhash(ctx.handle, segt, n, n_requests, _addr(prm), ctypes.cast(harr, _P),
+                                       _ptr(sig) if o.ntok else None, _ptr(o.tok["d"]) if o.ntok else None,
+                                       _addr(o.c_frm), _ptr(o.req["temporal"]), _ptr(o.workspace),
+                                       ctypes.c_size_t(o.ws_bytes), ctypes.c_void_p(st.cuda_stream)), ctx)
+    return o, sig
 
 
 def msao_select_tokens(segments, n_requests, z, d=None, mas=None, params=None, ctx=None, outputs=None,

@@ -85,7 +85,8 @@ msao_status validate_impl(const msao_segment* segs, int n, int R, const msao_par
         if (!(p->lambda_s[m] >= 0.0f && p->lambda_s[m] <= 1.0f) || !(p->lambda_t[m] >= 0.0f && p->lambda_t[m] <= 1.0f))
             return fail(err, MSAO_ERR_INVALID_ARG, "lambda_s and lambda_t must be in [0, 1]");
     }
-    if (p->flags & ~MSAO_FLAG_TEMPORAL_LITERAL) return fail(err, MSAO_ERR_INVALID_ARG, "unknown flag bits");
+    if (p->flags & ~(MSAO_FLAG_TEMPORAL_LITERAL | MSAO_FLAG_SELECT_PER_FRAME))
+        return fail(err, MSAO_ERR_INVALID_ARG, "unknown flag bits");
     int64_t total = 0;
     for (int i = 0; i < n; ++i) {
         const msao_segment& s = segs[i];
@@ -128,7 +129,9 @@ struct Plan {
     std::vector<float> alpha;
     int64_t ntok = 0, nframes = 0;
     int n_wi = 0, n_gwi = 0;
-    int max_n = 0;                 // largest segment (LDS key staging)
+    int max_n = 0;                 // largest selection (LDS key staging)
+    std::vector<SelUnit> sel_unit; // one selection block each: a segment, or a frame (per-frame scope)
+    std::vector<int32_t> hi_seg;   // SimHash calls: segment of each hash tile
     bool any_temporal = false, any_guided = false;
     bool any_copy = false;         // some segment is compacted by the scoring pass
     // learned calls (Eq. 3 heads, Eq. 6 descriptors)
@@ -138,10 +141,11 @@ struct Plan {
     int mlp_hidden = 0;            // > 0: the relevance MLP's u = W1[:, :P] p + b1 per request
     size_t off_hbseg = 0, off_partial_x = 0, off_proj = 0, off_head_count = 0, off_mlp_u = 0;
     size_t off_seg = 0, off_wi = 0, off_gi = 0, off_rmoff = 0, off_rmseg = 0, off_tseg = 0, off_alpha = 0;
+    size_t off_selu = 0, off_hiseg = 0;
     size_t table_bytes = 0, off_partial = 0, total_bytes = 0;
 };
 
-size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t n_hb = 0)
+size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t n_hb, int64_t n_sel, int64_t n_hi)
 {
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -157,20 +161,22 @@ size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t
     pl.off_tseg = take(sizeof(int32_t) * (size_t)std::max(n, 1));
     pl.off_alpha = take(sizeof(float) * (size_t)std::max(R * kNumMod, 1));
     pl.off_hbseg = take(sizeof(int32_t) * (size_t)std::max<int64_t>(n_hb, 1));
+    pl.off_selu = take(sizeof(SelUnit) * (size_t)std::max<int64_t>(n_sel, 1));
+    pl.off_hiseg = take(sizeof(int32_t) * (size_t)std::max<int64_t>(n_hi, 1));
     pl.table_bytes = o;
     return o;
 }
 
-// Workspace bound that does not depend on tuning: work items, gather items
-// and head blocks never outnumber tokens, so one Partial and table entries
-// per token, plus what a learned call adds (a PartialX per work item, one
+// Workspace bound that does not depend on tuning: work items, gather items,
+// head blocks, selections and hash tiles never outnumber tokens plus
+// segments, so one Partial and table entries per token, plus what a learned call adds (a PartialX per work item, one
 // projection and one head count per token, kMaxMlpHidden floats of the MLP's
 // prompt product per request).
 size_t workspace_bytes_for(int n, int R, int64_t ntok)
 {
     Plan pl;
     const int64_t items = ntok + n;
-    const size_t tb = table_layout(pl, n, R, items, items, items);
+    const size_t tb = table_layout(pl, n, R, items, items, items, items, items);
     return align_up(tb, kWsAlign) + align_up(sizeof(Partial) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
            align_up(sizeof(PartialX) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
            align_up(sizeof(float) * (size_t)std::max<int64_t>(ntok, 1), kWsAlign) +
@@ -182,8 +188,13 @@ size_t workspace_bytes_for(int n, int R, int64_t ntok)
 // are copied by the scoring pass (they get no gather items).
 void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* p,
                 const float* alpha, const int64_t* out_off, Plan& pl, bool fuse_copy = false,
-                const msao_spatial_head* heads = nullptr, bool learned = false, int mlp_hidden = 0)
+                const msao_spatial_head* heads = nullptr, bool learned = false, int mlp_hidden = 0,
+                const msao_simhash* hashes = nullptr)
 {
+    const bool per_frame = (p->flags & MSAO_FLAG_SELECT_PER_FRAME) != 0;
+    pl.sel_unit.clear();
+    pl.hi_seg.clear();
+    pl.max_n = 0;
     pl.learned = learned;
     pl.mlp_hidden = learned ? mlp_hidden : 0;
     pl.hb_seg.clear();
@@ -222,8 +233,29 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         d.L_t = q24(p->lambda_t[s.modality]);
         d.lam_s = p->lambda_s[s.modality];
         d.lam_t = p->lambda_t[s.modality];
-        d.k = s.keep_ratio < 0.0f ? -1 : (int32_t)keep_count(s.keep_ratio, N);
+        // selections: the segment, or each of its frames (per-frame scope)
+        const bool framed = per_frame && s.n_frames >= 2 && s.tokens_per_frame > 0;
+        if (framed) {
+            d.kf = s.keep_ratio < 0.0f ? -1 : (int32_t)keep_count(s.keep_ratio, s.tokens_per_frame);
+            d.k = d.kf < 0 ? -1 : d.kf * s.n_frames;
+            for (int f = 0; f < s.n_frames; ++f) pl.sel_unit.push_back(SelUnit{i, f});
+            pl.max_n = std::max(pl.max_n, s.tokens_per_frame);
+        } else {
+            d.kf = -1;
+            d.k = s.keep_ratio < 0.0f ? -1 : (int32_t)keep_count(s.keep_ratio, N);
+            pl.sel_unit.push_back(SelUnit{i, -1});
+            pl.max_n = std::max(pl.max_n, (int)N);
+        }
         d.cap = d.k < 0 ? (int32_t)N : d.k;
+        if (hashes) {
+            // SimHash tiles of kHashTokens tokens (segments without a hash get zeros)
+            d.hi_begin = (int32_t)pl.hi_seg.size();
+            if (d.temporal) {
+                d.planes = (const uint8_t*)hashes[i].planes;
+                d.hash_bits = hashes[i].bits;
+            }
+            for (int64_t r = 0; r < N; r += kHashTokens) pl.hi_seg.push_back(i);
+        }
         d.copy_in_score = (fuse_copy && out_off && N > 0 && d.k == (int32_t)N) ? 1 : 0;
         if (learned && heads && heads[i].weight && N > 0) {
             d.head_w = (const uint8_t*)heads[i].weight;
@@ -262,7 +294,6 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         pl.seg_gi[(size_t)i + 1] = gi;
         if (d.k < 0) pl.any_guided = true;
         if (d.copy_in_score) pl.any_copy = true;
-        pl.max_n = std::max(pl.max_n, (int)N);
         tok += N;
         if (d.temporal) frame += s.n_frames;
     }
@@ -298,7 +329,8 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
     pl.alpha.assign((size_t)std::max(R * kNumMod, 1), 0.0f);
     if (alpha)
         for (int x = 0; x < R * kNumMod; ++x) pl.alpha[(size_t)x] = alpha[x];
-    table_layout(pl, n, R, pl.n_wi, pl.n_gwi, (int64_t)pl.hb_seg.size());
+    table_layout(pl, n, R, pl.n_wi, pl.n_gwi, (int64_t)pl.hb_seg.size(), (int64_t)pl.sel_unit.size(),
+                 (int64_t)pl.hi_seg.size());
     pl.off_partial = align_up(pl.table_bytes, kWsAlign);
     pl.total_bytes = pl.off_partial + sizeof(Partial) * (size_t)std::max(pl.n_wi, 1);
     if (learned) {
@@ -363,6 +395,8 @@ msao_status upload(msao_ctx* ctx, const Plan& pl, void* ws, hipStream_t stream)
     put(pl.off_tseg, pl.tseg.data(), sizeof(int32_t) * pl.tseg.size());
     put(pl.off_alpha, pl.alpha.data(), sizeof(float) * pl.alpha.size());
     put(pl.off_hbseg, pl.hb_seg.data(), sizeof(int32_t) * pl.hb_seg.size());
+    put(pl.off_selu, pl.sel_unit.data(), sizeof(SelUnit) * pl.sel_unit.size());
+    put(pl.off_hiseg, pl.hi_seg.data(), sizeof(int32_t) * pl.hi_seg.size());
     if ((e = hipMemcpyAsync(ws, h, pl.table_bytes, hipMemcpyHostToDevice, stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipMemcpyAsync");
     if ((e = hipEventRecord(ctx->stage_ev[slot], stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
@@ -387,6 +421,9 @@ Tables device_tables(const Plan& pl, void* ws, int n, int R, const msao_params* 
     t.head_count = pl.learned ? (uint32_t*)(b + pl.off_head_count) : nullptr;
     t.hb_seg = (const int32_t*)(b + pl.off_hbseg);
     t.n_hb = (int32_t)pl.hb_seg.size();
+    t.sel_unit = (const SelUnit*)(b + pl.off_selu);
+    t.hi_seg = (const int32_t*)(b + pl.off_hiseg);
+    t.n_hi = (int32_t)pl.hi_seg.size();
     t.n = n;
     t.R = R;
     t.n_wi = pl.n_wi;
@@ -458,6 +495,11 @@ int run_post(const void* a, void* s, void* e0, void* e1) { return launch_post(*(
 int run_gather(const void* a, void* s, void* e0, void* e1) { return launch_gather(*(const GatherArgs*)a, s, e0, e1); }
 int run_entropy(const void* a, void* s, void* e0, void* e1) { return launch_entropy(*(const EntArgs*)a, s, e0, e1); }
 int run_head(const void* a, void* s, void* e0, void* e1) { return launch_head(*(const HeadArgs*)a, s, e0, e1); }
+int run_simhash(const void* a, void* s, void* e0, void* e1) { return launch_simhash(*(const HashArgs*)a, s, e0, e1); }
+int run_hash_post(const void* a, void* s, void* e0, void* e1)
+{
+    return launch_hash_post(*(const HashArgs*)a, s, e0, e1);
+}
 
 #define MSAO_TRY(x)                                                                                                   \
     do {                                                                                                              \
@@ -577,7 +619,9 @@ msao_status msao_compact_layout(const msao_segment* segs, int n, int64_t* out_by
         const int64_t N = (int64_t)s.n_frames * s.tokens_per_frame;
         if (s.n_frames < 1 || s.tokens_per_frame < 0 || std::isnan(s.keep_ratio))
             return fail(&g_err, MSAO_ERR_INVALID_ARG, "msao_compact_layout: bad segment");
-        const int64_t cap = s.keep_ratio < 0.0f ? N : keep_count(s.keep_ratio, N);
+        int64_t cap = s.keep_ratio < 0.0f ? N : keep_count(s.keep_ratio, N);
+        if (s.keep_ratio >= 0.0f && s.n_frames >= 2)  // room for the per-frame scope's count too
+            cap = std::max<int64_t>(cap, s.n_frames * keep_count(s.keep_ratio, s.tokens_per_frame));
         out_byte_off[i] = o;
         o = (int64_t)align_up((size_t)(o + cap * (int64_t)s.hidden * elt_size(s.dtype)), kWsAlign);
     }
@@ -736,6 +780,52 @@ msao_status msao_temporal_redundancy(msao_ctx* ctx, const msao_segment* segs, in
     return launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa);
 }
 
+msao_status msao_temporal_simhash(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
+                                  const msao_simhash* hashes, uint64_t* sig, uint32_t* d, const msao_frame_out* frm,
+                                  float* temporal, void* ws, size_t ws_bytes, void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
+    if (n > 0 && !hashes) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "hashes is NULL");
+    char buf[160];
+    for (int i = 0; i < n; ++i) {
+        const msao_segment& s = segs[i];
+        if (!is_temporal(s)) continue;
+        auto bad = [&](msao_status st, const char* what) {
+            std::snprintf(buf, sizeof buf, "hash of segment %d: %s", i, what);
+            return fail(&ctx->err, st, buf);
+        };
+        const msao_simhash& h = hashes[i];
+        if (!h.planes) return bad(MSAO_ERR_INVALID_ARG, "planes is NULL");
+        if (h.bits != 16 && h.bits != 32 && h.bits != 48 && h.bits != 64)
+            return bad(MSAO_ERR_INVALID_ARG, "bits must be 16, 32, 48 or 64");
+        if (!aligned(h.planes, 16)) return bad(MSAO_ERR_ALIGNMENT, "planes is not 16-byte aligned");
+        if (s.row_stride * elt_size(s.dtype) >= ((int64_t)1 << 26))
+            return bad(MSAO_ERR_UNSUPPORTED, "row pitch of 64 MiB or more");
+    }
+    Plan pl;
+    build_plan(ctx, segs, n, R, params, nullptr, nullptr, pl, false, nullptr, false, 0, hashes);
+    MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
+    if (pl.ntok > 0 && (!sig || !d)) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "sig and d are required");
+    MSAO_TRY(check_out_alignment(ctx, {{sig, 8}, {d, 4}, {temporal, 4}}));
+    if (frm) MSAO_TRY(check_out_alignment(ctx, {{frm->dframe, 8}, {frm->sim, 4}, {frm->gamma, 4}}));
+    DeviceGuard guard(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    MSAO_TRY(upload(ctx, pl, ws, st));
+    HashArgs ha;
+    std::memset(&ha, 0, sizeof ha);
+    ha.t = device_tables(pl, ws, n, R, params);
+    ha.sig = sig;
+    ha.d = d;
+    if (frm) ha.frm = FrameOut{frm->dframe, frm->sim, frm->gamma};
+    ha.temporal = temporal;
+    MSAO_TRY(launched(ctx, MSAO_KERNEL_SIMHASH, st, run_simhash, &ha));
+    // frame blocks write d for every temporal token, so they always run
+    ha.n_frame_blocks = (int)pl.nframes;
+    ha.n_req_blocks = temporal ? R : 0;
+    return launched(ctx, MSAO_KERNEL_POST, st, run_hash_post, &ha);
+}
+
 msao_status msao_select_tokens(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
                                const uint32_t* z, const uint32_t* d, const float* mas, const msao_select_out* sel,
                                void* ws, size_t ws_bytes, void* stream)
@@ -761,7 +851,7 @@ msao_status msao_select_tokens(msao_ctx* ctx, const msao_segment* segs, int n, i
     pa.z = z;
     pa.d = d;
     pa.mas_in = mas;
-    pa.n_sel_blocks = n;
+    pa.n_sel_blocks = (int)pl.sel_unit.size();
     pa.keys_cap = std::min(pl.max_n, kMaxLdsKeys);
     return launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa);
 }
@@ -967,7 +1057,7 @@ msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const ms
     const bool want_frames = frm && (frm->dframe || frm->sim || frm->gamma) && pl.nframes > 0;
     pa.n_req_blocks = want_req ? t.R : 0;
     pa.n_frame_blocks = want_frames ? (int)pl.nframes : 0;
-    pa.n_sel_blocks = t.n;
+    pa.n_sel_blocks = (int)pl.sel_unit.size();
     pa.keys_cap = std::min(pl.max_n, kMaxLdsKeys);
     MSAO_TRY(launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa));
     if (!out || t.n_gwi == 0) return MSAO_OK;

@@ -10,6 +10,7 @@ namespace msao {
 
 enum : int { kText = 0, kImage = 1, kVideo = 2, kAudio = 3, kNumMod = 4 };
 enum : int { kF32 = 0, kBF16 = 1 };
+constexpr uint32_t kFlagLiteral = 1u;  // Eq. 7 takes gamma_avg as printed (the public flag bit 1)
 enum : int { kModeScore = 0, kModeTemporal = 1 };
 
 // One segment as the kernels see it. Built on the host for every call and
@@ -41,6 +42,18 @@ struct DevSeg {
     int32_t grid_w;        // patches per row of a frame's grid
     int32_t pool;          // odd AvgPool window
     int32_t hb_begin;      // first head block (one per frame)
+    // per-frame selection scope
+    int32_t kf;            // fixed keep count per frame, or -1 when MAS-guided
+    // SimHash variant of Eq. 5, set only by SimHash calls
+    const uint8_t* planes; // [hash_bits][C] hyperplanes in the segment's dtype
+    int32_t hash_bits;     // K per token (16, 32, 48 or 64)
+    int32_t hi_begin;      // first hash tile (kHashTokens tokens each)
+};
+
+// One selection: a whole segment (frame -1) or one frame of a clip
+// (per-frame scope).
+struct SelUnit {
+    int32_t seg, frame;
 };
 
 // Integer partial sums of one scoring work item (no atomics, no zeroing).
@@ -88,6 +101,9 @@ struct Tables {
     uint32_t* head_count;    // [n_hb] tokens with importance < tau_s, per head block
     const int32_t* hb_seg;   // [n_hb] segment of each head block
     int32_t n_hb;
+    const SelUnit* sel_unit; // [n_sel] selections (one block each)
+    const int32_t* hi_seg;   // [n_hi] segment of each hash tile (SimHash calls)
+    int32_t n_hi;
     int32_t n, R, n_wi, n_gwi, n_tseg, n_frames;
     float tau, tau_s;
     float lam_s[kNumMod], lam_t[kNumMod];
@@ -167,6 +183,20 @@ constexpr int kHeadBlock = 256;
 constexpr int kMaxHeadFrame = 16384;  // tokens per frame of a segment with a head (LDS)
 constexpr int kMaxPool = 15;
 constexpr int kMaxMlpHidden = 4096;
+
+// The SimHash variant of Eq. 5: k_simhash computes each token's signature
+// (one wavefront per tile of kHashTokens tokens, MFMA over the channels);
+// k_hash_post derives d, D_t, sim, gamma (one block per frame) and the
+// temporal term (one block per request).
+constexpr int kHashTokens = 32;
+struct HashArgs {
+    Tables t;
+    uint64_t* sig;        // [Ntot]
+    uint32_t* d;          // [Ntot]
+    FrameOut frm;
+    float* temporal;      // [R*4] (NULL: not written)
+    int32_t n_frame_blocks, n_req_blocks;
+};
 constexpr int kMlpGroup = 8;          // requests per wavefront in the prompt product
 
 struct GatherArgs {
@@ -205,6 +235,8 @@ int launch_score(const ScoreArgs& a, void* stream, void* ev0, void* ev1);
 int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1);
 int launch_gather(const GatherArgs& a, void* stream, void* ev0, void* ev1);
 int launch_head(const HeadArgs& a, void* stream, void* ev0, void* ev1);
+int launch_simhash(const HashArgs& a, void* stream, void* ev0, void* ev1);
+int launch_hash_post(const HashArgs& a, void* stream, void* ev0, void* ev1);
 
 constexpr int kScoreBlock = 256;   // 4 wavefronts, one work item each
 #ifndef MSAO_POST_BLOCK

@@ -942,7 +942,7 @@ __device__ MasTerms mas_terms(const Tables& t, const RMAgg& g, double beta, int 
     o.tterm = 0.0;
     if (o.has_t) {
         const double gamma_avg = (double)g.dsum / (double)g.qbits;
-        o.tterm = (t.flags & 1u) ? gamma_avg : 1.0 - gamma_avg;
+        o.tterm = (t.flags & kFlagLiteral) ? gamma_avg : 1.0 - gamma_avg;
     }
     double inner = 1.0 - (double)t.lam_s[m] * o.rho;
     if (o.has_t) inner = inner - (double)t.lam_t[m] * o.tterm;
@@ -1254,11 +1254,12 @@ struct KeySrc {
     }
 };
 
-// Rank k-1 of the segment's keys (range [lo, hi]) by MSD radix select, then
-// keep flags and ascending kept indices. IN_LDS: every key is staged in LDS.
+// Rank k-1 of the N keys of a selection (range [lo, hi]) by MSD radix
+// select, then keep flags (at off + i) and ascending kept indices (iadd + i,
+// written from ioff). IN_LDS: every key is staged in LDS.
 template <int NT, bool IN_LDS>
 __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const KeySrc& src, uint64_t* cand,
-                                   int cand_cap, int N, int k, int off, uint64_t lo, uint64_t hi)
+                                   int cand_cap, int N, int k, int off, int ioff, int iadd, uint64_t lo, uint64_t hi)
 {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid >> 6;
     auto key_at = [&](int i) -> uint64_t { return src.at<IN_LDS>(i); };
@@ -1383,27 +1384,32 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
             const bool kp = isl || (ise && eq_run + lanes_below(me) < ties);
             const uint64_t mk = __ballot(kp);
             if (v && a.sel.keep) a.sel.keep[off + i] = kp ? 1 : 0;
-            if (kp) a.sel.kept_idx[off + (int)(kept_run + lanes_below(mk))] = i;
+            if (kp) a.sel.kept_idx[ioff + (int)(kept_run + lanes_below(mk))] = iadd + i;
             eq_run += (uint32_t)__popcll(me);
             kept_run += (uint32_t)__popcll(mk);
         }
     }
-    for (int i = k + tid; i < N; i += NT) a.sel.kept_idx[off + i] = -1;
 }
 
-// Top-k of one segment: the k smallest (key, index) pairs, kept indices
-// ascending (Sec. 4.1.1 pruning, k from the Eq. 11 floor or a fixed ratio).
-// Keys are staged in LDS when the segment fits (keys_cap entries), then an
-// MSD radix select finds the key of rank k-1 and each wavefront compacts a
-// contiguous index range with ballot/mbcnt.
+// Top-k of one selection: the k smallest (key, index) pairs of a segment, or
+// of one frame of a clip under the per-frame scope, kept indices ascending
+// (Sec. 4.1.1 pruning, k from the Eq. 11 floor or a fixed ratio). Keys are
+// staged in LDS when they fit (keys_cap entries), then an MSD radix select
+// finds the key of rank k-1 and each wavefront compacts a contiguous index
+// range with ballot/mbcnt. Frame f of a clip keeping k_f per frame writes
+// its kept indices at positions f k_f.. of the segment's range and its
+// share, P - k_f entries, of the -1 tail after the T k_f kept ones.
 template <int NT>
-__device__ void role_select(const PostArgs& a, int s, PostShared<NT>& sh, uint64_t* keys, int keys_cap)
+__device__ void role_select(const PostArgs& a, int unit, PostShared<NT>& sh, uint64_t* keys, int keys_cap)
 {
     const Tables& t = a.t;
+    const SelUnit su = t.sel_unit[unit];
+    const int s = su.seg, f = su.frame;
     const DevSeg sg = t.seg[s];
-    const int N = sg.n_tok;
+    const bool framed = f >= 0;
+    const int N = framed ? sg.P : sg.n_tok;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid >> 6;
-    int k = sg.k;
+    int k = framed ? sg.kf : sg.k;
     if (k < 0) {
         float mas;
         if (a.mas_in) {
@@ -1421,13 +1427,18 @@ __device__ void role_select(const PostArgs& a, int s, PostShared<NT>& sh, uint64
         }
         k = guided_keep_count(mas, N);
     }
-    if (tid == 0) a.sel.kept_count[s] = k;
-    const int off = sg.tok_off;
+    const int units = framed ? sg.T : 1;
+    if (tid == 0 && f <= 0) a.sel.kept_count[s] = k * units;
+    const int off = sg.tok_off + (framed ? f * sg.P : 0);      // keys and keep flags
+    const int ioff = sg.tok_off + (framed ? f * k : 0);        // kept indices
+    const int iadd = framed ? f * sg.P : 0;                    // local index of the selection's first token
+    const int fill = sg.tok_off + units * k + (framed ? f : 0) * (N - k);
+    for (int i = tid; i < N - k; i += NT) a.sel.kept_idx[fill + i] = -1;
     if (N == 0) return;
     if (k == 0 || k == N) {
         for (int i = tid; i < N; i += NT) {
             if (a.sel.keep) a.sel.keep[off + i] = k == N ? 1 : 0;
-            a.sel.kept_idx[off + i] = k == N ? i : -1;
+            if (k == N) a.sel.kept_idx[ioff + i] = iadd + i;
         }
         return;
     }
@@ -1464,8 +1475,8 @@ __device__ void role_select(const PostArgs& a, int s, PostShared<NT>& sh, uint64
 
     const KeySrc src{keys, z, d, kind, Ls, Lt, C};
     uint64_t* cand = keys + keys_cap;
-    if (in_lds) select_and_compact<NT, true>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, lo, hi);
-    else select_and_compact<NT, false>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, lo, hi);
+    if (in_lds) select_and_compact<NT, true>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, ioff, iadd, lo, hi);
+    else select_and_compact<NT, false>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, ioff, iadd, lo, hi);
 }
 
 // LR: a learned call (request role with head counts, descriptors and the

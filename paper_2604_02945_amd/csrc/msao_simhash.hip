@@ -1,0 +1,270 @@
+// msao_simhash.hip -- the SimHash variant of Eq. 5 (Sec. 4.1.2) on gfx950.
+//
+// Charikar's random-hyperplane hash of every token of a clip: bit k of the
+// token's signature is 1 iff r_k . f >= 0, for K = 16..64 caller hyperplanes.
+// The projections [tokens x C] . [C x K] are the path's one dense
+// contraction, so they run on the matrix cores (v_mfma_f32_16x16x32_bf16,
+// or v_mfma_f32_16x16x4_f32 for fp32 data): a wavefront streams a tile of
+// kHashTokens tokens once and turns the fp32 accumulators into signature
+// bits with one ballot per accumulator register. A second launch compares
+// each patch's signature with the previous frame's (d), sums D_t per frame
+// (one block per frame) and the temporal term per request (one block per
+// request). Nothing here is HBM traffic beyond one read of the rows and
+// 12 bytes per token written (signature, d).
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "msao_internal.h"
+
+namespace msao {
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kHashBlock = 256;                  // 4 wavefronts, one tile each
+constexpr int kMT = kHashTokens / 16;            // 16-token MFMA tiles per wavefront
+constexpr int kSteps = 4;                        // 64-byte column steps in flight per wavefront
+
+typedef unsigned int vec4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+// Raw buffer resource: loads at or past num_records return 0.
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, int bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+}
+
+// Rows are read once (nontemporal); hyperplanes are re-read by every tile.
+__device__ __forceinline__ vec4 load_row(rsrc_t r, int off) { return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2); }
+__device__ __forceinline__ vec4 load_plane(rsrc_t r, int off) { return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0); }
+
+constexpr int kOutOfRange = (int)0x80000000u;   // past any num_records of a tile
+
+// Signatures of tokens [r0, r0 + kHashTokens) of a temporal segment.
+//
+// MFMA operand layout (16 x 16 output tiles): lane l holds row l % 16 of A
+// and column l % 16 of B for the reduction slice of group g = l / 16, and
+// rows 4 g .. 4 g + 3 of column l % 16 of the result. A lane loads 16
+// bytes at column byte 64 s + 16 g of its token's row (A) and of its
+// hyperplane's row (B); since the reduction over channels may visit them in
+// any order, both operands only need the same assignment of channels to
+// (group, element). bf16: one 16x16x32 MFMA per 16-byte chunk (8 channels
+// per lane). fp32: four 16x16x4 MFMAs per chunk, element e of every lane
+// in the e-th.
+template <int DT, int KT>
+__device__ void hash_tile(const HashArgs& a, const DevSeg& sg, int r0, int lane)
+{
+    const int m = lane & 15, g = lane >> 4;
+    const int rows = min(kHashTokens, sg.n_tok - r0);
+    const int rb = sg.nchunk * 16;                       // row bytes
+    const int pitch = (int)sg.stride_bytes;              // < 64 MiB (host check)
+    const rsrc_t rx = make_rsrc(sg.data + (int64_t)r0 * sg.stride_bytes, rows * pitch);
+    const rsrc_t rr = make_rsrc(sg.planes, sg.hash_bits * rb);
+    f32x4 acc[kMT][KT];
+#pragma unroll
+    for (int i = 0; i < kMT; ++i)
+#pragma unroll
+        for (int j = 0; j < KT; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    const int nsteps = (rb + 63) / 64;
+    for (int s0 = 0; s0 < nsteps; s0 += kSteps) {
+        vec4 A[kSteps][kMT], B[kSteps][KT];
+#pragma unroll
+        for (int u = 0; u < kSteps; ++u) {
+            const int col = 64 * (s0 + u) + 16 * g;      // past the row: read as zero
+            const bool in = col < rb;
+#pragma unroll
+            for (int i = 0; i < kMT; ++i) A[u][i] = load_row(rx, in ? (16 * i + m) * pitch + col : kOutOfRange);
+#pragma unroll
+            for (int j = 0; j < KT; ++j) B[u][j] = load_plane(rr, in ? (16 * j + m) * rb + col : kOutOfRange);
+        }
+#pragma unroll
+        for (int u = 0; u < kSteps; ++u)
+#pragma unroll
+            for (int i = 0; i < kMT; ++i)
+#pragma unroll
+                for (int j = 0; j < KT; ++j) {
+                    if constexpr (DT == kBF16) {
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, A[u][i]),
+                                                                            __builtin_bit_cast(bf16x8, B[u][j]),
+                                                                            acc[i][j], 0, 0, 0);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(A[u][i][e]),
+                                                                             __uint_as_float(B[u][j][e]),
+                                                                             acc[i][j], 0, 0, 0);
+                    }
+                }
+    }
+    // signature bits: the ballot of result register e of tile (i, j) holds,
+    // at bit 16 g + n, the bit of hyperplane 16 j + n for token 16 i + 4 g + e;
+    // lane L assembles token L's signature (NaN compares false: bit 0)
+    const int li = lane >> 4, lg = (lane & 15) >> 2, le = lane & 3;
+    uint64_t sig = 0;
+#pragma unroll
+    for (int i = 0; i < kMT; ++i)
+#pragma unroll
+        for (int j = 0; j < KT; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint64_t b = __ballot(acc[i][j][e] >= 0.0f);
+                if (li == i && le == e) sig |= ((b >> (16 * lg)) & 0xFFFFull) << (16 * j);
+            }
+    if (lane < rows) a.sig[sg.tok_off + r0 + lane] = sig;
+}
+
+__global__ __launch_bounds__(kHashBlock) void k_simhash(HashArgs a)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (kHashBlock / kWave) + (threadIdx.x >> 6));
+    if (w >= a.t.n_hi) return;
+    const int s = __builtin_amdgcn_readfirstlane(a.t.hi_seg[w]);
+    const DevSeg sg = a.t.seg[s];
+    const int r0 = (w - sg.hi_begin) * kHashTokens;
+    if (!sg.temporal) {
+        // tokens outside temporal segments: no signature, no distance
+        if (lane < kHashTokens && r0 + lane < sg.n_tok) {
+            a.sig[sg.tok_off + r0 + lane] = 0ull;
+            a.d[sg.tok_off + r0 + lane] = 0u;
+        }
+        return;
+    }
+    const int kt = sg.hash_bits / 16;
+    if (sg.dtype == kBF16) {
+        switch (kt) {
+        case 1: hash_tile<kBF16, 1>(a, sg, r0, lane); break;
+        case 2: hash_tile<kBF16, 2>(a, sg, r0, lane); break;
+        case 3: hash_tile<kBF16, 3>(a, sg, r0, lane); break;
+        default: hash_tile<kBF16, 4>(a, sg, r0, lane); break;
+        }
+    } else {
+        switch (kt) {
+        case 1: hash_tile<kF32, 1>(a, sg, r0, lane); break;
+        case 2: hash_tile<kF32, 2>(a, sg, r0, lane); break;
+        case 3: hash_tile<kF32, 3>(a, sg, r0, lane); break;
+        default: hash_tile<kF32, 4>(a, sg, r0, lane); break;
+        }
+    }
+}
+
+// ------------------------------------------------------------ k_hash_post
+
+__device__ __forceinline__ uint64_t all_bits(int K) { return K >= 64 ? ~0ull : ((1ull << K) - 1ull); }
+
+// Block-wide sum of a 64-bit count, the same value in every thread.
+__device__ __forceinline__ uint64_t block_sum(uint64_t v, uint64_t* red)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, o);
+        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), o);
+        v += ((uint64_t)hi << 32) | lo;
+    }
+    __syncthreads();
+    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    uint64_t s = 0;
+#pragma unroll
+    for (int w = 0; w < kHashBlock / kWave; ++w) s += red[w];
+    return s;
+}
+
+// Frame f: d of its tokens against the previous frame (frame 0 against the
+// all-zero frame, all bits 1), D_t, sim = 1 - D_t / (P K), gamma.
+__device__ void hash_frame(const HashArgs& a, int f, uint64_t* red)
+{
+    const Tables& t = a.t;
+    int lo = 0, hi = t.n_tseg;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (t.seg[t.tseg[mid]].frame_off <= f) lo = mid; else hi = mid;
+    }
+    const DevSeg& sg = t.seg[t.tseg[lo]];
+    const int tt = f - sg.frame_off;
+    const int base = sg.tok_off + tt * sg.P;
+    const uint64_t ones = all_bits(sg.hash_bits);
+    uint64_t acc = 0;
+    for (int p = threadIdx.x; p < sg.P; p += kHashBlock) {
+        const uint64_t prev = tt > 0 ? a.sig[base + p - sg.P] : ones;
+        const uint32_t dd = (uint32_t)__popcll(a.sig[base + p] ^ prev);
+        a.d[base + p] = dd;
+        acc += dd;
+    }
+    const uint64_t D = block_sum(acc, red);
+    if (threadIdx.x == 0) {
+#pragma clang fp contract(off)
+        const double sim = 1.0 - (double)D / (double)((int64_t)sg.P * sg.hash_bits);
+        if (a.frm.dframe) a.frm.dframe[f] = D;
+        if (a.frm.sim) a.frm.sim[f] = (float)sim;
+        if (a.frm.gamma) a.frm.gamma[f] = (float)(1.0 - sim);
+    }
+}
+
+// Request r: per modality, the differing bits over frames 1..T-1 of its
+// clips (recomputed from the signatures) and (T - 1) P K, then the temporal
+// term of Eq. 7.
+__device__ void hash_request(const HashArgs& a, int r, uint64_t* red)
+{
+    const Tables& t = a.t;
+    for (int m = 0; m < kNumMod; ++m) {
+        const RmEntry e = t.rm[r * kNumMod + m];
+        uint64_t dsum = 0, qbits = 0;
+        for (int j = e.rng_begin; j < e.rng_end; ++j) {
+            const DevSeg& sg = t.seg[t.rm_rng[j].seg];
+            if (!sg.temporal) continue;
+            qbits += (uint64_t)(sg.T - 1) * (uint64_t)sg.P * (uint64_t)sg.hash_bits;
+            for (int i = sg.P + threadIdx.x; i < sg.n_tok; i += kHashBlock)
+                dsum += (uint64_t)__popcll(a.sig[sg.tok_off + i] ^ a.sig[sg.tok_off + i - sg.P]);
+        }
+        dsum = block_sum(dsum, red);
+        if (threadIdx.x == 0) {
+#pragma clang fp contract(off)
+            float term = 0.0f;
+            if (qbits > 0) {
+                const double gamma_avg = (double)dsum / (double)qbits;
+                term = (float)((t.flags & kFlagLiteral) ? gamma_avg : 1.0 - gamma_avg);
+            }
+            a.temporal[r * kNumMod + m] = term;
+        }
+    }
+}
+
+__global__ __launch_bounds__(kHashBlock) void k_hash_post(HashArgs a)
+{
+    __shared__ uint64_t red[kHashBlock / kWave];
+    const int b = blockIdx.x;
+    if (b < a.n_frame_blocks) hash_frame(a, b, red);
+    else hash_request(a, b - a.n_frame_blocks, red);
+}
+
+template <typename Args>
+int launch(void (*kernel)(Args), dim3 grid, dim3 block, void* stream, const Args& a, void* ev0, void* ev1)
+{
+    if (ev0 && ev1)
+        hipExtLaunchKernelGGL(kernel, grid, block, 0, (hipStream_t)stream, (hipEvent_t)ev0, (hipEvent_t)ev1, 0, a);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, 0, (hipStream_t)stream, a);
+    return (int)hipGetLastError();
+}
+
+}  // namespace
+
+int launch_simhash(const HashArgs& a, void* stream, void* ev0, void* ev1)
+{
+    if (a.t.n_hi <= 0) return 0;
+    if (!a.sig || !a.d) return (int)hipErrorInvalidValue;
+    const int waves = kHashBlock / kWave;
+    return launch(k_simhash, dim3((unsigned)((a.t.n_hi + waves - 1) / waves)), dim3(kHashBlock), stream, a, ev0, ev1);
+}
+
+int launch_hash_post(const HashArgs& a, void* stream, void* ev0, void* ev1)
+{
+    const int blocks = a.n_frame_blocks + a.n_req_blocks;
+    if (blocks <= 0) return 0;
+    if (!a.sig || !a.d || (a.n_req_blocks > 0 && !a.temporal)) return (int)hipErrorInvalidValue;
+    return launch(k_hash_post, dim3((unsigned)blocks), dim3(kHashBlock), stream, a, ev0, ev1);
+}
+
+}  // namespace msao

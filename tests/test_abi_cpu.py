@@ -127,8 +127,9 @@ def test_sizes_and_layout():
     off = (ctypes.c_int64 * 3)()
     total = ctypes.c_int64()
     assert L.msao_compact_layout(arr, 3, off, ctypes.byref(total)) == OK
-    # image: ceil(0.25*576) = 144 rows; video: ceil(0.25*40) = 10 rows; guided text: all 7 rows
-    assert off[0] == 0 and off[1] == 144 * 2048 and off[2] == 144 * 2048 + 10 * 2048
+    # image: ceil(0.25*576) = 144 rows; video: max(ceil(0.25*40), 4*ceil(0.25*10)) = 12 rows (room for
+    # the per-frame scope); guided text: all 7 rows
+    assert off[0] == 0 and off[1] == 144 * 2048 and off[2] == 144 * 2048 + 12 * 2048
     assert total.value == off[2] + 7 * 2048 + (256 - (7 * 2048) % 256) % 256
     assert all(o % 256 == 0 for o in off)
 

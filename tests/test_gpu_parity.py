@@ -120,7 +120,11 @@ def compare_selection(segments, R, got, ref, p, gpu_mas=None):
     for i, s in enumerate(segments):
         if kc[i] != ref["k"][i]:
             assert s.keep_ratio < 0
-            alt = oracle.keep_count(1.0 - float(gpu_mas[s.request * 4 + s.modality]), s.n_tokens)
+            kappa = 1.0 - float(gpu_mas[s.request * 4 + s.modality])
+            if p.get("flags", 0) & oracle.FLAG_SELECT_PER_FRAME and s.n_frames >= 2:
+                alt = s.n_frames * oracle.keep_count(kappa, s.tokens_per_frame)
+            else:
+                alt = oracle.keep_count(kappa, s.n_tokens)
             assert kc[i] == alt
     redo = oracle.select(segments, R, p, ref["z"], ref["d"], gpu_mas)
     assert np.array_equal(kc, redo["k"])
