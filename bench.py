@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--no-entropy", action="store_true",
                     help="skip the draft-confidence kernel and Algorithm 1 measurements")
     ap.add_argument("--entropy-steps", type=int, default=100, help="timed launches of the draft-confidence kernel")
+    ap.add_argument("--no-simhash", action="store_true",
+                    help="skip the SimHash variant of Eq. 5 on the video clips")
     ap.add_argument("--no-learned", action="store_true",
                     help="skip the learned-head variant (Eq. 3 heads and the Eq. 6 MLP) of the scoring pass")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -127,6 +129,11 @@ def committed_learned_traffic(config):
     if config != 4:
         return None
     return _committed("k_score_learned_trimodal_traffic.json", ("msao_kernels.hip", "msao_internal.h"))
+
+
+def committed_simhash_traffic():
+    """HBM bytes per k_simhash launch on the video clips (committed counters)."""
+    return _committed("k_simhash_video_traffic.json", ("msao_simhash.hip", "msao_internal.h"))
 
 
 def committed_entropy_traffic():
@@ -265,6 +272,81 @@ def learned_bench(args, dev, ctx, w, reps, fields):
         "roofline": {"bound": "hbm", "kernel": "k_score<true>", "achieved": gbs, "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "traffic": committed_learned_traffic(w.config)},
     }
+
+
+def simhash_bench(args, dev, ctx):
+    """The SimHash variant of Eq. 5 (K = 32 hyperplanes per token) on the video
+    clips (8 x 32 frames x 256 tokens x 1024 bf16, 134 MB), eight rotated
+    replicas (1.07 GB, a cold Infinity Cache), beside the bit-sampling
+    temporal pass (msao_temporal_redundancy) on the same replicas."""
+    import numpy as np
+    import torch
+
+    import paper_2604_02945_amd as msao
+    from workloads import make_workload, simhash_planes
+
+    w = make_workload(3)
+    reps, _ = pack_replicas(w, 8, dev)
+    R, K, C = w.n_requests, 32, w.segments[0].hidden
+    planes = torch.from_numpy(simhash_planes(K, C, seed=1).view(np.int16)).to(dev).view(torch.bfloat16)
+    hashes = [dict(planes=planes, bits=K) for _ in w.segments]
+    outs = [msao.Outputs(segs, R, compact=False) for segs in reps]
+    sigs = [torch.empty(w.n_tokens, dtype=torch.int64, device=dev) for _ in reps]
+    steps = max(1, min(args.steps, 100))
+
+    def kernels(fn):
+        for i in range(len(reps)):
+            fn(i)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(steps):
+            fn(i % len(reps))
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        ctx.set_profiling(True)
+        for i in range(steps):
+            fn(i % len(reps))
+        torch.cuda.synchronize()
+        k = ctx.kernel_times()
+        ctx.set_profiling(False)
+        return ms, k
+
+    ms_sh, k_sh = kernels(lambda i: msao.msao_temporal_simhash(reps[i], R, hashes, w.params, ctx=ctx, outputs=outs[i],
+                                                               sig=sigs[i]))
+    ms_bs, k_bs = kernels(lambda i: msao.msao_temporal_redundancy(reps[i], R, w.params, ctx=ctx, outputs=outs[i]))
+    ntok = w.n_tokens
+    b = w.input_bytes + 8 * ntok               # rows read once, signatures written
+    km = k_sh[msao.binding.KERNEL_SIMHASH]
+    gbs = b / (km * 1e-3) / 1e9
+    flops = 2.0 * ntok * C * K
+    res = {
+        "workload": f"{w.name}: 8 clips x 32 frames x 256 tokens x 1024 bf16, K = {K} hyperplanes",
+        "ms_per_call": ms_sh, "tokens_per_s": ntok / (ms_sh * 1e-3),
+        "kernel_ms": {"simhash": km, "hash_post": k_sh[msao.binding.KERNEL_POST],
+                      "bit_sampling_score": k_bs[msao.binding.KERNEL_SCORE],
+                      "bit_sampling_post": k_bs[msao.binding.KERNEL_POST]},
+        "ms_per_call_bit_sampling": ms_bs,
+        "algorithmic_bytes": b,
+        "mfma_tflops": flops / (km * 1e-3) / 1e12,
+        "roofline": {"bound": "hbm", "kernel": "k_simhash", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": gbs / PEAK_HBM_GBS, "traffic": committed_simhash_traffic()},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        seg = w.segments[0]
+        hp = simhash_planes(K, C, seed=1)
+        t0 = time.perf_counter()
+        oracle.temporal_simhash([seg], 1, w.params, [dict(planes=hp, bits=K)])
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": seg.n_tokens / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+                               "sample": f"one clip ({seg.n_tokens} tokens) of the same workload, single-threaded C "
+                                         f"oracle (fp64 projections), {dt:.2f} s"}
+    for o in outs:
+        del o
+    del reps
+    return res
 
 
 def cpu_baseline(w, budget_s):
@@ -441,6 +523,8 @@ def main():
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     if not args.no_learned:
         line["learned"] = learned_bench(args, dev, ctxs[0], w, reps, fields)
+    if not args.no_simhash:
+        line["simhash"] = simhash_bench(args, dev, ctxs[0])
     if not args.no_entropy:
         line["entropy"] = entropy_bench(args, dev, ctxs[0])
     for _, plan in plans:

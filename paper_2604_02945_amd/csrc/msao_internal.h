@@ -188,7 +188,10 @@ constexpr int kMaxMlpHidden = 4096;
 // (one wavefront per tile of kHashTokens tokens, MFMA over the channels);
 // k_hash_post derives d, D_t, sim, gamma (one block per frame) and the
 // temporal term (one block per request).
-constexpr int kHashTokens = 32;
+#ifndef MSAO_HASH_TOKENS
+#define MSAO_HASH_TOKENS 32
+#endif
+constexpr int kHashTokens = MSAO_HASH_TOKENS;  // 16, 32 or 64
 struct HashArgs {
     Tables t;
     uint64_t* sig;        // [Ntot]

@@ -23,7 +23,8 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kHashBlock = 256;                  // 4 wavefronts, one tile each
 constexpr int kMT = kHashTokens / 16;            // 16-token MFMA tiles per wavefront
-constexpr int kSteps = 4;                        // 64-byte column steps in flight per wavefront
+constexpr int kSteps = 4;                        // 64-byte column steps per 256-byte chunk
+static_assert(kHashTokens % 16 == 0 && kHashTokens <= 64, "tiles of 16, 32 or 64 tokens");
 
 typedef unsigned int vec4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -46,15 +47,33 @@ constexpr int kOutOfRange = (int)0x80000000u;   // past any num_records of a til
 //
 // MFMA operand layout (16 x 16 output tiles): lane l holds row l % 16 of A
 // and column l % 16 of B for the reduction slice of group g = l / 16, and
-// rows 4 g .. 4 g + 3 of column l % 16 of the result. A lane loads 16
-// bytes at column byte 64 s + 16 g of its token's row (A) and of its
-// hyperplane's row (B); since the reduction over channels may visit them in
-// any order, both operands only need the same assignment of channels to
-// (group, element). bf16: one 16x16x32 MFMA per 16-byte chunk (8 channels
-// per lane). fp32: four 16x16x4 MFMAs per chunk, element e of every lane
-// in the e-th.
+// rows 4 g .. 4 g + 3 of column l % 16 of the result. Since the reduction
+// over channels may visit them in any order, A and B only need the same
+// assignment of channels to (group, element): lane (m, g) takes the 16
+// bytes at column byte 64 u + 16 g of a 256-byte chunk, for its token (A)
+// and for hyperplane 16 j + m (B). bf16: one 16x16x32 MFMA per 16 bytes (8
+// channels per lane); fp32: four 16x16x4 MFMAs, element e in the e-th.
+//
+// Loading A in that layout would touch 16 rows x 64 bytes per instruction,
+// so the tile's rows are read 256 contiguous bytes per row (4 rows per
+// instruction) into a per-wavefront LDS slice with a 272-byte row pitch,
+// which keeps both the row writes and the column reads free of bank
+// conflicts, and the next chunk's loads are in flight during the MFMAs.
+constexpr int kChunk = 256;                       // bytes of every row per step
+constexpr int kLdsPitch = kChunk + 16;            // padded LDS row pitch
+constexpr int kLoadsPerChunk = kHashTokens / 4;   // 4 rows x 256 bytes per load
+
+// Orders this wavefront's LDS accesses across its lanes (no other
+// wavefront touches the slice).
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <int DT, int KT>
-__device__ void hash_tile(const HashArgs& a, const DevSeg& sg, int r0, int lane)
+__device__ void hash_tile(const HashArgs& a, const DevSeg& sg, int r0, int lane, uint8_t* lds)
 {
     const int m = lane & 15, g = lane >> 4;
     const int rows = min(kHashTokens, sg.n_tok - r0);
@@ -67,17 +86,32 @@ __device__ void hash_tile(const HashArgs& a, const DevSeg& sg, int r0, int lane)
     for (int i = 0; i < kMT; ++i)
 #pragma unroll
         for (int j = 0; j < KT; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    const int nsteps = (rb + 63) / 64;
-    for (int s0 = 0; s0 < nsteps; s0 += kSteps) {
+    // row loads: load q covers rows 4 q .. 4 q + 3; lane l takes row 4 q + l / 16, bytes 16 (l % 16) ..
+    const int lrow = lane >> 4, lcol = (lane & 15) * 16;
+    const int nchunks = (rb + kChunk - 1) / kChunk;
+    vec4 G[kLoadsPerChunk];
+#pragma unroll
+    for (int q = 0; q < kLoadsPerChunk; ++q) G[q] = load_row(rx, lcol < rb ? (4 * q + lrow) * pitch + lcol : kOutOfRange);
+    for (int c = 0; c < nchunks; ++c) {
+#pragma unroll
+        for (int q = 0; q < kLoadsPerChunk; ++q)
+            *reinterpret_cast<vec4*>(lds + (4 * q + lrow) * kLdsPitch + lcol) = G[q];
+        wave_lds_sync();
+        if (c + 1 < nchunks) {
+            const int col = (c + 1) * kChunk + lcol;        // past the row: zero
+#pragma unroll
+            for (int q = 0; q < kLoadsPerChunk; ++q)
+                G[q] = load_row(rx, col < rb ? (4 * q + lrow) * pitch + col : kOutOfRange);
+        }
         vec4 A[kSteps][kMT], B[kSteps][KT];
 #pragma unroll
         for (int u = 0; u < kSteps; ++u) {
-            const int col = 64 * (s0 + u) + 16 * g;      // past the row: read as zero
-            const bool in = col < rb;
+            const int col = c * kChunk + 64 * u + 16 * g;
 #pragma unroll
-            for (int i = 0; i < kMT; ++i) A[u][i] = load_row(rx, in ? (16 * i + m) * pitch + col : kOutOfRange);
+            for (int j = 0; j < KT; ++j) B[u][j] = load_plane(rr, col < rb ? (16 * j + m) * rb + col : kOutOfRange);
 #pragma unroll
-            for (int j = 0; j < KT; ++j) B[u][j] = load_plane(rr, in ? (16 * j + m) * rb + col : kOutOfRange);
+            for (int i = 0; i < kMT; ++i)
+                A[u][i] = *reinterpret_cast<const vec4*>(lds + (16 * i + m) * kLdsPitch + 64 * u + 16 * g);
         }
 #pragma unroll
         for (int u = 0; u < kSteps; ++u)
@@ -97,6 +131,7 @@ __device__ void hash_tile(const HashArgs& a, const DevSeg& sg, int r0, int lane)
                                                                              acc[i][j], 0, 0, 0);
                     }
                 }
+        wave_lds_sync();  // every lane has read the slice before it is rewritten
     }
     // signature bits: the ballot of result register e of tile (i, j) holds,
     // at bit 16 g + n, the bit of hyperplane 16 j + n for token 16 i + 4 g + e;
@@ -117,6 +152,7 @@ __device__ void hash_tile(const HashArgs& a, const DevSeg& sg, int r0, int lane)
 
 __global__ __launch_bounds__(kHashBlock) void k_simhash(HashArgs a)
 {
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kHashBlock / kWave][kHashTokens * kLdsPitch];
     const int lane = threadIdx.x & (kWave - 1);
     const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (kHashBlock / kWave) + (threadIdx.x >> 6));
     if (w >= a.t.n_hi) return;
@@ -134,17 +170,17 @@ __global__ __launch_bounds__(kHashBlock) void k_simhash(HashArgs a)
     const int kt = sg.hash_bits / 16;
     if (sg.dtype == kBF16) {
         switch (kt) {
-        case 1: hash_tile<kBF16, 1>(a, sg, r0, lane); break;
-        case 2: hash_tile<kBF16, 2>(a, sg, r0, lane); break;
-        case 3: hash_tile<kBF16, 3>(a, sg, r0, lane); break;
-        default: hash_tile<kBF16, 4>(a, sg, r0, lane); break;
+        case 1: hash_tile<kBF16, 1>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
+        case 2: hash_tile<kBF16, 2>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
+        case 3: hash_tile<kBF16, 3>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
+        default: hash_tile<kBF16, 4>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
         }
     } else {
         switch (kt) {
-        case 1: hash_tile<kF32, 1>(a, sg, r0, lane); break;
-        case 2: hash_tile<kF32, 2>(a, sg, r0, lane); break;
-        case 3: hash_tile<kF32, 3>(a, sg, r0, lane); break;
-        default: hash_tile<kF32, 4>(a, sg, r0, lane); break;
+        case 1: hash_tile<kF32, 1>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
+        case 2: hash_tile<kF32, 2>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
+        case 3: hash_tile<kF32, 3>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
+        default: hash_tile<kF32, 4>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
         }
     }
 }
@@ -215,8 +251,21 @@ __device__ void hash_request(const HashArgs& a, int r, uint64_t* red)
             const DevSeg& sg = t.seg[t.rm_rng[j].seg];
             if (!sg.temporal) continue;
             qbits += (uint64_t)(sg.T - 1) * (uint64_t)sg.P * (uint64_t)sg.hash_bits;
-            for (int i = sg.P + threadIdx.x; i < sg.n_tok; i += kHashBlock)
-                dsum += (uint64_t)__popcll(a.sig[sg.tok_off + i] ^ a.sig[sg.tok_off + i - sg.P]);
+            // 8 tokens per thread in flight (indices clamped, extras dropped)
+            constexpr int U = 8;
+            const uint64_t* sig = a.sig + sg.tok_off;
+            for (int i0 = sg.P + threadIdx.x; i0 < sg.n_tok; i0 += U * kHashBlock) {
+                uint64_t cur[U], prev[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int i = min(i0 + u * kHashBlock, sg.n_tok - 1);
+                    cur[u] = sig[i];
+                    prev[u] = sig[i - sg.P];
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (i0 + u * kHashBlock < sg.n_tok) dsum += (uint64_t)__popcll(cur[u] ^ prev[u]);
+            }
         }
         dsum = block_sum(dsum, red);
         if (threadIdx.x == 0) {
