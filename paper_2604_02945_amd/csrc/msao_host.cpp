@@ -248,13 +248,13 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         }
         d.cap = d.k < 0 ? (int32_t)N : d.k;
         if (hashes) {
-            // SimHash tiles of kHashTokens tokens (segments without a hash get zeros)
+            // SimHash blocks of kHashBlockTokens tokens (segments without a hash get zeros)
             d.hi_begin = (int32_t)pl.hi_seg.size();
             if (d.temporal) {
                 d.planes = (const uint8_t*)hashes[i].planes;
                 d.hash_bits = hashes[i].bits;
             }
-            for (int64_t r = 0; r < N; r += kHashTokens) pl.hi_seg.push_back(i);
+            for (int64_t r = 0; r < N; r += kHashBlockTokens) pl.hi_seg.push_back(i);
         }
         d.copy_in_score = (fuse_copy && out_off && N > 0 && d.k == (int32_t)N) ? 1 : 0;
         if (learned && heads && heads[i].weight && N > 0) {

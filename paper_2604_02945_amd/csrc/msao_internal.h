@@ -185,13 +185,16 @@ constexpr int kMaxPool = 15;
 constexpr int kMaxMlpHidden = 4096;
 
 // The SimHash variant of Eq. 5: k_simhash computes each token's signature
-// (one wavefront per tile of kHashTokens tokens, MFMA over the channels);
+// (one wavefront per tile of kHashTokens tokens, four tiles of one segment
+// per block, MFMA over the channels);
 // k_hash_post derives d, D_t, sim, gamma (one block per frame) and the
 // temporal term (one block per request).
 #ifndef MSAO_HASH_TOKENS
 #define MSAO_HASH_TOKENS 32
 #endif
 constexpr int kHashTokens = MSAO_HASH_TOKENS;  // 16, 32 or 64
+constexpr int kHashWaves = 4;                   // tiles (wavefronts) per block, one segment per block
+constexpr int kHashBlockTokens = kHashWaves * kHashTokens;
 struct HashArgs {
     Tables t;
     uint64_t* sig;        // [Ntot]

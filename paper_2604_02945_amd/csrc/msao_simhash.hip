@@ -21,7 +21,7 @@ namespace msao {
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kHashBlock = 256;                  // 4 wavefronts, one tile each
+constexpr int kHashBlock = 64 * kHashWaves;     // one wavefront per tile
 constexpr int kMT = kHashTokens / 16;            // 16-token MFMA tiles per wavefront
 constexpr int kSteps = 4;                        // 64-byte column steps per 256-byte chunk
 static_assert(kHashTokens % 16 == 0 && kHashTokens <= 64, "tiles of 16, 32 or 64 tokens");
@@ -54,64 +54,73 @@ constexpr int kOutOfRange = (int)0x80000000u;   // past any num_records of a til
 // and for hyperplane 16 j + m (B). bf16: one 16x16x32 MFMA per 16 bytes (8
 // channels per lane); fp32: four 16x16x4 MFMAs, element e in the e-th.
 //
-// Loading A in that layout would touch 16 rows x 64 bytes per instruction,
-// so the tile's rows are read 256 contiguous bytes per row (4 rows per
-// instruction) into a per-wavefront LDS slice with a 272-byte row pitch,
-// which keeps both the row writes and the column reads free of bank
-// conflicts, and the next chunk's loads are in flight during the MFMAs.
+// Reading A or B from memory in that layout would touch 16 rows x 64 bytes
+// per instruction. Instead each wavefront reads its tile 256 contiguous
+// bytes of 4 rows per instruction into its own LDS slice, and the block
+// reads the chunk's K hyperplane rows once into a shared slice (so the four
+// tiles of a block share them); both slices have a 272-byte row pitch,
+// which keeps the row writes and the column reads free of bank conflicts.
+// The next chunk's loads are in flight during the MFMAs.
 constexpr int kChunk = 256;                       // bytes of every row per step
 constexpr int kLdsPitch = kChunk + 16;            // padded LDS row pitch
 constexpr int kLoadsPerChunk = kHashTokens / 4;   // 4 rows x 256 bytes per load
 
-// Orders this wavefront's LDS accesses across its lanes (no other
-// wavefront touches the slice).
-__device__ __forceinline__ void wave_lds_sync()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
 template <int DT, int KT>
-__device__ void hash_tile(const HashArgs& a, const DevSeg& sg, int r0, int lane, uint8_t* lds)
+__device__ void hash_tile(const HashArgs& a, const DevSeg& sg, int r0, int lane, uint8_t* rows_lds,
+                          uint8_t* planes_lds)
 {
+    constexpr int K = 16 * KT;
+    constexpr int kPlaneLoads = K / 16;           // 16-byte pieces of the chunk's hyperplanes per thread
     const int m = lane & 15, g = lane >> 4;
-    const int rows = min(kHashTokens, sg.n_tok - r0);
+    const int rows = max(0, min(kHashTokens, sg.n_tok - r0));   // a tile past the end: no rows
     const int rb = sg.nchunk * 16;                       // row bytes
     const int pitch = (int)sg.stride_bytes;              // < 64 MiB (host check)
-    const rsrc_t rx = make_rsrc(sg.data + (int64_t)r0 * sg.stride_bytes, rows * pitch);
-    const rsrc_t rr = make_rsrc(sg.planes, sg.hash_bits * rb);
+    const rsrc_t rx = make_rsrc(sg.data + (int64_t)min(r0, sg.n_tok) * sg.stride_bytes, rows * pitch);
+    const rsrc_t rr = make_rsrc(sg.planes, K * rb);
     f32x4 acc[kMT][KT];
 #pragma unroll
     for (int i = 0; i < kMT; ++i)
 #pragma unroll
         for (int j = 0; j < KT; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    // row loads: load q covers rows 4 q .. 4 q + 3; lane l takes row 4 q + l / 16, bytes 16 (l % 16) ..
+    // tile rows: load q covers rows 4 q .. 4 q + 3; lane l takes row 4 q + l / 16, bytes 16 (l % 16) ..
     const int lrow = lane >> 4, lcol = (lane & 15) * 16;
-    const int nchunks = (rb + kChunk - 1) / kChunk;
-    vec4 G[kLoadsPerChunk];
+    // hyperplanes: piece p = tid + 256 v is row p / 16, bytes 16 (p % 16) .. of the chunk
+    const int tid = threadIdx.x;
+    auto load_chunk = [&](int c, vec4 (&G)[kLoadsPerChunk], vec4 (&H)[kPlaneLoads]) {
+        const int col = c * kChunk + lcol;               // past the row: zero
 #pragma unroll
-    for (int q = 0; q < kLoadsPerChunk; ++q) G[q] = load_row(rx, lcol < rb ? (4 * q + lrow) * pitch + lcol : kOutOfRange);
+        for (int q = 0; q < kLoadsPerChunk; ++q)
+            G[q] = load_row(rx, col < rb ? (4 * q + lrow) * pitch + col : kOutOfRange);
+#pragma unroll
+        for (int v = 0; v < kPlaneLoads; ++v) {
+            const int p = tid + kHashBlock * v;
+            const int pc = c * kChunk + (p & 15) * 16;
+            H[v] = load_plane(rr, pc < rb ? (p >> 4) * rb + pc : kOutOfRange);
+        }
+    };
+    const int nchunks = (rb + kChunk - 1) / kChunk;
+    vec4 G[kLoadsPerChunk], H[kPlaneLoads];
+    load_chunk(0, G, H);
     for (int c = 0; c < nchunks; ++c) {
 #pragma unroll
         for (int q = 0; q < kLoadsPerChunk; ++q)
-            *reinterpret_cast<vec4*>(lds + (4 * q + lrow) * kLdsPitch + lcol) = G[q];
-        wave_lds_sync();
-        if (c + 1 < nchunks) {
-            const int col = (c + 1) * kChunk + lcol;        // past the row: zero
+            *reinterpret_cast<vec4*>(rows_lds + (4 * q + lrow) * kLdsPitch + lcol) = G[q];
 #pragma unroll
-            for (int q = 0; q < kLoadsPerChunk; ++q)
-                G[q] = load_row(rx, col < rb ? (4 * q + lrow) * pitch + col : kOutOfRange);
+        for (int v = 0; v < kPlaneLoads; ++v) {
+            const int p = tid + kHashBlock * v;
+            *reinterpret_cast<vec4*>(planes_lds + (p >> 4) * kLdsPitch + (p & 15) * 16) = H[v];
         }
+        __syncthreads();
+        if (c + 1 < nchunks) load_chunk(c + 1, G, H);
         vec4 A[kSteps][kMT], B[kSteps][KT];
 #pragma unroll
         for (int u = 0; u < kSteps; ++u) {
-            const int col = c * kChunk + 64 * u + 16 * g;
 #pragma unroll
-            for (int j = 0; j < KT; ++j) B[u][j] = load_plane(rr, col < rb ? (16 * j + m) * rb + col : kOutOfRange);
+            for (int j = 0; j < KT; ++j)
+                B[u][j] = *reinterpret_cast<const vec4*>(planes_lds + (16 * j + m) * kLdsPitch + 64 * u + 16 * g);
 #pragma unroll
             for (int i = 0; i < kMT; ++i)
-                A[u][i] = *reinterpret_cast<const vec4*>(lds + (16 * i + m) * kLdsPitch + 64 * u + 16 * g);
+                A[u][i] = *reinterpret_cast<const vec4*>(rows_lds + (16 * i + m) * kLdsPitch + 64 * u + 16 * g);
         }
 #pragma unroll
         for (int u = 0; u < kSteps; ++u)
@@ -131,7 +140,7 @@ __device__ void hash_tile(const HashArgs& a, const DevSeg& sg, int r0, int lane,
                                                                              acc[i][j], 0, 0, 0);
                     }
                 }
-        wave_lds_sync();  // every lane has read the slice before it is rewritten
+        __syncthreads();  // every wavefront has read the slices before they are rewritten
     }
     // signature bits: the ballot of result register e of tile (i, j) holds,
     // at bit 16 g + n, the bit of hyperplane 16 j + n for token 16 i + 4 g + e;
@@ -150,37 +159,39 @@ __device__ void hash_tile(const HashArgs& a, const DevSeg& sg, int r0, int lane,
     if (lane < rows) a.sig[sg.tok_off + r0 + lane] = sig;
 }
 
+// One block per kHashBlockTokens tokens of a segment; wavefront w takes the
+// w-th tile. Segments that are not temporal get zero signatures and d.
 __global__ __launch_bounds__(kHashBlock) void k_simhash(HashArgs a)
 {
-    __shared__ __attribute__((aligned(16))) uint8_t lds[kHashBlock / kWave][kHashTokens * kLdsPitch];
-    const int lane = threadIdx.x & (kWave - 1);
-    const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (kHashBlock / kWave) + (threadIdx.x >> 6));
-    if (w >= a.t.n_hi) return;
-    const int s = __builtin_amdgcn_readfirstlane(a.t.hi_seg[w]);
+    __shared__ __attribute__((aligned(16))) uint8_t rows_lds[kHashWaves][kHashTokens * kLdsPitch];
+    __shared__ __attribute__((aligned(16))) uint8_t planes_lds[64 * kLdsPitch];
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+    const int b = blockIdx.x;
+    const int s = a.t.hi_seg[b];
     const DevSeg sg = a.t.seg[s];
-    const int r0 = (w - sg.hi_begin) * kHashTokens;
+    const int r0 = (b - sg.hi_begin) * kHashBlockTokens + wave * kHashTokens;
     if (!sg.temporal) {
-        // tokens outside temporal segments: no signature, no distance
         if (lane < kHashTokens && r0 + lane < sg.n_tok) {
             a.sig[sg.tok_off + r0 + lane] = 0ull;
             a.d[sg.tok_off + r0 + lane] = 0u;
         }
-        return;
+        return;  // the whole block: one segment
     }
+    uint8_t* mine = rows_lds[wave];
     const int kt = sg.hash_bits / 16;
     if (sg.dtype == kBF16) {
         switch (kt) {
-        case 1: hash_tile<kBF16, 1>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
-        case 2: hash_tile<kBF16, 2>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
-        case 3: hash_tile<kBF16, 3>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
-        default: hash_tile<kBF16, 4>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
+        case 1: hash_tile<kBF16, 1>(a, sg, r0, lane, mine, planes_lds); break;
+        case 2: hash_tile<kBF16, 2>(a, sg, r0, lane, mine, planes_lds); break;
+        case 3: hash_tile<kBF16, 3>(a, sg, r0, lane, mine, planes_lds); break;
+        default: hash_tile<kBF16, 4>(a, sg, r0, lane, mine, planes_lds); break;
         }
     } else {
         switch (kt) {
-        case 1: hash_tile<kF32, 1>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
-        case 2: hash_tile<kF32, 2>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
-        case 3: hash_tile<kF32, 3>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
-        default: hash_tile<kF32, 4>(a, sg, r0, lane, lds[threadIdx.x >> 6]); break;
+        case 1: hash_tile<kF32, 1>(a, sg, r0, lane, mine, planes_lds); break;
+        case 2: hash_tile<kF32, 2>(a, sg, r0, lane, mine, planes_lds); break;
+        case 3: hash_tile<kF32, 3>(a, sg, r0, lane, mine, planes_lds); break;
+        default: hash_tile<kF32, 4>(a, sg, r0, lane, mine, planes_lds); break;
         }
     }
 }
@@ -304,8 +315,7 @@ int launch_simhash(const HashArgs& a, void* stream, void* ev0, void* ev1)
 {
     if (a.t.n_hi <= 0) return 0;
     if (!a.sig || !a.d) return (int)hipErrorInvalidValue;
-    const int waves = kHashBlock / kWave;
-    return launch(k_simhash, dim3((unsigned)((a.t.n_hi + waves - 1) / waves)), dim3(kHashBlock), stream, a, ev0, ev1);
+    return launch(k_simhash, dim3((unsigned)a.t.n_hi), dim3(kHashBlock), stream, a, ev0, ev1);
 }
 
 int launch_hash_post(const HashArgs& a, void* stream, void* ev0, void* ev1)
