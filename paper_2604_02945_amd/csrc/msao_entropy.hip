@@ -118,10 +118,12 @@ __device__ __forceinline__ void acc_add(Acc& a, const float (&x)[N], IndexOf ind
 #pragma unroll
     for (int j = 1; j < N; ++j) cm = fmaxf(cm, x[j]);
     if (cm > a.m) {
-        int at = index(0);
+        // position of the first maximum, then its index (one computation)
+        int js = 0;
 #pragma unroll
         for (int j = N - 1; j >= 0; --j)
-            if (x[j] == cm) at = index(j);
+            if (x[j] == cm) js = j;
+        const int at = index(js);
         if (a.s > 0.0f) {
             const float dm = (a.m - cm) * kLog2e;
             const float sc = __builtin_amdgcn_exp2f(dm);
@@ -135,12 +137,28 @@ __device__ __forceinline__ void acc_add(Acc& a, const float (&x)[N], IndexOf ind
     // contribute 0) or NaN (which must reach s): take the exponent against 0,
     // since -inf - (-inf) would turn every -inf into NaN.
     const float nml = a.m == -INFINITY ? 0.0f : -a.m * kLog2e;
+    // A -inf logit gives e = 0 and d = -inf, whose product must be 0, not
+    // NaN: the clamp on d is needed only where the batch holds a -inf (one
+    // min per batch decides it for the whole wavefront).
+    float mn = x[0];
 #pragma unroll
-    for (int j = 0; j < N; ++j) {
-        const float d = fmaf(x[j], kLog2e, nml);  // L (x - m)
-        const float e = __builtin_amdgcn_exp2f(d);
-        a.s += e;
-        a.u = fmaf(e, fmaxf(d, kMinDiff * kLog2e), a.u);
+    for (int j = 1; j < N; ++j) mn = fminf(mn, x[j]);
+    if (__ballot(mn == -INFINITY) == 0) {
+#pragma unroll
+        for (int j = 0; j < N; ++j) {
+            const float d = fmaf(x[j], kLog2e, nml);  // L (x - m)
+            const float e = __builtin_amdgcn_exp2f(d);
+            a.s += e;
+            a.u = fmaf(e, d, a.u);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < N; ++j) {
+            const float d = fmaf(x[j], kLog2e, nml);
+            const float e = __builtin_amdgcn_exp2f(d);
+            a.s += e;
+            a.u = fmaf(e, fmaxf(d, kMinDiff * kLog2e), a.u);
+        }
     }
 }
 
