@@ -75,7 +75,7 @@ typedef enum {
     MSAO_ERR_INVALID_ARG = 1,   /* bad pointer, size, enum value, parameter or output set */
     MSAO_ERR_ALIGNMENT = 2,     /* data, row pitch or output not aligned as required */
     MSAO_ERR_WORKSPACE = 3,     /* workspace missing, not 256-byte aligned or too small */
-    MSAO_ERR_UNSUPPORTED = 4,   /* valid request this build does not handle */
+    MSAO_ERR_UNSUPPORTED = 4,   /* valid request outside what the library handles (sizes, pitches) */
     MSAO_ERR_HIP = 5            /* a HIP runtime call or a kernel launch failed */
 } msao_status;
 
