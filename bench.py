@@ -458,6 +458,22 @@ def main():
     ms_step, wall = timed(plans, args.steps, n_str)
     # the same steps one after another on one stream: per-batch latency
     ms_step_serial, _ = timed(plans, args.steps, 1)
+    # the same one-stream steps with each replica's plan replayed from a HIP graph
+    graphs = []
+    for _, plan in plans:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            plan(torch.cuda.current_stream())
+        graphs.append(g)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(main)
+    for i in range(args.steps):
+        graphs[i % n_rep].replay()
+    e1.record(main)
+    torch.cuda.synchronize()
+    ms_step_graph = e0.elapsed_time(e1) / args.steps
+    del graphs
 
     # per-kernel durations: HIP events recorded by the library around each launch,
     # on the stream the kernel is launched on (one stream, so kernels do not overlap)
@@ -510,6 +526,7 @@ def main():
             "compaction": compact, "batches_in_flight": n_str,
         },
         "ms_per_step_one_stream": ms_step_serial,
+        "ms_per_step_one_stream_graph": ms_step_graph,
         "hbm_gbps_step": b_step / (ms_step * 1e-3) / 1e9,
         "hbm_frac_step": b_step / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS,
         "algorithmic_bytes": {"score": b_score, "select": b_select, "gather_write": b_compact},
