@@ -212,9 +212,10 @@ msao_status msao_select_tokens(msao_ctx* ctx, const msao_segment* segs, int n, i
 /* Packed copy of each segment's kept rows: row j of segment s (j <
  * kept_count[s]) is row kept_idx[off_s + j] of its data, written bitwise at
  * out + out_byte_off[s] + j*hidden*element_size. out_byte_off is host [n],
- * 16-byte aligned; each segment needs room for min(N, k) rows where k is its
- * fixed keep count, or N rows if its keep ratio is negative; out_bytes bounds
- * every write. */
+ * 16-byte aligned; each segment needs room for its kept rows under either
+ * selection scope, max(ceil(kappa N), T ceil(kappa P)) for a fixed keep ratio
+ * (the room msao_compact_layout gives), or N rows if its keep ratio is
+ * negative; out_bytes bounds every write. */
 msao_status msao_compact(msao_ctx* ctx, const msao_segment* segs, int n,
                          const int32_t* kept_idx, const int32_t* kept_count,
                          void* out, const int64_t* out_byte_off, int64_t out_bytes,

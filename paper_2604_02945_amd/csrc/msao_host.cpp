@@ -189,7 +189,7 @@ size_t workspace_bytes_for(int n, int R, int64_t ntok)
 void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* p,
                 const float* alpha, const int64_t* out_off, Plan& pl, bool fuse_copy = false,
                 const msao_spatial_head* heads = nullptr, bool learned = false, int mlp_hidden = 0,
-                const msao_simhash* hashes = nullptr)
+                const msao_simhash* hashes = nullptr, bool cap_any_scope = false)
 {
     const bool per_frame = (p->flags & MSAO_FLAG_SELECT_PER_FRAME) != 0;
     pl.sel_unit.clear();
@@ -247,6 +247,10 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
             pl.max_n = std::max(pl.max_n, (int)N);
         }
         d.cap = d.k < 0 ? (int32_t)N : d.k;
+        // a compaction that does not know the selection's scope (msao_compact)
+        // takes room for either: T ceil(kappa P) may exceed ceil(kappa N)
+        if (cap_any_scope && d.k >= 0 && s.n_frames >= 2)
+            d.cap = std::max<int32_t>(d.cap, s.n_frames * (int32_t)keep_count(s.keep_ratio, s.tokens_per_frame));
         if (hashes) {
             // SimHash blocks of kHashBlockTokens tokens (segments without a hash get zeros)
             d.hi_begin = (int32_t)pl.hi_seg.size();
@@ -866,7 +870,7 @@ msao_status msao_compact(msao_ctx* ctx, const msao_segment* segs, int n, const i
     msao_params p = msao_default_params();
     MSAO_TRY(validate_impl(segs, n, R, &p, &ctx->err));
     Plan pl;
-    build_plan(ctx, segs, n, R, &p, nullptr, out_byte_off, pl);
+    build_plan(ctx, segs, n, R, &p, nullptr, out_byte_off, pl, false, nullptr, false, 0, nullptr, true);
     MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
     if (pl.ntok > 0 && (!kept_idx || !kept_count))
         return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "kept_idx and kept_count are required");

@@ -91,3 +91,24 @@ def test_plan_per_frame(dev):
         assert np.array_equal(host(got["kept_count"]), ref["k"])
         assert np.array_equal(host(got["kept_idx"]), ref["kept_idx"])
     plan.close()
+
+
+def test_select_then_compact_per_frame(dev):
+    # the standalone compaction does not know the scope: 32 x ceil(0.3 * 256)
+    # = 2,464 kept rows per clip exceed ceil(0.3 * 8192) = 2,458, and all of
+    # them must be copied
+    w = make_workload(3, n_requests=2)
+    p = per_frame(w.params)
+    ref = oracle.run(w.segments, 2, p)
+    assert np.all(ref["k"] == 2464)
+    dsegs = to_device(w.segments, dev)
+    z = torch.from_numpy(ref["z"].astype(np.int32)).to(dev)
+    d = torch.from_numpy(ref["d"].astype(np.int32)).to(dev)
+    out = msao.Outputs(dsegs, 2, compact=True)
+    msao.msao_select_tokens(dsegs, 2, z, d, None, p, outputs=out)
+    msao.msao_compact(dsegs, out)
+    torch.cuda.synchronize()
+    got = out.results(2, len(dsegs))
+    assert np.array_equal(host(got["kept_count"]), ref["k"])
+    from test_gpu_parity import compare_compaction
+    compare_compaction(dsegs, w.segments, out, oracle.compact_rows(w.segments, ref["k"], ref["kept_idx"]), ref["k"])
