@@ -1,0 +1,55 @@
+"""Seeded random segment tables through msao_run against the oracle: mixed
+modalities, fp32 and bf16, ragged widths (multiples of 8 channels up to
+1288), one to nine frames per clip, ragged frame sizes, fixed, zero, full and
+MAS-guided keep ratios, padded row strides, several segments per request and
+modality, and the literal and per-frame flags. Same bar as the parity tests
+(run_and_compare): integers, kept indices and compacted rows bit-exact."""
+import numpy as np
+import pytest
+import torch
+
+from test_gpu_parity import log, run_and_compare
+from workloads import AUDIO, IMAGE, TEXT, VIDEO, Segment, default_params, f32_to_bf16_bits
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda", 0)
+
+
+def random_table(seed):
+    rng = np.random.default_rng(1000 + seed)
+    R = int(rng.integers(1, 4))
+    segs = []
+    for _ in range(int(rng.integers(1, 7))):
+        m = int(rng.choice([TEXT, IMAGE, VIDEO, AUDIO]))
+        dtype = "bf16" if rng.random() < 0.6 else "f32"
+        C = int(rng.integers(1, 162)) * 8
+        T = int(rng.integers(1, 10)) if m == VIDEO else 1
+        P = int(rng.integers(0, 300 if T > 1 else 900))
+        keep = float(rng.choice([0.0, 1.0, -1.0, 0.13, 0.37, 0.5, 0.81]))
+        kind = rng.integers(3)
+        x = rng.standard_normal((T * P, C)).astype(np.float32)
+        if kind == 1:
+            x = np.maximum(x, 0) * np.where(rng.random((T * P, 1)) < 0.4, 0.05, 1.0).astype(np.float32)
+        elif kind == 2 and T > 1 and P > 0:
+            for t in range(1, T):   # slowly drifting frames
+                x[t * P:(t + 1) * P] = x[(t - 1) * P:t * P] + 0.02 * rng.standard_normal((P, C)).astype(np.float32)
+        data = x if dtype == "f32" else f32_to_bf16_bits(x)
+        segs.append(Segment(int(rng.integers(R)), m, T, P, C, dtype, keep, data))
+    p = default_params()
+    p["flags"] = int(rng.integers(4))            # literal and/or per-frame
+    pad = int(rng.choice([0, 0, 8, 24]))
+    return segs, R, p, pad
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_table(seed, dev):
+    segs, R, p, pad = random_table(seed)
+    log(f"[random] seed {seed}: {len(segs)} segments, R {R}, flags {p['flags']}, pad {pad}, "
+        f"tokens {sum(s.n_tokens for s in segs)}")
+    run_and_compare(segs, R, p, dev, pad=pad)
