@@ -53,3 +53,39 @@ def test_random_table(seed, dev):
     log(f"[random] seed {seed}: {len(segs)} segments, R {R}, flags {p['flags']}, pad {pad}, "
         f"tokens {sum(s.n_tokens for s in segs)}")
     run_and_compare(segs, R, p, dev, pad=pad)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_table_simhash(seed, dev):
+    from test_gpu_simhash import compare as compare_sh, run_case as run_sh
+    from workloads import simhash_planes
+    segs, R, p, pad = random_table(100 + seed)
+    rng = np.random.default_rng(seed)
+    hashes = [dict(planes=simhash_planes(int(rng.choice([16, 32, 48, 64])), s.hidden, seed=seed, dtype=s.dtype),
+                   bits=0) for s in segs]
+    for h in hashes:
+        h["bits"] = h["planes"].shape[0]
+    log(f"[random] simhash seed {seed}: {len(segs)} segments, R {R}, pad {pad}")
+    g, ref = run_sh(segs, R, hashes, dev, params=p, pad=pad)
+    compare_sh(segs, hashes, g, ref)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_table_learned(seed, dev):
+    from test_gpu_learned import compare as compare_l, make_head, mlp_for, run_case as run_l
+    segs, R, p, _ = random_table(200 + seed)
+    rng = np.random.default_rng(50 + seed)
+    heads = []
+    for s in segs:
+        P = s.tokens_per_frame
+        if s.n_tokens == 0 or rng.random() < 0.3:
+            heads.append(None)
+            continue
+        divs = [w for w in range(1, P + 1) if P % w == 0]
+        grid_w = int(rng.choice(divs)) if rng.random() < 0.7 else 0
+        heads.append(make_head(s, rng, grid_w, int(rng.choice([1, 3, 5, 7])), float(rng.uniform(-1, 1)))[1])
+    mlp = mlp_for(R, int(rng.choice([0, 16, 100])), int(rng.choice([8, 64])), rng) if rng.random() < 0.7 else None
+    log(f"[random] learned seed {seed}: {len(segs)} segments, R {R}, heads {sum(h is not None for h in heads)}, "
+        f"mlp {mlp is not None}")
+    g, ref = run_l(segs, R, heads, mlp, dev, params=p)
+    compare_l(segs, R, heads, g, ref, mlp)
