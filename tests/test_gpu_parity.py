@@ -350,11 +350,11 @@ def test_repeat_runs_bitwise_identical(dev):
     segs = [Segment(min(s.request, 3), s.modality, s.n_frames, s.tokens_per_frame, s.hidden, s.dtype,
                     s.keep_ratio, s.data) for s in segs]
     dsegs = to_device(segs, dev)
-    log("[parity] 20 repeated runs")
+    log("[parity] 50 repeated runs")
     first = None
     out = msao.Outputs(dsegs, R)
     call = msao.prepare("msao_run", dsegs, R, out, w.params)
-    for i in range(20):
+    for i in range(50):
         call()
         torch.cuda.synchronize()
         snap = {k: host(v).copy() for k, v in out.results(R, len(segs)).items()}
