@@ -94,6 +94,9 @@ def lib():
         L.orc_temporal_simhash.argtypes = [ctypes.POINTER(_Segment), ctypes.c_int, ctypes.c_int,
                                            ctypes.POINTER(_Params), _P, _P, _P, _P, _P, _P, _P, _P]
         L.orc_temporal_simhash.restype = ctypes.c_int
+        L.orc_run_simhash.argtypes = [ctypes.POINTER(_Segment), ctypes.c_int, ctypes.c_int,
+                                      ctypes.POINTER(_Params), _P, _P, _P, ctypes.POINTER(_Outputs)]
+        L.orc_run_simhash.restype = ctypes.c_int
         L.orc_q24.argtypes = [ctypes.c_float]
         L.orc_q24.restype = ctypes.c_uint64
         D, I64, I = ctypes.c_double, ctypes.c_int64, ctypes.c_int
@@ -165,12 +168,13 @@ def _is_temporal(s) -> bool:
 
 
 def run(segments: Sequence, n_requests: int, params: dict, alpha: Optional[np.ndarray] = None,
-        compact: bool = True) -> dict:
+        compact: bool = True, hashes: Optional[Sequence] = None) -> dict:
     """Run every step of the analysis on the CPU; returns numpy arrays.
 
     `segments` carry request, modality, n_frames, tokens_per_frame, hidden,
     dtype ("f32"/"bf16"), keep_ratio and data ([tokens, row_stride], float32
-    or uint16 bf16 bits).
+    or uint16 bf16 bits). With `hashes` (as for temporal_simhash), Eq. 5 uses
+    SimHash and every later step its d; the signatures come back as "sig".
     """
     L = lib()
     n = len(segments)
@@ -195,7 +199,14 @@ def run(segments: Sequence, n_requests: int, params: dict, alpha: Optional[np.nd
     al = None if alpha is None else np.ascontiguousarray(alpha, dtype=np.float32).reshape(-1)
     if al is not None and al.size != R * NMOD:
         raise ValueError("alpha must hold n_requests * 4 logits")
-    rc = L.orc_run(segt, n, R, ctypes.byref(prm), _ptr(al), ctypes.byref(outs))
+    if hashes is None:
+        rc = L.orc_run(segt, n, R, ctypes.byref(prm), _ptr(al), ctypes.byref(outs))
+    else:
+        harr, keep = _hash_table(hashes, n)
+        sig = np.zeros(max(ntok, 1), np.uint64)
+        rc = L.orc_run_simhash(segt, n, R, ctypes.byref(prm), ctypes.cast(harr, _P), _ptr(al), _ptr(sig),
+                               ctypes.byref(outs))
+        o["sig"] = sig[:ntok]
     if rc != 0:
         raise RuntimeError(f"orc_run failed ({rc})")
     o["k"] = o["k"][:n]
@@ -278,6 +289,19 @@ class _SimHash(ctypes.Structure):
     _fields_ = [("planes", _P), ("bits", ctypes.c_int32)]
 
 
+def _hash_table(hashes: Sequence, n: int):
+    """orc_simhash[n] from dicts (planes, bits) or None; also the arrays to keep alive."""
+    harr = (_SimHash * max(1, n))()
+    keep = []
+    for i, h in enumerate(hashes):
+        if h is None:
+            continue
+        a = np.ascontiguousarray(h["planes"])
+        keep.append(a)
+        harr[i] = _SimHash(a.ctypes.data, int(h["bits"]))
+    return harr, keep
+
+
 def temporal_simhash(segments: Sequence, n_requests: int, params: dict, hashes: Sequence) -> dict:
     """The SimHash variant of Eq. 5: hashes[s] = dict(planes=[bits, hidden]
     array in the segment's encoding, bits=K) for every temporal segment (None
@@ -292,14 +316,7 @@ def temporal_simhash(segments: Sequence, n_requests: int, params: dict, hashes: 
          "dframe": np.zeros(max(nframe, 1), np.uint64), "sim": np.zeros(max(nframe, 1), np.float32),
          "gamma": np.zeros(max(nframe, 1), np.float32), "dq": np.zeros(max(R * NMOD * 2, 1), np.uint64),
          "temporal": np.zeros(max(R * NMOD, 1), np.float32)}
-    harr = (_SimHash * max(1, n))()
-    keep = []
-    for i, h in enumerate(hashes):
-        if h is None:
-            continue
-        a = np.ascontiguousarray(h["planes"])
-        keep.append(a)
-        harr[i] = _SimHash(a.ctypes.data, int(h["bits"]))
+    harr, keep = _hash_table(hashes, n)
     rc = L.orc_temporal_simhash(_segment_table(segments), n, R, ctypes.byref(_params(params)),
                                 ctypes.cast(harr, _P), *[_ptr(o[k]) for k in ("sig", "d", "dframe", "sim", "gamma",
                                                                               "dq", "temporal")])

@@ -28,14 +28,19 @@
  *  - MAS uses the redundancy 1 - gamma_avg by default (flag LITERAL uses
  *    gamma_avg as printed); the inner bracket is clamped to [0, 1];
  *  - a token's selection key is the exact integer
- *        Ls*z + Lt*(C - d)   with Ls = rne(lambda_s * 2^24), Lt likewise,
+ *        Ls*z*E + Lt*(E - d)*C   with Ls = rne(lambda_s * 2^24), Lt likewise
+ *    and E the bits d compares per token (E = C for bit sampling), i.e.
+ *    C E (Ls z / C + Lt e / E) with e = E - d;
  *    the keep count is k = min(N, ceil(kappa * N)) and the k smallest
  *    (key, index) pairs of each segment are kept, ties by ascending index;
  *    with the per-frame scope flag each frame of P tokens is its own
  *    selection, k_f = min(P, ceil(kappa * P)) tokens per frame;
  *  - the SimHash variant of Eq. 5 hashes each token with K caller
  *    hyperplanes r_k: bit k is 1 iff r_k . f >= 0 (Charikar's hash); frame
- *    0 is compared with the all-zero frame, whose bits are all 1.
+ *    0 is compared with the all-zero frame, whose bits are all 1. Run with
+ *    SimHash (orc_run_simhash), its d (E = K bits per token) replaces bit
+ *    sampling's in every later step: D_t, sim, Qbits, the temporal term,
+ *    informativeness and the selection key.
  *
  * Parity pins for every function below live in the CPU test suite.
  */
@@ -74,7 +79,7 @@ typedef struct {
     uint32_t* z;      /* inactive channel count */
     float* l1;        /* sum |x| */
     float* l2;        /* sum x^2 */
-    float* info;      /* 1 - (lambda_s z + lambda_t e)/C */
+    float* info;      /* 1 - (lambda_s z/C + lambda_t e/E), e = E - d */
     uint32_t* d;      /* activity-bit Hamming distance to the previous frame (0 if not temporal) */
     float* res;       /* sum (x_t - x_{t-1})^2 (0 if not temporal) */
     /* per frame of temporal segments (VIDEO, T >= 2, P > 0), frames in table order */
@@ -165,10 +170,11 @@ static int is_sparse(uint32_t a, int C, float tau_s)
     return (double)a / (double)C < (double)tau_s;
 }
 
-/* Eq. 5 for one frame: sim = (1/K) sum_k [h_k equal], K = P*C. */
-static double frame_similarity(uint64_t D, int64_t P, int64_t C)
+/* Eq. 5 for one frame: sim = (1/K) sum_k [h_k equal] over its K = P*E hash
+ * functions (E per token: C activity bits, or K SimHash bits). */
+static double frame_similarity(uint64_t D, int64_t P, int64_t E)
 {
-    return 1.0 - (double)D / (double)(P * C);
+    return 1.0 - (double)D / (double)(P * E);
 }
 
 /* Sec. 4.1.3: softmax of the relevance logits over the modalities present in
@@ -229,9 +235,13 @@ static int pair_cmp(const void* a, const void* b)
 }
 
 /* Selection among tokens [i0, i0 + n) of a segment: sort (key, index)
- * ascending, keep the first k (keep flags set for the range only). */
+ * ascending, keep the first k (keep flags set for the range only). E is the
+ * number of bits d compares per token (C for bit sampling, K for SimHash);
+ * the key is C E 2^24 (lambda_s z / C + lambda_t (E - d) / E) with the
+ * weights in Q24, an exact integer (the temporal term only for temporal
+ * segments). */
 static int select_range(const orc_segment* s, const orc_params* p, const uint32_t* z,
-                        const uint32_t* d, int64_t i0, int64_t n, int64_t k, uint8_t* keep)
+                        const uint32_t* d, int64_t E, int64_t i0, int64_t n, int64_t k, uint8_t* keep)
 {
     int64_t C = s->hidden;
     uint64_t Ls = q24(p->lambda_s[s->modality]);
@@ -241,8 +251,8 @@ static int select_range(const orc_segment* s, const orc_params* p, const uint32_
     if (!pairs) return -1;
     for (int64_t j = 0; j < n; ++j) {
         int64_t i = i0 + j;
-        uint64_t key = Ls * (uint64_t)z[i];
-        if (temporal) key += Lt * (uint64_t)(C - (int64_t)d[i]);
+        uint64_t key = Ls * (uint64_t)z[i] * (uint64_t)E;
+        if (temporal) key += Lt * (uint64_t)(E - (int64_t)d[i]) * (uint64_t)C;
         pairs[j].key = key;
         pairs[j].idx = i;
     }
@@ -257,17 +267,17 @@ static int select_range(const orc_segment* s, const orc_params* p, const uint32_
  * (per-frame scope) each of its T frames of P tokens on its own. Kept
  * indices ascending, then -1. Returns the keep count. */
 static int64_t select_segment(const orc_segment* s, const orc_params* p, const uint32_t* z,
-                              const uint32_t* d, double kappa, uint8_t* keep, int32_t* kept_idx)
+                              const uint32_t* d, int64_t E, double kappa, uint8_t* keep, int32_t* kept_idx)
 {
     int64_t T = s->n_frames, P = s->tokens_per_frame, N = T * P, k = 0;
     if (p->flags & ORC_FLAG_SELECT_PER_FRAME) {
         int64_t kf = keep_count(kappa, P);
         for (int64_t t = 0; t < T; ++t)
-            if (select_range(s, p, z, d, t * P, P, kf, keep)) return -1;
+            if (select_range(s, p, z, d, E, t * P, P, kf, keep)) return -1;
         k = kf * T;
     } else {
         k = keep_count(kappa, N);
-        if (select_range(s, p, z, d, 0, N, k, keep)) return -1;
+        if (select_range(s, p, z, d, E, 0, N, k, keep)) return -1;
     }
     int64_t w = 0;
     for (int64_t i = 0; i < N; ++i)
@@ -276,11 +286,12 @@ static int64_t select_segment(const orc_segment* s, const orc_params* p, const u
     return k;
 }
 
-/* Selection over all segments from given per-token z, d and per-(request,
- * modality) MAS (used only by segments with a negative keep ratio). */
-int orc_select(const orc_segment* segs, int n, int R, const orc_params* p,
-               const uint32_t* z, const uint32_t* d, const float* mas,
-               int32_t* k_out, uint8_t* keep, int32_t* kept_idx)
+/* Selection over all segments from per-token z, d (E[s]: bits compared per
+ * token of segment s) and per-(request, modality) MAS (used only by segments
+ * with a negative keep ratio). */
+static int select_all(const orc_segment* segs, int n, int R, const orc_params* p,
+                      const uint32_t* z, const uint32_t* d, const int64_t* E, const float* mas,
+                      int32_t* k_out, uint8_t* keep, int32_t* kept_idx)
 {
     int64_t off = 0;
     for (int s = 0; s < n; ++s) {
@@ -293,7 +304,7 @@ int orc_select(const orc_segment* segs, int n, int R, const orc_params* p,
         } else {
             kappa = (double)sg->keep_ratio;
         }
-        int64_t k = select_segment(sg, p, z + off, d ? d + off : NULL, kappa, keep + off, kept_idx + off);
+        int64_t k = select_segment(sg, p, z + off, d ? d + off : NULL, E[s], kappa, keep + off, kept_idx + off);
         if (k < 0) return -1;
         k_out[s] = (int32_t)k;
         off += N;
@@ -301,16 +312,61 @@ int orc_select(const orc_segment* segs, int n, int R, const orc_params* p,
     return 0;
 }
 
-/* The whole analysis, step by step. Returns 0 on success. */
-int orc_run(const orc_segment* segs, int n, int R, const orc_params* p,
-            const float* alpha, orc_outputs* o)
+/* Selection over all segments from given per-token z, d (activity-bit
+ * distances, E = C) and per-(request, modality) MAS. */
+int orc_select(const orc_segment* segs, int n, int R, const orc_params* p,
+               const uint32_t* z, const uint32_t* d, const float* mas,
+               int32_t* k_out, uint8_t* keep, int32_t* kept_idx)
 {
+    int64_t* E = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    if (!E) return -1;
+    for (int s = 0; s < n; ++s) E[s] = segs[s].hidden;
+    int rc = select_all(segs, n, R, p, z, d, E, mas, k_out, keep, kept_idx);
+    free(E);
+    return rc;
+}
+
+/* SimHash hyperplanes of one segment (the SimHash variant of Eq. 5, below). */
+typedef struct {
+    const void* planes; /* [bits][hidden] in the segment's dtype: hyperplane r_k is row k */
+    int32_t bits;       /* K hash functions per token, 1..64 */
+} orc_simhash;
+
+static uint64_t simhash_token(const void* row, const void* planes, int dtype, int C, int K);
+static uint32_t popcount64(uint64_t v);
+
+/* The whole analysis, step by step. h == NULL: Eq. 5 by bit sampling over
+ * the activity bits (E = C bits compared per token). Otherwise the temporal
+ * segments hash with SimHash (h[s], E = K): their signatures go to sig, and
+ * d is the number of signature bits that differ from the same patch in the
+ * previous frame (frame 0: from the all-zero frame, all bits 1); every step
+ * after Eq. 5 then uses that d and E. Returns 0 on success. */
+static int run_impl(const orc_segment* segs, int n, int R, const orc_params* p,
+                    const float* alpha, const orc_simhash* h, uint64_t* sig, orc_outputs* o)
+{
+    int64_t* E = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    if (!E) return -1;
     /* O3/O4: per-token statistics and per-frame similarity */
     int64_t tok = 0, frame = 0;
     for (int s = 0; s < n; ++s) {
         const orc_segment* sg = &segs[s];
         int64_t T = sg->n_frames, P = sg->tokens_per_frame, C = sg->hidden;
         int temporal = is_temporal(sg);
+        int hashed = temporal && h != NULL;
+        E[s] = C;
+        uint64_t all = 0;
+        if (hashed) {
+            if (!h[s].planes || h[s].bits < 1 || h[s].bits > 64) {
+                free(E);
+                return -1;
+            }
+            E[s] = h[s].bits;
+            all = h[s].bits == 64 ? ~(uint64_t)0 : (((uint64_t)1 << h[s].bits) - 1);
+            for (int64_t i = 0; i < T * P; ++i)
+                sig[tok + i] = simhash_token(row_ptr(sg, i), h[s].planes, sg->dtype, (int)C, h[s].bits);
+        } else if (sig) {
+            for (int64_t i = 0; i < T * P; ++i) sig[tok + i] = 0;
+        }
         for (int64_t t = 0; t < T; ++t) {
             uint64_t D = 0;
             for (int64_t q = 0; q < P; ++q) {
@@ -325,21 +381,22 @@ int orc_run(const orc_segment* segs, int n, int R, const orc_params* p,
                 if (temporal) {
                     const void* prev = t > 0 ? row_ptr(sg, i - P) : NULL;
                     temporal_pair(row, prev, sg->dtype, (int)C, p->tau, &dd, &res);
+                    if (hashed) dd = popcount64(sig[g] ^ (t > 0 ? sig[g - P] : all));
                     D += dd;
                 }
                 double lam_s = (double)p->lambda_s[sg->modality];
                 double lam_t = (double)p->lambda_t[sg->modality];
-                double redundant = lam_s * (double)z;
-                if (temporal) redundant += lam_t * (double)((uint32_t)C - dd);
+                double redundant = lam_s * (double)z / (double)C;
+                if (temporal) redundant += lam_t * (double)((uint32_t)E[s] - dd) / (double)E[s];
                 o->z[g] = z;
                 o->l1[g] = (float)l1;
                 o->l2[g] = (float)l2;
-                o->info[g] = (float)(1.0 - redundant / (double)C);
+                o->info[g] = (float)(1.0 - redundant);
                 o->d[g] = dd;
                 o->res[g] = (float)res;
             }
             if (temporal) {
-                double sim = frame_similarity(D, P, C);
+                double sim = frame_similarity(D, P, E[s]);
                 o->dframe[frame + t] = D;
                 o->sim[frame + t] = (float)sim;
                 o->gamma[frame + t] = (float)(1.0 - sim);
@@ -364,7 +421,7 @@ int orc_run(const orc_segment* segs, int n, int R, const orc_params* p,
         }
         if (is_temporal(sg)) {
             for (int64_t t = 1; t < T; ++t) ag[2] += o->dframe[frame + t];
-            ag[3] += (uint64_t)((T - 1) * P * C);
+            ag[3] += (uint64_t)((T - 1) * P * E[s]);
             frame += T;
         }
         tok += N;
@@ -405,7 +462,26 @@ int orc_run(const orc_segment* segs, int n, int R, const orc_params* p,
     }
 
     /* O8-O10: keys, keep counts, selection */
-    return orc_select(segs, n, R, p, o->z, o->d, o->mas, o->k, o->keep, o->kept_idx);
+    int rc = select_all(segs, n, R, p, o->z, o->d, E, o->mas, o->k, o->keep, o->kept_idx);
+    free(E);
+    return rc;
+}
+
+/* The whole analysis with bit sampling in Eq. 5. Returns 0 on success. */
+int orc_run(const orc_segment* segs, int n, int R, const orc_params* p,
+            const float* alpha, orc_outputs* o)
+{
+    return run_impl(segs, n, R, p, alpha, NULL, NULL, o);
+}
+
+/* The whole analysis with SimHash in Eq. 5 (h[s] for every temporal
+ * segment; sig [Ntot] receives the signatures, 0 outside temporal segments).
+ * Returns 0 on success, -1 for a missing or invalid hash. */
+int orc_run_simhash(const orc_segment* segs, int n, int R, const orc_params* p, const orc_simhash* h,
+                    const float* alpha, uint64_t* sig, orc_outputs* o)
+{
+    if (!h || !sig) return -1;
+    return run_impl(segs, n, R, p, alpha, h, sig, o);
 }
 
 /* O11: compaction, a byte copy of each kept row into packed per-segment
@@ -632,11 +708,6 @@ int orc_run_learned(const orc_segment* segs, int n, int R, const orc_params* p, 
  * SimHash variant of Eq. 5 (Sec. 4.1.2): Charikar's random-hyperplane
  * hash in place of bit sampling over the activity bits.
  * ================================================================ */
-
-typedef struct {
-    const void* planes; /* [bits][hidden] in the segment's dtype: hyperplane r_k is row k */
-    int32_t bits;       /* K hash functions per token, 1..64 */
-} orc_simhash;
 
 /* Signature of one token: bit k is 1 iff r_k . f >= 0, the dot product
  * summed in double over the channels in order (NaN compares false: 0). */
