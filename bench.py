@@ -316,6 +316,11 @@ def simhash_bench(args, dev, ctx):
     ms_sh, k_sh = kernels(lambda i: msao.msao_temporal_simhash(reps[i], R, hashes, w.params, ctx=ctx, outputs=outs[i],
                                                                sig=sigs[i]))
     ms_bs, k_bs = kernels(lambda i: msao.msao_temporal_redundancy(reps[i], R, w.params, ctx=ctx, outputs=outs[i]))
+    # the whole analysis with SimHash in Eq. 5 (score, hash, MAS, selection, compaction) beside msao_run
+    routs = [msao.Outputs(segs, R, compact=True) for segs in reps]
+    ms_rs, k_rs = kernels(lambda i: msao.msao_run_simhash(reps[i], R, hashes, w.params, ctx=ctx, outputs=routs[i],
+                                                          sig=sigs[i]))
+    ms_rb, k_rb = kernels(lambda i: msao.msao_run(reps[i], R, w.params, ctx=ctx, outputs=routs[i]))
     ntok = w.n_tokens
     b = w.input_bytes + 8 * ntok               # rows read once, signatures written
     km = k_sh[msao.binding.KERNEL_SIMHASH]
@@ -324,10 +329,15 @@ def simhash_bench(args, dev, ctx):
     res = {
         "workload": f"{w.name}: 8 clips x 32 frames x 256 tokens x 1024 bf16, K = {K} hyperplanes",
         "ms_per_call": ms_sh, "tokens_per_s": ntok / (ms_sh * 1e-3),
-        "kernel_ms": {"simhash": km, "hash_post": k_sh[msao.binding.KERNEL_POST],
+        "kernel_ms": {"simhash": km, "hash_post": k_sh[msao.binding.KERNEL_HASH_POST],
                       "bit_sampling_score": k_bs[msao.binding.KERNEL_SCORE],
                       "bit_sampling_post": k_bs[msao.binding.KERNEL_POST]},
         "ms_per_call_bit_sampling": ms_bs,
+        "run": {"ms_per_call": ms_rs, "tokens_per_s": ntok / (ms_rs * 1e-3), "ms_per_call_msao_run": ms_rb,
+                "kernel_ms": {k: k_rs[getattr(msao.binding, "KERNEL_" + k.upper())]
+                              for k in ("score", "simhash", "hash_post", "post", "gather")},
+                "kernel_ms_msao_run": {k: k_rb[getattr(msao.binding, "KERNEL_" + k.upper())]
+                                       for k in ("score", "post", "gather")}},
         "algorithmic_bytes": b,
         "mfma_tflops": flops / (km * 1e-3) / 1e12,
         "roofline": {"bound": "hbm", "kernel": "k_simhash", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",

@@ -344,6 +344,33 @@ msao_status msao_temporal_simhash(msao_ctx* ctx, const msao_segment* segs, int n
                                   uint32_t* d, const msao_frame_out* frm, float* temporal, void* ws,
                                   size_t ws_bytes, void* stream);
 
+/* Sec. 4.1 with SimHash as Eq. 5's hash throughout: msao_run's outputs,
+ * where the d of every temporal segment is SimHash's (the bits of its K-bit
+ * signature that differ from the same patch in the previous frame, as in
+ * msao_temporal_simhash) and every later step counts it in K bits per token
+ * instead of C activity bits:
+ *   frm: sim = 1 - D_t / (P K), gamma = 1 - sim;
+ *   req: agg's Dsum is SimHash's, Qbits = sum over the clips of (T-1) P K,
+ *     and the temporal term and MAS follow;
+ *   tok->info of a clip's tokens: 1 - (lambda_s z / C + lambda_t (K - d) / K);
+ *   selection: the key orders a clip's tokens by lambda_s z / C + lambda_t
+ *     (K - d) / K with the Q24 weights, as an exact integer; ties by index.
+ * z, l1, l2 and res (the squared difference of the rows) are as in msao_run.
+ * hashes (host, [n]) as for msao_temporal_simhash. sig (device [total
+ * tokens] u64, 8-byte aligned) receives the signatures (0 outside temporal
+ * segments) and is required when a segment is temporal. Every other argument,
+ * the workspace size and the errors are those of msao_run, plus the hash
+ * errors of msao_temporal_simhash. Precision: the projections are fp32 sums
+ * on the matrix cores, so a signature bit whose projection is within
+ * rounding of 0 may differ from an exact evaluation, and with it d, the
+ * terms above and the choice among nearly tied tokens. */
+msao_status msao_run_simhash(msao_ctx* ctx, const msao_segment* segs, int n, int n_requests,
+                             const msao_params* params, const msao_simhash* hashes, const float* alpha,
+                             const msao_token_out* tok, uint64_t* sig, const msao_frame_out* frm,
+                             const msao_req_out* req, const msao_select_out* sel, void* out,
+                             const int64_t* out_byte_off, int64_t out_bytes, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
 /* ---- Sec. 4.2: the draft model's confidence ------------------------------- */
 
 /* Outputs of msao_draft_entropy, each [rows] device memory or NULL (not
@@ -452,8 +479,9 @@ double msao_expected_e2e_latency(const msao_latency_model* m);
 #define MSAO_KERNEL_GATHER 2  /* compaction */
 #define MSAO_KERNEL_ENTROPY 3 /* draft confidence */
 #define MSAO_KERNEL_HEAD 4    /* learned spatial head: pooling, sigmoid, Eq. 4 counts */
-#define MSAO_KERNEL_SIMHASH 5 /* SimHash signatures (the k_hash_post launch counts as POST) */
-#define MSAO_NUM_KERNELS 6
+#define MSAO_KERNEL_SIMHASH 5 /* SimHash signatures */
+#define MSAO_KERNEL_HASH_POST 6 /* SimHash d, per-frame terms, temporal term */
+#define MSAO_NUM_KERNELS 7
 
 /* When enabled, every launch is bracketed by a pair of HIP events recorded on
  * the caller's stream. */

@@ -22,7 +22,8 @@ TEXT, IMAGE, VIDEO, AUDIO = 0, 1, 2, 3
 F32, BF16 = 0, 1
 FLAG_TEMPORAL_LITERAL = 1
 FLAG_SELECT_PER_FRAME = 2
-KERNEL_SCORE, KERNEL_POST, KERNEL_GATHER, KERNEL_ENTROPY, KERNEL_HEAD, KERNEL_SIMHASH, NUM_KERNELS = 0, 1, 2, 3, 4, 5, 6
+(KERNEL_SCORE, KERNEL_POST, KERNEL_GATHER, KERNEL_ENTROPY, KERNEL_HEAD, KERNEL_SIMHASH, KERNEL_HASH_POST,
+ NUM_KERNELS) = 0, 1, 2, 3, 4, 5, 6, 7
 MODAL_DESC = 8
 DECIDE_HOLD, DECIDE_SEND, DECIDE_OFFLOAD = 0, 1, 2
 
@@ -136,6 +137,8 @@ SIGNATURES = [
                                               _P, _P, _P, ctypes.c_size_t, _P]),
     ("msao_temporal_simhash", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P,
                                              ctypes.c_size_t, _P]),
+    ("msao_run_simhash", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                        ctypes.c_int64, _P, ctypes.c_size_t, _P]),
     ("msao_draft_entropy", ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
                                           ctypes.c_float, _P, _P]),
     ("msao_sched_default_params", MsaoSchedParams, []),
@@ -497,13 +500,7 @@ def msao_temporal_simhash(segments, n_requests, hashes, params=None, ctx=None, o
     segt = segment_table(segments)
     prm = params_struct(params)
     n = len(segments)
-    harr = (MsaoSimHash * max(1, n))()
-    keep = [segt, prm, harr]
-    for i, h in enumerate(hashes):
-        if h is None:
-            continue
-        keep.append(h["planes"])
-        harr[i] = MsaoSimHash(h["planes"].data_ptr(), int(h["bits"]))
+    harr, keep = _hash_array(hashes, n)
     if sig is None:
         sig = torch.empty(max(o.ntok, 1), dtype=torch.int64, device=device)[:o.ntok]
     st = stream if stream is not None else torch.cuda.current_stream(device)
@@ -511,6 +508,47 @@ def msao_temporal_simhash(segments, n_requests, hashes, params=None, ctx=None, o
                                        _ptr(sig) if o.ntok else None, _ptr(o.tok["d"]) if o.ntok else None,
                                        _addr(o.c_frm), _ptr(o.req["temporal"]), _ptr(o.workspace),
                                        ctypes.c_size_t(o.ws_bytes), ctypes.c_void_p(st.cuda_stream)), ctx)
+    return o, sig
+
+
+def _hash_array(hashes, n):
+    harr = (MsaoSimHash * max(1, n))()
+    keep = [harr]
+    for i, h in enumerate(hashes):
+        if h is None:
+            continue
+        keep.append(h["planes"])
+        harr[i] = MsaoSimHash(h["planes"].data_ptr(), int(h["bits"]))
+    return harr, keep
+
+
+def msao_run_simhash(segments, n_requests, hashes, params=None, alpha=None, ctx=None, outputs=None, stream=None,
+                     compact=True, sig=None):
+    """msao_run with SimHash as Eq. 5's hash (hashes as for
+    msao_temporal_simhash): returns (outputs, sig)."""
+    device = _device_of(segments)
+    ctx = ctx or default_context(device.index if device.index is not None else torch.cuda.current_device())
+    o = outputs or Outputs(segments, n_requests, compact=compact)
+    segt = segment_table(segments)
+    prm = params_struct(params)
+    n, R = len(segments), n_requests
+    harr, keep = _hash_array(hashes, n)
+    al = None
+    if alpha is not None:
+        vals = list(alpha)
+        if len(vals) != R * NMOD:
+            raise ValueError("alpha needs n_requests * 4 logits")
+        al = (ctypes.c_float * len(vals))(*vals)
+    if sig is None:
+        sig = torch.empty(max(o.ntok, 1), dtype=torch.int64, device=device)[:o.ntok]
+    use_out = compact and o.out is not None
+    st = stream if stream is not None else torch.cuda.current_stream(device)
+    _check(lib().msao_run_simhash(ctx.handle, segt, n, R, _addr(prm), ctypes.cast(harr, _P), al, _addr(o.c_tok),
+                                  _ptr(sig) if o.ntok else None, _addr(o.c_frm), _addr(o.c_req), _addr(o.c_sel),
+                                  _ptr(o.out) if use_out else None, o.out_off if use_out else None,
+                                  ctypes.c_int64(o.out_bytes if use_out else 0), _ptr(o.workspace),
+                                  ctypes.c_size_t(o.ws_bytes), ctypes.c_void_p(st.cuda_stream)), ctx)
+    del keep
     return o, sig
 
 

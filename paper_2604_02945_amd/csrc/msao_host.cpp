@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <numeric>
 #include <string>
 #include <vector>
 
@@ -142,6 +143,8 @@ struct Plan {
     size_t off_hbseg = 0, off_partial_x = 0, off_proj = 0, off_head_count = 0, off_mlp_u = 0;
     size_t off_seg = 0, off_wi = 0, off_gi = 0, off_rmoff = 0, off_rmseg = 0, off_tseg = 0, off_alpha = 0;
     size_t off_selu = 0, off_hiseg = 0;
+    bool simhash_d = false;        // a run with SimHash: d of temporal segments in K-bit units
+    size_t off_hdsum = 0;          // [R*4] SimHash Dsum (simhash_d only)
     size_t table_bytes = 0, off_partial = 0, total_bytes = 0;
 };
 
@@ -171,7 +174,8 @@ size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t
 // head blocks, selections and hash tiles never outnumber tokens plus
 // segments, so one Partial and table entries per token, plus what a learned call adds (a PartialX per work item, one
 // projection and one head count per token, kMaxMlpHidden floats of the MLP's
-// prompt product per request).
+// prompt product per request). A run with SimHash adds 4 Dsum counts per
+// request, within the room of the prompt product.
 size_t workspace_bytes_for(int n, int R, int64_t ntok)
 {
     Plan pl;
@@ -189,7 +193,7 @@ size_t workspace_bytes_for(int n, int R, int64_t ntok)
 void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* p,
                 const float* alpha, const int64_t* out_off, Plan& pl, bool fuse_copy = false,
                 const msao_spatial_head* heads = nullptr, bool learned = false, int mlp_hidden = 0,
-                const msao_simhash* hashes = nullptr, bool cap_any_scope = false)
+                const msao_simhash* hashes = nullptr, bool cap_any_scope = false, bool simhash_d = false)
 {
     const bool per_frame = (p->flags & MSAO_FLAG_SELECT_PER_FRAME) != 0;
     pl.sel_unit.clear();
@@ -233,6 +237,16 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         d.L_t = q24(p->lambda_t[s.modality]);
         d.lam_s = p->lambda_s[s.modality];
         d.lam_t = p->lambda_t[s.modality];
+        d.E = s.hidden;
+        d.key_ms = d.L_s;
+        d.key_mt = d.L_t;
+        if (simhash_d && hashes && d.temporal) {
+            // d counts K SimHash bits: keys in units of C K / g
+            const int64_t K = hashes[i].bits, g = std::gcd((int64_t)s.hidden, K);
+            d.E = (int32_t)K;
+            d.key_ms = (uint64_t)d.L_s * (uint64_t)(K / g);
+            d.key_mt = (uint64_t)d.L_t * (uint64_t)(s.hidden / g);
+        }
         // selections: the segment, or each of its frames (per-frame scope)
         const bool framed = per_frame && s.n_frames >= 2 && s.tokens_per_frame > 0;
         if (framed) {
@@ -320,7 +334,7 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         const DevSeg& d = pl.seg[(size_t)i];
         RmEntry& e = pl.rm[(size_t)(s.request * kNumMod + s.modality)];
         e.ntok += (uint64_t)d.n_tok;
-        if (d.temporal) e.qbits += (uint64_t)(d.T - 1) * (uint64_t)d.P * (uint64_t)d.C;
+        if (d.temporal) e.qbits += (uint64_t)(d.T - 1) * (uint64_t)d.P * (uint64_t)d.E;
         pl.rm_rng[(size_t)count[(size_t)(s.request * kNumMod + s.modality)]++] =
             WiRange{pl.seg_wi[(size_t)i], pl.seg_wi[(size_t)i + 1], i, 0};
     }
@@ -337,6 +351,11 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
                  (int64_t)pl.hi_seg.size());
     pl.off_partial = align_up(pl.table_bytes, kWsAlign);
     pl.total_bytes = pl.off_partial + sizeof(Partial) * (size_t)std::max(pl.n_wi, 1);
+    pl.simhash_d = simhash_d && pl.any_temporal;
+    if (pl.simhash_d) {
+        pl.off_hdsum = align_up(pl.total_bytes, kWsAlign);
+        pl.total_bytes = pl.off_hdsum + sizeof(uint64_t) * (size_t)std::max(R * kNumMod, 1);
+    }
     if (learned) {
         pl.off_partial_x = align_up(pl.total_bytes, kWsAlign);
         pl.off_proj = align_up(pl.off_partial_x + sizeof(PartialX) * (size_t)std::max(pl.n_wi, 1), kWsAlign);
@@ -412,6 +431,7 @@ Tables device_tables(const Plan& pl, void* ws, int n, int R, const msao_params* 
 {
     uint8_t* b = (uint8_t*)ws;
     Tables t;
+    std::memset(&t, 0, sizeof t);
     t.seg = (const DevSeg*)(b + pl.off_seg);
     t.wi_seg = (const int32_t*)(b + pl.off_wi);
     t.gi_seg = (const int32_t*)(b + pl.off_gi);
@@ -427,6 +447,7 @@ Tables device_tables(const Plan& pl, void* ws, int n, int R, const msao_params* 
     t.n_hb = (int32_t)pl.hb_seg.size();
     t.sel_unit = (const SelUnit*)(b + pl.off_selu);
     t.hi_seg = (const int32_t*)(b + pl.off_hiseg);
+    t.hdsum = pl.simhash_d ? (const uint64_t*)(b + pl.off_hdsum) : nullptr;
     t.n_hi = (int32_t)pl.hi_seg.size();
     t.n = n;
     t.R = R;
@@ -539,6 +560,29 @@ msao_status check_compact_out(msao_ctx* ctx, const Plan& pl, const msao_segment*
         const int64_t need = (int64_t)d.cap * segs[i].hidden * elt_size(segs[i].dtype);
         if (off[i] < 0 || off[i] % 16 != 0) return fail(&ctx->err, MSAO_ERR_ALIGNMENT, "out_byte_off entry negative or not 16-byte aligned");
         if (off[i] + need > out_bytes) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "compaction output too small for a segment's rows");
+    }
+    return MSAO_OK;
+}
+
+// The hash of every temporal segment (SimHash calls).
+msao_status check_hashes(msao_ctx* ctx, const msao_segment* segs, int n, const msao_simhash* hashes)
+{
+    if (n > 0 && !hashes) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "hashes is NULL");
+    char buf[160];
+    for (int i = 0; i < n; ++i) {
+        const msao_segment& s = segs[i];
+        if (!is_temporal(s)) continue;
+        auto bad = [&](msao_status st, const char* what) {
+            std::snprintf(buf, sizeof buf, "hash of segment %d: %s", i, what);
+            return fail(&ctx->err, st, buf);
+        };
+        const msao_simhash& h = hashes[i];
+        if (!h.planes) return bad(MSAO_ERR_INVALID_ARG, "planes is NULL");
+        if (h.bits != 16 && h.bits != 32 && h.bits != 48 && h.bits != 64)
+            return bad(MSAO_ERR_INVALID_ARG, "bits must be 16, 32, 48 or 64");
+        if (!aligned(h.planes, 16)) return bad(MSAO_ERR_ALIGNMENT, "planes is not 16-byte aligned");
+        if (s.row_stride * elt_size(s.dtype) >= ((int64_t)1 << 26))
+            return bad(MSAO_ERR_UNSUPPORTED, "row pitch of 64 MiB or more");
     }
     return MSAO_OK;
 }
@@ -790,23 +834,7 @@ msao_status msao_temporal_simhash(msao_ctx* ctx, const msao_segment* segs, int n
 {
     if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
     MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
-    if (n > 0 && !hashes) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "hashes is NULL");
-    char buf[160];
-    for (int i = 0; i < n; ++i) {
-        const msao_segment& s = segs[i];
-        if (!is_temporal(s)) continue;
-        auto bad = [&](msao_status st, const char* what) {
-            std::snprintf(buf, sizeof buf, "hash of segment %d: %s", i, what);
-            return fail(&ctx->err, st, buf);
-        };
-        const msao_simhash& h = hashes[i];
-        if (!h.planes) return bad(MSAO_ERR_INVALID_ARG, "planes is NULL");
-        if (h.bits != 16 && h.bits != 32 && h.bits != 48 && h.bits != 64)
-            return bad(MSAO_ERR_INVALID_ARG, "bits must be 16, 32, 48 or 64");
-        if (!aligned(h.planes, 16)) return bad(MSAO_ERR_ALIGNMENT, "planes is not 16-byte aligned");
-        if (s.row_stride * elt_size(s.dtype) >= ((int64_t)1 << 26))
-            return bad(MSAO_ERR_UNSUPPORTED, "row pitch of 64 MiB or more");
-    }
+    MSAO_TRY(check_hashes(ctx, segs, n, hashes));
     Plan pl;
     build_plan(ctx, segs, n, R, params, nullptr, nullptr, pl, false, nullptr, false, 0, hashes);
     MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
@@ -827,7 +855,7 @@ msao_status msao_temporal_simhash(msao_ctx* ctx, const msao_segment* segs, int n
     // frame blocks write d for every temporal token, so they always run
     ha.n_frame_blocks = (int)pl.nframes;
     ha.n_req_blocks = temporal ? R : 0;
-    return launched(ctx, MSAO_KERNEL_POST, st, run_hash_post, &ha);
+    return launched(ctx, MSAO_KERNEL_HASH_POST, st, run_hash_post, &ha);
 }
 
 msao_status msao_select_tokens(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
@@ -1035,10 +1063,14 @@ msao_status check_run_outputs(msao_ctx* ctx, const Plan& pl, const std::vector<m
     return MSAO_OK;
 }
 
-// The three launches of a full run, on tables already in the workspace.
+// The three launches of a full run, on tables already in the workspace. A
+// run with SimHash (pl.simhash_d) puts two between scoring and the post
+// launch: the signatures (into sig), then d, the clips' informativeness and
+// Dsum per (request, modality) from them (t.hdsum), which replace bit
+// sampling's before MAS, the per-frame terms and selection read them.
 msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const msao_token_out* tok,
                         const msao_frame_out* frm, const msao_req_out* req, const msao_select_out* sel, void* out,
-                        int64_t out_bytes, hipStream_t st)
+                        int64_t out_bytes, hipStream_t st, uint64_t* sig = nullptr)
 {
     ScoreArgs sa;
     std::memset(&sa, 0, sizeof sa);
@@ -1048,6 +1080,20 @@ msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const ms
     sa.mode = kModeScore;
     sa.xcd_order = xcd_order_for(ctx, out && pl.any_copy);
     MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
+    if (pl.simhash_d) {
+        HashArgs ha;
+        std::memset(&ha, 0, sizeof ha);
+        ha.t = t;
+        ha.sig = sig;
+        ha.d = tok->d;
+        ha.z = tok->z;
+        ha.info = tok->info;
+        ha.hdsum = const_cast<uint64_t*>(t.hdsum);
+        MSAO_TRY(launched(ctx, MSAO_KERNEL_SIMHASH, st, run_simhash, &ha));
+        ha.n_frame_blocks = (int)pl.nframes;
+        ha.n_req_blocks = t.R;
+        MSAO_TRY(launched(ctx, MSAO_KERNEL_HASH_POST, st, run_hash_post, &ha));
+    }
     PostArgs pa;
     std::memset(&pa, 0, sizeof pa);
     pa.t = t;
@@ -1104,6 +1150,29 @@ msao_status msao_run(msao_ctx* ctx, const msao_segment* segs, int n, int R, cons
     hipStream_t st = (hipStream_t)stream;
     MSAO_TRY(upload(ctx, pl, ws, st));
     return enqueue_run(ctx, pl, device_tables(pl, ws, n, R, params), tok, frm, req, sel, out, out_bytes, st);
+}
+
+msao_status msao_run_simhash(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
+                             const msao_simhash* hashes, const float* alpha, const msao_token_out* tok,
+                             uint64_t* sig, const msao_frame_out* frm, const msao_req_out* req,
+                             const msao_select_out* sel, void* out, const int64_t* out_byte_off, int64_t out_bytes,
+                             void* ws, size_t ws_bytes, void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
+    MSAO_TRY(check_hashes(ctx, segs, n, hashes));
+    Plan pl;
+    build_plan(ctx, segs, n, R, params, alpha, out_byte_off, pl, out != nullptr, nullptr, false, 0, hashes, false,
+               true);
+    MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
+    const std::vector<msao_segment> sv(segs, segs + n);
+    MSAO_TRY(check_run_outputs(ctx, pl, sv, tok, frm, req, sel, out, out_byte_off, out_bytes));
+    if (pl.any_temporal && !sig) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "sig is required with temporal segments");
+    MSAO_TRY(check_out_alignment(ctx, {{sig, 8}}));
+    DeviceGuard guard(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    MSAO_TRY(upload(ctx, pl, ws, st));
+    return enqueue_run(ctx, pl, device_tables(pl, ws, n, R, params), tok, frm, req, sel, out, out_bytes, st, sig);
 }
 
 msao_status msao_plan_create(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,

@@ -48,6 +48,13 @@ struct DevSeg {
     const uint8_t* planes; // [hash_bits][C] hyperplanes in the segment's dtype
     int32_t hash_bits;     // K per token (16, 32, 48 or 64)
     int32_t hi_begin;      // first hash tile (kHashTokens tokens each)
+    // Eq. 5's d counts E bits per token: C activity bits, or K SimHash bits
+    // in a run with SimHash. The selection key Ms z + Mt (E - d) orders the
+    // tokens as L_s z / C + L_t (E - d) / E: Ms = L_s E / g, Mt = L_t C / g
+    // with g = gcd(C, E) (Ms = L_s, Mt = L_t for bit sampling).
+    int32_t E;
+    int32_t pad_;
+    uint64_t key_ms, key_mt;
 };
 
 // One selection: a whole segment (frame -1) or one frame of a clip
@@ -103,6 +110,7 @@ struct Tables {
     int32_t n_hb;
     const SelUnit* sel_unit; // [n_sel] selections (one block each)
     const int32_t* hi_seg;   // [n_hi] segment of each hash tile (SimHash calls)
+    const uint64_t* hdsum;   // [R*4] SimHash Dsum per (request, modality) in a run with SimHash, else NULL
     int32_t n_hi;
     int32_t n, R, n_wi, n_gwi, n_tseg, n_frames;
     float tau, tau_s;
@@ -201,6 +209,12 @@ struct HashArgs {
     uint32_t* d;          // [Ntot]
     FrameOut frm;
     float* temporal;      // [R*4] (NULL: not written)
+    // a run with SimHash: the frame blocks also rewrite the informativeness
+    // of the clip's tokens from z and the new d, and the request blocks write
+    // Dsum per (request, modality) for the MAS of the following launch
+    const uint32_t* z;    // [Ntot]
+    float* info;          // [Ntot] (NULL: not written)
+    uint64_t* hdsum;      // [R*4] (NULL: not written)
     int32_t n_frame_blocks, n_req_blocks;
 };
 constexpr int kMlpGroup = 8;          // requests per wavefront in the prompt product

@@ -906,7 +906,7 @@ __device__ void rm_aggregate_all(const Tables& t, int r, PostShared<NT>& sh, RMA
             b += sh.dsum[q * kNumMod + mm];
         }
         g[mm].nsparse = a;
-        g[mm].dsum = b;
+        g[mm].dsum = t.hdsum ? t.hdsum[r * kNumMod + mm] : b;
     }
 }
 
@@ -1179,24 +1179,25 @@ __device__ void role_frame(const PostArgs& a, int f, PostShared<NT>& sh)
     const uint64_t D = block_sum_u64(acc, sh);
     if (threadIdx.x == 0) {
 #pragma clang fp contract(off)
-        const double sim = 1.0 - (double)D / (double)((int64_t)sg.P * sg.C);
+        const double sim = 1.0 - (double)D / (double)((int64_t)sg.P * sg.E);
         if (a.frm.dframe) a.frm.dframe[f] = D;
         if (a.frm.sim) a.frm.sim[f] = (float)sim;
         if (a.frm.gamma) a.frm.gamma[f] = (float)(1.0 - sim);
     }
 }
 
-// Selection key, order-equivalent to Ls*z + Lt*(C - d): when one weight is 0
-// the other term alone orders the tokens, so it is used unscaled.
+// Selection key Ms*z + Mt*(E - d), order-equivalent to L_s z / C + L_t (E -
+// d) / E (E = C for bit sampling, where Ms = L_s and Mt = L_t): when one
+// weight is 0 the other term alone orders the tokens, so it is used unscaled.
 enum { kKeyZero = 0, kKeyZ = 1, kKeyE = 2, kKeyFull = 3 };
 
 __device__ __forceinline__ uint64_t sel_key(const uint32_t* __restrict__ z, const uint32_t* __restrict__ d,
-                                            int g, int kind, uint64_t Ls, uint64_t Lt, uint32_t C)
+                                            int g, int kind, uint64_t Ms, uint64_t Mt, uint32_t E)
 {
     switch (kind) {
     case kKeyZ: return (uint64_t)z[g];
-    case kKeyE: return (uint64_t)(C - d[g]);
-    case kKeyFull: return Ls * (uint64_t)z[g] + Lt * (uint64_t)(C - d[g]);
+    case kKeyE: return (uint64_t)(E - d[g]);
+    case kKeyFull: return Ms * (uint64_t)z[g] + Mt * (uint64_t)(E - d[g]);
     default: return 0ull;
     }
 }
@@ -1207,14 +1208,14 @@ __device__ __forceinline__ uint64_t sel_key(const uint32_t* __restrict__ z, cons
 // keys dropped) so that no load sits behind a branch.
 template <int NT, int KIND>
 __device__ __forceinline__ void stage_keys(const uint32_t* __restrict__ z, const uint32_t* __restrict__ d, int N,
-                                           uint64_t Ls, uint64_t Lt, uint32_t C, bool in_lds, uint64_t* keys,
+                                           uint64_t Ms, uint64_t Mt, uint32_t E, bool in_lds, uint64_t* keys,
                                            uint64_t& lo, uint64_t& hi)
 {
     constexpr int U = 8;
     for (int i0 = threadIdx.x; i0 < N; i0 += U * NT) {
         uint64_t kk[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) kk[u] = sel_key(z, d, min(i0 + u * NT, N - 1), KIND, Ls, Lt, C);
+        for (int u = 0; u < U; ++u) kk[u] = sel_key(z, d, min(i0 + u * NT, N - 1), KIND, Ms, Mt, E);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int i = i0 + u * NT;
@@ -1244,13 +1245,13 @@ struct KeySrc {
     const uint32_t* z;
     const uint32_t* d;
     int kind;
-    uint64_t Ls, Lt;
-    uint32_t C;
+    uint64_t Ms, Mt;
+    uint32_t E;
     template <bool IN_LDS>
     __device__ __forceinline__ uint64_t at(int i) const
     {
         if constexpr (IN_LDS) return keys[i];
-        else return sel_key(z, d, i, kind, Ls, Lt, C);
+        else return sel_key(z, d, i, kind, Ms, Mt, E);
     }
 };
 
@@ -1443,8 +1444,8 @@ __device__ void role_select(const PostArgs& a, int unit, PostShared<NT>& sh, uin
         return;
     }
     const int kind = sg.temporal && sg.L_t > 0 ? (sg.L_s > 0 ? kKeyFull : kKeyE) : (sg.L_s > 0 ? kKeyZ : kKeyZero);
-    const uint64_t Ls = sg.L_s, Lt = sg.L_t;
-    const uint32_t C = (uint32_t)sg.C;
+    const uint64_t Ms = sg.key_ms, Mt = sg.key_mt;
+    const uint32_t E = (uint32_t)sg.E;
     const uint32_t* z = a.z + off;
     const uint32_t* d = a.d ? a.d + off : nullptr;
     const bool in_lds = N <= keys_cap;
@@ -1458,10 +1459,10 @@ __device__ void role_select(const PostArgs& a, int unit, PostShared<NT>& sh, uin
     {
         uint64_t lo = ~0ull, hi = 0ull;
         switch (kind) {
-        case kKeyZ: stage_keys<NT, kKeyZ>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
-        case kKeyE: stage_keys<NT, kKeyE>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
-        case kKeyFull: stage_keys<NT, kKeyFull>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
-        default: stage_keys<NT, kKeyZero>(z, d, N, Ls, Lt, C, in_lds, keys, lo, hi); break;
+        case kKeyZ: stage_keys<NT, kKeyZ>(z, d, N, Ms, Mt, E, in_lds, keys, lo, hi); break;
+        case kKeyE: stage_keys<NT, kKeyE>(z, d, N, Ms, Mt, E, in_lds, keys, lo, hi); break;
+        case kKeyFull: stage_keys<NT, kKeyFull>(z, d, N, Ms, Mt, E, in_lds, keys, lo, hi); break;
+        default: stage_keys<NT, kKeyZero>(z, d, N, Ms, Mt, E, in_lds, keys, lo, hi); break;
         }
         lo = wave_min_u64(lo);
         hi = wave_max_u64(hi);
@@ -1473,7 +1474,7 @@ __device__ void role_select(const PostArgs& a, int unit, PostShared<NT>& sh, uin
     __syncthreads();
     const uint64_t lo = sh.lo, hi = sh.hi;
 
-    const KeySrc src{keys, z, d, kind, Ls, Lt, C};
+    const KeySrc src{keys, z, d, kind, Ms, Mt, E};
     uint64_t* cand = keys + keys_cap;
     if (in_lds) select_and_compact<NT, true>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, ioff, iadd, lo, hi);
     else select_and_compact<NT, false>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, ioff, iadd, lo, hi);

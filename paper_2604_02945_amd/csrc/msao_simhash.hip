@@ -221,7 +221,9 @@ __device__ __forceinline__ uint64_t block_sum(uint64_t v, uint64_t* red)
 }
 
 // Frame f: d of its tokens against the previous frame (frame 0 against the
-// all-zero frame, all bits 1), D_t, sim = 1 - D_t / (P K), gamma.
+// all-zero frame, all bits 1), D_t, sim = 1 - D_t / (P K), gamma. In a run
+// with SimHash also the tokens' informativeness 1 - (lambda_s z / C +
+// lambda_t (K - d) / K).
 __device__ void hash_frame(const HashArgs& a, int f, uint64_t* red)
 {
     const Tables& t = a.t;
@@ -234,11 +236,16 @@ __device__ void hash_frame(const HashArgs& a, int f, uint64_t* red)
     const int tt = f - sg.frame_off;
     const int base = sg.tok_off + tt * sg.P;
     const uint64_t ones = all_bits(sg.hash_bits);
+    const float rc = __builtin_amdgcn_rcpf((float)sg.C), rk = __builtin_amdgcn_rcpf((float)sg.hash_bits);
     uint64_t acc = 0;
     for (int p = threadIdx.x; p < sg.P; p += kHashBlock) {
         const uint64_t prev = tt > 0 ? a.sig[base + p - sg.P] : ones;
         const uint32_t dd = (uint32_t)__popcll(a.sig[base + p] ^ prev);
         a.d[base + p] = dd;
+        if (a.info) {
+            const float red = sg.lam_s * (float)a.z[base + p] * rc + sg.lam_t * (float)(sg.hash_bits - (int)dd) * rk;
+            a.info[base + p] = 1.0f - red;
+        }
         acc += dd;
     }
     const uint64_t D = block_sum(acc, red);
@@ -252,8 +259,8 @@ __device__ void hash_frame(const HashArgs& a, int f, uint64_t* red)
 }
 
 // Request r: per modality, the differing bits over frames 1..T-1 of its
-// clips (recomputed from the signatures) and (T - 1) P K, then the temporal
-// term of Eq. 7.
+// clips (recomputed from the signatures; written to hdsum in a run with
+// SimHash) and (T - 1) P K, then the temporal term of Eq. 7.
 __device__ void hash_request(const HashArgs& a, int r, uint64_t* red)
 {
     const Tables& t = a.t;
@@ -288,7 +295,8 @@ __device__ void hash_request(const HashArgs& a, int r, uint64_t* red)
                 const double gamma_avg = (double)dsum / (double)qbits;
                 term = (float)((t.flags & kFlagLiteral) ? gamma_avg : 1.0 - gamma_avg);
             }
-            a.temporal[r * kNumMod + m] = term;
+            if (a.temporal) a.temporal[r * kNumMod + m] = term;
+            if (a.hdsum) a.hdsum[r * kNumMod + m] = dsum;
         }
     }
 }
@@ -324,7 +332,8 @@ int launch_hash_post(const HashArgs& a, void* stream, void* ev0, void* ev1)
 {
     const int blocks = a.n_frame_blocks + a.n_req_blocks;
     if (blocks <= 0) return 0;
-    if (!a.sig || !a.d || (a.n_req_blocks > 0 && !a.temporal)) return (int)hipErrorInvalidValue;
+    if (!a.sig || !a.d || (a.n_req_blocks > 0 && !a.temporal && !a.hdsum) || (a.info && !a.z))
+        return (int)hipErrorInvalidValue;
     return launch(k_hash_post, dim3((unsigned)blocks), dim3(kHashBlock), stream, a, ev0, ev1);
 }
 
