@@ -338,7 +338,7 @@ typedef struct {
  * msao_workspace_size. Errors: those of msao_temporal_redundancy, plus
  * MSAO_ERR_INVALID_ARG for a missing hash entry or bits not in {16, 32, 48,
  * 64}, MSAO_ERR_ALIGNMENT for planes, sig or d, MSAO_ERR_UNSUPPORTED for a
- * row pitch of 64 MiB or more. */
+ * row pitch of 64 MiB or more (32 MiB in a build with 64-token hash tiles). */
 msao_status msao_temporal_simhash(msao_ctx* ctx, const msao_segment* segs, int n, int n_requests,
                                   const msao_params* params, const msao_simhash* hashes, uint64_t* sig,
                                   uint32_t* d, const msao_frame_out* frm, float* temporal, void* ws,

@@ -581,8 +581,9 @@ msao_status check_hashes(msao_ctx* ctx, const msao_segment* segs, int n, const m
         if (h.bits != 16 && h.bits != 32 && h.bits != 48 && h.bits != 64)
             return bad(MSAO_ERR_INVALID_ARG, "bits must be 16, 32, 48 or 64");
         if (!aligned(h.planes, 16)) return bad(MSAO_ERR_ALIGNMENT, "planes is not 16-byte aligned");
-        if (s.row_stride * elt_size(s.dtype) >= ((int64_t)1 << 26))
-            return bad(MSAO_ERR_UNSUPPORTED, "row pitch of 64 MiB or more");
+        // a hash tile's rows are one buffer resource of kHashTokens pitches (32-bit size)
+        if (s.row_stride * elt_size(s.dtype) * kHashTokens > (int64_t)INT32_MAX)
+            return bad(MSAO_ERR_UNSUPPORTED, "row pitch too large for a hash tile (64 MiB or more)");
     }
     return MSAO_OK;
 }
