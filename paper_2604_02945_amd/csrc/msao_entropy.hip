@@ -5,7 +5,7 @@
 //
 // HBM-bound streaming reduction, one pass over the logits: one workgroup per
 // row, each lane reading 16-byte chunks with nontemporal buffer loads, the
-// next batch in flight while the current one is reduced. A lane keeps a
+// next two batches in flight while the current one is reduced. A lane keeps a
 // running maximum m, s = sum exp(x - m) and t = sum exp(x - m)(x - m) over its
 // chunks, so that H = ln s - t / s needs no second pass and no cancellation
 // against m. Per batch of chunks the batch maximum is taken first; only when
@@ -138,28 +138,29 @@ __device__ __forceinline__ void acc_add(Acc& a, const float (&x)[N], IndexOf ind
     // since -inf - (-inf) would turn every -inf into NaN.
     const float nml = a.m == -INFINITY ? 0.0f : -a.m * kLog2e;
     // A -inf logit gives e = 0 and d = -inf, whose product must be 0, not
-    // NaN: the clamp on d is needed only where the batch holds a -inf (one
-    // min per batch decides it for the whole wavefront).
-    float mn = x[0];
+    // NaN. The sums are taken without a clamp on d; a -inf then shows as a
+    // NaN u beside a finite s (a NaN logit makes s NaN too), and only then is
+    // u summed again with d clamped, from the values still in registers. Both
+    // ways give the same bits wherever no -inf occurs.
+    float s = a.s, u = a.u;
 #pragma unroll
-    for (int j = 1; j < N; ++j) mn = fminf(mn, x[j]);
-    if (__ballot(mn == -INFINITY) == 0) {
-#pragma unroll
-        for (int j = 0; j < N; ++j) {
-            const float d = fmaf(x[j], kLog2e, nml);  // L (x - m)
-            const float e = __builtin_amdgcn_exp2f(d);
-            a.s += e;
-            a.u = fmaf(e, d, a.u);
-        }
-    } else {
+    for (int j = 0; j < N; ++j) {
+        const float d = fmaf(x[j], kLog2e, nml);  // L (x - m)
+        const float e = __builtin_amdgcn_exp2f(d);
+        s += e;
+        u = fmaf(e, d, u);
+    }
+    if (__ballot(__builtin_isnan(u) && !__builtin_isnan(s)) != 0) {
+        u = a.u;
 #pragma unroll
         for (int j = 0; j < N; ++j) {
             const float d = fmaf(x[j], kLog2e, nml);
             const float e = __builtin_amdgcn_exp2f(d);
-            a.s += e;
-            a.u = fmaf(e, fmaxf(d, kMinDiff * kLog2e), a.u);
+            u = fmaf(e, fmaxf(d, kMinDiff * kLog2e), u);
         }
     }
+    a.s = s;
+    a.u = u;
 }
 
 template <int DT, int U>
@@ -172,40 +173,58 @@ __global__ __launch_bounds__(kEntBlock) void k_entropy(EntArgs a)
     const int tid = threadIdx.x, lane = tid & (kEntWave - 1), wid = tid >> 6;
     const uint8_t* base = a.logits + (int64_t)row * a.row_bytes;
     const int nfull = a.vocab / EPC;         // whole 16-byte chunks
-    const int nmain = nfull / STEP * STEP;   // chunks of whole batches
+    const int npair = nfull / (2 * STEP) * (2 * STEP);  // chunks of whole pairs of batches
     const ent_rsrc_t rs = ent_rsrc(base, nfull * 16);
     Acc acc{-INFINITY, 0.0f, 0.0f, 0};
     float x[U * EPC];
-    // whole batches, the next one loading while the current one is reduced
-    ent_vec4 cur[U];
-    if (nmain > 0) {
+    // batches in two register sets used in turn: once a batch is widened its
+    // set loads the batch after next, so two batches are in flight while one
+    // is reduced. The loads are unconditional, so that no register set needs
+    // a copy and the loop has one way back to its head (whose wait is then for
+    // the first set only): past the row they fall outside the buffer
+    // resource, read nothing and return zeros (the offsets stay below 2^31: a
+    // row is at most 2^31 - 2^20 bytes).
+    ent_vec4 ba[U], bb[U];
+    auto load = [&](ent_vec4 (&b)[U], int c0) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) cur[u] = ent_load(rs, (u * kEntBlock + tid) * 16);
-    }
-    for (int c0 = 0; c0 < nmain; c0 += STEP) {
-        ent_vec4 nxt[U];
-        if (c0 + STEP < nmain) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) nxt[u] = ent_load(rs, (c0 + STEP + u * kEntBlock + tid) * 16);
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) L::widen(cur[u], &x[u * EPC]);
+        for (int u = 0; u < U; ++u) b[u] = ent_load(rs, (c0 + u * kEntBlock + tid) * 16);
+    };
+    auto reduce = [&](int c0) {
         acc_add<U * EPC>(acc, x, [&](int j) { return (c0 + (j / EPC) * kEntBlock + tid) * EPC + j % EPC; });
-#pragma unroll
-        for (int u = 0; u < U; ++u) cur[u] = nxt[u];
-    }
-    // the last, partial batch: chunks past the row read as -inf
-    if (nmain < nfull) {
+    };
+    // widen a set whose chunks may pass the row's last whole chunk: those read as -inf
+    auto widen_masked = [&](const ent_vec4 (&b)[U], int c0) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int c = nmain + u * kEntBlock + tid;
-            L::widen(ent_load(rs, c * 16), &x[u * EPC]);
-            if (c >= nfull) {
+            L::widen(b[u], &x[u * EPC]);
+            if (c0 + u * kEntBlock + tid >= nfull) {
 #pragma unroll
                 for (int j = 0; j < EPC; ++j) x[u * EPC + j] = -INFINITY;
             }
         }
-        acc_add<U * EPC>(acc, x, [&](int j) { return (nmain + (j / EPC) * kEntBlock + tid) * EPC + j % EPC; });
+    };
+    load(ba, 0);
+    // all of the first set's loads are issued before the second set's
+    __builtin_amdgcn_sched_barrier(0);
+    load(bb, STEP);
+    for (int c0 = 0; c0 < npair; c0 += 2 * STEP) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) L::widen(ba[u], &x[u * EPC]);
+        load(ba, c0 + 2 * STEP);
+        reduce(c0);
+#pragma unroll
+        for (int u = 0; u < U; ++u) L::widen(bb[u], &x[u * EPC]);
+        load(bb, c0 + 3 * STEP);
+        reduce(c0 + STEP);
+    }
+    // the rest of the whole chunks, fewer than two batches, already loaded
+    if (npair < nfull) {
+        widen_masked(ba, npair);
+        reduce(npair);
+    }
+    if (npair + STEP < nfull) {
+        widen_masked(bb, npair + STEP);
+        reduce(npair + STEP);
     }
     // the elements past the last whole chunk, one per thread
     const int tail = a.vocab - nfull * EPC;
