@@ -357,8 +357,8 @@ msao_status msao_temporal_simhash(msao_ctx* ctx, const msao_segment* segs, int n
  *     (K - d) / K with the Q24 weights, as an exact integer; ties by index.
  * z, l1, l2 and res (the squared difference of the rows) are as in msao_run.
  * hashes (host, [n]) as for msao_temporal_simhash. sig (device [total
- * tokens] u64, 8-byte aligned) receives the signatures (0 outside temporal
- * segments) and is required when a segment is temporal. Every other argument,
+ * tokens] u64, 8-byte aligned, required when there are tokens) receives
+ * the signatures, 0 outside temporal segments. Every other argument,
  * the workspace size and the errors are those of msao_run, plus the hash
  * errors of msao_temporal_simhash. Precision: the projections are fp32 sums
  * on the matrix cores, so a signature bit whose projection is within

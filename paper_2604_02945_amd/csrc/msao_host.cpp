@@ -1081,7 +1081,8 @@ msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const ms
     sa.mode = kModeScore;
     sa.xcd_order = xcd_order_for(ctx, out && pl.any_copy);
     MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
-    if (pl.simhash_d) {
+    if (sig && t.n_hi > 0) {
+        // signatures of every token (zeros outside temporal segments)
         HashArgs ha;
         std::memset(&ha, 0, sizeof ha);
         ha.t = t;
@@ -1091,9 +1092,11 @@ msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const ms
         ha.info = tok->info;
         ha.hdsum = const_cast<uint64_t*>(t.hdsum);
         MSAO_TRY(launched(ctx, MSAO_KERNEL_SIMHASH, st, run_simhash, &ha));
-        ha.n_frame_blocks = (int)pl.nframes;
-        ha.n_req_blocks = t.R;
-        MSAO_TRY(launched(ctx, MSAO_KERNEL_HASH_POST, st, run_hash_post, &ha));
+        if (pl.simhash_d) {
+            ha.n_frame_blocks = (int)pl.nframes;
+            ha.n_req_blocks = t.R;
+            MSAO_TRY(launched(ctx, MSAO_KERNEL_HASH_POST, st, run_hash_post, &ha));
+        }
     }
     PostArgs pa;
     std::memset(&pa, 0, sizeof pa);
@@ -1168,7 +1171,7 @@ msao_status msao_run_simhash(msao_ctx* ctx, const msao_segment* segs, int n, int
     MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
     const std::vector<msao_segment> sv(segs, segs + n);
     MSAO_TRY(check_run_outputs(ctx, pl, sv, tok, frm, req, sel, out, out_byte_off, out_bytes));
-    if (pl.any_temporal && !sig) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "sig is required with temporal segments");
+    if (pl.ntok > 0 && !sig) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "sig is required");
     MSAO_TRY(check_out_alignment(ctx, {{sig, 8}}));
     DeviceGuard guard(ctx->device);
     hipStream_t st = (hipStream_t)stream;

@@ -3,7 +3,10 @@ modalities, fp32 and bf16, ragged widths (multiples of 8 channels up to
 1288), one to nine frames per clip, ragged frame sizes, fixed, zero, full and
 MAS-guided keep ratios, padded row strides, several segments per request and
 modality, and the literal and per-frame flags. Same bar as the parity tests
-(run_and_compare): integers, kept indices and compacted rows bit-exact."""
+(run_and_compare): integers, kept indices and compacted rows bit-exact. The
+same kind of tables also go through the SimHash entry points and the learned
+heads at their bars; for msao_run_simhash the tables hold integer values, so
+that every projection is exact and the whole run is compared bit for bit."""
 import numpy as np
 import pytest
 import torch
@@ -89,3 +92,25 @@ def test_random_table_learned(seed, dev):
         f"mlp {mlp is not None}")
     g, ref = run_l(segs, R, heads, mlp, dev, params=p)
     compare_l(segs, R, heads, g, ref, mlp)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_table_simhash_run(seed, dev):
+    from test_gpu_simhash_run import exact_compare, int_clip, int_planes, int_rows
+    segs, R, p, pad = random_table(300 + seed)
+    rng = np.random.default_rng(70 + seed)
+    isegs = []
+    for s in segs:   # the same shapes and parameters with integer values (exact projections)
+        x = int_clip(rng, s.n_frames, s.tokens_per_frame, s.hidden) if s.n_frames > 1 else \
+            int_rows(rng, s.n_tokens, s.hidden)
+        data = x if s.dtype == "f32" else f32_to_bf16_bits(x)
+        isegs.append(Segment(s.request, s.modality, s.n_frames, s.tokens_per_frame, s.hidden, s.dtype,
+                             s.keep_ratio, data))
+    hashes = []
+    for s in isegs:
+        K = int(rng.choice([16, 32, 48, 64]))
+        temporal = s.modality == VIDEO and s.n_frames >= 2 and s.tokens_per_frame > 0
+        hashes.append(dict(planes=int_planes(rng, K, s.hidden, s.dtype), bits=K) if temporal else None)
+    log(f"[random] simhash run seed {seed}: {len(isegs)} segments, R {R}, flags {p['flags']}, pad {pad}, "
+        f"tokens {sum(s.n_tokens for s in isegs)}")
+    exact_compare(isegs, R, p, hashes, dev, pad=pad)

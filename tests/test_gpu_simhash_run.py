@@ -166,9 +166,10 @@ def test_without_clips_equals_msao_run(dev):
     p = default_params()
     dsegs = to_device(segs, dev)
     a = msao.msao_run(dsegs, 1, p).results(1, 2)
-    out, _ = msao.msao_run_simhash(dsegs, 1, [None, None], p)
+    out, sig = msao.msao_run_simhash(dsegs, 1, [None, None], p)
     b = out.results(1, 2)
     torch.cuda.synchronize()
+    assert sig.numel() == 100 and int(torch.count_nonzero(sig)) == 0   # signatures written, all zero
     for k in ("z", "l1", "l2", "info", "d", "res", "agg", "rho", "temporal", "beta", "mas", "present", "keep",
               "kept_idx", "kept_count"):
         assert torch.equal(a[k], b[k]), k
