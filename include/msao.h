@@ -124,15 +124,17 @@ typedef struct {
     uint32_t* z;     /* inactive channels (importance = 1 - z/C, Eq. 3 stand-in) */
     float* l1;       /* sum |x| */
     float* l2;       /* sum x^2 */
-    float* info;     /* 1 - (lambda_s*z + lambda_t*e)/C: informativeness, orders like -key */
-    uint32_t* d;     /* Hamming distance of activity bits to the previous frame (Eq. 5) */
+    float* info;     /* 1 - (lambda_s*z + lambda_t*e)/C: informativeness, orders like -key
+                        (with SimHash: 1 - lambda_s*z/C - lambda_t*(K - d)/K) */
+    uint32_t* d;     /* Hamming distance of activity bits to the previous frame (Eq. 5;
+                        with SimHash: of the K signature bits) */
     float* res;      /* sum (x_t - x_{t-1})^2, the residual energy of Sec. 4.1.2 */
 } msao_token_out;
 
 /* Per-frame outputs of temporal segments, [total temporal frames] each; NULL skips. */
 typedef struct {
     uint64_t* dframe;/* D_t = sum over the frame's tokens of d */
-    float* sim;      /* Eq. 5: 1 - D_t/(P*C) */
+    float* sim;      /* Eq. 5: 1 - D_t/(P*C) (P*K with SimHash) */
     float* gamma;    /* 1 - sim (Sec. 4.1.2) */
 } msao_frame_out;
 
