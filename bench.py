@@ -335,7 +335,7 @@ def simhash_bench(args, dev, ctx):
         "ms_per_call_bit_sampling": ms_bs,
         "run": {"ms_per_call": ms_rs, "tokens_per_s": ntok / (ms_rs * 1e-3), "ms_per_call_msao_run": ms_rb,
                 "kernel_ms": {k: k_rs[getattr(msao.binding, "KERNEL_" + k.upper())]
-                              for k in ("score", "simhash", "hash_post", "post", "gather")},
+                              for k in ("score", "clip", "simhash", "hash_post", "post", "gather")},
                 "kernel_ms_msao_run": {k: k_rb[getattr(msao.binding, "KERNEL_" + k.upper())]
                                        for k in ("score", "post", "gather")}},
         "algorithmic_bytes": b,

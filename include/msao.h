@@ -483,7 +483,8 @@ double msao_expected_e2e_latency(const msao_latency_model* m);
 #define MSAO_KERNEL_HEAD 4    /* learned spatial head: pooling, sigmoid, Eq. 4 counts */
 #define MSAO_KERNEL_SIMHASH 5 /* SimHash signatures */
 #define MSAO_KERNEL_HASH_POST 6 /* SimHash d, per-frame terms, temporal term */
-#define MSAO_NUM_KERNELS 7
+#define MSAO_KERNEL_CLIP 7    /* the SimHash run's clips: statistics and signatures in one pass */
+#define MSAO_NUM_KERNELS 8
 
 /* When enabled, every launch is bracketed by a pair of HIP events recorded on
  * the caller's stream. */

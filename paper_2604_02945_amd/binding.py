@@ -23,7 +23,7 @@ F32, BF16 = 0, 1
 FLAG_TEMPORAL_LITERAL = 1
 FLAG_SELECT_PER_FRAME = 2
 (KERNEL_SCORE, KERNEL_POST, KERNEL_GATHER, KERNEL_ENTROPY, KERNEL_HEAD, KERNEL_SIMHASH, KERNEL_HASH_POST,
- NUM_KERNELS) = 0, 1, 2, 3, 4, 5, 6, 7
+ KERNEL_CLIP, NUM_KERNELS) = 0, 1, 2, 3, 4, 5, 6, 7, 8
 MODAL_DESC = 8
 DECIDE_HOLD, DECIDE_SEND, DECIDE_OFFLOAD = 0, 1, 2
 

@@ -255,7 +255,7 @@ __global__ __launch_bounds__(kEntBlock) void k_entropy(EntArgs a)
 
 int launch_entropy(const EntArgs& a, void* stream, void* ev0, void* ev1)
 {
-    if (a.rows <= 0) return 0;
+    if (a.rows <= 0) return kNoLaunch;
     const dim3 grid((unsigned)a.rows), block(kEntBlock);
     if (a.dtype == kBF16) {
         if (ev0 && ev1)

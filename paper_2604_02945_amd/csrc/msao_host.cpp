@@ -36,6 +36,7 @@ struct msao_ctx {
     int row_item_bytes = 8192;
     int chain_frames = 0;       // frames per temporal work item; 0 = automatic
     int xcd_order = -1;         // scoring block order: -1 automatic, 0 dispatch order, 1 one range per XCD
+    int clip_fuse = 1;          // the SimHash run scores and hashes its clips in one pass (k_clip)
 };
 
 namespace {
@@ -123,7 +124,8 @@ msao_status validate_impl(const msao_segment* segs, int n, int R, const msao_par
 // Per-call tables, built on the host and uploaded into the workspace.
 struct Plan {
     std::vector<DevSeg> seg;
-    std::vector<int32_t> seg_wi, seg_gi, tseg;   // seg_wi, seg_gi: per-segment prefixes (host only)
+    std::vector<int32_t> wi_b, wi_e;             // per segment: its scoring work items [wi_b, wi_e) (host only)
+    std::vector<int32_t> seg_gi, tseg;           // seg_gi: per-segment prefix of gather items (host only)
     std::vector<int32_t> wi_seg, gi_seg;         // segment of every work item
     std::vector<RmEntry> rm;
     std::vector<WiRange> rm_rng;
@@ -142,13 +144,18 @@ struct Plan {
     int mlp_hidden = 0;            // > 0: the relevance MLP's u = W1[:, :P] p + b1 per request
     size_t off_hbseg = 0, off_partial_x = 0, off_proj = 0, off_head_count = 0, off_mlp_u = 0;
     size_t off_seg = 0, off_wi = 0, off_gi = 0, off_rmoff = 0, off_rmseg = 0, off_tseg = 0, off_alpha = 0;
-    size_t off_selu = 0, off_hiseg = 0;
+    size_t off_selu = 0, off_hiseg = 0, off_clseg = 0;
     bool simhash_d = false;        // a run with SimHash: d of temporal segments in K-bit units
-    size_t off_hdsum = 0;          // [R*4] SimHash Dsum (simhash_d only)
+    size_t off_hdsum = 0;          // [R*4] SimHash Dsum (simhash_d without clip_fused)
+    bool clip_fused = false;       // a run with SimHash whose clips k_clip scores and hashes in one pass
+    int clip_dtype = -1, clip_bits = 0;
+    std::vector<int32_t> cl_seg;   // segment of each k_clip block
+    int n_wi_score = 0;            // k_score's work items [0, n_wi_score); the fused clips' follow
     size_t table_bytes = 0, off_partial = 0, total_bytes = 0;
 };
 
-size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t n_hb, int64_t n_sel, int64_t n_hi)
+size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t n_hb, int64_t n_sel, int64_t n_hi,
+                    int64_t n_cl)
 {
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -166,6 +173,7 @@ size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t
     pl.off_hbseg = take(sizeof(int32_t) * (size_t)std::max<int64_t>(n_hb, 1));
     pl.off_selu = take(sizeof(SelUnit) * (size_t)std::max<int64_t>(n_sel, 1));
     pl.off_hiseg = take(sizeof(int32_t) * (size_t)std::max<int64_t>(n_hi, 1));
+    pl.off_clseg = take(sizeof(int32_t) * (size_t)std::max<int64_t>(n_cl, 1));
     pl.table_bytes = o;
     return o;
 }
@@ -180,7 +188,7 @@ size_t workspace_bytes_for(int n, int R, int64_t ntok)
 {
     Plan pl;
     const int64_t items = ntok + n;
-    const size_t tb = table_layout(pl, n, R, items, items, items, items, items);
+    const size_t tb = table_layout(pl, n, R, items, items, items, items, items, items);
     return align_up(tb, kWsAlign) + align_up(sizeof(Partial) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
            align_up(sizeof(PartialX) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
            align_up(sizeof(float) * (size_t)std::max<int64_t>(ntok, 1), kWsAlign) +
@@ -204,8 +212,29 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
     pl.hb_seg.clear();
     pl.max_head_p = 0;
     pl.seg.resize((size_t)n);
-    pl.seg_wi.assign((size_t)n + 1, 0);
+    pl.wi_b.assign((size_t)std::max(n, 1), 0);
+    pl.wi_e.assign((size_t)std::max(n, 1), 0);
     pl.seg_gi.assign((size_t)n + 1, 0);
+    pl.cl_seg.clear();
+    pl.clip_fused = false;
+    // a run with SimHash scores and hashes its clips in one pass when every
+    // clip's tiles of 16 frames fit a 32-bit buffer resource
+    // and all clips share one element type and signature width (one kernel instance)
+    bool fuse = simhash_d && hashes != nullptr && (!ctx || ctx->clip_fuse);
+    int clip_dtype = -1, clip_bits = 0;
+    for (int i = 0; fuse && i < n; ++i) {
+        if (!is_temporal(segs[i])) continue;
+        if ((int64_t)segs[i].tokens_per_frame * segs[i].row_stride * elt_size(segs[i].dtype) * 16 > (int64_t)INT32_MAX)
+            fuse = false;
+        if (clip_dtype < 0) {
+            clip_dtype = segs[i].dtype;
+            clip_bits = hashes[i].bits;
+        } else if (segs[i].dtype != clip_dtype || hashes[i].bits != clip_bits) {
+            fuse = false;
+        }
+    }
+    pl.clip_dtype = clip_dtype;
+    pl.clip_bits = clip_bits;
     pl.tseg.clear();
     int64_t tok = 0, frame = 0;
     int wi = 0, gi = 0;
@@ -274,7 +303,9 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
             }
             for (int64_t r = 0; r < N; r += kHashBlockTokens) pl.hi_seg.push_back(i);
         }
-        d.copy_in_score = (fuse_copy && out_off && N > 0 && d.k == (int32_t)N) ? 1 : 0;
+        d.fused = (fuse && d.temporal) ? 1 : 0;
+        // (a fused clip's kept rows are always left to the gather)
+        d.copy_in_score = (fuse_copy && out_off && N > 0 && d.k == (int32_t)N && !d.fused) ? 1 : 0;
         if (learned && heads && heads[i].weight && N > 0) {
             d.head_w = (const uint8_t*)heads[i].weight;
             d.head_b = heads[i].bias;
@@ -286,7 +317,15 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         }
         // scoring work items, one wavefront each
         int items = 0;
-        if (d.temporal) {
+        if (d.fused) {
+            // tiles of at most 15 new frames of one position, the frames split
+            // evenly; their work items follow all others
+            d.ntiles = (s.n_frames + kClipFrames - 1) / kClipFrames;
+            d.per_item = (s.n_frames + d.ntiles - 1) / d.ntiles;
+            pl.tseg.push_back(i);
+            pl.any_temporal = true;
+            pl.clip_fused = true;
+        } else if (d.temporal) {
             int fpi = ctx && ctx->chain_frames > 0 ? ctx->chain_frames : s.n_frames;
             if (!(ctx && ctx->chain_frames > 0)) {
                 // split long chains until there are enough wavefronts to cover the chip
@@ -305,8 +344,9 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
             d.per_item = 1;
         }
         d.wi_begin = wi;
+        pl.wi_b[(size_t)i] = wi;
         wi += items;
-        pl.seg_wi[(size_t)i + 1] = wi;
+        pl.wi_e[(size_t)i] = wi;
         d.g_begin = gi;
         if (!d.copy_in_score) gi += (d.cap + kGatherRows - 1) / kGatherRows;
         pl.seg_gi[(size_t)i + 1] = gi;
@@ -314,6 +354,18 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         if (d.copy_in_score) pl.any_copy = true;
         tok += N;
         if (d.temporal) frame += s.n_frames;
+    }
+    pl.n_wi_score = wi;
+    for (int i = 0; i < n; ++i) {
+        DevSeg& d = pl.seg[(size_t)i];
+        if (!d.fused) continue;
+        const int items = d.P * d.ntiles;
+        d.wi_begin = wi;
+        pl.wi_b[(size_t)i] = wi;
+        wi += items;
+        pl.wi_e[(size_t)i] = wi;
+        d.cl_begin = (int32_t)pl.cl_seg.size();
+        for (int b = 0; b < (items + kClipWaves - 1) / kClipWaves; ++b) pl.cl_seg.push_back(i);
     }
     pl.ntok = tok;
     pl.nframes = frame;
@@ -336,23 +388,23 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         e.ntok += (uint64_t)d.n_tok;
         if (d.temporal) e.qbits += (uint64_t)(d.T - 1) * (uint64_t)d.P * (uint64_t)d.E;
         pl.rm_rng[(size_t)count[(size_t)(s.request * kNumMod + s.modality)]++] =
-            WiRange{pl.seg_wi[(size_t)i], pl.seg_wi[(size_t)i + 1], i, 0};
+            WiRange{pl.wi_b[(size_t)i], pl.wi_e[(size_t)i], i, 0};
     }
     pl.wi_seg.resize((size_t)pl.n_wi);
     pl.gi_seg.resize((size_t)pl.n_gwi);
     for (int i = 0; i < n; ++i) {
-        std::fill(pl.wi_seg.begin() + pl.seg_wi[(size_t)i], pl.wi_seg.begin() + pl.seg_wi[(size_t)i + 1], i);
+        std::fill(pl.wi_seg.begin() + pl.wi_b[(size_t)i], pl.wi_seg.begin() + pl.wi_e[(size_t)i], i);
         std::fill(pl.gi_seg.begin() + pl.seg_gi[(size_t)i], pl.gi_seg.begin() + pl.seg_gi[(size_t)i + 1], i);
     }
     pl.alpha.assign((size_t)std::max(R * kNumMod, 1), 0.0f);
     if (alpha)
         for (int x = 0; x < R * kNumMod; ++x) pl.alpha[(size_t)x] = alpha[x];
     table_layout(pl, n, R, pl.n_wi, pl.n_gwi, (int64_t)pl.hb_seg.size(), (int64_t)pl.sel_unit.size(),
-                 (int64_t)pl.hi_seg.size());
+                 (int64_t)pl.hi_seg.size(), (int64_t)pl.cl_seg.size());
     pl.off_partial = align_up(pl.table_bytes, kWsAlign);
     pl.total_bytes = pl.off_partial + sizeof(Partial) * (size_t)std::max(pl.n_wi, 1);
     pl.simhash_d = simhash_d && pl.any_temporal;
-    if (pl.simhash_d) {
+    if (pl.simhash_d && !pl.clip_fused) {
         pl.off_hdsum = align_up(pl.total_bytes, kWsAlign);
         pl.total_bytes = pl.off_hdsum + sizeof(uint64_t) * (size_t)std::max(R * kNumMod, 1);
     }
@@ -420,6 +472,7 @@ msao_status upload(msao_ctx* ctx, const Plan& pl, void* ws, hipStream_t stream)
     put(pl.off_hbseg, pl.hb_seg.data(), sizeof(int32_t) * pl.hb_seg.size());
     put(pl.off_selu, pl.sel_unit.data(), sizeof(SelUnit) * pl.sel_unit.size());
     put(pl.off_hiseg, pl.hi_seg.data(), sizeof(int32_t) * pl.hi_seg.size());
+    put(pl.off_clseg, pl.cl_seg.data(), sizeof(int32_t) * pl.cl_seg.size());
     if ((e = hipMemcpyAsync(ws, h, pl.table_bytes, hipMemcpyHostToDevice, stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipMemcpyAsync");
     if ((e = hipEventRecord(ctx->stage_ev[slot], stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
@@ -447,7 +500,10 @@ Tables device_tables(const Plan& pl, void* ws, int n, int R, const msao_params* 
     t.n_hb = (int32_t)pl.hb_seg.size();
     t.sel_unit = (const SelUnit*)(b + pl.off_selu);
     t.hi_seg = (const int32_t*)(b + pl.off_hiseg);
-    t.hdsum = pl.simhash_d ? (const uint64_t*)(b + pl.off_hdsum) : nullptr;
+    t.hdsum = pl.simhash_d && !pl.clip_fused ? (const uint64_t*)(b + pl.off_hdsum) : nullptr;
+    t.cl_seg = (const int32_t*)(b + pl.off_clseg);
+    t.n_cl = (int32_t)pl.cl_seg.size();
+    t.n_wi_score = pl.n_wi_score;
     t.n_hi = (int32_t)pl.hi_seg.size();
     t.n = n;
     t.R = R;
@@ -510,6 +566,11 @@ msao_status launched(msao_ctx* ctx, int kernel, hipStream_t stream, int (*fn)(co
         if (!e0 || !e1) return fail(&ctx->err, MSAO_ERR_HIP, "hipEventCreate failed");
     }
     const int rc = fn(args, stream, e0, e1);
+    if (rc == kNoLaunch) {  // nothing to launch: the events were not recorded
+        if (e0) ctx->pool.push_back(e0);
+        if (e1) ctx->pool.push_back(e1);
+        return MSAO_OK;
+    }
     if (rc != 0) return hip_fail(ctx, (hipError_t)rc, "kernel launch");
     if (ctx->profiling) ctx->rec[kernel].push_back({e0, e1});
     return MSAO_OK;
@@ -521,6 +582,7 @@ int run_gather(const void* a, void* s, void* e0, void* e1) { return launch_gathe
 int run_entropy(const void* a, void* s, void* e0, void* e1) { return launch_entropy(*(const EntArgs*)a, s, e0, e1); }
 int run_head(const void* a, void* s, void* e0, void* e1) { return launch_head(*(const HeadArgs*)a, s, e0, e1); }
 int run_simhash(const void* a, void* s, void* e0, void* e1) { return launch_simhash(*(const HashArgs*)a, s, e0, e1); }
+int run_clip(const void* a, void* s, void* e0, void* e1) { return launch_clip(*(const ClipArgs*)a, s, e0, e1); }
 int run_hash_post(const void* a, void* s, void* e0, void* e1)
 {
     return launch_hash_post(*(const HashArgs*)a, s, e0, e1);
@@ -699,6 +761,7 @@ msao_status msao_create(msao_ctx** out, int device)
     if (const char* v = std::getenv("MSAO_ROW_ITEM_BYTES")) c->row_item_bytes = std::max(1, std::atoi(v));
     if (const char* v = std::getenv("MSAO_CHAIN_FRAMES")) c->chain_frames = std::max(0, std::atoi(v));
     if (const char* v = std::getenv("MSAO_XCD_ORDER")) c->xcd_order = std::atoi(v) < 0 ? -1 : (std::atoi(v) ? 1 : 0);
+    if (const char* v = std::getenv("MSAO_CLIP_FUSE")) c->clip_fuse = std::atoi(v) ? 1 : 0;
     *out = c;
     return MSAO_OK;
 }
@@ -1077,11 +1140,22 @@ msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const ms
     std::memset(&sa, 0, sizeof sa);
     sa.t = t;
     sa.tok = token_out(tok);
+    if (pl.clip_fused) sa.tok.sig = sig;
     sa.out = (uint8_t*)out;
     sa.mode = kModeScore;
     sa.xcd_order = xcd_order_for(ctx, out && pl.any_copy);
     MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
-    if (sig && t.n_hi > 0) {
+    if (pl.clip_fused) {
+        // the clips: statistics, signatures, d and partials in one pass
+        ClipArgs ca;
+        std::memset(&ca, 0, sizeof ca);
+        ca.t = t;
+        ca.tok = token_out(tok);
+        ca.tok.sig = sig;
+        ca.clip_dtype = pl.clip_dtype;
+        ca.clip_bits = pl.clip_bits;
+        MSAO_TRY(launched(ctx, MSAO_KERNEL_CLIP, st, run_clip, &ca));
+    } else if (sig && t.n_hi > 0) {
         // signatures of every token (zeros outside temporal segments)
         HashArgs ha;
         std::memset(&ha, 0, sizeof ha);

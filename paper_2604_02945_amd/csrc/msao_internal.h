@@ -53,8 +53,11 @@ struct DevSeg {
     // tokens as L_s z / C + L_t (E - d) / E: Ms = L_s E / g, Mt = L_t C / g
     // with g = gcd(C, E) (Ms = L_s, Mt = L_t for bit sampling).
     int32_t E;
-    int32_t pad_;
+    // a clip of a run with SimHash scored and hashed in one pass (k_clip):
+    // work items of 15 frames x 1 position, cl_begin its first k_clip block
+    int32_t fused;
     uint64_t key_ms, key_mt;
+    int32_t cl_begin, ntiles;
 };
 
 // One selection: a whole segment (frame -1) or one frame of a clip
@@ -111,6 +114,9 @@ struct Tables {
     const SelUnit* sel_unit; // [n_sel] selections (one block each)
     const int32_t* hi_seg;   // [n_hi] segment of each hash tile (SimHash calls)
     const uint64_t* hdsum;   // [R*4] SimHash Dsum per (request, modality) in a run with SimHash, else NULL
+    const int32_t* cl_seg;   // [n_cl] segment of each k_clip block (fused clips)
+    int32_t n_cl;
+    int32_t n_wi_score;      // work items of k_score: [0, n_wi_score); the fused clips' follow
     int32_t n_hi;
     int32_t n, R, n_wi, n_gwi, n_tseg, n_frames;
     float tau, tau_s;
@@ -120,6 +126,7 @@ struct Tables {
 
 struct TokenOut {
     uint32_t* z; float* l1; float* l2; float* info; uint32_t* d; float* res;
+    uint64_t* sig;  // a run with SimHash: signatures (k_score writes 0 for its tokens)
 };
 struct FrameOut {
     uint64_t* dframe; float* sim; float* gamma;
@@ -219,6 +226,23 @@ struct HashArgs {
 };
 constexpr int kMlpGroup = 8;          // requests per wavefront in the prompt product
 
+// The run with SimHash reads each clip once: k_clip scores and hashes tiles
+// of up to 16 consecutive frames of one patch position (one wavefront each,
+// kClipWaves per block, all of one clip). Consecutive tiles overlap by one
+// frame, so a tile holds the predecessor of each of its new frames (at most
+// 15, the clip's frames split evenly; the first tile starts at the all-zero
+// frame -1): z, l1, l2, res, the signature, d against the previous frame and
+// the informativeness of those tokens, and the work item's integer partials.
+constexpr int kClipWaves = 8;
+constexpr int kClipFrames = 15;                 // most new frames per tile (16 rows with the predecessor)
+struct ClipArgs {
+    Tables t;
+    TokenOut tok;         // z, l1, l2, info, d, res, sig of the clips' tokens
+    int32_t clip_dtype;   // element type and signature width shared by every fused clip
+    int32_t clip_bits;
+};
+int launch_clip(const ClipArgs& a, void* stream, void* ev0, void* ev1);
+
 struct GatherArgs {
     Tables t;
     const int32_t* kept_idx;
@@ -249,8 +273,10 @@ constexpr int kEntBlock = MSAO_ENT_BLOCK;  // threads per row of logits
 constexpr int kEntUnits = MSAO_ENT_UNITS;  // 16-byte chunks per thread per batch
 int launch_entropy(const EntArgs& a, void* stream, void* ev0, void* ev1);
 
-// Launchers (msao_kernels.hip). Return the HIP error code of the launch. ev0 and
-// ev1 (hipEvent_t, may be NULL) are recorded at the kernel's start and end.
+// Launchers (msao_kernels.hip). Return the HIP error code of the launch, or
+// kNoLaunch when there is nothing to launch (then nothing is enqueued). ev0
+// and ev1 (hipEvent_t, may be NULL) are recorded at the kernel's start and end.
+constexpr int kNoLaunch = -1;
 int launch_score(const ScoreArgs& a, void* stream, void* ev0, void* ev1);
 int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1);
 int launch_gather(const GatherArgs& a, void* stream, void* ev0, void* ev1);

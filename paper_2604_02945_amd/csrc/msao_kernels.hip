@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "msao_device.h"
 #include "msao_internal.h"
 
 namespace msao {
@@ -151,35 +152,6 @@ template <> struct Lane<kF32> {
         x[2] = __uint_as_float(v.z); x[3] = __uint_as_float(v.w);
     }
 };
-
-// Active iff NOT(|x| <= tau): NaN is active, -0 is not.
-__device__ __forceinline__ bool active(float x, float tau) { return !(fabsf(x) <= tau); }
-
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-// Two bf16 products summed into an fp32 accumulator (products of bf16 values
-// are exact in fp32).
-__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c)
-{
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
-}
-
-// Activity thresholds on bf16 magnitude bits. A bf16 value widens to a float
-// whose bits are its 16 bits shifted up, so |x| <= tau exactly when the 15
-// magnitude bits are at most lo = bits(tau) >> 16 (NaN and inf lie above).
-// For the high channel of a dword the low channel's bits ride below it, hence
-// hi = lo << 16 | 0xFFFF.
-struct Thr {
-    uint32_t hi, lo;
-};
-
-__device__ __forceinline__ Thr bf16_thresholds(float tau)
-{
-    const uint32_t lo = __float_as_uint(tau) >> 16;
-    return Thr{(lo << 16) | 0xFFFFu, lo};
-}
-
-constexpr uint32_t kBf16OnePair = 0x3F803F80u;  // (1.0, 1.0) in bf16
 
 // Ballot of (low 16 bits of ax) > lo: one 16-bit compare, no masking step.
 __device__ __forceinline__ uint64_t ballot_lo16_gt(uint32_t ax, uint32_t lo)
@@ -359,6 +331,7 @@ __device__ __forceinline__ void tokbuf_flush(const ScoreArgs& a, const DevSeg& s
     }
     if (o.d) o.d[g] = temporal ? b.d : 0u;
     if (o.res) o.res[g] = temporal ? b.res : 0.0f;
+    if (o.sig) o.sig[g] = 0ull;  // a run with SimHash: this pass scores no clip
 }
 
 // A segment that keeps every row is compacted by the scoring pass itself: the
@@ -751,7 +724,7 @@ __global__ __launch_bounds__(kScoreBlock) __attribute__((amdgpu_waves_per_eu(5, 
 {
     const int lane = threadIdx.x & (kWave - 1);
     const int w = uniform(score_block(a) * (kScoreBlock / kWave) + (threadIdx.x >> 6));
-    if (w >= a.t.n_wi) return;
+    if (w >= a.t.n_wi_score) return;
     const int s = uniform(a.t.wi_seg[w]);
     const DevSeg sg = a.t.seg[s];
     const int q = w - sg.wi_begin;
@@ -1694,9 +1667,9 @@ static int launch(void (*kernel)(Args), dim3 grid, dim3 block, size_t lds, void*
 
 int launch_score(const ScoreArgs& a, void* stream, void* ev0, void* ev1)
 {
-    if (a.t.n_wi <= 0) return 0;
+    if (a.t.n_wi_score <= 0) return kNoLaunch;
     const int waves = kScoreBlock / kWave;
-    const unsigned grid = (unsigned)((a.t.n_wi + waves - 1) / waves);
+    const unsigned grid = (unsigned)((a.t.n_wi_score + waves - 1) / waves);
     if (a.learned) {
         if (!a.t.partial_x || !a.t.proj) return (int)hipErrorInvalidValue;  // a learned plan's tables
         return launch(k_score<true>, dim3(grid), dim3(kScoreBlock), 0, stream, a, ev0, ev1);
@@ -1722,7 +1695,7 @@ static int launch_post_nt(const PostArgs& a, int blocks, size_t lds, void* strea
 int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1)
 {
     const int blocks = a.n_req_blocks + a.n_frame_blocks + a.n_sel_blocks;
-    if (blocks <= 0) return 0;
+    if (blocks <= 0) return kNoLaunch;
     const size_t lds = (size_t)(a.keys_cap + cand_cap_for(a.keys_cap)) * sizeof(uint64_t);
     if (a.learned && (!a.t.partial_x || !a.t.head_count || (a.use_mlp && !a.mlp_u))) return (int)hipErrorInvalidValue;
     if (a.learned) return launch_post_nt<kPostBlock, true>(a, a.n_req_blocks + a.n_frame_blocks, lds, stream, ev0, ev1);
@@ -1734,7 +1707,7 @@ int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1)
 int launch_head(const HeadArgs& a, void* stream, void* ev0, void* ev1)
 {
     const int blocks = a.t.n_hb + a.n_mlp_blocks;
-    if (blocks <= 0) return 0;
+    if (blocks <= 0) return kNoLaunch;
     if (a.t.n_hb > 0 && (!a.t.proj || !a.t.head_count || a.max_p < 1 || a.max_p > kMaxHeadFrame))
         return (int)hipErrorInvalidValue;
     if (a.n_mlp_blocks > 0 && (!a.u || !a.mlp.w1 || !a.mlp.b1 || a.mlp.hidden < 1 || a.mlp.hidden > kMaxMlpHidden ||
@@ -1750,7 +1723,7 @@ int launch_head(const HeadArgs& a, void* stream, void* ev0, void* ev1)
 
 int launch_gather(const GatherArgs& a, void* stream, void* ev0, void* ev1)
 {
-    if (a.t.n_gwi <= 0) return 0;
+    if (a.t.n_gwi <= 0) return kNoLaunch;
     const int waves = kGatherBlock / kWave;
     const unsigned grid = (unsigned)((a.t.n_gwi + waves - 1) / waves);
     return launch(k_gather, dim3(grid), dim3(kGatherBlock), 0, stream, a, ev0, ev1);

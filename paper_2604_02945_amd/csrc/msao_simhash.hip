@@ -15,6 +15,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "msao_device.h"
 #include "msao_internal.h"
 
 namespace msao {
@@ -198,6 +199,258 @@ __global__ __launch_bounds__(kHashBlock) void k_simhash(HashArgs a)
     }
 }
 
+// ------------------------------------------------------------ k_clip
+
+constexpr int kClipBlock = 64 * kClipWaves;
+
+// DPP row_ror:n (rotation by n lanes within each 16-lane row).
+template <int N>
+__device__ __forceinline__ int dpp_ror(int v)
+{
+    return __builtin_amdgcn_update_dpp(0, v, 0x120 + N, 0xF, 0xF, false);
+}
+
+// Sum over the 16 lanes of each row; every lane of the row gets a sum (the
+// float sums of different lanes may round differently: read one fixed lane).
+__device__ __forceinline__ float row16_sum(float v)
+{
+    v += __int_as_float(dpp_ror<8>(__float_as_int(v)));
+    v += __int_as_float(dpp_ror<4>(__float_as_int(v)));
+    v += __int_as_float(dpp_ror<2>(__float_as_int(v)));
+    v += __int_as_float(dpp_ror<1>(__float_as_int(v)));
+    return v;
+}
+__device__ __forceinline__ uint32_t row16_sum(uint32_t v)
+{
+    v += (uint32_t)dpp_ror<8>((int)v);
+    v += (uint32_t)dpp_ror<4>((int)v);
+    v += (uint32_t)dpp_ror<2>((int)v);
+    v += (uint32_t)dpp_ror<1>((int)v);
+    return v;
+}
+
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// Per-lane statistics of 16 bytes of a row x against the same bytes of its
+// predecessor pv: active count, L1, L2 and squared difference. For bf16 the
+// active count is kept per 16-bit half: a channel's magnitude bits minus
+// the threshold bits, saturated at 0 and capped at 1, is 1 exactly when it
+// is active (NaN included); a half counts at most C / 32 channels per lane,
+// below 2^16.
+template <int DT>
+__device__ __forceinline__ void clip_stats(const vec4& x, const vec4& pv, float tau, const Thr& th, uint32_t& act,
+                                           float& l1, float& l2, float& res)
+{
+    if constexpr (DT == kBF16) {
+        const u16x2 th2 = {(unsigned short)th.lo, (unsigned short)th.lo};
+        const u16x2 one2 = {1, 1};
+        u16x2 cnt = __builtin_bit_cast(u16x2, act);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const uint32_t xw = x[w], pw = pv[w];
+            const uint32_t ax = xw & 0x7FFF7FFFu;
+            cnt += __builtin_elementwise_min(__builtin_elementwise_sub_sat(__builtin_bit_cast(u16x2, ax), th2), one2);
+            l1 = dot2(ax, kBf16OnePair, l1);
+            l2 = dot2(xw, xw, l2);
+            const float dlo = __uint_as_float(xw << 16) - __uint_as_float(pw << 16);
+            const float dhi = __uint_as_float(xw & 0xFFFF0000u) - __uint_as_float(pw & 0xFFFF0000u);
+            res = fmaf(dlo, dlo, res);
+            res = fmaf(dhi, dhi, res);
+        }
+        act = __builtin_bit_cast(uint32_t, cnt);
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float xf = __uint_as_float(x[e]), pf = __uint_as_float(pv[e]);
+            act += active(xf, tau) ? 1u : 0u;
+            l1 += fabsf(xf);
+            l2 = fmaf(xf, xf, l2);
+            const float df = xf - pf;
+            res = fmaf(df, df, res);
+        }
+    }
+}
+
+// One tile: rows r = 0..nf are frames f0 + r of patch position p (f0 =
+// nf j - 1 with nf <= 15 new frames per tile; frame -1 reads as zero, rows
+// past the tile or the clip too). Per 256-byte
+// chunk of the rows, the wavefront stages its tile in LDS (4 rows x 256
+// contiguous bytes per load), reads each row and its predecessor back for
+// the statistics, and runs the tile through the matrix cores against the
+// block's shared hyperplane chunk, as k_simhash does. Rows 1..nf are the
+// tile's tokens; row 0 only supplies their predecessor. Row groups of four
+// that hold no row of the tile skip the statistics.
+template <int DT, int KT>
+__device__ void clip_tile(const ClipArgs& a, const DevSeg& sg, int item, int lane, uint8_t* rows_lds,
+                          uint8_t* planes_lds, uint32_t& nsp, uint64_t& dsum)
+{
+    constexpr int K = 16 * KT;
+    constexpr int kPieces = K * (kChunk / 16);                      // 16-byte pieces of a hyperplane chunk
+    constexpr int kPlaneLoads = (kPieces + kClipBlock - 1) / kClipBlock;
+    const int m = lane & 15, g = lane >> 4;
+    const bool valid = item < sg.P * sg.ntiles;
+    const int p = valid ? item / sg.ntiles : 0;
+    const int j = valid ? item % sg.ntiles : 0;
+    const int nf = sg.per_item;                          // new frames per tile (the frames split evenly)
+    const int f0 = nf * j - 1;
+    const int r_lo = f0 < 0 ? 1 : 0;                    // row 0 of the first tile: the zero frame
+    const int r_hi = valid ? min(nf + 1, sg.T - f0) : 0; // rows from r_hi on: past the tile or the clip
+    const int rb = sg.nchunk * 16;
+    const int fstride = (int)((int64_t)sg.P * sg.stride_bytes);   // 16 x fstride <= 2^31 - 1 (host check)
+    const int nrows = max(0, r_hi - r_lo);
+    const rsrc_t rx = make_rsrc(sg.data + (int64_t)p * sg.stride_bytes + (int64_t)(f0 + r_lo) * fstride,
+                                nrows > 0 ? (nrows - 1) * fstride + rb : 0);
+    const rsrc_t rr = make_rsrc(sg.planes, K * rb);
+    const float tau = a.t.tau;
+    const Thr th = bf16_thresholds(tau);
+    f32x4 acc[KT];
+#pragma unroll
+    for (int jj = 0; jj < KT; ++jj) acc[jj] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    uint32_t act[4] = {0u, 0u, 0u, 0u};
+    float l1[4] = {0.0f, 0.0f, 0.0f, 0.0f}, l2[4] = {0.0f, 0.0f, 0.0f, 0.0f}, res[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    // load q covers rows 4 q .. 4 q + 3: lane l takes row 4 q + l / 16, bytes 16 (l % 16) .. of the chunk
+    const int lrow = lane >> 4, lcol = (lane & 15) * 16;
+    const int tid = threadIdx.x;
+    auto load_chunk = [&](int c, vec4 (&G)[4], vec4 (&H)[kPlaneLoads]) {
+        const int col = c * kChunk + lcol;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int r = 4 * q + lrow;
+            G[q] = load_row(rx, (col < rb && r >= r_lo && r < r_hi) ? (r - r_lo) * fstride + col : kOutOfRange);
+        }
+#pragma unroll
+        for (int v = 0; v < kPlaneLoads; ++v) {
+            const int pp = tid + kClipBlock * v;
+            const int pc = c * kChunk + (pp & 15) * 16;
+            H[v] = load_plane(rr, (pp < kPieces && pc < rb) ? (pp >> 4) * rb + pc : kOutOfRange);
+        }
+    };
+    const int nchunks = (rb + kChunk - 1) / kChunk;
+    vec4 G[4], H[kPlaneLoads];
+    load_chunk(0, G, H);
+    for (int c = 0; c < nchunks; ++c) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) *reinterpret_cast<vec4*>(rows_lds + (4 * q + lrow) * kLdsPitch + lcol) = G[q];
+#pragma unroll
+        for (int v = 0; v < kPlaneLoads; ++v) {
+            const int pp = tid + kClipBlock * v;
+            if (pp < kPieces)
+                *reinterpret_cast<vec4*>(planes_lds + (pp >> 4) * kLdsPitch + (pp & 15) * 16) = H[v];
+        }
+        __syncthreads();
+        if (c + 1 < nchunks) load_chunk(c + 1, G, H);
+        // statistics: each lane's 16 bytes of rows 4 q + l / 16 against the row above
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (4 * q >= r_hi) break;
+            const int r = 4 * q + lrow;
+            const vec4 x = *reinterpret_cast<const vec4*>(rows_lds + r * kLdsPitch + lcol);
+            const vec4 pv = *reinterpret_cast<const vec4*>(rows_lds + (r > 0 ? r - 1 : 0) * kLdsPitch + lcol);
+            clip_stats<DT>(x, pv, tau, th, act[q], l1[q], l2[q], res[q]);
+        }
+        // one 64-byte column step at a time (the operands of one step live at once)
+#pragma unroll
+        for (int u = 0; u < kSteps; ++u) {
+            const vec4 A = *reinterpret_cast<const vec4*>(rows_lds + m * kLdsPitch + 64 * u + 16 * g);
+#pragma unroll
+            for (int jj = 0; jj < KT; ++jj) {
+                const vec4 B = *reinterpret_cast<const vec4*>(planes_lds + (16 * jj + m) * kLdsPitch + 64 * u + 16 * g);
+                if constexpr (DT == kBF16) {
+                    acc[jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, A),
+                                                                      __builtin_bit_cast(bf16x8, B), acc[jj], 0, 0, 0);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        acc[jj] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(A[e]), __uint_as_float(B[e]),
+                                                                       acc[jj], 0, 0, 0);
+                }
+            }
+        }
+        __syncthreads();  // every wavefront has read the slices before they are rewritten
+    }
+    // signature of row L in lane L < 16: the ballot of result register e of
+    // tile column block jj holds, at bit 16 lg + n, hyperplane 16 jj + n of row 4 lg + e
+    const int lg = (lane & 15) >> 2, le = lane & 3;
+    uint64_t sig = 0;
+#pragma unroll
+    for (int jj = 0; jj < KT; ++jj)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint64_t b = __ballot(acc[jj][e] >= 0.0f);
+            if (g == 0 && le == e) sig |= ((b >> (16 * lg)) & 0xFFFFull) << (16 * jj);
+        }
+    // d against the row above (lane L - 1 holds it)
+    const int up = lane > 0 ? lane - 1 : 0;
+    const uint32_t slo = (uint32_t)__shfl((int)(uint32_t)sig, up), shi = (uint32_t)__shfl((int)(uint32_t)(sig >> 32), up);
+    const uint32_t d = (uint32_t)__popcll(sig ^ (((uint64_t)shi << 32) | slo));
+    // row r = 4 q + g's sums (every lane of row group g holds them): lane r
+    // takes them from lane 16 (r & 3), register q = r >> 2
+    const int src = 16 * (lane & 3), qr = (lane >> 2) & 3;
+    uint32_t A_r = 0u;
+    float L1 = 0.0f, L2 = 0.0f, RS = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const uint32_t aq = (uint32_t)__shfl((int)row16_sum(DT == kBF16 ? (act[q] & 0xFFFFu) + (act[q] >> 16) : act[q]), src);
+        const float l1q = __shfl(row16_sum(l1[q]), src);
+        const float l2q = __shfl(row16_sum(l2[q]), src);
+        const float rq = __shfl(row16_sum(res[q]), src);
+        if (qr == q) {
+            A_r = aq;
+            L1 = l1q;
+            L2 = l2q;
+            RS = rq;
+        }
+    }
+    const int f = f0 + lane;
+    const bool out = valid && lane >= 1 && lane < r_hi;
+    if (out) {
+        const int tk = sg.tok_off + f * sg.P + p;
+        const uint32_t z = (uint32_t)sg.C - A_r;
+        const TokenOut& o = a.tok;
+        if (o.z) o.z[tk] = z;
+        if (o.l1) o.l1[tk] = L1;
+        if (o.l2) o.l2[tk] = L2;
+        if (o.res) o.res[tk] = RS;
+        if (o.d) o.d[tk] = d;
+        if (o.sig) o.sig[tk] = sig;
+        if (o.info) {
+            const float red = sg.lam_s * (float)z * __builtin_amdgcn_rcpf((float)sg.C) +
+                              sg.lam_t * (float)(K - (int)d) * __builtin_amdgcn_rcpf((float)K);
+            o.info[tk] = 1.0f - red;
+        }
+    }
+    nsp += (uint32_t)__popcll(__ballot(out && A_r < (uint32_t)sg.A_s));
+    uint32_t dd = (out && f >= 1) ? d : 0u;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) dd += (uint32_t)__shfl_xor((int)dd, o);
+    dsum += (uint64_t)__shfl((int)dd, 0);
+}
+
+// One block per kClipWaves work items (tiles) of one fused clip; each
+// wavefront writes its work item's integer partials. One instance per
+// element type and signature width, so that each holds only its own
+// accumulators.
+template <int DT, int KT>
+__global__ __launch_bounds__(kClipBlock) void k_clip(ClipArgs a)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t rows_lds[kClipWaves][16 * kLdsPitch];
+    __shared__ __attribute__((aligned(16))) uint8_t planes_lds[16 * KT * kLdsPitch];
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+    const int s = a.t.cl_seg[blockIdx.x];
+    const DevSeg sg = a.t.seg[s];
+    const int item = (blockIdx.x - sg.cl_begin) * kClipWaves + wave;
+    uint32_t nsp = 0;
+    uint64_t dsum = 0;
+    clip_tile<DT, KT>(a, sg, item, lane, rows_lds[wave], planes_lds, nsp, dsum);
+    if (lane == 0 && item < sg.P * sg.ntiles) {
+        Partial pr;
+        pr.nsparse = nsp;
+        pr.pad_ = 0u;
+        pr.dsum = dsum;
+        a.t.partial[sg.wi_begin + item] = pr;
+    }
+}
+
 // ------------------------------------------------------------ k_hash_post
 
 __device__ __forceinline__ uint64_t all_bits(int K) { return K >= 64 ? ~0ull : ((1ull << K) - 1ull); }
@@ -323,15 +576,34 @@ int launch(void (*kernel)(Args), dim3 grid, dim3 block, void* stream, const Args
 
 int launch_simhash(const HashArgs& a, void* stream, void* ev0, void* ev1)
 {
-    if (a.t.n_hi <= 0) return 0;
+    if (a.t.n_hi <= 0) return kNoLaunch;
     if (!a.sig || !a.d) return (int)hipErrorInvalidValue;
     return launch(k_simhash, dim3((unsigned)a.t.n_hi), dim3(kHashBlock), stream, a, ev0, ev1);
+}
+
+int launch_clip(const ClipArgs& a, void* stream, void* ev0, void* ev1)
+{
+    if (a.t.n_cl <= 0) return kNoLaunch;
+    if (!a.tok.z || !a.tok.d || !a.tok.sig || !a.t.cl_seg) return (int)hipErrorInvalidValue;
+    // every fused clip of a run has the same element type and signature width (host check)
+    const dim3 grid((unsigned)a.t.n_cl), block(kClipBlock);
+    switch (a.clip_dtype * 8 + a.clip_bits / 16) {
+    case kBF16 * 8 + 1: return launch(k_clip<kBF16, 1>, grid, block, stream, a, ev0, ev1);
+    case kBF16 * 8 + 2: return launch(k_clip<kBF16, 2>, grid, block, stream, a, ev0, ev1);
+    case kBF16 * 8 + 3: return launch(k_clip<kBF16, 3>, grid, block, stream, a, ev0, ev1);
+    case kBF16 * 8 + 4: return launch(k_clip<kBF16, 4>, grid, block, stream, a, ev0, ev1);
+    case kF32 * 8 + 1: return launch(k_clip<kF32, 1>, grid, block, stream, a, ev0, ev1);
+    case kF32 * 8 + 2: return launch(k_clip<kF32, 2>, grid, block, stream, a, ev0, ev1);
+    case kF32 * 8 + 3: return launch(k_clip<kF32, 3>, grid, block, stream, a, ev0, ev1);
+    case kF32 * 8 + 4: return launch(k_clip<kF32, 4>, grid, block, stream, a, ev0, ev1);
+    default: return (int)hipErrorInvalidValue;
+    }
 }
 
 int launch_hash_post(const HashArgs& a, void* stream, void* ev0, void* ev1)
 {
     const int blocks = a.n_frame_blocks + a.n_req_blocks;
-    if (blocks <= 0) return 0;
+    if (blocks <= 0) return kNoLaunch;
     if (!a.sig || !a.d || (a.n_req_blocks > 0 && !a.temporal && !a.hdsum) || (a.info && !a.z))
         return (int)hipErrorInvalidValue;
     return launch(k_hash_post, dim3((unsigned)blocks), dim3(kHashBlock), stream, a, ev0, ev1);

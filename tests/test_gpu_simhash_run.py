@@ -1,5 +1,6 @@
 """GPU parity of the whole analysis with SimHash as Eq. 5's hash
-(msao_run_simhash) against the oracle (oracle.run with hashes).
+(msao_run_simhash) against the oracle (oracle.run with hashes), through the
+fused clip pass (the default) and through the two-pass path.
 
 Exact cases. Integer activations (|x| <= 3) and hyperplanes (entries -1, 0,
 1) make every projection an integer of magnitude below 2^24, which the
@@ -78,19 +79,19 @@ def hashes_for(segments, planes_of):
     return [planes_of(i, s) if is_temporal(s) else None for i, s in enumerate(segments)]
 
 
-def gpu_run(segments, R, params, hashes, dev, alpha=None, pad=0, compact=True):
+def gpu_run(segments, R, params, hashes, dev, alpha=None, pad=0, compact=True, ctx=None):
     dsegs = to_device(segments, dev, pad)
     dh = [None if h is None else dict(planes=dev_tensor(h["planes"], s.dtype, dev), bits=h["bits"])
           for s, h in zip(segments, hashes)]
-    out, sig = msao.msao_run_simhash(dsegs, R, dh, params, alpha, compact=compact)
+    out, sig = msao.msao_run_simhash(dsegs, R, dh, params, alpha, ctx=ctx, compact=compact)
     torch.cuda.synchronize()
     got = out.results(R, len(segments))
     got["sig"] = sig
     return dsegs, out, got
 
 
-def exact_compare(segments, R, p, hashes, dev, alpha=None, pad=0):
-    dsegs, out, got = gpu_run(segments, R, p, hashes, dev, alpha, pad)
+def exact_compare(segments, R, p, hashes, dev, alpha=None, pad=0, ctx=None):
+    dsegs, out, got = gpu_run(segments, R, p, hashes, dev, alpha, pad, ctx=ctx)
     ref = oracle.run(segments, R, p, alpha, hashes=hashes)
     assert np.array_equal(host(got["sig"]).view(np.uint64), ref["sig"]), "sig"
     compare_scores(segments, R, got, ref)
@@ -128,6 +129,24 @@ def test_exact_mixed_table(K, flags, dtype, dev):
     got, ref = exact_compare(segs, 2, p, hashes, dev, alpha=[0.3, -0.2, 0.5, 0.0, 0.1, 0.0, 0.4, -0.3])
     agg = ref["agg"].reshape(-1, 4)
     assert agg[1 * 4 + VIDEO, 3] == (2 * 64 + 1 * 130) * K   # Qbits in K-bit units
+
+
+@pytest.mark.parametrize("K", [16, 64])
+def test_exact_unfused_path(K, dev, monkeypatch):
+    # MSAO_CLIP_FUSE=0: the clips are scored by k_score and hashed by k_simhash
+    # (two passes over their rows), the path taken when a clip's 16-frame tiles
+    # do not fit a 32-bit buffer resource
+    monkeypatch.setenv("MSAO_CLIP_FUSE", "0")
+    ctx = msao.Context(0)
+    try:
+        for flags in (0, 2):
+            segs, hashes = mixed_int_table(500 + K + flags, K, "bf16")
+            p = default_params()
+            p["flags"] = flags
+            log(f"[simhash-run] unfused path K {K} flags {flags}")
+            exact_compare(segs, 2, p, hashes, dev, ctx=ctx)
+    finally:
+        ctx.close()
 
 
 def test_exact_padded_rows_and_weights(dev):
