@@ -331,7 +331,11 @@ __device__ __forceinline__ void tokbuf_flush(const ScoreArgs& a, const DevSeg& s
     }
     if (o.d) o.d[g] = temporal ? b.d : 0u;
     if (o.res) o.res[g] = temporal ? b.res : 0.0f;
-    if (o.sig) o.sig[g] = 0ull;  // a run with SimHash: this pass scores no clip
+    // a run with SimHash (never learned): this pass scores no clip; the
+    // learned instance leaves the store out, which keeps it from spilling
+    if constexpr (!LR) {
+        if (o.sig) o.sig[g] = 0ull;
+    }
 }
 
 // A segment that keeps every row is compacted by the scoring pass itself: the
