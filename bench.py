@@ -377,6 +377,36 @@ def cpu_baseline(w, budget_s):
             "host_cpu": platform.processor() or platform.machine()}
 
 
+def cpu_baseline_threads(w, budget_s):
+    """The same oracle on up to 16 host threads: requests are independent (one
+    request's MAS, selection and compaction read only its own segments), so
+    each thread runs the unchanged oracle on one request at a time (ctypes
+    releases the interpreter lock during the C call)."""
+    import dataclasses
+    from concurrent.futures import ThreadPoolExecutor
+
+    import oracle
+
+    oracle.lib()
+    jobs = []
+    for r in range(w.n_requests):
+        segs = [dataclasses.replace(s, request=0) for s in w.segments if s.request == r]
+        if segs:
+            jobs.append(segs)
+    threads = max(1, min(16, os.cpu_count() or 1, len(jobs)))
+    runs, t0 = 0, time.perf_counter()
+    with ThreadPoolExecutor(threads) as ex:
+        while True:
+            list(ex.map(lambda segs: oracle.run(segs, 1, w.params, compact=True), jobs))
+            runs += 1
+            if time.perf_counter() - t0 > budget_s:
+                break
+    dt = time.perf_counter() - t0
+    return {"value": w.n_tokens * runs / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"whole workload ({w.n_tokens} tokens) x {runs} runs, its {len(jobs)} requests spread over "
+                      f"{threads} threads of the C oracle, {dt:.1f} s"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -548,6 +578,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        line["cpu_baseline_threads"] = cpu_baseline_threads(w, args.cpu_seconds / 2)
     if not args.no_learned:
         line["learned"] = learned_bench(args, dev, ctxs[0], w, reps, fields)
     if not args.no_simhash:
