@@ -439,3 +439,25 @@ def test_multiple_segments_per_modality_aggregate():
     agg = o["agg"].reshape(-1, 4, 4)[0, IMAGE]
     assert agg[0] == 80 and agg[1] == 50
     assert o["rho"][IMAGE] == np.float32(50 / 80)
+
+
+def test_requests_are_independent():
+    """Each request's outputs depend only on its own segments: running the
+    requests one at a time (as the threaded CPU baseline does) gives the
+    whole table's statistics, MAS, keep counts, kept indices and rows."""
+    import dataclasses
+    w = make_workload(4, n_requests=5)
+    whole = oracle.run(w.segments, w.n_requests, w.params)
+    tok = np.cumsum([0] + [s.n_tokens for s in w.segments])
+    for r in range(w.n_requests):
+        idx = [i for i, s in enumerate(w.segments) if s.request == r]
+        segs = [dataclasses.replace(w.segments[i], request=0) for i in idx]
+        o = oracle.run(segs, 1, w.params)
+        sel = np.concatenate([np.arange(tok[i], tok[i + 1]) for i in idx])
+        for k in ("z", "l1", "l2", "info", "keep", "kept_idx"):
+            assert np.array_equal(o[k], whole[k][sel]), k
+        for k in ("rho", "temporal", "beta", "mas", "present"):
+            assert np.array_equal(o[k], whole[k][r * 4:(r + 1) * 4]), k
+        assert np.array_equal(o["k"], whole["k"][idx])
+        for a, b in zip(o["compact"], [whole["compact"][i] for i in idx]):
+            assert np.array_equal(a, b)
