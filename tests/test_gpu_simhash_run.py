@@ -149,6 +149,26 @@ def test_exact_unfused_path(K, dev, monkeypatch):
         ctx.close()
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_exact_tile_boundaries(dtype, dev):
+    # clips whose frame counts sit at the fused pass's tile boundaries (tiles
+    # of at most 15 new frames, split evenly: 15 = one tile, 16 = 8 + 8,
+    # 17 = 9 + 8, 30 = 15 + 15, 31 = 11 + 10 + 10), positions not a multiple
+    # of the eight tiles per block, one signature width (the fused path)
+    rng = np.random.default_rng(77)
+    C, K = 136 if dtype == "f32" else 144, 48
+    segs = []
+    for r, (T, P) in enumerate([(15, 9), (16, 5), (17, 3), (30, 7), (31, 2), (2, 11)]):
+        segs.append(Segment(r % 3, VIDEO, T, P, C, dtype, [0.3, -1.0, 0.5][r % 3],
+                            encode(int_clip(rng, T, P, C), dtype)))
+    hashes = hashes_for(segs, lambda i, s: dict(planes=int_planes(rng, K, C, dtype), bits=K))
+    for flags in (0, 2):
+        p = default_params()
+        p["flags"] = flags
+        log(f"[simhash-run] tile boundaries {dtype} flags {flags}")
+        exact_compare(segs, 3, p, hashes, dev)
+
+
 def test_exact_padded_rows_and_weights(dev):
     rng = np.random.default_rng(5)
     C = 264
