@@ -76,6 +76,8 @@ def head_bound(s, w_host, grid_w, pool):
     win = np.zeros_like(m)
     for di in range(-r, r + 1):
         for dj in range(-r, r + 1):
+            if abs(di) >= H or abs(dj) >= W:
+                continue  # the shifted window lies outside the grid (and a negative stop would wrap)
             sh = np.full_like(m, 0.0)
             src = m[:, max(0, di):H + min(0, di), max(0, dj):W + min(0, dj)]
             sh[:, max(0, -di):H - max(0, di), max(0, -dj):W - max(0, dj)] = src
@@ -224,6 +226,23 @@ def test_heads_on_video_and_odd_widths(dev):
     log("[learned] video clip, generic widths, fp32; MLP without prompt")
     g, ref = run_case(segs, 3, heads, mlp, dev)
     compare(segs, 3, heads, g, ref, mlp)
+
+
+def test_windows_wider_than_the_grid(dev):
+    # pooling windows of 5 and 7 on grids 1 or 2 patches wide (and 1 row
+    # high): the window is cut to the grid on every side
+    rng = np.random.default_rng(21)
+    segs, heads = [], []
+    for i, (P, W, pool, dtype) in enumerate([(9, 1, 7, "bf16"), (14, 2, 5, "bf16"), (3, 3, 7, "f32"),
+                                             (40, 2, 7, "f32"), (6, 0, 5, "bf16")]):
+        x = rng.standard_normal((P, 200)).astype(np.float32)
+        s = Segment(i % 2, IMAGE if i % 2 == 0 else AUDIO, 1, P, 200, dtype, 0.5,
+                    x if dtype == "f32" else f32_to_bf16_bits(x))
+        segs.append(s)
+        heads.append(make_head(s, rng, W, pool, float(rng.uniform(-0.5, 0.5)))[1])
+    log("[learned] windows wider than the grid")
+    g, ref = run_case(segs, 2, heads, None, dev)
+    compare(segs, 2, heads, g, ref)
 
 
 def test_mlp_without_heads_many_requests(dev):
