@@ -110,7 +110,7 @@ typedef struct {
 
 /* Thresholds and weights (Sec. 5.1.4 defaults from msao_default_params). */
 typedef struct {
-    float tau;                          /* channel activity threshold, >= 0, finite */
+    float tau;                          /* channel activity threshold, >= 0, finite (-0 is 0) */
     float tau_s;                        /* Eq. 4 importance threshold, in [0, 1] */
     float lambda_s[MSAO_NUM_MODALITIES];/* Eq. 7 spatial weight per modality, in [0, 1] */
     float lambda_t[MSAO_NUM_MODALITIES];/* Eq. 7 temporal weight per modality, in [0, 1] */

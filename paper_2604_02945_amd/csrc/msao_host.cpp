@@ -511,7 +511,10 @@ Tables device_tables(const Plan& pl, void* ws, int n, int R, const msao_params* 
     t.n_gwi = pl.n_gwi;
     t.n_tseg = (int)pl.tseg.size();
     t.n_frames = (int)pl.nframes;
-    t.tau = p->tau;
+    // -0 passes the tau >= 0 check; the bf16 kernels take their threshold
+    // from the float's bits, where -0 would read as 0x8000 (above every
+    // magnitude), so it goes down as +0, the same threshold.
+    t.tau = p->tau == 0.0f ? 0.0f : p->tau;
     t.tau_s = p->tau_s;
     for (int m = 0; m < kNumMod; ++m) {
         t.lam_s[m] = p->lambda_s[m];

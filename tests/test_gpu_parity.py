@@ -267,7 +267,8 @@ def test_adversarial(name, dev):
     run_and_compare(segs, R, default_params(), dev)
 
 
-@pytest.mark.parametrize("variant", ["alpha", "literal", "lambda_s0", "lambda_t0", "tau0", "tau_s_extremes"])
+@pytest.mark.parametrize("variant", ["alpha", "literal", "lambda_s0", "lambda_t0", "tau0", "tau_neg0",
+                                     "tau_s_extremes"])
 def test_parameter_variants(variant, dev):
     segs = ADV["guided"] + ADV["video"][:3]
     segs = [Segment(s.request if s.request < 2 else 1, s.modality, s.n_frames, s.tokens_per_frame, s.hidden,
@@ -285,6 +286,8 @@ def test_parameter_variants(variant, dev):
         p["lambda_t"] = [0.0] * 4
     elif variant == "tau0":
         p["tau"] = 0.0
+    elif variant == "tau_neg0":
+        p["tau"] = -0.0   # |x| <= -0 iff |x| <= 0: zeros inactive, the rest active
     elif variant == "tau_s_extremes":
         p["tau_s"] = 1.0
     log(f"[parity] parameter variant {variant}")

@@ -131,6 +131,19 @@ def test_exact_mixed_table(K, flags, dtype, dev):
     assert agg[1 * 4 + VIDEO, 3] == (2 * 64 + 1 * 130) * K   # Qbits in K-bit units
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_exact_negative_zero_threshold(dtype, dev):
+    """tau = -0 is the threshold 0: half of every integer row is exact zeros
+    (inactive), the rest active, in the fused clip pass as in the rest."""
+    segs, hashes = mixed_int_table(77, 32, dtype)
+    p = default_params()
+    p["tau"] = -0.0
+    log(f"[simhash-run] exact mixed table with tau -0 {dtype}")
+    got, ref = exact_compare(segs, 2, p, hashes, dev)
+    z0 = oracle.run(segs, 2, dict(p, tau=0.0), hashes=hashes)["z"]
+    assert np.array_equal(ref["z"], z0)
+
+
 @pytest.mark.parametrize("K", [16, 64])
 def test_exact_unfused_path(K, dev, monkeypatch):
     # MSAO_CLIP_FUSE=0: the clips are scored by k_score and hashed by k_simhash

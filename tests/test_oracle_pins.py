@@ -61,6 +61,17 @@ def test_all_zero_row_is_fully_sparse(tau, dtype):
     assert oracle.token_stats(neg0, "f32", tau)[0] == 0
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_negative_zero_threshold_is_zero(dtype):
+    """|x| <= -0 holds exactly when |x| <= 0: a threshold of -0 keeps every
+    nonzero channel (and NaN) active, the same as +0. (A bf16 threshold taken
+    from the float's bits would see -0 as 0x8000, above every magnitude.)"""
+    x = f32([0.0, -0.0, 1e-30, -2.5, np.nan, np.inf, 0.0, 3.0])
+    row = x if dtype == "f32" else f32_to_bf16_bits(x)
+    a_neg = oracle.token_stats(row, dtype, -0.0)[0]
+    assert a_neg == oracle.token_stats(row, dtype, 0.0)[0] == 5
+
+
 def test_activity_boundary_is_inclusive_and_nan_active():
     tau = np.float32(0.1)
     above = np.nextafter(tau, np.float32(1))
