@@ -11,6 +11,13 @@
 namespace msao {
 namespace {
 
+// A value every lane of the wavefront holds, moved to a scalar register so
+// that what is derived from it (buffer descriptors, loop bounds, branches)
+// stays scalar: the compiler treats anything computed from threadIdx as
+// varying per lane, and a per-lane buffer descriptor costs a loop of
+// readfirstlanes around every load.
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
 // Active iff NOT(|x| <= tau): NaN is active, -0 is not.
 __device__ __forceinline__ bool active(float x, float tau) { return !(fabsf(x) <= tau); }
 

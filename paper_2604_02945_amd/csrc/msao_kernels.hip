@@ -27,8 +27,6 @@ namespace {
 
 constexpr int kWave = 64;
 
-__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
-
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float v)
 {

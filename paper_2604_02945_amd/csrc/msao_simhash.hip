@@ -75,7 +75,7 @@ __device__ void hash_tile(const HashArgs& a, const DevSeg& sg, int r0, int lane,
     constexpr int K = 16 * KT;
     constexpr int kPlaneLoads = K / 16;           // 16-byte pieces of the chunk's hyperplanes per thread
     const int m = lane & 15, g = lane >> 4;
-    const int rows = max(0, min(kHashTokens, sg.n_tok - r0));   // a tile past the end: no rows
+    const int rows = uniform(max(0, min(kHashTokens, sg.n_tok - r0)));   // a tile past the end: no rows
     const int rb = sg.nchunk * 16;                       // row bytes
     const int pitch = (int)sg.stride_bytes;              // < 64 MiB (host check)
     const rsrc_t rx = make_rsrc(sg.data + (int64_t)min(r0, sg.n_tok) * sg.stride_bytes, rows * pitch);
@@ -168,7 +168,7 @@ __global__ __launch_bounds__(kHashBlock) void k_simhash(HashArgs a)
 {
     __shared__ __attribute__((aligned(16))) uint8_t rows_lds[kHashWaves][kHashTokens * kLdsPitch];
     __shared__ __attribute__((aligned(16))) uint8_t planes_lds[64 * kLdsPitch];
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & (kWave - 1), wave = uniform(threadIdx.x >> 6);
     const int b = blockIdx.x;
     const int s = a.t.hi_seg[b];
     const DevSeg sg = a.t.seg[s];
@@ -435,7 +435,7 @@ __global__ __launch_bounds__(kClipBlock) void k_clip(ClipArgs a)
 {
     __shared__ __attribute__((aligned(16))) uint8_t rows_lds[kClipWaves][16 * kLdsPitch];
     __shared__ __attribute__((aligned(16))) uint8_t planes_lds[16 * KT * kLdsPitch];
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & (kWave - 1), wave = uniform(threadIdx.x >> 6);
     const int s = a.t.cl_seg[blockIdx.x];
     const DevSeg sg = a.t.seg[s];
     const int item = (blockIdx.x - sg.cl_begin) * kClipWaves + wave;
