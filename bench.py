@@ -121,19 +121,20 @@ def committed_traffic(config):
     """HBM bytes per k_score launch on the tri-modal workload (committed counters)."""
     if config != 4:
         return None
-    return _committed("k_score_trimodal_traffic.json", ("msao_kernels.hip", "msao_internal.h"))
+    return _committed("k_score_trimodal_traffic.json", ("msao_kernels.hip", "msao_device.h", "msao_internal.h"))
 
 
 def committed_learned_traffic(config):
     """HBM bytes per learned k_score launch on the tri-modal workload (committed counters)."""
     if config != 4:
         return None
-    return _committed("k_score_learned_trimodal_traffic.json", ("msao_kernels.hip", "msao_internal.h"))
+    return _committed("k_score_learned_trimodal_traffic.json",
+                      ("msao_kernels.hip", "msao_device.h", "msao_internal.h"))
 
 
 def committed_simhash_traffic():
     """HBM bytes per k_simhash launch on the video clips (committed counters)."""
-    return _committed("k_simhash_video_traffic.json", ("msao_simhash.hip", "msao_internal.h"))
+    return _committed("k_simhash_video_traffic.json", ("msao_simhash.hip", "msao_device.h", "msao_internal.h"))
 
 
 def committed_entropy_traffic():

@@ -233,7 +233,10 @@ constexpr int kMlpGroup = 8;          // requests per wavefront in the prompt pr
 // 15, the clip's frames split evenly; the first tile starts at the all-zero
 // frame -1): z, l1, l2, res, the signature, d against the previous frame and
 // the informativeness of those tokens, and the work item's integer partials.
-constexpr int kClipWaves = 8;
+#ifndef MSAO_CLIP_WAVES
+#define MSAO_CLIP_WAVES 4
+#endif
+constexpr int kClipWaves = MSAO_CLIP_WAVES;      // tiles (wavefronts) per block: 4 or 8
 constexpr int kClipFrames = 15;                 // most new frames per tile (16 rows with the predecessor)
 struct ClipArgs {
     Tables t;

@@ -203,6 +203,12 @@ __global__ __launch_bounds__(kHashBlock) void k_simhash(HashArgs a)
 
 constexpr int kClipBlock = 64 * kClipWaves;
 
+// Hyperplane slices per block: two (used in turn, one barrier per chunk)
+// for K <= 32, where the block's LDS stays small enough for four 4-wavefront
+// blocks per CU; one (and a second barrier per chunk) for K = 48 and 64.
+template <int KT>
+constexpr int kClipPlaneBufs = KT <= 2 ? 2 : 1;
+
 // DPP row_ror:n (rotation by n lanes within each 16-lane row).
 template <int N>
 __device__ __forceinline__ int dpp_ror(int v)
@@ -231,29 +237,56 @@ __device__ __forceinline__ uint32_t row16_sum(uint32_t v)
 
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 
-// Per-lane statistics of 16 bytes of a row x against the same bytes of its
-// predecessor pv: active count, L1, L2 and squared difference. For bf16 the
-// active count is kept per 16-bit half: a channel's magnitude bits minus
-// the threshold bits, saturated at 0 and capped at 1, is 1 exactly when it
-// is active (NaN included); a half counts at most C / 32 channels per lane,
-// below 2^16.
+// The channels of 16 bytes of a row widened to floats: the low and high
+// halves of each dword for bf16 (8 channels), the dwords for fp32 (4).
+struct Wide {
+    float v[8];
+};
+
 template <int DT>
-__device__ __forceinline__ void clip_stats(const vec4& x, const vec4& pv, float tau, const Thr& th, uint32_t& act,
+__device__ __forceinline__ Wide widen(const vec4& x)
+{
+    Wide w;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if constexpr (DT == kBF16) {
+            w.v[2 * k] = __uint_as_float(x[k] << 16);
+            w.v[2 * k + 1] = __uint_as_float(x[k] & 0xFFFF0000u);
+        } else {
+            w.v[k] = __uint_as_float(x[k]);
+        }
+    }
+    return w;
+}
+
+// Per-lane statistics of 16 bytes of a row x against the same bytes of its
+// predecessor, given widened in pw (on return pw holds x widened, the
+// predecessor of the next row): active count, L1, L2 and squared
+// difference. For bf16 the active count is kept per 16-bit half: the
+// threshold bits minus a channel's magnitude bits, both below 2^15 (tau is
+// finite and not -0), wrap below zero, setting bit 15, exactly when the
+// channel is active (NaN included); the bit shifted down is added to the
+// half's count, which counts at most C / 32 channels per lane, below 2^16.
+// (Written as a saturating subtraction capped at 1, the compiler turns it
+// into a compare and select per half.)
+template <int DT>
+__device__ __forceinline__ void clip_stats(const vec4& x, Wide& pw, float tau, const Thr& th, uint32_t& act,
                                            float& l1, float& l2, float& res)
 {
+    const Wide xw = widen<DT>(x);
     if constexpr (DT == kBF16) {
         const u16x2 th2 = {(unsigned short)th.lo, (unsigned short)th.lo};
-        const u16x2 one2 = {1, 1};
+        const u16x2 sh15 = {15, 15};
         u16x2 cnt = __builtin_bit_cast(u16x2, act);
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-            const uint32_t xw = x[w], pw = pv[w];
-            const uint32_t ax = xw & 0x7FFF7FFFu;
-            cnt += __builtin_elementwise_min(__builtin_elementwise_sub_sat(__builtin_bit_cast(u16x2, ax), th2), one2);
+            const uint32_t xv = x[w];
+            const uint32_t ax = xv & 0x7FFF7FFFu;
+            cnt += (th2 - __builtin_bit_cast(u16x2, ax)) >> sh15;
             l1 = dot2(ax, kBf16OnePair, l1);
-            l2 = dot2(xw, xw, l2);
-            const float dlo = __uint_as_float(xw << 16) - __uint_as_float(pw << 16);
-            const float dhi = __uint_as_float(xw & 0xFFFF0000u) - __uint_as_float(pw & 0xFFFF0000u);
+            l2 = dot2(xv, xv, l2);
+            const float dlo = xw.v[2 * w] - pw.v[2 * w];
+            const float dhi = xw.v[2 * w + 1] - pw.v[2 * w + 1];
             res = fmaf(dlo, dlo, res);
             res = fmaf(dhi, dhi, res);
         }
@@ -261,14 +294,15 @@ __device__ __forceinline__ void clip_stats(const vec4& x, const vec4& pv, float 
     } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const float xf = __uint_as_float(x[e]), pf = __uint_as_float(pv[e]);
+            const float xf = xw.v[e];
             act += active(xf, tau) ? 1u : 0u;
             l1 += fabsf(xf);
             l2 = fmaf(xf, xf, l2);
-            const float df = xf - pf;
+            const float df = xf - pw.v[e];
             res = fmaf(df, df, res);
         }
     }
+    pw = xw;
 }
 
 // One tile: rows r = 0..nf are frames f0 + r of patch position p (f0 =
@@ -278,8 +312,10 @@ __device__ __forceinline__ void clip_stats(const vec4& x, const vec4& pv, float 
 // contiguous bytes per load), reads each row and its predecessor back for
 // the statistics, and runs the tile through the matrix cores against the
 // block's shared hyperplane chunk, as k_simhash does. Rows 1..nf are the
-// tile's tokens; row 0 only supplies their predecessor. Row groups of four
-// that hold no row of the tile skip the statistics.
+// tile's tokens; row 0 only supplies their predecessor. For the statistics
+// lane group g (lanes 16 g ..) takes rows g rpg .. g rpg + rpg - 1, rpg =
+// ceil(r_hi / 4), so that each row's predecessor is the row before it in the
+// same lanes (read and widened once) and rows past the tile are skipped.
 template <int DT, int KT>
 __device__ void clip_tile(const ClipArgs& a, const DevSeg& sg, int item, int lane, uint8_t* rows_lds,
                           uint8_t* planes_lds, uint32_t& nsp, uint64_t& dsum)
@@ -310,6 +346,8 @@ __device__ void clip_tile(const ClipArgs& a, const DevSeg& sg, int item, int lan
     float l1[4] = {0.0f, 0.0f, 0.0f, 0.0f}, l2[4] = {0.0f, 0.0f, 0.0f, 0.0f}, res[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     // load q covers rows 4 q .. 4 q + 3: lane l takes row 4 q + l / 16, bytes 16 (l % 16) .. of the chunk
     const int lrow = lane >> 4, lcol = (lane & 15) * 16;
+    const int rpg = (r_hi + 3) >> 2;                    // statistics rows per lane group (<= 4)
+    const int rg0 = lrow * rpg;                          // the group's first row (rg0 + rpg - 1 <= 15)
     const int tid = threadIdx.x;
     auto load_chunk = [&](int c, vec4 (&G)[4], vec4 (&H)[kPlaneLoads]) {
         const int col = c * kChunk + lcol;
@@ -329,24 +367,28 @@ __device__ void clip_tile(const ClipArgs& a, const DevSeg& sg, int item, int lan
     vec4 G[4], H[kPlaneLoads];
     load_chunk(0, G, H);
     for (int c = 0; c < nchunks; ++c) {
+        // the wavefront's own row slice: rewritten only after its own reads
+        // of the previous chunk (one wavefront's LDS operations run in order)
 #pragma unroll
         for (int q = 0; q < 4; ++q) *reinterpret_cast<vec4*>(rows_lds + (4 * q + lrow) * kLdsPitch + lcol) = G[q];
+        uint8_t* const pl = planes_lds + (kClipPlaneBufs<KT> == 2 ? (c & 1) : 0) * (16 * KT * kLdsPitch);
 #pragma unroll
         for (int v = 0; v < kPlaneLoads; ++v) {
             const int pp = tid + kClipBlock * v;
             if (pp < kPieces)
-                *reinterpret_cast<vec4*>(planes_lds + (pp >> 4) * kLdsPitch + (pp & 15) * 16) = H[v];
+                *reinterpret_cast<vec4*>(pl + (pp >> 4) * kLdsPitch + (pp & 15) * 16) = H[v];
         }
         __syncthreads();
         if (c + 1 < nchunks) load_chunk(c + 1, G, H);
-        // statistics: each lane's 16 bytes of rows 4 q + l / 16 against the row above
+        // statistics: each lane's 16 bytes of rows rg0 + i against the row above
+        if (rpg > 0) {
+            Wide pw = widen<DT>(*reinterpret_cast<const vec4*>(rows_lds + (rg0 > 0 ? rg0 - 1 : 0) * kLdsPitch + lcol));
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            if (4 * q >= r_hi) break;
-            const int r = 4 * q + lrow;
-            const vec4 x = *reinterpret_cast<const vec4*>(rows_lds + r * kLdsPitch + lcol);
-            const vec4 pv = *reinterpret_cast<const vec4*>(rows_lds + (r > 0 ? r - 1 : 0) * kLdsPitch + lcol);
-            clip_stats<DT>(x, pv, tau, th, act[q], l1[q], l2[q], res[q]);
+            for (int i = 0; i < 4; ++i) {
+                if (i >= rpg) break;
+                const vec4 x = *reinterpret_cast<const vec4*>(rows_lds + (rg0 + i) * kLdsPitch + lcol);
+                clip_stats<DT>(x, pw, tau, th, act[i], l1[i], l2[i], res[i]);
+            }
         }
         // one 64-byte column step at a time (the operands of one step live at once)
 #pragma unroll
@@ -354,7 +396,7 @@ __device__ void clip_tile(const ClipArgs& a, const DevSeg& sg, int item, int lan
             const vec4 A = *reinterpret_cast<const vec4*>(rows_lds + m * kLdsPitch + 64 * u + 16 * g);
 #pragma unroll
             for (int jj = 0; jj < KT; ++jj) {
-                const vec4 B = *reinterpret_cast<const vec4*>(planes_lds + (16 * jj + m) * kLdsPitch + 64 * u + 16 * g);
+                const vec4 B = *reinterpret_cast<const vec4*>(pl + (16 * jj + m) * kLdsPitch + 64 * u + 16 * g);
                 if constexpr (DT == kBF16) {
                     acc[jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, A),
                                                                       __builtin_bit_cast(bf16x8, B), acc[jj], 0, 0, 0);
@@ -366,7 +408,10 @@ __device__ void clip_tile(const ClipArgs& a, const DevSeg& sg, int item, int lan
                 }
             }
         }
-        __syncthreads();  // every wavefront has read the slices before they are rewritten
+        // with one hyperplane slice, every wavefront has read it before it is
+        // rewritten; with two, the next chunk writes the other one, and the
+        // one after waits for the barrier above
+        if constexpr (kClipPlaneBufs<KT> == 1) __syncthreads();
     }
     // signature of row L in lane L < 16: the ballot of result register e of
     // tile column block jj holds, at bit 16 lg + n, hyperplane 16 jj + n of row 4 lg + e
@@ -383,9 +428,11 @@ __device__ void clip_tile(const ClipArgs& a, const DevSeg& sg, int item, int lan
     const int up = lane > 0 ? lane - 1 : 0;
     const uint32_t slo = (uint32_t)__shfl((int)(uint32_t)sig, up), shi = (uint32_t)__shfl((int)(uint32_t)(sig >> 32), up);
     const uint32_t d = (uint32_t)__popcll(sig ^ (((uint64_t)shi << 32) | slo));
-    // row r = 4 q + g's sums (every lane of row group g holds them): lane r
-    // takes them from lane 16 (r & 3), register q = r >> 2
-    const int src = 16 * (lane & 3), qr = (lane >> 2) & 3;
+    // row r's sums (every lane of its group holds them): group gr = r / rpg,
+    // register r - gr rpg; lane r takes them from lane 16 gr
+    const int rp = max(rpg, 1), lr = lane & 15;
+    const int gr = min(lr / rp, 3), qr = lr - gr * rp;
+    const int src = 16 * gr;
     uint32_t A_r = 0u;
     float L1 = 0.0f, L2 = 0.0f, RS = 0.0f;
 #pragma unroll
@@ -430,11 +477,14 @@ __device__ void clip_tile(const ClipArgs& a, const DevSeg& sg, int item, int lan
 // wavefront writes its work item's integer partials. One instance per
 // element type and signature width, so that each holds only its own
 // accumulators.
+#ifndef MSAO_CLIP_WPE
+#define MSAO_CLIP_WPE 1
+#endif
 template <int DT, int KT>
-__global__ __launch_bounds__(kClipBlock) void k_clip(ClipArgs a)
+__global__ __launch_bounds__(kClipBlock) __attribute__((amdgpu_waves_per_eu(MSAO_CLIP_WPE, 8))) void k_clip(ClipArgs a)
 {
     __shared__ __attribute__((aligned(16))) uint8_t rows_lds[kClipWaves][16 * kLdsPitch];
-    __shared__ __attribute__((aligned(16))) uint8_t planes_lds[16 * KT * kLdsPitch];
+    __shared__ __attribute__((aligned(16))) uint8_t planes_lds[kClipPlaneBufs<KT> * 16 * KT * kLdsPitch];
     const int lane = threadIdx.x & (kWave - 1), wave = uniform(threadIdx.x >> 6);
     const int s = a.t.cl_seg[blockIdx.x];
     const DevSeg sg = a.t.seg[s];
