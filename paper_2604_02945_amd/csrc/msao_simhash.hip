@@ -480,15 +480,28 @@ __device__ void clip_tile(const ClipArgs& a, const DevSeg& sg, int item, int lan
 #ifndef MSAO_CLIP_WPE
 #define MSAO_CLIP_WPE 1
 #endif
+// Block order: with 1 (the default) consecutive blocks of the plan run on
+// one XCD. The hardware deals blocks to the 8 XCDs in turn, so in plan order
+// the tiles of neighbouring patch positions sit in different L2s and their
+// 4-byte outputs, a frame stride apart, leave as partial lines (5x the
+// output bytes at L2 on the video clips; with the remap, 1.0x).
+#ifndef MSAO_CLIP_XCD
+#define MSAO_CLIP_XCD 1
+#endif
 template <int DT, int KT>
 __global__ __launch_bounds__(kClipBlock) __attribute__((amdgpu_waves_per_eu(MSAO_CLIP_WPE, 8))) void k_clip(ClipArgs a)
 {
     __shared__ __attribute__((aligned(16))) uint8_t rows_lds[kClipWaves][16 * kLdsPitch];
     __shared__ __attribute__((aligned(16))) uint8_t planes_lds[kClipPlaneBufs<KT> * 16 * KT * kLdsPitch];
     const int lane = threadIdx.x & (kWave - 1), wave = uniform(threadIdx.x >> 6);
-    const int s = a.t.cl_seg[blockIdx.x];
+    int blk = blockIdx.x;
+    if (MSAO_CLIP_XCD) {  // a bijection of [0, nb): XCD x gets the x-th run of consecutive blocks
+        const int nb = gridDim.x, x = blk & 7, per = nb >> 3, rem = nb & 7;
+        blk = x * per + min(x, rem) + (blk >> 3);
+    }
+    const int s = a.t.cl_seg[blk];
     const DevSeg sg = a.t.seg[s];
-    const int item = (blockIdx.x - sg.cl_begin) * kClipWaves + wave;
+    const int item = (blk - sg.cl_begin) * kClipWaves + wave;
     uint32_t nsp = 0;
     uint64_t dsum = 0;
     clip_tile<DT, KT>(a, sg, item, lane, rows_lds[wave], planes_lds, nsp, dsum);

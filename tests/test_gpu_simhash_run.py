@@ -167,7 +167,7 @@ def test_exact_tile_boundaries(dtype, dev):
     # clips whose frame counts sit at the fused pass's tile boundaries (tiles
     # of at most 15 new frames, split evenly: 15 = one tile, 16 = 8 + 8,
     # 17 = 9 + 8, 30 = 15 + 15, 31 = 11 + 10 + 10), positions not a multiple
-    # of the eight tiles per block, one signature width (the fused path)
+    # of the tiles per block, one signature width (the fused path)
     rng = np.random.default_rng(77)
     C, K = 136 if dtype == "f32" else 144, 48
     segs = []
@@ -180,6 +180,27 @@ def test_exact_tile_boundaries(dtype, dev):
         p["flags"] = flags
         log(f"[simhash-run] tile boundaries {dtype} flags {flags}")
         exact_compare(segs, 3, p, hashes, dev)
+
+
+def test_exact_every_tile_height(dev):
+    # clips of 2..17 frames: a tile holds r = 3..16 rows (its new frames and
+    # their predecessor), and the statistics give each 16-lane group
+    # ceil(r / 4) consecutive rows, so every group height (1..4) and every
+    # split of the rows over the groups occurs; both element types, every
+    # signature width
+    for T in range(2, 18):
+        rng = np.random.default_rng(300 + T)
+        dtype = "bf16" if T % 2 == 0 else "f32"
+        K = [16, 32, 48, 64][T % 4]
+        C = [8, 40, 200, 72][T % 4]
+        P = 1 + T % 7
+        segs = [Segment(0, VIDEO, T, P, C, dtype, 0.4, encode(int_clip(rng, T, P, C), dtype)),
+                Segment(1, VIDEO, T, 5, C, dtype, -1.0, encode(int_clip(rng, T, 5, C), dtype))]
+        hashes = hashes_for(segs, lambda i, s: dict(planes=int_planes(rng, K, C, dtype), bits=K))
+        p = default_params()
+        p["flags"] = T % 3
+        log(f"[simhash-run] tile height T {T} {dtype} K {K} C {C}")
+        exact_compare(segs, 2, p, hashes, dev)
 
 
 def test_exact_padded_rows_and_weights(dev):
