@@ -790,6 +790,8 @@ void msao_destroy(msao_ctx* ctx)
     delete ctx;
 }
 
+static_assert(kClipWaves == 4 || kClipWaves == 8, "k_clip is built and tested with 4 or 8 tiles per block");
+
 msao_status msao_set_profiling(msao_ctx* ctx, int enable)
 {
     if (!ctx) return MSAO_ERR_INVALID_ARG;

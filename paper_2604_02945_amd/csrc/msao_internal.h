@@ -237,7 +237,6 @@ constexpr int kMlpGroup = 8;          // requests per wavefront in the prompt pr
 #define MSAO_CLIP_WAVES 4
 #endif
 constexpr int kClipWaves = MSAO_CLIP_WAVES;      // tiles (wavefronts) per block: 4 or 8
-static_assert(kClipWaves == 4 || kClipWaves == 8, "k_clip is built and tested with 4 or 8 tiles per block");
 constexpr int kClipFrames = 15;                 // most new frames per tile (16 rows with the predecessor)
 struct ClipArgs {
     Tables t;
