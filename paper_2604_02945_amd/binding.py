@@ -428,7 +428,9 @@ class Plan:
     """msao_plan: the tables of one segment table uploaded once into the
     workspace of `outputs`; each call enqueues the three launches of msao_run
     with no host-to-device copy. The segments' input buffers and `outputs`
-    must outlive the plan."""
+    must outlive the plan. The upload is enqueued on `stream` (the current
+    stream when None) and waited for before the constructor returns, so runs
+    may then be launched on any stream."""
 
     def __init__(self, segments: Sequence[DeviceSegment], n_requests: int, outputs: Outputs,
                  params: Optional[dict] = None, alpha: Optional[Sequence[float]] = None,
@@ -447,10 +449,13 @@ class Plan:
         o = self.outputs = outputs
         self.compact = compact and o.out is not None
         h = ctypes.c_void_p()
+        up = stream if stream is not None else torch.cuda.current_stream(device)
         _check(lib().msao_plan_create(self.ctx.handle, self.segt, n, R, _addr(self.prm), self.al,
                                       o.out_off if self.compact else None, _ptr(o.workspace),
-                                      ctypes.c_size_t(o.ws_bytes), _stream_ptr(stream), ctypes.byref(h)), self.ctx)
+                                      ctypes.c_size_t(o.ws_bytes), _stream_ptr(up), ctypes.byref(h)), self.ctx)
         self.handle = h
+        # the tables must be in the workspace before a run on another stream reads them
+        up.synchronize()
         self.segments = list(segments)
         self._args = [h, _addr(o.c_tok), _addr(o.c_frm), _addr(o.c_req), _addr(o.c_sel),
                       _ptr(o.out) if self.compact else None,
