@@ -231,6 +231,33 @@ msao_status msao_run(msao_ctx* ctx, const msao_segment* segs, int n, int n_reque
                      const msao_select_out* sel, void* out, const int64_t* out_byte_off, int64_t out_bytes,
                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- msao_run for callers that cannot allocate device memory -------------- */
+
+/* Limits of msao_run_noalloc: its scratch (per-call tables, then one 16-byte
+ * integer partial per scoring work item) and, within it, its tables. */
+#define MSAO_NOALLOC_SCRATCH_BYTES 16777216
+#define MSAO_NOALLOC_TABLE_BYTES 2097152
+
+/* msao_run with no workspace argument, for callers that cannot call hipMalloc
+ * or anything that allocates device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid it): it allocates nothing, host
+ * pinned memory included. Its scratch is the library's own array of
+ * MSAO_NOALLOC_SCRATCH_BYTES, one per GPU, held from the first msao_create on
+ * that GPU until the process ends; msao_create also reserves the context's
+ * pinned staging for tables of up to MSAO_NOALLOC_TABLE_BYTES. Every other
+ * argument, the outputs and the errors are those of msao_run, plus
+ * MSAO_ERR_UNSUPPORTED (nothing enqueued) when the call's tables or scratch
+ * exceed those limits (msao_workspace_size bounds the scratch a table needs;
+ * the five benchmark workloads need at most about 4.4 MB). Every call on a
+ * GPU shares that GPU's array and overwrites all of it that the call uses
+ * before reading it: calls that overlap on one GPU (other streams, other
+ * contexts, other threads) race on it and must be ordered by the caller. */
+msao_status msao_run_noalloc(msao_ctx* ctx, const msao_segment* segs, int n, int n_requests,
+                             const msao_params* params, const float* alpha,
+                             const msao_token_out* tok, const msao_frame_out* frm, const msao_req_out* req,
+                             const msao_select_out* sel, void* out, const int64_t* out_byte_off, int64_t out_bytes,
+                             void* stream);
+
 /* ---- plans: tables uploaded once, runs with no host-to-device copy -------- */
 
 /* A plan holds the per-call tables of msao_run (offsets, work items, integer

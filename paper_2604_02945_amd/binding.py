@@ -127,6 +127,8 @@ SIGNATURES = [
                                     ctypes.c_size_t, _P]),
     ("msao_run", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P,
                                 ctypes.c_int64, _P, ctypes.c_size_t, _P]),
+    ("msao_run_noalloc", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P,
+                                        ctypes.c_int64, _P]),
     ("msao_plan_create", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, ctypes.c_size_t, _P,
                                         ctypes.POINTER(_P)]),
     ("msao_plan_run", ctypes.c_int, [_P, _P, _P, _P, _P, _P, ctypes.c_int64, _P]),
@@ -315,7 +317,8 @@ class Outputs:
     """Device buffers of every output of the analysis for one segment table."""
 
     def __init__(self, segments: Sequence[DeviceSegment], n_requests: int, device=None,
-                 token_fields=("z", "l1", "l2", "info", "d", "res"), compact: bool = True):
+                 token_fields=("z", "l1", "l2", "info", "d", "res"), compact: bool = True,
+                 workspace: bool = True):
         device = device or _device_of(segments)
         ntok, nfr, ws = sizes(segments, n_requests)
         self.ntok, self.nframes, self.ws_bytes = ntok, nfr, ws
@@ -330,7 +333,8 @@ class Outputs:
                     "mas": e(R * NMOD, torch.float32), "present": e(R * NMOD, torch.uint8)}
         self.sel = {"keep": e(ntok, torch.uint8), "kept_idx": e(ntok, torch.int32),
                     "kept_count": e(n, torch.int32)}
-        self.workspace = _workspace(ws, device)
+        # msao_run_noalloc takes no workspace (workspace=False leaves it out)
+        self.workspace = _workspace(ws, device) if workspace else None
         self.out = None
         self.out_off = None
         if compact:
@@ -405,6 +409,12 @@ def prepare(entry: str, segments: Sequence[DeviceSegment], n_requests: int, outp
         ob = ctypes.c_int64(o.out_bytes if out is not None else 0)
         args = [ctx.handle, segt, n, R, _addr(prm), al, _addr(o.c_tok), _addr(o.c_frm), _addr(o.c_req),
                 _addr(o.c_sel), out, off, ob, ws, wsb, None]
+    elif entry == "msao_run_noalloc":
+        out = _ptr(o.out) if (compact and o.out is not None) else None
+        off = o.out_off if (compact and o.out is not None) else None
+        ob = ctypes.c_int64(o.out_bytes if out is not None else 0)
+        args = [ctx.handle, segt, n, R, _addr(prm), al, _addr(o.c_tok), _addr(o.c_frm), _addr(o.c_req),
+                _addr(o.c_sel), out, off, ob, None]
     elif entry == "msao_mas_score":
         args = [ctx.handle, segt, n, R, _addr(prm), al, _addr(o.c_tok), _addr(o.c_frm), _addr(o.c_req),
                 ws, wsb, None]
@@ -574,6 +584,14 @@ def msao_compact(segments, outputs, ctx=None, stream=None):
 def msao_run(segments, n_requests, params=None, alpha=None, ctx=None, outputs=None, stream=None, compact=True):
     """Scoring, MAS, selection and compaction in one call."""
     return _one_shot("msao_run", segments, n_requests, params, alpha, ctx, outputs, stream, compact=compact)
+
+
+def msao_run_noalloc(segments, n_requests, params=None, alpha=None, ctx=None, outputs=None, stream=None,
+                     compact=True):
+    """msao_run on the library's own scratch (no workspace; the call
+    allocates nothing). `outputs` may be built with workspace=False."""
+    return _one_shot("msao_run_noalloc", segments, n_requests, params, alpha, ctx, outputs, stream,
+                     compact=compact)
 
 
 def compacted_rows(segments: Sequence[DeviceSegment], outputs: Outputs, kept_count) -> list:

@@ -420,6 +420,12 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
     }
 }
 
+#define MSAO_TRY(x)                                                                                                   \
+    do {                                                                                                              \
+        msao_status st_ = (x);                                                                                        \
+        if (st_ != MSAO_OK) return st_;                                                                               \
+    } while (0)
+
 msao_status hip_fail(msao_ctx* ctx, hipError_t e, const char* what)
 {
     ctx->err = std::string(what) + ": " + hipGetErrorString(e);
@@ -439,24 +445,34 @@ struct DeviceGuard {
     }
 };
 
-// Copy the tables into a pinned slot and enqueue its upload into the workspace.
-msao_status upload(msao_ctx* ctx, const Plan& pl, void* ws, hipStream_t stream)
+// Pinned staging slot `slot` of at least `bytes` (grown when smaller).
+msao_status reserve_stage(msao_ctx* ctx, int slot, size_t bytes)
+{
+    if (ctx->stage_cap[slot] >= bytes) return MSAO_OK;
+    if (ctx->stage[slot]) (void)hipHostFree(ctx->stage[slot]);
+    ctx->stage[slot] = nullptr;
+    ctx->stage_cap[slot] = 0;
+    const size_t cap = align_up(std::max<size_t>(bytes, 65536), 65536);
+    const hipError_t e = hipHostMalloc(&ctx->stage[slot], cap, hipHostMallocDefault);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipHostMalloc");
+    ctx->stage_cap[slot] = cap;
+    return MSAO_OK;
+}
+
+// Copy the tables into a pinned slot and enqueue its upload into the
+// workspace. With grow false a slot smaller than the tables is an error
+// instead of a new pinned allocation (msao_run_noalloc allocates nothing).
+msao_status upload(msao_ctx* ctx, const Plan& pl, void* ws, hipStream_t stream, bool grow = true)
 {
     const int slot = ctx->next_slot;
-    ctx->next_slot ^= 1;
     hipError_t e;
+    if (!grow && ctx->stage_cap[slot] < pl.table_bytes)
+        return fail(&ctx->err, MSAO_ERR_UNSUPPORTED, "per-call tables larger than the context's reserved staging");
+    ctx->next_slot ^= 1;
     if (ctx->stage_used[slot]) {
         if ((e = hipEventSynchronize(ctx->stage_ev[slot])) != hipSuccess) return hip_fail(ctx, e, "hipEventSynchronize");
     }
-    if (ctx->stage_cap[slot] < pl.table_bytes) {
-        if (ctx->stage[slot]) (void)hipHostFree(ctx->stage[slot]);
-        ctx->stage[slot] = nullptr;
-        ctx->stage_cap[slot] = 0;
-        const size_t cap = align_up(std::max<size_t>(pl.table_bytes, 65536), 65536);
-        if ((e = hipHostMalloc(&ctx->stage[slot], cap, hipHostMallocDefault)) != hipSuccess)
-            return hip_fail(ctx, e, "hipHostMalloc");
-        ctx->stage_cap[slot] = cap;
-    }
+    if (ctx->stage_cap[slot] < pl.table_bytes) MSAO_TRY(reserve_stage(ctx, slot, pl.table_bytes));
     uint8_t* h = (uint8_t*)ctx->stage[slot];
     std::memset(h, 0, pl.table_bytes);
     auto put = [&](size_t off, const void* src, size_t bytes) {
@@ -590,12 +606,6 @@ int run_hash_post(const void* a, void* s, void* e0, void* e1)
 {
     return launch_hash_post(*(const HashArgs*)a, s, e0, e1);
 }
-
-#define MSAO_TRY(x)                                                                                                   \
-    do {                                                                                                              \
-        msao_status st_ = (x);                                                                                        \
-        if (st_ != MSAO_OK) return st_;                                                                               \
-    } while (0)
 
 // Scoring block order. The order with one contiguous range of work items per
 // XCD makes the per-token statistic stores cheaper, but was measured slower
@@ -760,6 +770,21 @@ msao_status msao_create(msao_ctx** out, int device)
             msao_destroy(c);
             return MSAO_ERR_HIP;
         }
+    }
+    // set-up of msao_run_noalloc, which allocates nothing: both staging slots
+    // hold its largest tables, and this device's copy of the library's
+    // scratch array has its device address looked up
+    for (int i = 0; i < 2; ++i) {
+        if (reserve_stage(c, i, kNoAllocTableBytes) != MSAO_OK) {
+            g_err = c->err;
+            msao_destroy(c);
+            return MSAO_ERR_HIP;
+        }
+    }
+    if ((e = (hipError_t)scratch_init(device)) != hipSuccess) {
+        g_err = std::string("hipGetSymbolAddress of the scratch array: ") + hipGetErrorString(e);
+        msao_destroy(c);
+        return MSAO_ERR_HIP;
     }
     if (const char* v = std::getenv("MSAO_ROW_ITEM_BYTES")) c->row_item_bytes = std::max(1, std::atoi(v));
     if (const char* v = std::getenv("MSAO_CHAIN_FRAMES")) c->chain_frames = std::max(0, std::atoi(v));
@@ -1232,6 +1257,37 @@ msao_status msao_run(msao_ctx* ctx, const msao_segment* segs, int n, int R, cons
     DeviceGuard guard(ctx->device);
     hipStream_t st = (hipStream_t)stream;
     MSAO_TRY(upload(ctx, pl, ws, st));
+    return enqueue_run(ctx, pl, device_tables(pl, ws, n, R, params), tok, frm, req, sel, out, out_bytes, st);
+}
+
+static_assert(kNoAllocScratchBytes == MSAO_NOALLOC_SCRATCH_BYTES && kNoAllocTableBytes == MSAO_NOALLOC_TABLE_BYTES,
+              "the header states the scratch limits");
+
+msao_status msao_run_noalloc(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
+                             const float* alpha, const msao_token_out* tok, const msao_frame_out* frm,
+                             const msao_req_out* req, const msao_select_out* sel, void* out,
+                             const int64_t* out_byte_off, int64_t out_bytes, void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
+    Plan pl;
+    build_plan(ctx, segs, n, R, params, alpha, out_byte_off, pl, out != nullptr);
+    char buf[200];
+    if (pl.table_bytes > kNoAllocTableBytes || pl.total_bytes > kNoAllocScratchBytes) {
+        std::snprintf(buf, sizeof buf,
+                      "msao_run_noalloc: the call needs %zu bytes of tables and %zu of scratch; the limits are "
+                      "%zu and %zu (use msao_run with a workspace)",
+                      pl.table_bytes, pl.total_bytes, kNoAllocTableBytes, kNoAllocScratchBytes);
+        return fail(&ctx->err, MSAO_ERR_UNSUPPORTED, buf);
+    }
+    const std::vector<msao_segment> sv(segs, segs + n);
+    MSAO_TRY(check_run_outputs(ctx, pl, sv, tok, frm, req, sel, out, out_byte_off, out_bytes));
+    // the device address of this GPU's scratch array, looked up by msao_create
+    void* ws = scratch_ptr(ctx->device);
+    if (!ws) return fail(&ctx->err, MSAO_ERR_HIP, "the scratch array of this device was not set up");
+    DeviceGuard guard(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    MSAO_TRY(upload(ctx, pl, ws, st, false));
     return enqueue_run(ctx, pl, device_tables(pl, ws, n, R, params), tok, frm, req, sel, out, out_bytes, st);
 }
 

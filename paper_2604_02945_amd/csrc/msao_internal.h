@@ -306,4 +306,13 @@ constexpr int kGatherBlock = MSAO_GATHER_BLOCK;
 constexpr int kGatherRows = MSAO_GATHER_ROWS;  // kept rows per gather work item
 constexpr int kMaxLdsKeys = 16384; // 128 KiB of LDS per selection block
 
+// msao_run_noalloc: the library's own scratch (msao_scratch.hip), one array
+// per GPU in place of the caller's workspace. Its per-call tables are at most
+// kNoAllocTableBytes (the pinned staging every context reserves at creation).
+constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
+constexpr size_t kNoAllocTableBytes = (size_t)2 << 20;
+constexpr int kMaxScratchDevices = 64;
+int scratch_init(int device);   // with `device` current; returns a HIP error code
+void* scratch_ptr(int device);  // NULL before scratch_init succeeded
+
 }  // namespace msao

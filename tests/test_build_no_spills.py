@@ -25,7 +25,7 @@ import pytest
 from paper_2604_02945_amd import build as B
 
 HIPCC = B.HIPCC
-KERNEL_SOURCES = [s for s in B.SOURCES if s.endswith(".hip")]
+KERNEL_SOURCES = [s for s in B.SOURCES if s.endswith(".hip") and "__global__" in open(s).read()]
 
 
 @pytest.fixture(scope="module", params=KERNEL_SOURCES, ids=os.path.basename)
