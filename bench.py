@@ -46,6 +46,10 @@ def parse():
                     help="skip the learned-head variant (Eq. 3 heads and the Eq. 6 MLP) of the scoring pass")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (calibrates HBM byte counters)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="measure only --config, not the other workloads")
+    ap.add_argument("--only-config", action="store_true",
+                    help="measure only --config (no other workloads, learned, SimHash or entropy blocks)")
     ap.add_argument("--streams", type=int, default=3,
                     help="batches in flight: consecutive steps alternate over this many HIP streams")
     return ap.parse_args()
@@ -77,7 +81,7 @@ def pack_replicas(w, n_rep, dev):
             segs.append(msao.DeviceSegment(t.view(s.n_tokens, s.hidden), s.request, s.modality, s.keep_ratio,
                                            s.n_frames))
         reps.append(segs)
-    return reps, total
+    return reps, total, bufs
 
 
 def algorithmic_bytes(w, kept_count, compact):
@@ -103,43 +107,64 @@ def algorithmic_bytes(w, kept_count, compact):
     return score + fused, select, gather
 
 
-def _committed(profile, sources):
-    """traffic_bytes_per_launch of a committed rocprofv3 counter summary, or
-    None when it is absent or the kernel sources changed since it was taken."""
+# Sources whose text decides a kernel's memory traffic: its own file, the
+# shared device headers and the host planner (work-item sizes, chain split,
+# block order, launch shapes).
+TRAFFIC_SOURCES = ("msao_device.h", "msao_internal.h", "msao_host.cpp")
+
+
+def source_hash(kernel_file):
     import hashlib
+    h = hashlib.sha256()
+    for f in (kernel_file,) + TRAFFIC_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2604_02945_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
+def _committed(profile, kernel_file):
+    """traffic_bytes_per_launch of a committed rocprofv3 counter summary, or
+    None when it is absent or the kernel or planner sources changed since it
+    was taken."""
     path = os.path.join(ROOT, "profiles", profile)
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    h = hashlib.sha256()
-    for f in sources:
-        h.update(open(os.path.join(ROOT, "paper_2604_02945_amd", "csrc", f), "rb").read())
-    return rec["traffic_bytes_per_launch"] if rec.get("kernel_source_sha256") == h.hexdigest() else None
+    return rec["traffic_bytes_per_launch"] if rec.get("kernel_source_sha256") == source_hash(kernel_file) else None
 
 
-def committed_traffic(config):
-    """HBM bytes per k_score launch on the tri-modal workload (committed counters)."""
-    if config != 4:
-        return None
-    return _committed("k_score_trimodal_traffic.json", ("msao_kernels.hip", "msao_device.h", "msao_internal.h"))
+TRAFFIC_PROFILES = {  # (config, compacting run) -> counter summary of that k_score launch
+    (4, True): "k_score_trimodal_traffic.json",
+    (4, False): "k_score_trimodal_scoreonly_traffic.json",
+    (3, True): "k_score_video_traffic.json",
+    (3, False): "k_score_video_scoreonly_traffic.json",
+    (5, True): "k_score_highres_traffic.json",
+    (5, False): "k_score_highres_scoreonly_traffic.json",
+    (2, True): "k_score_imagebatch_traffic.json",
+    (2, False): "k_score_imagebatch_scoreonly_traffic.json",
+}
+
+
+def committed_traffic(config, compact=True):
+    """HBM bytes per k_score launch of a workload (committed counters)."""
+    name = TRAFFIC_PROFILES.get((config, compact))
+    return _committed(name, "msao_kernels.hip") if name else None
 
 
 def committed_learned_traffic(config):
     """HBM bytes per learned k_score launch on the tri-modal workload (committed counters)."""
     if config != 4:
         return None
-    return _committed("k_score_learned_trimodal_traffic.json",
-                      ("msao_kernels.hip", "msao_device.h", "msao_internal.h"))
+    return _committed("k_score_learned_trimodal_traffic.json", "msao_kernels.hip")
 
 
 def committed_simhash_traffic():
     """HBM bytes per k_simhash launch on the video clips (committed counters)."""
-    return _committed("k_simhash_video_traffic.json", ("msao_simhash.hip", "msao_device.h", "msao_internal.h"))
+    return _committed("k_simhash_video_traffic.json", "msao_simhash.hip")
 
 
 def committed_entropy_traffic():
     """HBM bytes per k_entropy launch (committed counters)."""
-    return _committed("k_entropy_draft_logits_traffic.json", ("msao_entropy.hip", "msao_internal.h"))
+    return _committed("k_entropy_draft_logits_traffic.json", "msao_entropy.hip")
 
 
 def entropy_bench(args, dev, ctx):
@@ -287,7 +312,7 @@ def simhash_bench(args, dev, ctx):
     from workloads import make_workload, simhash_planes
 
     w = make_workload(3)
-    reps, _ = pack_replicas(w, 8, dev)
+    reps, _, _ = pack_replicas(w, 8, dev)
     R, K, C = w.n_requests, 32, w.segments[0].hidden
     planes = torch.from_numpy(simhash_planes(K, C, seed=1).view(np.int16)).to(dev).view(torch.bfloat16)
     hashes = [dict(planes=planes, bits=K) for _ in w.segments]
@@ -360,22 +385,47 @@ def simhash_bench(args, dev, ctx):
     return res
 
 
-def cpu_baseline(w, budget_s):
+def host_cpu():
+    """The host's logical CPU count and model name (from /proc/cpuinfo)."""
+    model = platform.processor() or platform.machine()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"host_cpus": os.cpu_count(), "host_cpu_model": model}
+
+
+def cpu_baseline(w, budget_s, n_requests=None):
+    """The oracle, single-threaded, on whole runs of the workload (or of its
+    first n_requests requests: requests are independent), for about budget_s."""
+    import dataclasses
+
     import oracle
 
+    segs, R = w.segments, w.n_requests
+    if n_requests is not None and n_requests < R:
+        segs = [s for s in w.segments if s.request < n_requests]
+        R = n_requests
+    ntok = sum(s.n_tokens for s in segs)
     runs, t0 = 0, time.perf_counter()
     t_oracle = 0.0
     while True:
         a = time.perf_counter()
-        oracle.run(w.segments, w.n_requests, w.params, compact=True)
+        oracle.run(segs, R, w.params, compact=True)
         t_oracle += time.perf_counter() - a
         runs += 1
         if time.perf_counter() - t0 > budget_s:
             break
-    return {"value": w.n_tokens * runs / t_oracle, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"whole workload ({w.n_tokens} tokens) x {runs} runs of the single-threaded C oracle "
-                      f"(fp64 sums, sort-based selection, compaction), {t_oracle:.1f} s",
-            "host_cpu": platform.processor() or platform.machine()}
+    what = "whole workload" if R == w.n_requests else f"its first {R} of {w.n_requests} requests"
+    res = {"value": ntok * runs / t_oracle, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+           "sample": f"{what} ({ntok} tokens) x {runs} runs of the single-threaded C oracle "
+                     f"(fp64 sums, sort-based selection, compaction), {t_oracle:.1f} s"}
+    res.update(host_cpu())
+    return res
 
 
 def cpu_baseline_threads(w, budget_s):
@@ -403,18 +453,269 @@ def cpu_baseline_threads(w, budget_s):
             if time.perf_counter() - t0 > budget_s:
                 break
     dt = time.perf_counter() - t0
-    return {"value": w.n_tokens * runs / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"whole workload ({w.n_tokens} tokens) x {runs} runs, its {len(jobs)} requests spread over "
-                      f"{threads} threads of the C oracle, {dt:.1f} s"}
+    res = {"value": w.n_tokens * runs / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "sample": f"whole workload ({w.n_tokens} tokens) x {runs} runs, its {len(jobs)} requests spread over "
+                     f"{threads} threads of the C oracle, {dt:.1f} s"}
+    res.update(host_cpu())
+    return res
+
+
+class Bench:
+    """Timed steps of one workload: one plan per input replica (each with its
+    own outputs and workspace, so that neither a step's inputs nor its outputs
+    are still in the Infinity Cache), steps rotating over the replicas, n_str
+    batches in flight on as many HIP streams."""
+
+    def __init__(self, w, dev, n_str, replicas=0, max_replicas=128):
+        import torch
+
+        import paper_2604_02945_amd as msao
+
+        self.w, self.dev, self.n_str = w, dev, max(1, n_str)
+        n_rep = replicas or max(2, -(-1_000_000_000 // w.input_bytes))
+        n_rep = min(n_rep, max_replicas)
+        n_rep = -(-n_rep // self.n_str) * self.n_str  # a whole number of replicas per stream
+        self.reps, self.buf_bytes, self.bufs = pack_replicas(w, n_rep, dev)
+        self.n_rep = n_rep
+        self.R, self.n = w.n_requests, len(w.segments)
+        has_video = any(s.modality == 2 and s.n_frames >= 2 for s in w.segments)
+        self.fields = ("z", "l1", "l2", "info", "d", "res") if has_video else ("z", "l1", "l2", "info")
+        self.main = torch.cuda.current_stream()
+        # steps run on streams of their own (not the default stream, which would
+        # serialize with them); the timing events are on the default stream
+        self.streams = [torch.cuda.Stream() for _ in range(self.n_str)]
+        self.ctxs = [msao.Context(0) for _ in range(self.n_str)]  # one context per stream
+        self.plans, self.outs = [], []
+
+    def make_plans(self, compact):
+        import torch
+
+        import paper_2604_02945_amd as msao
+
+        self.close_plans()
+        for r, segs in enumerate(self.reps):
+            k = r % self.n_str
+            o = msao.Outputs(segs, self.R, token_fields=self.fields, compact=compact)
+            self.outs.append(o)
+            self.plans.append((k, msao.Plan(segs, self.R, o, self.w.params, ctx=self.ctxs[k], compact=compact,
+                                            stream=self.main)))
+        torch.cuda.synchronize()
+
+    def close_plans(self):
+        for _, p in self.plans:
+            p.close()
+        self.plans, self.outs = [], []
+
+    def run_steps(self, count, nstreams):
+        """Enqueue `count` steps; step i runs plan i % n_rep on its stream."""
+        import torch
+
+        start = torch.cuda.Event()
+        start.record(self.main)
+        for st in self.streams[:nstreams]:
+            st.wait_event(start)
+        used = set()
+        for i in range(count):
+            k, plan = self.plans[i % self.n_rep]
+            k = k if nstreams > 1 else 0
+            plan(self.streams[k])
+            used.add(k)
+        for k in used:
+            ev = torch.cuda.Event()
+            ev.record(self.streams[k])
+            self.main.wait_event(ev)
+
+    def timed(self, count, nstreams):
+        """Mean ms per step over `count` steps (events on the default stream
+        around the whole region), and the host wall time of the region."""
+        import torch
+
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        e0.record(self.main)
+        self.run_steps(count, nstreams)
+        e1.record(self.main)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / count, time.perf_counter() - t
+
+    def median_one_stream(self, count):
+        """Median over `count` steps on one stream of each step's own duration
+        (an event before and after every step on that stream)."""
+        import numpy as np
+        import torch
+
+        st = self.streams[0]
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(count + 1)]
+        ev[0].record(st)
+        for i in range(count):
+            self.plans[i % self.n_rep][1](st)
+            ev[i + 1].record(st)
+        torch.cuda.synchronize()
+        return float(np.median([ev[i].elapsed_time(ev[i + 1]) for i in range(count)]))
+
+    def kernel_ms(self, count):
+        """Mean duration of each kernel: HIP events recorded by the library at
+        the kernel's own start and end, on the stream it is launched on (one
+        stream, so kernels do not overlap)."""
+        import numpy as np
+
+        for c in self.ctxs:
+            c.set_profiling(True)
+        for i in range(count):
+            self.plans[i % self.n_rep][1](self.streams[0])
+        per_ctx = np.array([c.kernel_times() for c in self.ctxs])  # each context's mean per kernel (0: none)
+        for c in self.ctxs:
+            c.set_profiling(False)
+        n = (per_ctx > 0).sum(axis=0)
+        return np.where(n > 0, per_ctx.sum(axis=0) / np.maximum(n, 1), 0.0)
+
+    def read_ceiling(self, count):
+        """A plain streaming read of the replicas' input buffers (the same
+        bytes the scoring pass reads), best of four chunk sizes: GB/s of the
+        library's read kernel by its own launch events."""
+        import torch
+
+        import paper_2604_02945_amd as msao
+
+        c = self.ctxs[0]
+        sink = torch.empty(-(-self.buf_bytes // 8192), dtype=torch.int32, device=self.dev)
+        best = None
+        for kib in (8, 16, 32, 64):
+            for buf in self.bufs:
+                msao.msao_stream_read(buf, kib, ctx=c, stream=self.streams[0], sink=sink)
+            c.set_profiling(True)
+            for i in range(count):
+                msao.msao_stream_read(self.bufs[i % len(self.bufs)], kib, ctx=c, stream=self.streams[0], sink=sink)
+            ms = c.kernel_times()[msao.binding.KERNEL_READ]
+            c.set_profiling(False)
+            gbs = self.buf_bytes / (ms * 1e-3) / 1e9
+            if best is None or gbs > best["gbps"]:
+                best = {"gbps": gbs, "ms": ms, "bytes": self.buf_bytes, "chunk_kib": kib}
+        best["frac_of_peak"] = best["gbps"] / PEAK_HBM_GBS
+        return best
+
+    def close(self):
+        self.close_plans()
+        for c in self.ctxs:
+            c.close()
+
+
+def measure(w, args, dev, n_str, graph=False, with_compact=True, with_score_select=True, max_replicas=128):
+    """Full steps (score, MAS, selection, compaction) and score+select steps of
+    workload w: in flight over n_str streams, one after another on one
+    stream, per-step medians on one stream, kernel durations, roofline of the
+    scoring pass."""
+    import numpy as np
+    import torch
+
+    b = Bench(w, dev, n_str, args.replicas, max_replicas)
+    res = {"replicas_rotated": b.n_rep, "batches_in_flight": b.n_str}
+    steps = args.steps
+    kept_count = None
+    if with_compact:
+        b.make_plans(True)
+        b.run_steps(args.warmup, b.n_str)
+        torch.cuda.synchronize()
+        kept_count = b.outs[0].sel["kept_count"][:b.n].cpu().numpy()
+        ms_step, wall = b.timed(steps, b.n_str)
+        ms_serial, _ = b.timed(steps, 1)
+        med = b.median_one_stream(steps)
+        k_ms = b.kernel_ms(steps)
+        res.update({"ms_per_step": ms_step, "wall_s_timed": wall, "ms_per_step_one_stream": ms_serial,
+                    "ms_per_step_one_stream_median": med, "tokens_per_s": w.n_tokens / (ms_step * 1e-3)})
+        if graph:
+            # the same one-stream steps with each replica's plan replayed from a HIP graph
+            graphs = []
+            for _, plan in b.plans:
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g):
+                    plan(torch.cuda.current_stream())
+                graphs.append(g)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(b.main)
+            for i in range(steps):
+                graphs[i % b.n_rep].replay()
+            e1.record(b.main)
+            torch.cuda.synchronize()
+            res["ms_per_step_one_stream_graph"] = e0.elapsed_time(e1) / steps
+            del graphs
+        b_score, b_select, b_compact = algorithmic_bytes(w, kept_count, True)
+        b_step = b_score + b_select + b_compact
+        score_gbs = b_score / (k_ms[0] * 1e-3) / 1e9
+        res.update({
+            "kept_tokens": int(kept_count.sum()),
+            "hbm_gbps_step": b_step / (ms_step * 1e-3) / 1e9,
+            "hbm_frac_step": b_step / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "algorithmic_bytes": {"score": b_score, "select": b_select, "gather_write": b_compact},
+            "kernel_ms": {"score": float(k_ms[0]), "post": float(k_ms[1]), "gather": float(k_ms[2])},
+            "roofline": {"bound": "hbm", "kernel": "k_score", "achieved": score_gbs, "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": score_gbs / PEAK_HBM_GBS,
+                         "traffic": committed_traffic(w.config, compact=True)},
+        })
+    if with_score_select:
+        # scoring and selection alone (no compaction), same replicas and streams
+        b.make_plans(False)
+        b.run_steps(args.warmup, b.n_str)
+        torch.cuda.synchronize()
+        if kept_count is None:
+            kept_count = b.outs[0].sel["kept_count"][:b.n].cpu().numpy()
+            res["kept_tokens"] = int(kept_count.sum())
+        ms_ss, _ = b.timed(steps, b.n_str)
+        ms_ss_serial, _ = b.timed(steps, 1)
+        med_ss = b.median_one_stream(steps)
+        k_ss = b.kernel_ms(steps)
+        b_s, b_sel, _ = algorithmic_bytes(w, kept_count, False)
+        bb = b_s + b_sel
+        gbs_s = b_s / (k_ss[0] * 1e-3) / 1e9
+        res["score_select"] = {
+            "ms_per_step": ms_ss, "ms_per_step_one_stream": ms_ss_serial,
+            "ms_per_step_one_stream_median": med_ss,
+            "tokens_per_s": w.n_tokens / (ms_ss * 1e-3), "algorithmic_bytes": bb,
+            "hbm_gbps": bb / (ms_ss * 1e-3) / 1e9, "hbm_frac": bb / (ms_ss * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "hbm_frac_one_stream": bb / (ms_ss_serial * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "hbm_frac_one_stream_median": bb / (med_ss * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "kernel_ms": {"score": float(k_ss[0]), "post": float(k_ss[1])},
+            "roofline": {"bound": "hbm", "kernel": "k_score (score only)", "achieved": gbs_s, "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": gbs_s / PEAK_HBM_GBS,
+                         "traffic": committed_traffic(w.config, compact=False)},
+        }
+    res["read_ceiling"] = b.read_ceiling(max(steps, 8))
+    b.close()
+    return res
+
+
+def config_block(c, args, dev):
+    """One of the other workloads, measured like the headline one (with a
+    bounded oracle sample for its CPU baseline)."""
+    import torch
+
+    from workloads import CONFIG_NAMES, make_workload
+
+    w = make_workload(c)
+    t0 = time.perf_counter()
+    res = {"workload": f"{CONFIG_NAMES[c]} (config {c})", "requests": w.n_requests, "segments": len(w.segments),
+           "tokens": w.n_tokens, "input_bytes": w.input_bytes}
+    res.update(measure(w, args, dev, args.streams, max_replicas=128 if c != 1 else 100))
+    if not args.no_cpu_baseline:
+        sample = {1: None, 2: 8, 3: 1, 5: 4}.get(c)
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds / 4, sample)
+    res["bench_s"] = time.perf_counter() - t0
+    del w
+    torch.cuda.empty_cache()
+    return res
 
 
 def main():
     args = parse()
+    if args.only_config:
+        args.no_configs = args.no_learned = args.no_simhash = args.no_entropy = True
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the analysis shards by request "
               "with no exchange, so more GPUs would repeat the one-GPU line", file=sys.stderr)
         sys.exit(2)
-    import numpy as np
     import torch
 
     if args.copy_calibration:
@@ -427,134 +728,22 @@ def main():
         print(json.dumps({"copy_calibration_bytes": nbytes, "copies": args.steps}), flush=True)
         return
 
-    import paper_2604_02945_amd as msao
     from workloads import CONFIG_NAMES, make_workload
 
     dev = torch.device("cuda", 0)
     w = make_workload(args.config)
-    n_rep = args.replicas or max(2, -(-1_000_000_000 // w.input_bytes))
-    reps, buf_bytes = pack_replicas(w, n_rep, dev)
-    R, n = w.n_requests, len(w.segments)
-    has_video = any(s.modality == 2 and s.n_frames >= 2 for s in w.segments)
-    fields = ("z", "l1", "l2", "info", "d", "res") if has_video else ("z", "l1", "l2", "info")
     compact = not args.no_compact
-    n_str = max(1, args.streams)
-    n_rep = -(-n_rep // n_str) * n_str  # a whole number of replicas per stream
-    while len(reps) < n_rep:
-        extra, _ = pack_replicas(w, 1, dev)
-        reps += extra
-    main = torch.cuda.current_stream()
-    # steps run on streams of their own (not the default stream, which would
-    # serialize with them); the timing events are on the default stream
-    streams = [torch.cuda.Stream() for _ in range(n_str)]
-    ctxs = [msao.Context(0) for _ in range(n_str)]  # one context per stream
-
-    def make_plans(with_compaction):
-        """One plan per replica, each with its own outputs and workspace, so that
-        neither the inputs nor the outputs of a step are still in the Infinity Cache."""
-        plans, outs = [], []
-        for r, segs in enumerate(reps):
-            k = r % n_str
-            o = msao.Outputs(segs, R, token_fields=fields, compact=with_compaction)
-            outs.append(o)
-            plans.append((k, msao.Plan(segs, R, o, w.params, ctx=ctxs[k], compact=with_compaction, stream=main)))
-        torch.cuda.synchronize()
-        return plans, outs
-
-    def run_steps(plans, count, nstreams):
-        """Enqueue `count` steps; step i runs plan i % n_rep on its stream."""
-        start = torch.cuda.Event()
-        start.record(main)
-        for st in streams[:nstreams]:
-            st.wait_event(start)
-        used = set()
-        for i in range(count):
-            k, plan = plans[i % n_rep]
-            k = k if nstreams > 1 else 0
-            plan(streams[k])
-            used.add(k)
-        for k in used:
-            ev = torch.cuda.Event()
-            ev.record(streams[k])
-            main.wait_event(ev)
-
-    def timed(plans, count, nstreams):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t = time.perf_counter()
-        e0.record(main)
-        run_steps(plans, count, nstreams)
-        e1.record(main)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / count, time.perf_counter() - t
-
-    plans, outs = make_plans(compact)
-    run_steps(plans, args.warmup, n_str)
-    torch.cuda.synchronize()
-    out = outs[0]
-    kept_count = out.sel["kept_count"][:n].cpu().numpy()
-    kept_total = int(kept_count.sum())
-
-    # timed region: K whole steps over rotated replicas, n_str batches in flight
-    ms_step, wall = timed(plans, args.steps, n_str)
-    # the same steps one after another on one stream: per-batch latency
-    ms_step_serial, _ = timed(plans, args.steps, 1)
-    # the same one-stream steps with each replica's plan replayed from a HIP graph
-    graphs = []
-    for _, plan in plans:
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            plan(torch.cuda.current_stream())
-        graphs.append(g)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(main)
-    for i in range(args.steps):
-        graphs[i % n_rep].replay()
-    e1.record(main)
-    torch.cuda.synchronize()
-    ms_step_graph = e0.elapsed_time(e1) / args.steps
-    del graphs
-
-    # per-kernel durations: HIP events recorded by the library around each launch,
-    # on the stream the kernel is launched on (one stream, so kernels do not overlap)
-    for c in ctxs:
-        c.set_profiling(True)
-    for i in range(args.steps):
-        plans[i % n_rep][1](streams[0])
-    k_ms = np.mean([np.array(c.kernel_times()) for c in ctxs], axis=0)
-    for c in ctxs:
-        c.set_profiling(False)
-
-    b_score, b_select, b_compact = algorithmic_bytes(w, kept_count, compact)
-    b_step = b_score + b_select + b_compact
-
-    # scoring and selection alone (no compaction), same replicas and streams
-    score_select = None
-    if compact and not args.no_score_select:
-        torch.cuda.synchronize()
-        for _, plan in plans:
-            plan.close()
-        del plans, outs
-        plans_ss, _ = make_plans(False)
-        run_steps(plans_ss, args.warmup, n_str)
-        ms_ss, _ = timed(plans_ss, args.steps, n_str)
-        ms_ss_serial, _ = timed(plans_ss, args.steps, 1)
-        b_s, b_sel, _ = algorithmic_bytes(w, kept_count, False)
-        score_select = {"ms_per_step": ms_ss, "ms_per_step_one_stream": ms_ss_serial,
-                        "tokens_per_s": w.n_tokens / (ms_ss * 1e-3), "algorithmic_bytes": b_s + b_sel,
-                        "hbm_gbps": (b_s + b_sel) / (ms_ss * 1e-3) / 1e9,
-                        "hbm_frac": (b_s + b_sel) / (ms_ss * 1e-3) / 1e9 / PEAK_HBM_GBS}
-        plans = plans_ss
-    score_gbs = b_score / (k_ms[0] * 1e-3) / 1e9
+    m = measure(w, args, dev, args.streams, graph=compact, with_compact=compact,
+                with_score_select=not args.no_score_select)
+    head = m if compact else m["score_select"]
     line = {
         "metric": METRIC,
-        "value": w.n_tokens / (ms_step * 1e-3),
+        "value": w.n_tokens / (head["ms_per_step"] * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_step,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -562,34 +751,44 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{CONFIG_NAMES[args.config]} (config {args.config})",
-            "requests": R, "segments": n, "tokens": w.n_tokens, "input_dtype": sorted({s.dtype for s in w.segments}),
-            "input_bytes": w.input_bytes, "kept_tokens": kept_total, "replicas_rotated": n_rep,
-            "compaction": compact, "batches_in_flight": n_str,
+            "requests": w.n_requests, "segments": len(w.segments), "tokens": w.n_tokens,
+            "input_dtype": sorted({s.dtype for s in w.segments}),
+            "input_bytes": w.input_bytes, "kept_tokens": m.get("kept_tokens"), "replicas_rotated": m["replicas_rotated"],
+            "compaction": compact, "batches_in_flight": m["batches_in_flight"],
+            "timing": f"{m['batches_in_flight']} batches in flight on as many HIP streams; the one_stream "
+                      "fields are per-batch latency on one stream",
         },
-        "ms_per_step_one_stream": ms_step_serial,
-        "ms_per_step_one_stream_graph": ms_step_graph,
-        "hbm_gbps_step": b_step / (ms_step * 1e-3) / 1e9,
-        "hbm_frac_step": b_step / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS,
-        "algorithmic_bytes": {"score": b_score, "select": b_select, "gather_write": b_compact},
-        "kernel_ms": {"score": k_ms[0], "post": k_ms[1], "gather": k_ms[2]},
-        "roofline": {"bound": "hbm", "kernel": "k_score", "achieved": score_gbs, "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": score_gbs / PEAK_HBM_GBS, "traffic": committed_traffic(args.config)},
-        "wall_s_timed": wall,
-        "score_select": score_select,
     }
+    for k in ("ms_per_step_one_stream", "ms_per_step_one_stream_median", "ms_per_step_one_stream_graph",
+              "hbm_gbps_step", "hbm_frac_step", "algorithmic_bytes", "kernel_ms", "roofline", "wall_s_timed",
+              "score_select", "read_ceiling"):
+        if k in m:
+            line[k] = m[k]
+    if "roofline" not in line and "score_select" in m:
+        line["roofline"] = m["score_select"]["roofline"]
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
         line["cpu_baseline_threads"] = cpu_baseline_threads(w, args.cpu_seconds / 2)
+    if not args.no_configs:
+        line["configs"] = {}
+        for c in (1, 2, 3, 5):
+            if c != args.config:
+                line["configs"][str(c)] = config_block(c, args, dev)
+    ctx = None
+    if not (args.no_learned and args.no_simhash and args.no_entropy):
+        import paper_2604_02945_amd as msao
+        ctx = msao.Context(0)
     if not args.no_learned:
-        line["learned"] = learned_bench(args, dev, ctxs[0], w, reps, fields)
+        b = Bench(w, dev, 1, args.replicas)
+        line["learned"] = learned_bench(args, dev, ctx, w, b.reps, b.fields)
+        b.close()
+        del b
     if not args.no_simhash:
-        line["simhash"] = simhash_bench(args, dev, ctxs[0])
+        line["simhash"] = simhash_bench(args, dev, ctx)
     if not args.no_entropy:
-        line["entropy"] = entropy_bench(args, dev, ctxs[0])
-    for _, plan in plans:
-        plan.close()
-    for c in ctxs:
-        c.close()
+        line["entropy"] = entropy_bench(args, dev, ctx)
+    if ctx is not None:
+        ctx.close()
     print(json.dumps(line), flush=True)
 
 

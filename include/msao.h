@@ -37,7 +37,8 @@
  * Conventions
  *  - Every data pointer is HIP device memory owned by the caller unless it is
  *    marked "host". The library allocates no device memory: scratch comes
- *    from the caller's workspace (size from msao_workspace_size). The context
+ *    from the caller's workspace (size from msao_workspace_size), except for
+ *    msao_run_noalloc, which uses the library's own static array. The context
  *    owns host state only (pinned staging for the small per-call tables, HIP
  *    events, the last error message).
  *  - Calls are asynchronous: they enqueue on `stream` (a hipStream_t; NULL is
@@ -511,7 +512,8 @@ double msao_expected_e2e_latency(const msao_latency_model* m);
 #define MSAO_KERNEL_SIMHASH 5 /* SimHash signatures */
 #define MSAO_KERNEL_HASH_POST 6 /* SimHash d, per-frame terms, temporal term */
 #define MSAO_KERNEL_CLIP 7    /* the SimHash run's clips: statistics and signatures in one pass */
-#define MSAO_NUM_KERNELS 8
+#define MSAO_KERNEL_READ 8    /* msao_stream_read: the plain streaming read */
+#define MSAO_NUM_KERNELS 9
 
 /* When enabled, every launch is bracketed by a pair of HIP events recorded on
  * the caller's stream. */
@@ -520,6 +522,20 @@ msao_status msao_set_profiling(msao_ctx* ctx, int enable);
  * launches recorded since the previous query (0 if none); blocks until they
  * have completed, then forgets them. */
 msao_status msao_kernel_times(msao_ctx* ctx, float* ms);
+
+/* ---- measurement ---------------------------------------------------------- */
+
+/* A plain streaming read of `bytes` of device memory at `data`, the
+ * ceiling the HBM-bound passes are measured against on the same machine (it
+ * computes nothing of the analysis). Wavefront w reads bytes [w*chunk,
+ * (w+1)*chunk) with chunk = chunk_kib KiB (8, 16, 32 or 64) as 128-bit
+ * nontemporal loads, eight 1-KiB units in flight, and writes the XOR of the
+ * 32-bit words it read to sink[w] (device, ceil(bytes / chunk) words,
+ * sink_words at least that). data 16-byte aligned, bytes > 0. Errors:
+ * MSAO_ERR_INVALID_ARG, MSAO_ERR_ALIGNMENT, MSAO_ERR_HIP. With profiling on,
+ * its launch time is reported as MSAO_KERNEL_READ. */
+msao_status msao_stream_read(msao_ctx* ctx, const void* data, int64_t bytes, int chunk_kib, uint32_t* sink,
+                             int64_t sink_words, void* stream);
 
 #ifdef __cplusplus
 }

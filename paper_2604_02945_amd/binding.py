@@ -23,7 +23,7 @@ F32, BF16 = 0, 1
 FLAG_TEMPORAL_LITERAL = 1
 FLAG_SELECT_PER_FRAME = 2
 (KERNEL_SCORE, KERNEL_POST, KERNEL_GATHER, KERNEL_ENTROPY, KERNEL_HEAD, KERNEL_SIMHASH, KERNEL_HASH_POST,
- KERNEL_CLIP, NUM_KERNELS) = 0, 1, 2, 3, 4, 5, 6, 7, 8
+ KERNEL_CLIP, KERNEL_READ, NUM_KERNELS) = 0, 1, 2, 3, 4, 5, 6, 7, 8, 9
 MODAL_DESC = 8
 DECIDE_HOLD, DECIDE_SEND, DECIDE_OFFLOAD = 0, 1, 2
 
@@ -143,6 +143,7 @@ SIGNATURES = [
                                         ctypes.c_int64, _P, ctypes.c_size_t, _P]),
     ("msao_draft_entropy", ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
                                           ctypes.c_float, _P, _P]),
+    ("msao_stream_read", ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int, _P, ctypes.c_int64, _P]),
     ("msao_sched_default_params", MsaoSchedParams, []),
     ("msao_sched_init", ctypes.c_int, [_P, ctypes.c_int64, _P, _P]),
     ("msao_sched_step", ctypes.c_int, [_P, _P, ctypes.c_float, _P]),
@@ -633,6 +634,24 @@ def msao_draft_entropy(logits: torch.Tensor, theta: float, vocab: Optional[int] 
     _check(lib().msao_draft_entropy(ctx.handle, _ptr(logits) if logits.numel() else None, rows, V, stride, dt,
                                     float(theta), _addr(out), ctypes.c_void_p(st.cuda_stream)), ctx)
     return o
+
+
+def msao_stream_read(data: torch.Tensor, chunk_kib: int = 8, ctx: Optional[Context] = None, stream=None,
+                     sink: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """A plain streaming read of a contiguous device tensor (the read
+    ceiling of the HBM-bound passes); returns the sink of one XOR per
+    wavefront."""
+    nbytes = data.numel() * data.element_size()
+    dev = data.device
+    if ctx is None:
+        ctx = default_context(dev.index if dev.index is not None else torch.cuda.current_device())
+    waves = -(-nbytes // (chunk_kib * 1024))
+    if sink is None:
+        sink = torch.empty(max(waves, 1), dtype=torch.int32, device=dev)
+    st = stream if stream is not None else torch.cuda.current_stream(dev)
+    _check(lib().msao_stream_read(ctx.handle, _ptr(data), nbytes, int(chunk_kib), _ptr(sink), sink.numel(),
+                                  ctypes.c_void_p(st.cuda_stream)), ctx)
+    return sink
 
 
 def sched_default_params() -> MsaoSchedParams:

@@ -10,7 +10,7 @@ ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libmsao.so")
 SOURCES = [os.path.join(HERE, "csrc", f) for f in
            ("msao_host.cpp", "msao_sched.cpp", "msao_kernels.hip", "msao_entropy.hip", "msao_simhash.hip",
-            "msao_scratch.hip")]
+            "msao_scratch.hip", "msao_calib.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

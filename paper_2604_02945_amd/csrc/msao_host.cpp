@@ -144,7 +144,8 @@ struct Plan {
     int mlp_hidden = 0;            // > 0: the relevance MLP's u = W1[:, :P] p + b1 per request
     size_t off_hbseg = 0, off_partial_x = 0, off_proj = 0, off_head_count = 0, off_mlp_u = 0;
     size_t off_seg = 0, off_wi = 0, off_gi = 0, off_rmoff = 0, off_rmseg = 0, off_tseg = 0, off_alpha = 0;
-    size_t off_selu = 0, off_hiseg = 0, off_clseg = 0;
+    size_t off_selu = 0, off_hiseg = 0, off_clseg = 0, off_frseg = 0;
+    std::vector<int32_t> frame_seg;  // segment of every temporal frame
     bool simhash_d = false;        // a run with SimHash: d of temporal segments in K-bit units
     size_t off_hdsum = 0;          // [R*4] SimHash Dsum (simhash_d without clip_fused)
     bool clip_fused = false;       // a run with SimHash whose clips k_clip scores and hashes in one pass
@@ -155,7 +156,7 @@ struct Plan {
 };
 
 size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t n_hb, int64_t n_sel, int64_t n_hi,
-                    int64_t n_cl)
+                    int64_t n_cl, int64_t n_fr)
 {
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -174,21 +175,27 @@ size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t
     pl.off_selu = take(sizeof(SelUnit) * (size_t)std::max<int64_t>(n_sel, 1));
     pl.off_hiseg = take(sizeof(int32_t) * (size_t)std::max<int64_t>(n_hi, 1));
     pl.off_clseg = take(sizeof(int32_t) * (size_t)std::max<int64_t>(n_cl, 1));
+    pl.off_frseg = take(sizeof(int32_t) * (size_t)std::max<int64_t>(n_fr, 1));
     pl.table_bytes = o;
     return o;
 }
 
 // Workspace bound that does not depend on tuning: work items, gather items,
-// head blocks, selections and hash tiles never outnumber tokens plus
-// segments, so one Partial and table entries per token, plus what a learned call adds (a PartialX per work item, one
+// head blocks and hash tiles never outnumber tokens plus segments, and
+// selection blocks are bounded by segments, frames and one per
+// kSelPartTokens tokens, so one Partial and table entries per token, plus
+// what a learned call adds (a PartialX per work item, one
 // projection and one head count per token, kMaxMlpHidden floats of the MLP's
 // prompt product per request). A run with SimHash adds 4 Dsum counts per
 // request, within the room of the prompt product.
-size_t workspace_bytes_for(int n, int R, int64_t ntok)
+size_t workspace_bytes_for(int n, int R, int64_t ntok, int64_t nframes)
 {
     Plan pl;
     const int64_t items = ntok + n;
-    const size_t tb = table_layout(pl, n, R, items, items, items, items, items, items);
+    // selection blocks: one per segment, or per frame of a clip, plus the
+    // extra blocks of selections of kSelSplitMin tokens or more
+    const int64_t sels = n + nframes + ntok / kSelPartTokens + 1;
+    const size_t tb = table_layout(pl, n, R, items, items, items, sels, items, items, items);
     return align_up(tb, kWsAlign) + align_up(sizeof(Partial) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
            align_up(sizeof(PartialX) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
            align_up(sizeof(float) * (size_t)std::max<int64_t>(ntok, 1), kWsAlign) +
@@ -276,17 +283,45 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
             d.key_ms = (uint64_t)d.L_s * (uint64_t)(K / g);
             d.key_mt = (uint64_t)d.L_t * (uint64_t)(s.hidden / g);
         }
-        // selections: the segment, or each of its frames (per-frame scope)
+        // selections: the segment, or each of its frames (per-frame scope);
+        // a large one is written by several blocks, each of a slice
         const bool framed = per_frame && s.n_frames >= 2 && s.tokens_per_frame > 0;
+        const int kind = d.temporal && d.L_t > 0 ? (d.L_s > 0 ? kKeyFull : kKeyE) : (d.L_s > 0 ? kKeyZ : kKeyZero);
+        auto push_selection = [&](int frame, int n_u, int kfix) {
+            const int parts = n_u >= kSelSplitMin ? (n_u + kSelPartTokens - 1) / kSelPartTokens : 1;
+            for (int q = 0; q < parts; ++q) {
+                SelUnit u;
+                std::memset(&u, 0, sizeof u);
+                u.Ms = d.key_ms;
+                u.Mt = d.key_mt;
+                u.kmax = kind == kKeyZ ? (uint64_t)d.C
+                         : kind == kKeyE ? (uint64_t)d.E
+                         : kind == kKeyFull ? d.key_ms * (uint64_t)d.C + d.key_mt * (uint64_t)d.E : 0ull;
+                u.seg = i;
+                u.frame = frame;
+                u.part = q;
+                u.nparts = parts;
+                u.off = d.tok_off + (frame >= 0 ? frame * s.tokens_per_frame : 0);
+                u.N = n_u;
+                u.kfix = kfix;
+                u.kind = kind;
+                u.E = (uint32_t)d.E;
+                u.units = frame >= 0 ? s.n_frames : 1;
+                u.seg_off = d.tok_off;
+                u.request = s.request;
+                u.modality = s.modality;
+                pl.sel_unit.push_back(u);
+            }
+        };
         if (framed) {
             d.kf = s.keep_ratio < 0.0f ? -1 : (int32_t)keep_count(s.keep_ratio, s.tokens_per_frame);
             d.k = d.kf < 0 ? -1 : d.kf * s.n_frames;
-            for (int f = 0; f < s.n_frames; ++f) pl.sel_unit.push_back(SelUnit{i, f});
+            for (int f = 0; f < s.n_frames; ++f) push_selection(f, s.tokens_per_frame, d.kf);
             pl.max_n = std::max(pl.max_n, s.tokens_per_frame);
         } else {
             d.kf = -1;
             d.k = s.keep_ratio < 0.0f ? -1 : (int32_t)keep_count(s.keep_ratio, N);
-            pl.sel_unit.push_back(SelUnit{i, -1});
+            push_selection(-1, (int)N, d.k);
             pl.max_n = std::max(pl.max_n, (int)N);
         }
         d.cap = d.k < 0 ? (int32_t)N : d.k;
@@ -399,8 +434,11 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
     pl.alpha.assign((size_t)std::max(R * kNumMod, 1), 0.0f);
     if (alpha)
         for (int x = 0; x < R * kNumMod; ++x) pl.alpha[(size_t)x] = alpha[x];
+    pl.frame_seg.clear();
+    for (int i = 0; i < n; ++i)
+        if (pl.seg[(size_t)i].temporal) pl.frame_seg.insert(pl.frame_seg.end(), (size_t)pl.seg[(size_t)i].T, i);
     table_layout(pl, n, R, pl.n_wi, pl.n_gwi, (int64_t)pl.hb_seg.size(), (int64_t)pl.sel_unit.size(),
-                 (int64_t)pl.hi_seg.size(), (int64_t)pl.cl_seg.size());
+                 (int64_t)pl.hi_seg.size(), (int64_t)pl.cl_seg.size(), (int64_t)pl.frame_seg.size());
     pl.off_partial = align_up(pl.table_bytes, kWsAlign);
     pl.total_bytes = pl.off_partial + sizeof(Partial) * (size_t)std::max(pl.n_wi, 1);
     pl.simhash_d = simhash_d && pl.any_temporal;
@@ -489,6 +527,7 @@ msao_status upload(msao_ctx* ctx, const Plan& pl, void* ws, hipStream_t stream, 
     put(pl.off_selu, pl.sel_unit.data(), sizeof(SelUnit) * pl.sel_unit.size());
     put(pl.off_hiseg, pl.hi_seg.data(), sizeof(int32_t) * pl.hi_seg.size());
     put(pl.off_clseg, pl.cl_seg.data(), sizeof(int32_t) * pl.cl_seg.size());
+    put(pl.off_frseg, pl.frame_seg.data(), sizeof(int32_t) * pl.frame_seg.size());
     if ((e = hipMemcpyAsync(ws, h, pl.table_bytes, hipMemcpyHostToDevice, stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipMemcpyAsync");
     if ((e = hipEventRecord(ctx->stage_ev[slot], stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
@@ -518,6 +557,7 @@ Tables device_tables(const Plan& pl, void* ws, int n, int R, const msao_params* 
     t.hi_seg = (const int32_t*)(b + pl.off_hiseg);
     t.hdsum = pl.simhash_d && !pl.clip_fused ? (const uint64_t*)(b + pl.off_hdsum) : nullptr;
     t.cl_seg = (const int32_t*)(b + pl.off_clseg);
+    t.frame_seg = (const int32_t*)(b + pl.off_frseg);
     t.n_cl = (int32_t)pl.cl_seg.size();
     t.n_wi_score = pl.n_wi_score;
     t.n_hi = (int32_t)pl.hi_seg.size();
@@ -602,6 +642,7 @@ int run_entropy(const void* a, void* s, void* e0, void* e1) { return launch_entr
 int run_head(const void* a, void* s, void* e0, void* e1) { return launch_head(*(const HeadArgs*)a, s, e0, e1); }
 int run_simhash(const void* a, void* s, void* e0, void* e1) { return launch_simhash(*(const HashArgs*)a, s, e0, e1); }
 int run_clip(const void* a, void* s, void* e0, void* e1) { return launch_clip(*(const ClipArgs*)a, s, e0, e1); }
+int run_read(const void* a, void* s, void* e0, void* e1) { return launch_read(*(const ReadArgs*)a, s, e0, e1); }
 int run_hash_post(const void* a, void* s, void* e0, void* e1)
 {
     return launch_hash_post(*(const HashArgs*)a, s, e0, e1);
@@ -729,7 +770,10 @@ msao_status msao_workspace_size(const msao_segment* segs, int n, int n_requests,
     MSAO_TRY(validate_impl(segs, n, n_requests, &p, &g_err));
     int64_t t = 0, f = 0;
     MSAO_TRY(msao_count(segs, n, &t, &f));
-    *bytes = workspace_bytes_for(n, n_requests, t);
+    int64_t frames_all = 0;  // frames of every segment of two or more (per-frame scope)
+    for (int i = 0; i < n; ++i)
+        if (segs[i].n_frames >= 2) frames_all += segs[i].n_frames;
+    *bytes = workspace_bytes_for(n, n_requests, t, frames_all);
     return MSAO_OK;
 }
 
@@ -1099,6 +1143,27 @@ msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int 
     pa.n_req_blocks = R;
     pa.n_frame_blocks = want_frames ? (int)pl.nframes : 0;
     return launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa);
+}
+
+msao_status msao_stream_read(msao_ctx* ctx, const void* data, int64_t bytes, int chunk_kib, uint32_t* sink,
+                             int64_t sink_words, void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    if (!data || bytes <= 0) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "data is NULL or bytes <= 0");
+    if (chunk_kib != 8 && chunk_kib != 16 && chunk_kib != 32 && chunk_kib != 64)
+        return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "chunk_kib must be 8, 16, 32 or 64");
+    const int64_t chunk = (int64_t)chunk_kib * 1024, waves = (bytes + chunk - 1) / chunk;
+    if (!sink || sink_words < waves) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "sink is NULL or too small");
+    if (!aligned(data, 16) || !aligned(sink, 4)) return fail(&ctx->err, MSAO_ERR_ALIGNMENT, "data or sink misaligned");
+    if (waves > ((int64_t)1 << 31) * (kReadBlock / 64)) return fail(&ctx->err, MSAO_ERR_UNSUPPORTED, "buffer too large");
+    DeviceGuard guard(ctx->device);
+    ReadArgs a;
+    a.data = (const uint8_t*)data;
+    a.bytes = bytes;
+    a.waves = waves;
+    a.chunk_bytes = (int32_t)chunk;
+    a.sink = sink;
+    return launched(ctx, MSAO_KERNEL_READ, (hipStream_t)stream, run_read, &a);
 }
 
 msao_status msao_draft_entropy(msao_ctx* ctx, const void* logits, int64_t rows, int64_t vocab, int64_t row_stride,

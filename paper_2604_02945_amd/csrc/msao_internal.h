@@ -60,11 +60,34 @@ struct DevSeg {
     int32_t cl_begin, ntiles;
 };
 
-// One selection: a whole segment (frame -1) or one frame of a clip
-// (per-frame scope).
+// Key kinds of a selection: Ms z + Mt (E - d) in general, z or E - d alone
+// when the other weight is 0 (the same order, a narrower range).
+enum : int { kKeyZero = 0, kKeyZ = 1, kKeyE = 2, kKeyFull = 3 };
+
+// One selection block: a whole segment (frame -1) or one frame of a clip
+// (per-frame scope), or one of the nparts blocks of a large selection. Every
+// block of a selection finds the same threshold from all of its keys; block
+// `part` then writes the keep flags and kept indices of its own slice. It
+// holds everything the block needs before its first load of z and d.
 struct SelUnit {
-    int32_t seg, frame;
+    uint64_t Ms, Mt;        // key multipliers
+    uint64_t kmax;          // largest key the selection can hold (z <= C, d <= E)
+    int32_t seg, frame;     // segment; frame of a clip under the per-frame scope, else -1
+    int32_t part, nparts;   // slice written by this block
+    int32_t off, N;         // global token id of the selection's first token; its tokens
+    int32_t kfix, kind;     // fixed keep count (-1: MAS-guided); key kind
+    uint32_t E;             // bits d counts per token
+    int32_t units;          // selections of the segment (T under the per-frame scope, else 1)
+    int32_t seg_off;        // global token id of the segment's first token
+    int32_t request, modality, pad_;
 };
+// Selections of at least kSelSplitMin tokens are split into blocks of about
+// kSelPartTokens tokens each for their counting and writing.
+#ifndef MSAO_SEL_PART_TOKENS
+#define MSAO_SEL_PART_TOKENS 2048
+#endif
+constexpr int kSelPartTokens = MSAO_SEL_PART_TOKENS;
+constexpr int kSelSplitMin = 4096;
 
 // Integer partial sums of one scoring work item (no atomics, no zeroing).
 struct Partial {
@@ -103,6 +126,7 @@ struct Tables {
     const RmEntry* rm;       // [R*4]
     const WiRange* rm_rng;   // [n] work-item ranges grouped by (request, modality)
     const int32_t* tseg;     // [n_tseg] temporal segment ids in table order
+    const int32_t* frame_seg;// [n_frames] segment of every temporal frame
     const float* alpha;      // [R*4] relevance logits
     Partial* partial;        // [n_wi]
     // learned calls only
@@ -158,7 +182,7 @@ struct PostArgs {
     const uint32_t* z;    // selection inputs
     const uint32_t* d;
     const float* mas_in;  // MAS from the caller (selection only); NULL: recompute
-    int32_t n_sel_blocks; // blocks [0, n_sel_blocks): one per segment
+    int32_t n_sel_blocks; // blocks [0, n_sel_blocks): one per selection unit (SelUnit)
     int32_t n_req_blocks; // then one per request
     int32_t n_frame_blocks;// then one per temporal frame
     int32_t temporal_only;// request role writes only the temporal term
@@ -305,6 +329,19 @@ constexpr int kGatherBlock = MSAO_GATHER_BLOCK;
 #endif
 constexpr int kGatherRows = MSAO_GATHER_ROWS;  // kept rows per gather work item
 constexpr int kMaxLdsKeys = 16384; // 128 KiB of LDS per selection block
+
+// A plain streaming read (msao_calib.hip): wavefront w reads bytes
+// [w * chunk_bytes, (w + 1) * chunk_bytes) of data and writes the XOR of
+// the words it read to sink[w].
+struct ReadArgs {
+    const uint8_t* data;
+    int64_t bytes;
+    int64_t waves;
+    int32_t chunk_bytes;  // a multiple of 8 KiB
+    uint32_t* sink;       // [waves]
+};
+constexpr int kReadBlock = 256;
+int launch_read(const ReadArgs& a, void* stream, void* ev0, void* ev1);
 
 // msao_run_noalloc: the library's own scratch (msao_scratch.hip), one array
 // per GPU in place of the caller's workspace. Its per-call tables are at most

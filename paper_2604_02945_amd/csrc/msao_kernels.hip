@@ -778,7 +778,7 @@ struct PostShared {
     static_assert(kRadixBins % NT == 0, "every thread owns the same number of radix bins");
     uint32_t hist[kRadixBins];
     uint32_t scan[kWaves];
-    uint32_t wcnt[kWaves][2];
+    uint32_t wcnt[kWaves][4];
     unsigned long long lo, hi, red;
     uint64_t nsp[kWaves], dsum[kWaves], ntok[kNumMod], qbits[kNumMod];
     uint32_t digit, below, in_bin, ncand;
@@ -850,12 +850,20 @@ __device__ void rm_aggregate_all(const Tables& t, int r, PostShared<NT>& sh, RMA
     const int lane = threadIdx.x & (kWave - 1);
     const RmEntry e = t.rm[r * kNumMod + m];
     uint64_t nsp = 0, ds = 0;
+    constexpr int U = 8;  // partials in flight per lane (an audio track has ~500)
     for (int j = e.rng_begin; j < e.rng_end; ++j) {
         const WiRange wr = t.rm_rng[j];
-        for (int w = wr.begin + part * kWave + lane; w < wr.end; w += kParts * kWave) {
-            const Partial pr = t.partial[w];
-            nsp += pr.nsparse;
-            ds += pr.dsum;
+        for (int w0 = wr.begin + part * kWave + lane; w0 < wr.end; w0 += U * kParts * kWave) {
+            Partial pr[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) pr[u] = t.partial[min(w0 + u * kParts * kWave, wr.end - 1)];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (w0 + u * kParts * kWave < wr.end) {
+                    nsp += pr[u].nsparse;
+                    ds += pr[u].dsum;
+                }
+            }
         }
     }
     nsp = wave_sum_u64(nsp);
@@ -893,12 +901,17 @@ __device__ void modal_softmax(const double al[kNumMod], const bool pres[kNumMod]
 #pragma unroll
     for (int m = 0; m < kNumMod; ++m)
         if (pres[m] && al[m] > mx) mx = al[m];
-    double den = 0.0;
+    // each exponential once; exp(0) is exactly 1 (the logits of equal
+    // relevance, e.g. none given), so it is not evaluated
+    double ex[kNumMod], den = 0.0;
 #pragma unroll
-    for (int m = 0; m < kNumMod; ++m)
-        if (pres[m]) den += exp(al[m] - mx);
+    for (int m = 0; m < kNumMod; ++m) {
+        const double x = al[m] - mx;
+        ex[m] = pres[m] ? (x == 0.0 ? 1.0 : exp(x)) : 0.0;
+        if (pres[m]) den += ex[m];
+    }
 #pragma unroll
-    for (int m = 0; m < kNumMod; ++m) beta[m] = pres[m] ? exp(al[m] - mx) / den : 0.0;
+    for (int m = 0; m < kNumMod; ++m) beta[m] = pres[m] ? ex[m] / den : 0.0;
 }
 
 struct MasTerms {
@@ -1141,12 +1154,7 @@ template <int NT>
 __device__ void role_frame(const PostArgs& a, int f, PostShared<NT>& sh)
 {
     const Tables& t = a.t;
-    int lo = 0, hi = t.n_tseg;
-    while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (t.seg[t.tseg[mid]].frame_off <= f) lo = mid; else hi = mid;
-    }
-    const DevSeg& sg = t.seg[t.tseg[lo]];
+    const DevSeg& sg = t.seg[t.frame_seg[f]];
     const int tt = f - sg.frame_off;
     const int base = sg.tok_off + tt * sg.P;
     uint64_t acc = 0;
@@ -1164,8 +1172,6 @@ __device__ void role_frame(const PostArgs& a, int f, PostShared<NT>& sh)
 // Selection key Ms*z + Mt*(E - d), order-equivalent to L_s z / C + L_t (E -
 // d) / E (E = C for bit sampling, where Ms = L_s and Mt = L_t): when one
 // weight is 0 the other term alone orders the tokens, so it is used unscaled.
-enum { kKeyZero = 0, kKeyZ = 1, kKeyE = 2, kKeyFull = 3 };
-
 __device__ __forceinline__ uint64_t sel_key(const uint32_t* __restrict__ z, const uint32_t* __restrict__ d,
                                             int g, int kind, uint64_t Ms, uint64_t Mt, uint32_t E)
 {
@@ -1177,27 +1183,78 @@ __device__ __forceinline__ uint64_t sel_key(const uint32_t* __restrict__ z, cons
     }
 }
 
-// Keys of tokens [0, N) of a segment staged into LDS (when in_lds) and their
-// range. U tokens per thread are loaded before any is used, so that the
-// global loads of one thread overlap; indices past N are clamped (and their
-// keys dropped) so that no load sits behind a branch.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_u(uint32_t old, uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROW_MASK, 0xF, false);
+}
+
+// Inclusive prefix sum over the 64 lanes: row_shr 1, 2, 4, 8 give every
+// 16-lane row its own prefix; row_bcast:15 and row_bcast:31 then carry the
+// totals of the rows before.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
+{
+    x += dpp_u<0x111, 0xF>(0u, x);
+    x += dpp_u<0x112, 0xF>(0u, x);
+    x += dpp_u<0x114, 0xF>(0u, x);
+    x += dpp_u<0x118, 0xF>(0u, x);
+    x += dpp_u<0x142, 0xA>(0u, x);
+    x += dpp_u<0x143, 0xC>(0u, x);
+    return x;
+}
+
+// Block-wide exclusive scan of 32-bit counts in thread order (DPP wavefront
+// scans, then the wavefront totals through LDS); *total gets the sum.
+template <int NT>
+__device__ __forceinline__ uint32_t block_exscan_dpp(uint32_t v, PostShared<NT>& sh, uint32_t* total)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wid = threadIdx.x >> 6;
+    const uint32_t inc = wave_incl_scan(v);
+    __syncthreads();
+    if (lane == kWave - 1) sh.scan[wid] = inc;
+    __syncthreads();
+    uint32_t before = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < (NT / kWave); ++i) {
+        const uint32_t t = sh.scan[i];
+        if (i < wid) before += t;
+        tot += t;
+    }
+    *total = tot;
+    return before + inc - v;
+}
+
+// Keys of tokens [0, N) of a selection staged into LDS (when in_lds), each
+// also counted in the histogram of the first radix digit, key >> shift (the
+// keys lie in [0, kmax], so the first digit needs no range of its own). U
+// tokens per thread are loaded before any is used, so that the global loads
+// of one thread overlap; indices past N are clamped (and their values
+// dropped) so that no load sits behind a branch.
 template <int NT, int KIND>
 __device__ __forceinline__ void stage_keys(const uint32_t* __restrict__ z, const uint32_t* __restrict__ d, int N,
                                            uint64_t Ms, uint64_t Mt, uint32_t E, bool in_lds, uint64_t* keys,
-                                           uint64_t& lo, uint64_t& hi)
+                                           uint32_t* hist, int shift, bool count)
 {
     constexpr int U = 8;
     for (int i0 = threadIdx.x; i0 < N; i0 += U * NT) {
-        uint64_t kk[U];
+        uint32_t zz[U], ee[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) kk[u] = sel_key(z, d, min(i0 + u * NT, N - 1), KIND, Ms, Mt, E);
+        for (int u = 0; u < U; ++u) {
+            const int g = min(i0 + u * NT, N - 1);
+            zz[u] = KIND == kKeyZ || KIND == kKeyFull ? z[g] : 0u;
+            ee[u] = KIND == kKeyE || KIND == kKeyFull ? E - d[g] : 0u;
+        }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int i = i0 + u * NT;
             if (i < N) {
-                if (in_lds) keys[i] = kk[u];
-                lo = kk[u] < lo ? kk[u] : lo;
-                hi = kk[u] > hi ? kk[u] : hi;
+                uint64_t key = 0ull;
+                if constexpr (KIND == kKeyZ) key = zz[u];
+                else if constexpr (KIND == kKeyE) key = ee[u];
+                else if constexpr (KIND == kKeyFull) key = Ms * (uint64_t)zz[u] + Mt * (uint64_t)ee[u];
+                if (in_lds) keys[i] = key;
+                if (count) atomicAdd(&hist[(uint32_t)(key >> shift)], 1u);
             }
         }
     }
@@ -1214,7 +1271,7 @@ __device__ __forceinline__ int guided_keep_count(float mas, int N)
 }
 
 // Where the selection keys are read from: staged in LDS, or recomputed from
-// z and d for segments larger than the LDS staging area.
+// z and d for selections larger than the LDS staging area.
 struct KeySrc {
     const uint64_t* keys;
     const uint32_t* z;
@@ -1231,13 +1288,16 @@ struct KeySrc {
 };
 
 // Rank k-1 of the N keys of a selection (range [lo, hi]) by MSD radix
-// select, then keep flags (at off + i) and ascending kept indices (iadd + i,
-// written from ioff). IN_LDS: every key is staged in LDS.
+// select; then this block's slice [s0, s1) of keep flags (at off + i) and
+// ascending kept indices (iadd + i, written from ioff). IN_LDS: every key is
+// staged in LDS.
 template <int NT, bool IN_LDS>
 __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const KeySrc& src, uint64_t* cand,
-                                   int cand_cap, int N, int k, int off, int ioff, int iadd, uint64_t lo, uint64_t hi)
+                                   int cand_cap, int N, int k, int off, int ioff, int iadd, uint64_t lo, uint64_t hi,
+                                   int s0, int s1, bool first_hist_ready)
 {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid >> 6;
+    constexpr int kW = NT / kWave;
     auto key_at = [&](int i) -> uint64_t { return src.at<IN_LDS>(i); };
     // radix select of the key of rank k-1 among key - lo, most significant digit
     // first. Once the candidate range holds at most cand_cap keys, the next
@@ -1248,51 +1308,57 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
     uint32_t below = 0;            // keys below the current candidate range
     uint32_t rank = (uint32_t)k - 1;
     int bits = hi > lo ? 64 - __clzll((long long)(hi - lo)) : 0;
+    bool built = first_hist_ready;  // the first digit's histogram was counted while staging
     while (bits > 0) {
         const int db = bits < kRadixBits ? bits : kRadixBits;
         const int shift = bits - db;
         const uint64_t mask = (1ull << db) - 1ull;
         // copy out the candidates once they are few (and fewer than half the keys)
         const bool collect = ncand < 0 && in_range <= (uint32_t)cand_cap && 2 * in_range < (uint32_t)N;
-        for (int b = tid; b < kRadixBins; b += NT) sh.hist[b] = 0u;
-        if (tid == 0) sh.ncand = 0u;
-        __syncthreads();
-        // wave-uniform loop over the keys (or candidates), U x 64 per step
-        constexpr int U = 4;
-        const int nscan = ncand >= 0 ? ncand : N;
-        for (int base = wid * kWave; base < nscan; base += U * NT) {
-            uint64_t x[U];
-            // clamped indices: every load is issued before any is used
-            if (ncand >= 0) {
+        const bool first = in_range == (uint32_t)N && below == 0u && prefix == 0ull;
+        if (!built) {
+            for (int b = tid; b < kRadixBins; b += NT) sh.hist[b] = 0u;
+            if (tid == 0) sh.ncand = 0u;
+            __syncthreads();
+            // wave-uniform loop over the keys (or candidates), U x 64 per step
+            constexpr int U = 4;
+            const int nscan = ncand >= 0 ? ncand : N;
+            for (int base = wid * kWave; base < nscan; base += U * NT) {
+                uint64_t x[U];
+                // clamped indices: every load is issued before any is used
+                if (ncand >= 0) {
 #pragma unroll
-                for (int u = 0; u < U; ++u) x[u] = cand[min(base + u * NT + lane, nscan - 1)];
-            } else {
+                    for (int u = 0; u < U; ++u) x[u] = cand[min(base + u * NT + lane, nscan - 1)];
+                } else {
 #pragma unroll
-                for (int u = 0; u < U; ++u) x[u] = key_at(min(base + u * NT + lane, N - 1)) - lo;
-            }
+                    for (int u = 0; u < U; ++u) x[u] = key_at(min(base + u * NT + lane, N - 1)) - lo;
+                }
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const bool match = base + u * NT + lane < nscan &&
-                                   (bits >= 64 ? 0ull : (x[u] >> bits)) == prefix;
-                if (match) atomicAdd(&sh.hist[(x[u] >> shift) & mask], 1u);
-                if (collect) {
-                    const uint64_t m = __ballot(match);
-                    if (m) {
-                        uint32_t at = 0;
-                        if (lane == 0) at = atomicAdd(&sh.ncand, (uint32_t)__popcll(m));
-                        at = (uint32_t)__shfl((int)at, 0);
-                        if (match) cand[at + lanes_below(m)] = x[u];
+                for (int u = 0; u < U; ++u) {
+                    // the first pass (no digit fixed yet) takes every key
+                    const bool match = base + u * NT + lane < nscan &&
+                                       (first || (bits >= 64 ? 0ull : (x[u] >> bits)) == prefix);
+                    if (match) atomicAdd(&sh.hist[(x[u] >> shift) & mask], 1u);
+                    if (collect) {
+                        const uint64_t m = __ballot(match);
+                        if (m) {
+                            uint32_t at = 0;
+                            if (lane == 0) at = atomicAdd(&sh.ncand, (uint32_t)__popcll(m));
+                            at = (uint32_t)__shfl((int)at, 0);
+                            if (match) cand[at + lanes_below(m)] = x[u];
+                        }
                     }
                 }
             }
+            __syncthreads();
+            if (collect) ncand = (int)sh.ncand;
         }
-        __syncthreads();
-        if (collect) ncand = (int)sh.ncand;
+        built = false;
         uint32_t local = 0;
 #pragma unroll
         for (int j = 0; j < (kRadixBins / NT); ++j) local += sh.hist[tid * (kRadixBins / NT) + j];
         uint32_t tot;
-        const uint32_t ex = block_exscan(local, sh, &tot);
+        const uint32_t ex = block_exscan_dpp(local, sh, &tot);
         if (ex <= rank && rank < ex + local) {
             uint32_t cum = ex;
             for (int j = 0; j < (kRadixBins / NT); ++j) {
@@ -1318,11 +1384,26 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
     const uint64_t vstar = lo + prefix;        // key of rank k-1
     const uint32_t ties = (uint32_t)k - below; // keys equal to vstar that are kept, lowest index first
 
-    // each wavefront compacts one contiguous range of indices, 4 x 64 at a time
+    // counts of keys below and equal to vstar before this block's slice (the
+    // prefix [0, s0) split evenly over the wavefronts), and in each
+    // wavefront's contiguous range of the slice
     constexpr int U = 4;
-    const int per = (((N + (NT / kWave) - 1) / (NT / kWave)) + kWave - 1) / kWave * kWave;
-    const int b0 = min(N, wid * per), b1 = min(N, b0 + per);
-    uint32_t nlt = 0, neq = 0;
+    const int pw = (((s0 + kW - 1) / kW) + kWave - 1) / kWave * kWave;
+    const int per = ((((s1 - s0) + kW - 1) / kW) + kWave - 1) / kWave * kWave;
+    const int p0 = min(s0, wid * pw), p1 = min(s0, p0 + pw);
+    const int b0 = min(s1, s0 + wid * per), b1 = min(s1, b0 + per);
+    uint32_t plt = 0, peq = 0, nlt = 0, neq = 0;
+    for (int base = p0; base < p1; base += U * kWave) {
+        uint64_t kv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) kv[u] = key_at(min(base + u * kWave + lane, p1 - 1));
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const bool v = base + u * kWave + lane < p1;
+            plt += (uint32_t)__popcll(__ballot(v && kv[u] < vstar));
+            peq += (uint32_t)__popcll(__ballot(v && kv[u] == vstar));
+        }
+    }
     for (int base = b0; base < b1; base += U * kWave) {
         uint64_t kv[U];
 #pragma unroll
@@ -1337,12 +1418,15 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
     if (lane == 0) {
         sh.wcnt[wid][0] = nlt;
         sh.wcnt[wid][1] = neq;
+        sh.wcnt[wid][2] = plt;
+        sh.wcnt[wid][3] = peq;
     }
     __syncthreads();
     uint32_t lt_before = 0, eq_before = 0;
-    for (int q = 0; q < wid; ++q) {
-        lt_before += sh.wcnt[q][0];
-        eq_before += sh.wcnt[q][1];
+#pragma unroll
+    for (int q = 0; q < kW; ++q) {
+        lt_before += sh.wcnt[q][2] + (q < wid ? sh.wcnt[q][0] : 0u);
+        eq_before += sh.wcnt[q][3] + (q < wid ? sh.wcnt[q][1] : 0u);
     }
     uint32_t eq_run = eq_before;
     uint32_t kept_run = lt_before + min(eq_before, ties);
@@ -1372,87 +1456,85 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
 // (Sec. 4.1.1 pruning, k from the Eq. 11 floor or a fixed ratio). Keys are
 // staged in LDS when they fit (keys_cap entries), then an MSD radix select
 // finds the key of rank k-1 and each wavefront compacts a contiguous index
-// range with ballot/mbcnt. Frame f of a clip keeping k_f per frame writes
-// its kept indices at positions f k_f.. of the segment's range and its
-// share, P - k_f entries, of the -1 tail after the T k_f kept ones.
+// range of the block's slice with ballot/mbcnt. A selection split over
+// nparts blocks has every block find the same key from all of the keys and
+// write its own slice (and its share of the -1 tail). Frame f of a clip
+// keeping k_f per frame writes its kept indices at positions f k_f.. of the
+// segment's range and its share, P - k_f entries, of the -1 tail after the
+// T k_f kept ones.
 template <int NT>
 __device__ void role_select(const PostArgs& a, int unit, PostShared<NT>& sh, uint64_t* keys, int keys_cap)
 {
     const Tables& t = a.t;
     const SelUnit su = t.sel_unit[unit];
-    const int s = su.seg, f = su.frame;
-    const DevSeg sg = t.seg[s];
+    const int N = su.N, f = su.frame, tid = threadIdx.x, lane = tid & (kWave - 1);
     const bool framed = f >= 0;
-    const int N = framed ? sg.P : sg.n_tok;
-    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid >> 6;
-    int k = framed ? sg.kf : sg.k;
+    int k = su.kfix;
     if (k < 0) {
         float mas;
         if (a.mas_in) {
-            mas = a.mas_in[sg.request * kNumMod + sg.modality];
+            mas = a.mas_in[su.request * kNumMod + su.modality];
         } else {
             RMAgg g[kNumMod];
-            rm_aggregate_all(t, sg.request, sh, g);
+            rm_aggregate_all(t, su.request, sh, g);
             MasTerms o[kNumMod];
             bool pres[kNumMod];
-            request_terms(t, sg.request, g, o, pres);
+            request_terms(t, su.request, g, o, pres);
             mas = 0.0f;
 #pragma unroll
             for (int m = 0; m < kNumMod; ++m)
-                if (m == sg.modality) mas = (float)o[m].mas;
+                if (m == su.modality) mas = (float)o[m].mas;
         }
         k = guided_keep_count(mas, N);
     }
-    const int units = framed ? sg.T : 1;
-    if (tid == 0 && f <= 0) a.sel.kept_count[s] = k * units;
-    const int off = sg.tok_off + (framed ? f * sg.P : 0);      // keys and keep flags
-    const int ioff = sg.tok_off + (framed ? f * k : 0);        // kept indices
-    const int iadd = framed ? f * sg.P : 0;                    // local index of the selection's first token
-    const int fill = sg.tok_off + units * k + (framed ? f : 0) * (N - k);
-    for (int i = tid; i < N - k; i += NT) a.sel.kept_idx[fill + i] = -1;
+    if (tid == 0 && f <= 0 && su.part == 0) a.sel.kept_count[su.seg] = k * su.units;
+    const int off = su.off;                                     // keys and keep flags
+    const int ioff = su.seg_off + (framed ? f * k : 0);         // kept indices
+    const int iadd = framed ? f * N : 0;                        // local index of the selection's first token
+    const int fill = su.seg_off + su.units * k + (framed ? f : 0) * (N - k);
+    {
+        const int tail = N - k, share = (tail + su.nparts - 1) / su.nparts;
+        const int t0 = min(tail, su.part * share), t1 = min(tail, t0 + share);
+        for (int i = t0 + tid; i < t1; i += NT) a.sel.kept_idx[fill + i] = -1;
+    }
     if (N == 0) return;
+    // this block's slice of the tokens (whole wavefront chunks)
+    const int slice = ((N + su.nparts - 1) / su.nparts + kWave - 1) / kWave * kWave;
+    const int s0 = min(N, su.part * slice), s1 = min(N, s0 + slice);
     if (k == 0 || k == N) {
-        for (int i = tid; i < N; i += NT) {
+        for (int i = s0 + tid; i < s1; i += NT) {
             if (a.sel.keep) a.sel.keep[off + i] = k == N ? 1 : 0;
             if (k == N) a.sel.kept_idx[ioff + i] = iadd + i;
         }
         return;
     }
-    const int kind = sg.temporal && sg.L_t > 0 ? (sg.L_s > 0 ? kKeyFull : kKeyE) : (sg.L_s > 0 ? kKeyZ : kKeyZero);
-    const uint64_t Ms = sg.key_ms, Mt = sg.key_mt;
-    const uint32_t E = (uint32_t)sg.E;
+    const int kind = su.kind;
+    const uint64_t Ms = su.Ms, Mt = su.Mt;
+    const uint32_t E = su.E;
     const uint32_t* z = a.z + off;
     const uint32_t* d = a.d ? a.d + off : nullptr;
     const bool in_lds = N <= keys_cap;
 
-    // keys (staged in LDS) and their range
-    if (tid == 0) {
-        sh.lo = ~0ull;
-        sh.hi = 0ull;
+    // keys (staged in LDS) in [0, kmax], counted in the first digit's histogram
+    const uint64_t lo = 0ull, hi = su.kmax;
+    const int bits = hi > 0 ? 64 - __clzll((long long)hi) : 0;
+    const int shift0 = bits > kRadixBits ? bits - kRadixBits : 0;
+    for (int b = tid; b < kRadixBins; b += NT) sh.hist[b] = 0u;
+    __syncthreads();
+    switch (kind) {
+    case kKeyZ: stage_keys<NT, kKeyZ>(z, d, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
+    case kKeyE: stage_keys<NT, kKeyE>(z, d, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
+    case kKeyFull: stage_keys<NT, kKeyFull>(z, d, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
+    default: stage_keys<NT, kKeyZero>(z, d, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, false); break;
     }
     __syncthreads();
-    {
-        uint64_t lo = ~0ull, hi = 0ull;
-        switch (kind) {
-        case kKeyZ: stage_keys<NT, kKeyZ>(z, d, N, Ms, Mt, E, in_lds, keys, lo, hi); break;
-        case kKeyE: stage_keys<NT, kKeyE>(z, d, N, Ms, Mt, E, in_lds, keys, lo, hi); break;
-        case kKeyFull: stage_keys<NT, kKeyFull>(z, d, N, Ms, Mt, E, in_lds, keys, lo, hi); break;
-        default: stage_keys<NT, kKeyZero>(z, d, N, Ms, Mt, E, in_lds, keys, lo, hi); break;
-        }
-        lo = wave_min_u64(lo);
-        hi = wave_max_u64(hi);
-        if (lane == 0) {
-            atomicMin(&sh.lo, (unsigned long long)lo);
-            atomicMax(&sh.hi, (unsigned long long)hi);
-        }
-    }
-    __syncthreads();
-    const uint64_t lo = sh.lo, hi = sh.hi;
 
     const KeySrc src{keys, z, d, kind, Ms, Mt, E};
     uint64_t* cand = keys + keys_cap;
-    if (in_lds) select_and_compact<NT, true>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, ioff, iadd, lo, hi);
-    else select_and_compact<NT, false>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, ioff, iadd, lo, hi);
+    if (in_lds)
+        select_and_compact<NT, true>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, ioff, iadd, lo, hi, s0, s1, true);
+    else
+        select_and_compact<NT, false>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, ioff, iadd, lo, hi, s0, s1, true);
 }
 
 // LR: a learned call (request role with head counts, descriptors and the

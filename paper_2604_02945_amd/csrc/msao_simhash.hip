@@ -543,12 +543,7 @@ __device__ __forceinline__ uint64_t block_sum(uint64_t v, uint64_t* red)
 __device__ void hash_frame(const HashArgs& a, int f, uint64_t* red)
 {
     const Tables& t = a.t;
-    int lo = 0, hi = t.n_tseg;
-    while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (t.seg[t.tseg[mid]].frame_off <= f) lo = mid; else hi = mid;
-    }
-    const DevSeg& sg = t.seg[t.tseg[lo]];
+    const DevSeg& sg = t.seg[t.frame_seg[f]];
     const int tt = f - sg.frame_off;
     const int base = sg.tok_off + tt * sg.P;
     const uint64_t ones = all_bits(sg.hash_bits);

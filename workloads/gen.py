@@ -14,6 +14,7 @@ either as float32 or as bf16 bit patterns (uint16, round-to-nearest-even).
 from __future__ import annotations
 
 import dataclasses
+import os
 from typing import List, Optional
 
 import numpy as np
@@ -151,22 +152,21 @@ def _image_gelu(rng, n_tok, hidden, bg_mask, bg_scale=0.05):
     return x
 
 
-def _config1(seed, n_req):
+def _config1(seed, r):
     segs = []
-    for r in range(n_req):
-        rng = _rng(seed, 1, r, 0)
-        h, w = (15, 23) if rng.integers(2) == 0 else (23, 15)
-        top = int(rng.integers(24 - h + 1))
-        left = int(rng.integers(24 - w + 1))
-        mask = np.zeros((24, 24), dtype=bool)
-        mask[top:top + h, left:left + w] = True
-        mask = mask.reshape(-1)
-        img = _image_relu(rng, 576, 1024, mask)
-        segs.append(Segment(r, IMAGE, 1, 576, 1024, "f32", 0.5, _encode(img, "f32"),
-                            {"bg_mask": mask}))
-        rng_t = _rng(seed, 1, r, 1)
-        txt = np.maximum(rng_t.standard_normal((32, 1024), dtype=np.float32), 0.0)
-        segs.append(Segment(r, TEXT, 1, 32, 1024, "f32", 1.0, _encode(txt, "f32")))
+    rng = _rng(seed, 1, r, 0)
+    h, w = (15, 23) if rng.integers(2) == 0 else (23, 15)
+    top = int(rng.integers(24 - h + 1))
+    left = int(rng.integers(24 - w + 1))
+    mask = np.zeros((24, 24), dtype=bool)
+    mask[top:top + h, left:left + w] = True
+    mask = mask.reshape(-1)
+    img = _image_relu(rng, 576, 1024, mask)
+    segs.append(Segment(r, IMAGE, 1, 576, 1024, "f32", 0.5, _encode(img, "f32"),
+                        {"bg_mask": mask}))
+    rng_t = _rng(seed, 1, r, 1)
+    txt = np.maximum(rng_t.standard_normal((32, 1024), dtype=np.float32), 0.0)
+    segs.append(Segment(r, TEXT, 1, 32, 1024, "f32", 1.0, _encode(txt, "f32")))
     return segs
 
 
@@ -184,12 +184,8 @@ def _text_bf16_gelu_segment(seed, config, r, seg_id, n_tok):
     return Segment(r, TEXT, 1, n_tok, 4096, "bf16", 1.0, _encode(txt, "bf16"))
 
 
-def _config2(seed, n_req):
-    segs = []
-    for r in range(n_req):
-        segs.append(_image_bf16_gelu_segment(seed, 2, r, 0, 0.25))
-        segs.append(_text_bf16_gelu_segment(seed, 2, r, 1, 64))
-    return segs
+def _config2(seed, r):
+    return [_image_bf16_gelu_segment(seed, 2, r, 0, 0.25), _text_bf16_gelu_segment(seed, 2, r, 1, 64)]
 
 
 def video_clip(rng, n_frames, grid, hidden, static_frac=0.7, step_sigma=0.02):
@@ -212,13 +208,10 @@ def video_clip(rng, n_frames, grid, hidden, static_frac=0.7, step_sigma=0.02):
     return out, static
 
 
-def _config3(seed, n_req):
-    segs = []
-    for r in range(n_req):
-        rng = _rng(seed, 3, r, 0)
-        data, static = video_clip(rng, 32, 16, 1024)
-        segs.append(Segment(r, VIDEO, 32, 256, 1024, "bf16", 0.3, data, {"static_mask": static}))
-    return segs
+def _config3(seed, r):
+    rng = _rng(seed, 3, r, 0)
+    data, static = video_clip(rng, 32, 16, 1024)
+    return [Segment(r, VIDEO, 32, 256, 1024, "bf16", 0.3, data, {"static_mask": static})]
 
 
 def silence_runs(rng, n_frames, n_silent, n_runs):
@@ -235,49 +228,57 @@ def silence_runs(rng, n_frames, n_silent, n_runs):
     return mask
 
 
-def _config4(seed, n_req):
-    segs = []
-    for r in range(n_req):
-        segs.append(_image_bf16_gelu_segment(seed, 4, r, 0, 0.25))
-        rng = _rng(seed, 4, r, 1)
-        mask = silence_runs(rng, 1500, 600, 4)
-        aud = rng.standard_normal((1500, 1280), dtype=np.float32)
-        aud[mask] *= np.float32(1e-3)
-        segs.append(Segment(r, AUDIO, 1, 1500, 1280, "bf16", 0.5, _encode(aud, "bf16"),
-                            {"silence_mask": mask}))
-        segs.append(_text_bf16_gelu_segment(seed, 4, r, 2, 128))
+def _config4(seed, r):
+    segs = [_image_bf16_gelu_segment(seed, 4, r, 0, 0.25)]
+    rng = _rng(seed, 4, r, 1)
+    mask = silence_runs(rng, 1500, 600, 4)
+    aud = rng.standard_normal((1500, 1280), dtype=np.float32)
+    aud[mask] *= np.float32(1e-3)
+    segs.append(Segment(r, AUDIO, 1, 1500, 1280, "bf16", 0.5, _encode(aud, "bf16"),
+                        {"silence_mask": mask}))
+    segs.append(_text_bf16_gelu_segment(seed, 4, r, 2, 128))
     return segs
 
 
-def _config5(seed, n_req):
-    segs = []
+def _config5(seed, r):
     shapes = [(12, 24), (16, 18), (18, 16), (24, 12)]
-    for r in range(n_req):
-        rng = _rng(seed, 5, r, 0)
-        masks = []
-        for _tile in range(5):
-            h, w = shapes[int(rng.integers(4))]
-            top = int(rng.integers(24 - h + 1))
-            left = int(rng.integers(24 - w + 1))
-            m = np.zeros((24, 24), dtype=bool)
-            m[top:top + h, left:left + w] = True
-            masks.append(m.reshape(-1))
-        bg = np.concatenate(masks)
-        img = _image_relu(rng, 2880, 1024, bg)
-        segs.append(Segment(r, IMAGE, 1, 2880, 1024, "bf16", 0.25, _encode(img, "bf16"),
-                            {"bg_mask": bg}))
-    return segs
+    rng = _rng(seed, 5, r, 0)
+    masks = []
+    for _tile in range(5):
+        h, w = shapes[int(rng.integers(4))]
+        top = int(rng.integers(24 - h + 1))
+        left = int(rng.integers(24 - w + 1))
+        m = np.zeros((24, 24), dtype=bool)
+        m[top:top + h, left:left + w] = True
+        masks.append(m.reshape(-1))
+    bg = np.concatenate(masks)
+    img = _image_relu(rng, 2880, 1024, bg)
+    return [Segment(r, IMAGE, 1, 2880, 1024, "bf16", 0.25, _encode(img, "bf16"), {"bg_mask": bg})]
 
 
 _FULL_REQUESTS = {1: 1, 2: 64, 3: 8, 4: 32, 5: 256}
 _BUILDERS = {1: _config1, 2: _config2, 3: _config3, 4: _config4, 5: _config5}
 
 
-def make_workload(config: int, seed: int = 0, n_requests: Optional[int] = None) -> Workload:
-    """Build benchmark workload `config` (1..5); `n_requests` takes a prefix of its requests."""
+def make_workload(config: int, seed: int = 0, n_requests: Optional[int] = None, threads: int = 0) -> Workload:
+    """Build benchmark workload `config` (1..5); `n_requests` takes a prefix of its requests.
+
+    Requests are drawn independently (each from its own seeded generator), so
+    they may be built on several threads (numpy's generators and ufuncs release
+    the interpreter lock on large arrays); the result is the same for any
+    `threads` (0: up to 16, the host's cores permitting)."""
+    from concurrent.futures import ThreadPoolExecutor
+
     full = _FULL_REQUESTS[config]
     n = full if n_requests is None else min(int(n_requests), full)
-    segs = _BUILDERS[config](seed, n)
+    nt = threads if threads > 0 else max(1, min(16, os.cpu_count() or 1))
+    build = _BUILDERS[config]
+    if nt == 1 or n <= 1:
+        parts = [build(seed, r) for r in range(n)]
+    else:
+        with ThreadPoolExecutor(min(nt, n)) as ex:
+            parts = list(ex.map(lambda r: build(seed, r), range(n)))
+    segs = [s for p in parts for s in p]
     return Workload(CONFIG_NAMES[config], config, n, segs, default_params(), None)
 
 
