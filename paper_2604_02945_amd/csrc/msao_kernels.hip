@@ -780,6 +780,7 @@ struct PostShared {
     uint32_t scan[kWaves];
     uint32_t wcnt[kWaves][4];
     unsigned long long lo, hi, red;
+    uint64_t vsel;            // selection: key of the wanted rank among few candidates
     uint64_t nsp[kWaves], dsum[kWaves], ntok[kNumMod], qbits[kNumMod];
     uint32_t digit, below, in_bin, ncand;
     // learned calls
@@ -792,6 +793,7 @@ struct PostShared {
 // Radix candidates copied out of the staged keys once few remain (LDS entries
 // after the keys).
 constexpr int kMaxCand = 2048;
+constexpr int kSmallCand = 256;  // candidates ranked directly instead of by further digit passes
 __device__ __host__ __forceinline__ int cand_cap_for(int keys_cap) { return keys_cap < kMaxCand ? keys_cap : kMaxCand; }
 
 // Block-wide sum of a 64-bit integer (exact, so the order does not matter).
@@ -1309,6 +1311,7 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
     uint32_t rank = (uint32_t)k - 1;
     int bits = hi > lo ? 64 - __clzll((long long)(hi - lo)) : 0;
     bool built = first_hist_ready;  // the first digit's histogram was counted while staging
+    constexpr int U = 4;
     while (bits > 0) {
         const int db = bits < kRadixBits ? bits : kRadixBits;
         const int shift = bits - db;
@@ -1316,12 +1319,81 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
         // copy out the candidates once they are few (and fewer than half the keys)
         const bool collect = ncand < 0 && in_range <= (uint32_t)cand_cap && 2 * in_range < (uint32_t)N;
         const bool first = in_range == (uint32_t)N && below == 0u && prefix == 0ull;
+        if (!built && collect && in_range <= (uint32_t)kSmallCand) {
+            // so few keys are left that a copy of them and a direct rank among
+            // them cost less than the remaining digit passes
+            if (tid == 0) sh.ncand = 0u;
+            __syncthreads();
+            for (int base = wid * kWave; base < N; base += U * NT) {
+                uint64_t x[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) x[u] = key_at(min(base + u * NT + lane, N - 1)) - lo;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const bool match = base + u * NT + lane < N && (x[u] >> bits) == prefix;
+                    const uint64_t m = __ballot(match);
+                    if (m) {
+                        uint32_t at = 0;
+                        if (lane == 0) at = atomicAdd(&sh.ncand, (uint32_t)__popcll(m));
+                        at = (uint32_t)__shfl((int)at, 0);
+                        if (match) cand[at + lanes_below(m)] = x[u];
+                    }
+                }
+            }
+            __syncthreads();
+            // candidate c = (w % cw) * 64 + lane is counted against the j-range
+            // part w / cw of the candidates by wavefront w; the parts' counts
+            // of smaller and of not larger candidates meet in LDS
+            const int m = (int)sh.ncand;
+            const int cw = (m + kWave - 1) / kWave, nparts = kW / cw;
+            const int c = (wid % cw) * kWave + lane, part = wid / cw;
+            const int per = (m + nparts - 1) / nparts, j0 = min(m, part * per), j1 = min(m, j0 + per);
+            uint32_t lt = 0, le = 0;
+            if (part < nparts && c < m) {
+                const uint64_t v = cand[c];
+                for (int j = j0; j < j1; j += 4) {
+                    uint64_t x[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) x[u] = cand[min(j + u, j1 - 1)];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const bool in = j + u < j1;
+                        lt += in && x[u] < v ? 1u : 0u;
+                        le += in && x[u] <= v ? 1u : 0u;
+                    }
+                }
+            }
+            const int slot = part * cw * kWave + c;  // < kW * 64 = NT
+            if (part < nparts) {
+                sh.hist[slot] = lt;
+                sh.hist[NT + slot] = le;
+            }
+            __syncthreads();
+            if (tid < m) {
+                const int cc = tid;
+                uint32_t lt_all = 0, le_all = 0;
+                for (int q = 0; q < nparts; ++q) {
+                    lt_all += sh.hist[q * cw * kWave + cc];
+                    le_all += sh.hist[NT + q * cw * kWave + cc];
+                }
+                // every candidate equal to the one of this rank writes the same values
+                if (lt_all <= rank && rank < le_all) {
+                    sh.vsel = cand[cc];
+                    sh.below = lt_all;
+                }
+            }
+            __syncthreads();
+            prefix = sh.vsel;
+            below += sh.below;
+            bits = 0;
+            __syncthreads();
+            break;
+        }
         if (!built) {
             for (int b = tid; b < kRadixBins; b += NT) sh.hist[b] = 0u;
             if (tid == 0) sh.ncand = 0u;
             __syncthreads();
             // wave-uniform loop over the keys (or candidates), U x 64 per step
-            constexpr int U = 4;
             const int nscan = ncand >= 0 ? ncand : N;
             for (int base = wid * kWave; base < nscan; base += U * NT) {
                 uint64_t x[U];
@@ -1387,7 +1459,6 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
     // counts of keys below and equal to vstar before this block's slice (the
     // prefix [0, s0) split evenly over the wavefronts), and in each
     // wavefront's contiguous range of the slice
-    constexpr int U = 4;
     const int pw = (((s0 + kW - 1) / kW) + kWave - 1) / kWave * kWave;
     const int per = ((((s1 - s0) + kW - 1) / kW) + kWave - 1) / kWave * kWave;
     const int p0 = min(s0, wid * pw), p1 = min(s0, p0 + pw);
