@@ -233,8 +233,12 @@ def run_learned(segments: Sequence, n_requests: int, params: dict, heads: Option
     (Eq. 6). heads[s] is None or a dict(weight=[hidden] array in the
     segment's encoding, bias, grid_w, pool); mlp is None or a dict(w1=[hidden,
     prompt_dim + 8], b1, w2, b2, prompt=[n_requests, prompt_dim]) of float32.
-    Returns the outputs of run() (rho, beta, mas, agg updated) plus
-    importance (per token), alpha and desc (per request and modality)."""
+    Returns the outputs of run() (rho, beta, mas, agg updated), the
+    selection by the learned importance (k, keep, kept_idx: a segment with a
+    head keeps its k tokens of largest Eq. 3 importance, ties by index, a NaN
+    importance as 0; the others as run(); a negative keep ratio takes this
+    MAS) and its compacted rows (compact), plus importance (per token), alpha
+    and desc (per request and modality)."""
     L = lib()
     n = len(segments)
     ntok = sum(s.n_frames * s.tokens_per_frame for s in segments)
@@ -282,6 +286,7 @@ def run_learned(segments: Sequence, n_requests: int, params: dict, heads: Option
     o["alpha"] = alpha[:R * NMOD]
     o["desc"] = desc[:R * NMOD * DESC].reshape(R * NMOD, DESC)
     o["k"] = o["k"][:n]
+    o["compact"] = compact_rows(segments, o["k"], o["kept_idx"])
     return o
 
 

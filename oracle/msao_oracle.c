@@ -263,21 +263,59 @@ static int select_range(const orc_segment* s, const orc_params* p, const uint32_
     return 0;
 }
 
+typedef struct { double m; int64_t idx; } orc_imp_pair;
+
+/* The more important token first: larger importance, then smaller index. */
+static int imp_cmp(const void* a, const void* b)
+{
+    const orc_imp_pair* x = (const orc_imp_pair*)a;
+    const orc_imp_pair* y = (const orc_imp_pair*)b;
+    if (x->m != y->m) return x->m > y->m ? -1 : 1;
+    if (x->idx != y->idx) return x->idx < y->idx ? -1 : 1;
+    return 0;
+}
+
+/* Selection among tokens [i0, i0 + n) of a segment by a learned importance
+ * (Sec. 4.1.1: the patches of low Eq. 3 importance are pruned): the k of
+ * largest importance, ties by ascending index; an importance that is NaN or
+ * not above 0 counts as 0, the least important. */
+static int select_range_importance(const double* imp, int64_t i0, int64_t n, int64_t k, uint8_t* keep)
+{
+    orc_imp_pair* pairs = (orc_imp_pair*)malloc(sizeof(orc_imp_pair) * (size_t)(n > 0 ? n : 1));
+    if (!pairs) return -1;
+    for (int64_t j = 0; j < n; ++j) {
+        const double m = imp[i0 + j];
+        pairs[j].m = (m > 0.0) ? m : 0.0;  /* NaN compares false */
+        pairs[j].idx = i0 + j;
+    }
+    qsort(pairs, (size_t)n, sizeof(orc_imp_pair), imp_cmp);
+    for (int64_t j = 0; j < n; ++j) keep[i0 + j] = 0;
+    for (int64_t j = 0; j < k; ++j) keep[pairs[j].idx] = 1;
+    free(pairs);
+    return 0;
+}
+
 /* Selection of one segment with keep ratio kappa: the whole segment, or
- * (per-frame scope) each of its T frames of P tokens on its own. Kept
+ * (per-frame scope) each of its T frames of P tokens on its own. imp (the
+ * segment's tokens' learned importance) or NULL (the redundancy key). Kept
  * indices ascending, then -1. Returns the keep count. */
 static int64_t select_segment(const orc_segment* s, const orc_params* p, const uint32_t* z,
-                              const uint32_t* d, int64_t E, double kappa, uint8_t* keep, int32_t* kept_idx)
+                              const uint32_t* d, int64_t E, double kappa, const double* imp, uint8_t* keep,
+                              int32_t* kept_idx)
 {
     int64_t T = s->n_frames, P = s->tokens_per_frame, N = T * P, k = 0;
     if (p->flags & ORC_FLAG_SELECT_PER_FRAME) {
         int64_t kf = keep_count(kappa, P);
-        for (int64_t t = 0; t < T; ++t)
-            if (select_range(s, p, z, d, E, t * P, P, kf, keep)) return -1;
+        for (int64_t t = 0; t < T; ++t) {
+            const int rc = imp ? select_range_importance(imp, t * P, P, kf, keep)
+                               : select_range(s, p, z, d, E, t * P, P, kf, keep);
+            if (rc) return -1;
+        }
         k = kf * T;
     } else {
         k = keep_count(kappa, N);
-        if (select_range(s, p, z, d, E, 0, N, k, keep)) return -1;
+        const int rc = imp ? select_range_importance(imp, 0, N, k, keep) : select_range(s, p, z, d, E, 0, N, k, keep);
+        if (rc) return -1;
     }
     int64_t w = 0;
     for (int64_t i = 0; i < N; ++i)
@@ -288,10 +326,11 @@ static int64_t select_segment(const orc_segment* s, const orc_params* p, const u
 
 /* Selection over all segments from per-token z, d (E[s]: bits compared per
  * token of segment s) and per-(request, modality) MAS (used only by segments
- * with a negative keep ratio). */
+ * with a negative keep ratio). by_imp (may be NULL): segments s with
+ * by_imp[s] set are ranked by the per-token importance imp instead. */
 static int select_all(const orc_segment* segs, int n, int R, const orc_params* p,
                       const uint32_t* z, const uint32_t* d, const int64_t* E, const float* mas,
-                      int32_t* k_out, uint8_t* keep, int32_t* kept_idx)
+                      const double* imp, const int* by_imp, int32_t* k_out, uint8_t* keep, int32_t* kept_idx)
 {
     int64_t off = 0;
     for (int s = 0; s < n; ++s) {
@@ -304,7 +343,8 @@ static int select_all(const orc_segment* segs, int n, int R, const orc_params* p
         } else {
             kappa = (double)sg->keep_ratio;
         }
-        int64_t k = select_segment(sg, p, z + off, d ? d + off : NULL, E[s], kappa, keep + off, kept_idx + off);
+        const double* im = (by_imp && by_imp[s]) ? imp + off : NULL;
+        int64_t k = select_segment(sg, p, z + off, d ? d + off : NULL, E[s], kappa, im, keep + off, kept_idx + off);
         if (k < 0) return -1;
         k_out[s] = (int32_t)k;
         off += N;
@@ -321,7 +361,7 @@ int orc_select(const orc_segment* segs, int n, int R, const orc_params* p,
     int64_t* E = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
     if (!E) return -1;
     for (int s = 0; s < n; ++s) E[s] = segs[s].hidden;
-    int rc = select_all(segs, n, R, p, z, d, E, mas, k_out, keep, kept_idx);
+    int rc = select_all(segs, n, R, p, z, d, E, mas, NULL, NULL, k_out, keep, kept_idx);
     free(E);
     return rc;
 }
@@ -462,7 +502,7 @@ static int run_impl(const orc_segment* segs, int n, int R, const orc_params* p,
     }
 
     /* O8-O10: keys, keep counts, selection */
-    int rc = select_all(segs, n, R, p, o->z, o->d, E, o->mas, o->k, o->keep, o->kept_idx);
+    int rc = select_all(segs, n, R, p, o->z, o->d, E, o->mas, NULL, NULL, o->k, o->keep, o->kept_idx);
     free(E);
     return rc;
 }
@@ -599,11 +639,15 @@ static void head_frame(const orc_segment* s, const orc_head* h, int64_t t0, doub
  *    ln(1 + Ntok) / 16, the sums over the modality's tokens (L1, L2 as the
  *    per-token float values);
  *  - Eq. 6: alpha = w2 . relu(W1 [p; z_m] + b1) + b2 (alpha = 0 without an
- *    MLP), then the softmax over the modalities present and Eq. 7.
+ *    MLP), then the softmax over the modalities present and Eq. 7;
+ *  - the selection (Sec. 4.1.1 pruning): a segment with a head keeps its k
+ *    tokens of largest Eq. 3 importance M (ties by ascending index, a NaN M
+ *    as 0); a segment without one keeps the k smallest (key, index) pairs of
+ *    orc_run; k from the keep ratio, or from this MAS when it is negative;
+ *    the per-frame scope as in orc_run.
  * heads may be NULL (no head anywhere), heads[s].weight NULL for no head on
  * segment s. o receives the token, frame and request outputs of orc_run with
- * agg[.][1], rho, beta and mas replaced; its selection outputs are those of
- * the plain run and are not meaningful here. */
+ * agg[.][1], rho, beta and mas replaced, and the selection above. */
 int orc_run_learned(const orc_segment* segs, int n, int R, const orc_params* p, const orc_head* heads,
                     const orc_mlp* mlp, orc_outputs* o, double* importance, double* alpha_out, double* desc)
 {
@@ -701,7 +745,22 @@ int orc_run_learned(const orc_segment* segs, int n, int R, const orc_params* p, 
     free(CC);
     free(L1);
     free(L2);
-    return 0;
+    /* selection with the learned MAS; segments with a head by importance */
+    int64_t* E = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int* by_imp = (int*)calloc((size_t)(n > 0 ? n : 1), sizeof(int));
+    if (!E || !by_imp) {
+        free(E);
+        free(by_imp);
+        return -1;
+    }
+    for (int s = 0; s < n; ++s) {
+        E[s] = segs[s].hidden;
+        by_imp[s] = heads && heads[s].weight ? 1 : 0;
+    }
+    rc = select_all(segs, n, R, p, o->z, o->d, E, o->mas, importance, by_imp, o->k, o->keep, o->kept_idx);
+    free(E);
+    free(by_imp);
+    return rc;
 }
 
 /* ==================================================================
