@@ -338,6 +338,31 @@ msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int 
                                    float* importance, const msao_frame_out* frm, const msao_req_out* req,
                                    float* alpha_out, float* desc, void* ws, size_t ws_bytes, void* stream);
 
+/* Sec. 4.1 with learned heads through to the kept tokens: the outputs of
+ * msao_mas_score_learned, then the selection and compaction of msao_run,
+ * where the pruning of Sec. 4.1.1 follows the learned importance:
+ *   - a segment with a head keeps its k tokens of largest Eq. 3 importance M
+ *     (ties by ascending index; an M that is NaN or not above 0 counts as 0,
+ *     the least important);
+ *   - a segment without a head keeps the k smallest (key, index) pairs of
+ *     msao_run (activity and temporal redundancy);
+ *   - k = min(N, ceil(kappa N)) from the keep ratio, or, for a negative keep
+ *     ratio, kappa = 1 - MAS with the learned MAS (the MLP's beta and the
+ *     heads' rho); the per-frame scope as in msao_run.
+ * M is the float32 value the library computes (it is written to importance
+ * when that is not NULL), so a token whose importance is within rounding of
+ * the k-th one may fall on either side compared with an exact evaluation.
+ * tok->z is required, and tok->d if any segment is temporal; sel, out,
+ * out_byte_off and out_bytes as for msao_run. The workspace is the one
+ * msao_workspace_size gives. Errors: those of msao_mas_score_learned and of
+ * msao_run. */
+msao_status msao_run_learned(msao_ctx* ctx, const msao_segment* segs, int n, int n_requests,
+                             const msao_params* params, const msao_spatial_head* heads, const msao_modal_mlp* mlp,
+                             const float* alpha, const msao_token_out* tok, float* importance,
+                             const msao_frame_out* frm, const msao_req_out* req, float* alpha_out, float* desc,
+                             const msao_select_out* sel, void* out, const int64_t* out_byte_off, int64_t out_bytes,
+                             void* ws, size_t ws_bytes, void* stream);
+
 /* ---- the SimHash variant of Eq. 5 ----------------------------------------- */
 
 /* Random hyperplanes of one segment for Charikar's hash (Sec. 4.1.2 Eq. 5

@@ -14,5 +14,5 @@ from .binding import (  # noqa: F401
     DECIDE_HOLD, DECIDE_OFFLOAD, DECIDE_SEND, Scheduler, comm_latency, expected_e2e_latency,
     expected_spec_tokens, msao_draft_entropy, p_conf, retention_floor, sched_default_params,
     msao_mas_score_learned, msao_temporal_simhash, msao_run_simhash, FLAG_SELECT_PER_FRAME,
-    msao_run_noalloc, msao_stream_read,
+    msao_run_noalloc, msao_stream_read, msao_run_learned,
 )

@@ -137,6 +137,8 @@ SIGNATURES = [
     ("msao_kernel_times", ctypes.c_int, [_P, _P]),
     ("msao_mas_score_learned", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P,
                                               _P, _P, _P, ctypes.c_size_t, _P]),
+    ("msao_run_learned", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                        _P, _P, _P, ctypes.c_int64, _P, ctypes.c_size_t, _P]),
     ("msao_temporal_simhash", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P,
                                              ctypes.c_size_t, _P]),
     ("msao_run_simhash", ctypes.c_int, [_P, _P, ctypes.c_int, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
@@ -716,19 +718,13 @@ def expected_e2e_latency(**terms) -> float:
 
 # ---- Sec. 4.1.1 Eq. 3 and Sec. 4.1.3 Eq. 6 with caller weights ----------------
 
-def msao_mas_score_learned(segments, n_requests, params=None, heads=None, mlp=None, alpha=None, ctx=None,
-                           outputs=None, stream=None):
-    """msao_mas_score with learned probe heads: heads[s] is None or a dict
-    (weight=[hidden] device tensor in the segment's dtype, bias, grid_w, pool);
-    mlp is None or a dict of device float32 tensors (w1 [hidden, prompt_dim +
-    8], b1, w2, prompt [n_requests, prompt_dim]) and b2. Returns
-    (outputs, extra) with extra = importance, alpha and desc device tensors."""
+def _learned_args(segments, n_requests, params, heads, mlp, alpha, ctx):
+    """Marshalled heads, MLP and logits of a learned call (and what must stay alive)."""
     device = _device_of(segments)
     ctx = ctx or default_context(device.index if device.index is not None else torch.cuda.current_device())
-    o = outputs or Outputs(segments, n_requests, compact=False)
     segt = segment_table(segments)
     prm = params_struct(params)
-    n, R = len(segments), n_requests
+    n = len(segments)
     keep = [segt, prm]
     harr = None
     if heads is not None:
@@ -752,9 +748,27 @@ def msao_mas_score_learned(segments, n_requests, params=None, heads=None, mlp=No
         vals = list(alpha)
         al = (ctypes.c_float * len(vals))(*vals)
         keep.append(al)
-    extra = {"importance": torch.empty(max(o.ntok, 1), dtype=torch.float32, device=device)[:o.ntok],
-             "alpha": torch.empty(R * NMOD, dtype=torch.float32, device=device),
-             "desc": torch.empty(R * NMOD * MODAL_DESC, dtype=torch.float32, device=device)}
+    return device, ctx, segt, prm, harr, m, al, keep
+
+
+def _learned_extra(o, n_requests, device):
+    R = n_requests
+    return {"importance": torch.empty(max(o.ntok, 1), dtype=torch.float32, device=device)[:o.ntok],
+            "alpha": torch.empty(R * NMOD, dtype=torch.float32, device=device),
+            "desc": torch.empty(R * NMOD * MODAL_DESC, dtype=torch.float32, device=device)}
+
+
+def msao_mas_score_learned(segments, n_requests, params=None, heads=None, mlp=None, alpha=None, ctx=None,
+                           outputs=None, stream=None):
+    """msao_mas_score with learned probe heads: heads[s] is None or a dict
+    (weight=[hidden] device tensor in the segment's dtype, bias, grid_w, pool);
+    mlp is None or a dict of device float32 tensors (w1 [hidden, prompt_dim +
+    8], b1, w2, prompt [n_requests, prompt_dim]) and b2. Returns
+    (outputs, extra) with extra = importance, alpha and desc device tensors."""
+    device, ctx, segt, prm, harr, m, al, keep = _learned_args(segments, n_requests, params, heads, mlp, alpha, ctx)
+    o = outputs or Outputs(segments, n_requests, compact=False)
+    n, R = len(segments), n_requests
+    extra = _learned_extra(o, R, device)
     st = stream if stream is not None else torch.cuda.current_stream(device)
     _check(lib().msao_mas_score_learned(ctx.handle, segt, n, R, _addr(prm),
                                         ctypes.cast(harr, _P) if harr is not None else None,
@@ -763,5 +777,28 @@ def msao_mas_score_learned(segments, n_requests, params=None, heads=None, mlp=No
                                         _addr(o.c_req), _ptr(extra["alpha"]), _ptr(extra["desc"]),
                                         _ptr(o.workspace), ctypes.c_size_t(o.ws_bytes), ctypes.c_void_p(st.cuda_stream)),
            ctx)
+    extra["_keep"] = keep
+    return o, extra
+
+
+def msao_run_learned(segments, n_requests, params=None, heads=None, mlp=None, alpha=None, ctx=None, outputs=None,
+                     stream=None, compact=True):
+    """msao_mas_score_learned plus the selection and compaction of msao_run,
+    with segments that have a head ranked by their Eq. 3 importance (heads
+    and mlp as for msao_mas_score_learned). Returns (outputs, extra)."""
+    device, ctx, segt, prm, harr, m, al, keep = _learned_args(segments, n_requests, params, heads, mlp, alpha, ctx)
+    o = outputs or Outputs(segments, n_requests, compact=compact)
+    n, R = len(segments), n_requests
+    extra = _learned_extra(o, R, device)
+    use_out = compact and o.out is not None
+    st = stream if stream is not None else torch.cuda.current_stream(device)
+    _check(lib().msao_run_learned(ctx.handle, segt, n, R, _addr(prm),
+                                  ctypes.cast(harr, _P) if harr is not None else None,
+                                  _addr(m) if m is not None else None, al, _addr(o.c_tok),
+                                  _ptr(extra["importance"]) if o.ntok else None, _addr(o.c_frm), _addr(o.c_req),
+                                  _ptr(extra["alpha"]), _ptr(extra["desc"]), _addr(o.c_sel),
+                                  _ptr(o.out) if use_out else None, o.out_off if use_out else None,
+                                  ctypes.c_int64(o.out_bytes if use_out else 0), _ptr(o.workspace),
+                                  ctypes.c_size_t(o.ws_bytes), ctypes.c_void_p(st.cuda_stream)), ctx)
     extra["_keep"] = keep
     return o, extra

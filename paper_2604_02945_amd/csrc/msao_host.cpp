@@ -142,7 +142,7 @@ struct Plan {
     std::vector<int32_t> hb_seg;   // segment of each head block (one per frame of a segment with a head)
     int max_head_p = 0;            // largest frame among segments with a head
     int mlp_hidden = 0;            // > 0: the relevance MLP's u = W1[:, :P] p + b1 per request
-    size_t off_hbseg = 0, off_partial_x = 0, off_proj = 0, off_head_count = 0, off_mlp_u = 0;
+    size_t off_hbseg = 0, off_partial_x = 0, off_proj = 0, off_head_count = 0, off_mlp_u = 0, off_mas = 0;
     size_t off_seg = 0, off_wi = 0, off_gi = 0, off_rmoff = 0, off_rmseg = 0, off_tseg = 0, off_alpha = 0;
     size_t off_selu = 0, off_hiseg = 0, off_clseg = 0, off_frseg = 0;
     std::vector<int32_t> frame_seg;  // segment of every temporal frame
@@ -186,8 +186,9 @@ size_t table_layout(Plan& pl, int n, int R, int64_t n_wi, int64_t n_gwi, int64_t
 // kSelPartTokens tokens, so one Partial and table entries per token, plus
 // what a learned call adds (a PartialX per work item, one
 // projection and one head count per token, kMaxMlpHidden floats of the MLP's
-// prompt product per request). A run with SimHash adds 4 Dsum counts per
-// request, within the room of the prompt product.
+// prompt product per request, and the MAS of every (request, modality) that
+// a learned run's selection reads). A run with SimHash adds 4 Dsum counts
+// per request, within the room of the prompt product.
 size_t workspace_bytes_for(int n, int R, int64_t ntok, int64_t nframes)
 {
     Plan pl;
@@ -200,7 +201,8 @@ size_t workspace_bytes_for(int n, int R, int64_t ntok, int64_t nframes)
            align_up(sizeof(PartialX) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
            align_up(sizeof(float) * (size_t)std::max<int64_t>(ntok, 1), kWsAlign) +
            align_up(sizeof(uint32_t) * (size_t)std::max<int64_t>(items, 1), kWsAlign) +
-           align_up(sizeof(float) * (size_t)kMaxMlpHidden * (size_t)std::max(R, 1), kWsAlign);
+           align_up(sizeof(float) * (size_t)kMaxMlpHidden * (size_t)std::max(R, 1), kWsAlign) +
+           align_up(sizeof(float) * (size_t)kNumMod * (size_t)std::max(R, 1), kWsAlign);
 }
 
 // fuse_copy: a full run with compaction, where segments that keep every row
@@ -208,7 +210,8 @@ size_t workspace_bytes_for(int n, int R, int64_t ntok, int64_t nframes)
 void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* p,
                 const float* alpha, const int64_t* out_off, Plan& pl, bool fuse_copy = false,
                 const msao_spatial_head* heads = nullptr, bool learned = false, int mlp_hidden = 0,
-                const msao_simhash* hashes = nullptr, bool cap_any_scope = false, bool simhash_d = false)
+                const msao_simhash* hashes = nullptr, bool cap_any_scope = false, bool simhash_d = false,
+                bool select_imp = false)
 {
     const bool per_frame = (p->flags & MSAO_FLAG_SELECT_PER_FRAME) != 0;
     pl.sel_unit.clear();
@@ -286,7 +289,10 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         // selections: the segment, or each of its frames (per-frame scope);
         // a large one is written by several blocks, each of a slice
         const bool framed = per_frame && s.n_frames >= 2 && s.tokens_per_frame > 0;
-        const int kind = d.temporal && d.L_t > 0 ? (d.L_s > 0 ? kKeyFull : kKeyE) : (d.L_s > 0 ? kKeyZ : kKeyZero);
+        // a learned run ranks a segment with a head by its Eq. 3 importance
+        const bool by_imp = select_imp && learned && heads && heads[i].weight && N > 0;
+        const int kind = by_imp ? kKeyImp
+                         : d.temporal && d.L_t > 0 ? (d.L_s > 0 ? kKeyFull : kKeyE) : (d.L_s > 0 ? kKeyZ : kKeyZero);
         auto push_selection = [&](int frame, int n_u, int kfix) {
             const int parts = n_u >= kSelSplitMin ? (n_u + kSelPartTokens - 1) / kSelPartTokens : 1;
             for (int q = 0; q < parts; ++q) {
@@ -296,7 +302,8 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
                 u.Mt = d.key_mt;
                 u.kmax = kind == kKeyZ ? (uint64_t)d.C
                          : kind == kKeyE ? (uint64_t)d.E
-                         : kind == kKeyFull ? d.key_ms * (uint64_t)d.C + d.key_mt * (uint64_t)d.E : 0ull;
+                         : kind == kKeyFull ? d.key_ms * (uint64_t)d.C + d.key_mt * (uint64_t)d.E
+                         : kind == kKeyImp ? 0xFFFFFFFFull : 0ull;
                 u.seg = i;
                 u.frame = frame;
                 u.part = q;
@@ -454,6 +461,10 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         if (pl.mlp_hidden > 0) {
             pl.off_mlp_u = align_up(pl.total_bytes, kWsAlign);
             pl.total_bytes = pl.off_mlp_u + sizeof(float) * (size_t)pl.mlp_hidden * (size_t)std::max(R, 1);
+        }
+        if (select_imp) {  // the learned MAS, read by the selection launch
+            pl.off_mas = align_up(pl.total_bytes, kWsAlign);
+            pl.total_bytes = pl.off_mas + sizeof(float) * (size_t)std::max(R * kNumMod, 1);
         }
     }
 }
@@ -1055,14 +1066,14 @@ msao_status msao_compact(msao_ctx* ctx, const msao_segment* segs, int n, const i
     return launched(ctx, MSAO_KERNEL_GATHER, st, run_gather, &ga);
 }
 
-msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
-                                   const msao_spatial_head* heads, const msao_modal_mlp* mlp, const float* alpha,
-                                   const msao_token_out* tok, float* importance, const msao_frame_out* frm,
-                                   const msao_req_out* req, float* alpha_out, float* desc, void* ws, size_t ws_bytes,
-                                   void* stream)
+}  // extern "C"
+
+namespace {
+
+// The heads (Eq. 3) and MLP (Eq. 6) of a learned call.
+msao_status check_learned(msao_ctx* ctx, const msao_segment* segs, int n, const msao_spatial_head* heads,
+                          const msao_modal_mlp* mlp)
 {
-    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
-    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
     char buf[160];
     for (int i = 0; heads && i < n; ++i) {
         const msao_spatial_head& h = heads[i];
@@ -1089,6 +1100,22 @@ msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int 
         if (!std::isfinite(mlp->b2)) return fail(&ctx->err, MSAO_ERR_INVALID_ARG, "b2 is not finite");
         MSAO_TRY(check_out_alignment(ctx, {{mlp->w1, 4}, {mlp->b1, 4}, {mlp->w2, 4}, {mlp->prompt, 4}}));
     }
+    return MSAO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+msao_status msao_mas_score_learned(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
+                                   const msao_spatial_head* heads, const msao_modal_mlp* mlp, const float* alpha,
+                                   const msao_token_out* tok, float* importance, const msao_frame_out* frm,
+                                   const msao_req_out* req, float* alpha_out, float* desc, void* ws, size_t ws_bytes,
+                                   void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
+    MSAO_TRY(check_learned(ctx, segs, n, heads, mlp));
     Plan pl;
     build_plan(ctx, segs, n, R, params, alpha, nullptr, pl, false, heads, true, mlp ? mlp->hidden : 0);
     MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
@@ -1377,6 +1404,98 @@ msao_status msao_run_simhash(msao_ctx* ctx, const msao_segment* segs, int n, int
     hipStream_t st = (hipStream_t)stream;
     MSAO_TRY(upload(ctx, pl, ws, st));
     return enqueue_run(ctx, pl, device_tables(pl, ws, n, R, params), tok, frm, req, sel, out, out_bytes, st, sig);
+}
+
+msao_status msao_run_learned(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,
+                             const msao_spatial_head* heads, const msao_modal_mlp* mlp, const float* alpha,
+                             const msao_token_out* tok, float* importance, const msao_frame_out* frm,
+                             const msao_req_out* req, float* alpha_out, float* desc, const msao_select_out* sel,
+                             void* out, const int64_t* out_byte_off, int64_t out_bytes, void* ws, size_t ws_bytes,
+                             void* stream)
+{
+    if (!ctx) return fail(&g_err, MSAO_ERR_INVALID_ARG, "ctx is NULL");
+    MSAO_TRY(validate_impl(segs, n, R, params, &ctx->err));
+    MSAO_TRY(check_learned(ctx, segs, n, heads, mlp));
+    Plan pl;
+    build_plan(ctx, segs, n, R, params, alpha, out_byte_off, pl, out != nullptr, heads, true, mlp ? mlp->hidden : 0,
+               nullptr, false, false, true);
+    MSAO_TRY(check_ws(ctx, pl, ws, ws_bytes));
+    const std::vector<msao_segment> sv(segs, segs + n);
+    MSAO_TRY(check_run_outputs(ctx, pl, sv, tok, frm, req, sel, out, out_byte_off, out_bytes));
+    MSAO_TRY(check_out_alignment(ctx, {{importance, 4}, {alpha_out, 4}, {desc, 4}}));
+    DeviceGuard guard(ctx->device);
+    hipStream_t st = (hipStream_t)stream;
+    MSAO_TRY(upload(ctx, pl, ws, st));
+    const Tables t = device_tables(pl, ws, n, R, params);
+    // statistics, head projections (and the rows of segments kept whole)
+    ScoreArgs sa;
+    std::memset(&sa, 0, sizeof sa);
+    sa.t = t;
+    sa.tok = token_out(tok);
+    sa.out = (uint8_t*)out;
+    sa.mode = kModeScore;
+    sa.xcd_order = xcd_order_for(ctx, out && pl.any_copy);
+    sa.learned = 1;
+    sa.importance = importance;
+    MSAO_TRY(launched(ctx, MSAO_KERNEL_SCORE, st, run_score, &sa));
+    // Eq. 3 importance of the head segments, kept in the workspace for the selection
+    float* mlp_u = mlp ? (float*)((uint8_t*)ws + pl.off_mlp_u) : nullptr;
+    if (!pl.hb_seg.empty() || mlp) {
+        HeadArgs ha;
+        std::memset(&ha, 0, sizeof ha);
+        ha.t = t;
+        ha.importance = importance;
+        ha.max_p = pl.max_head_p;
+        if (mlp) {
+            ha.mlp = ModalMlp{mlp->w1, mlp->b1, mlp->w2, mlp->b2, mlp->hidden, mlp->prompt_dim, mlp->prompt};
+            ha.u = mlp_u;
+            const int64_t waves = (int64_t)mlp->hidden * ((R + kMlpGroup - 1) / kMlpGroup);
+            ha.n_mlp_blocks = (int32_t)((waves + kHeadBlock / 64 - 1) / (kHeadBlock / 64));
+        }
+        MSAO_TRY(launched(ctx, MSAO_KERNEL_HEAD, st, run_head, &ha));
+    }
+    // Eq. 4 on the heads, the descriptor, Eq. 6, softmax and Eq. 7; the MAS
+    // also into the workspace for MAS-guided keep counts
+    float* mas_ws = (float*)((uint8_t*)ws + pl.off_mas);
+    PostArgs pa;
+    std::memset(&pa, 0, sizeof pa);
+    pa.t = t;
+    if (req) pa.req = ReqOut{req->agg, req->rho, req->temporal, req->beta, req->mas, req->present};
+    if (frm) pa.frm = FrameOut{frm->dframe, frm->sim, frm->gamma};
+    pa.d = tok ? tok->d : nullptr;
+    pa.learned = 1;
+    if (mlp) {
+        pa.use_mlp = 1;
+        pa.mlp = ModalMlp{mlp->w1, mlp->b1, mlp->w2, mlp->b2, mlp->hidden, mlp->prompt_dim, mlp->prompt};
+        pa.mlp_u = mlp_u;
+    }
+    pa.alpha_out = alpha_out;
+    pa.desc_out = desc;
+    pa.mas_ws = mas_ws;
+    const bool want_frames = frm && (frm->dframe || frm->sim || frm->gamma) && pl.nframes > 0;
+    pa.n_req_blocks = R;
+    pa.n_frame_blocks = want_frames ? (int)pl.nframes : 0;
+    MSAO_TRY(launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa));
+    // Sec. 4.1.1 pruning: head segments by importance, the others by the redundancy key
+    PostArgs ps;
+    std::memset(&ps, 0, sizeof ps);
+    ps.t = t;
+    ps.sel = SelOut{sel->keep, sel->kept_idx, sel->kept_count};
+    ps.z = tok ? tok->z : nullptr;
+    ps.d = tok ? tok->d : nullptr;
+    ps.mas_in = mas_ws;
+    ps.n_sel_blocks = (int)pl.sel_unit.size();
+    ps.keys_cap = std::min(pl.max_n, kMaxLdsKeys);
+    MSAO_TRY(launched(ctx, MSAO_KERNEL_POST, st, run_post, &ps));
+    if (!out || t.n_gwi == 0) return MSAO_OK;
+    GatherArgs ga;
+    std::memset(&ga, 0, sizeof ga);
+    ga.t = t;
+    ga.kept_idx = sel->kept_idx;
+    ga.kept_count = sel->kept_count;
+    ga.out = (uint8_t*)out;
+    ga.out_bytes = out_bytes;
+    return launched(ctx, MSAO_KERNEL_GATHER, st, run_gather, &ga);
 }
 
 msao_status msao_plan_create(msao_ctx* ctx, const msao_segment* segs, int n, int R, const msao_params* params,

@@ -61,8 +61,9 @@ struct DevSeg {
 };
 
 // Key kinds of a selection: Ms z + Mt (E - d) in general, z or E - d alone
-// when the other weight is 0 (the same order, a narrower range).
-enum : int { kKeyZero = 0, kKeyZ = 1, kKeyE = 2, kKeyFull = 3 };
+// when the other weight is 0 (the same order, a narrower range); or, in a
+// learned run, a segment with a head ranked by its Eq. 3 importance.
+enum : int { kKeyZero = 0, kKeyZ = 1, kKeyE = 2, kKeyFull = 3, kKeyImp = 4 };
 
 // One selection block: a whole segment (frame -1) or one frame of a clip
 // (per-frame scope), or one of the nparts blocks of a large selection. Every
@@ -194,6 +195,7 @@ struct PostArgs {
     float* alpha_out;     // [R*4] (NULL: not written)
     float* desc_out;      // [R*4*kDesc]
     const float* mlp_u;   // [R][hidden] prompt half of the MLP's first layer plus b1
+    float* mas_ws;        // learned request role: MAS per (request, modality) for a later selection (NULL: none)
 };
 
 struct ScoreArgs {

@@ -1144,6 +1144,7 @@ __device__ void role_request_learned(const PostArgs& a, int r, PostShared<NT>& s
         if (a.req.temporal) a.req.temporal[x] = (float)o.tterm;
         if (a.req.beta) a.req.beta[x] = (float)o.beta;
         if (a.req.mas) a.req.mas[x] = (float)o.mas;
+        if (a.mas_ws) a.mas_ws[x] = (float)o.mas;
         if (a.req.present) a.req.present[x] = pres[mm] ? 1 : 0;
         if (a.alpha_out) a.alpha_out[x] = pres[mm] ? (float)al[mm] : 0.0f;
         if (a.desc_out)
@@ -1174,13 +1175,23 @@ __device__ void role_frame(const PostArgs& a, int f, PostShared<NT>& sh)
 // Selection key Ms*z + Mt*(E - d), order-equivalent to L_s z / C + L_t (E -
 // d) / E (E = C for bit sampling, where Ms = L_s and Mt = L_t): when one
 // weight is 0 the other term alone orders the tokens, so it is used unscaled.
+// A learned importance as a key: larger importance first. The bits of a
+// positive float grow with its value, so their complement orders it
+// downwards; NaN and values not above 0 take the largest key (importance 0).
+__device__ __forceinline__ uint64_t imp_key(float m)
+{
+    return m > 0.0f ? (uint64_t)(~__float_as_uint(m)) : 0xFFFFFFFFull;
+}
+
 __device__ __forceinline__ uint64_t sel_key(const uint32_t* __restrict__ z, const uint32_t* __restrict__ d,
-                                            int g, int kind, uint64_t Ms, uint64_t Mt, uint32_t E)
+                                            const float* __restrict__ imp, int g, int kind, uint64_t Ms, uint64_t Mt,
+                                            uint32_t E)
 {
     switch (kind) {
     case kKeyZ: return (uint64_t)z[g];
     case kKeyE: return (uint64_t)(E - d[g]);
     case kKeyFull: return Ms * (uint64_t)z[g] + Mt * (uint64_t)(E - d[g]);
+    case kKeyImp: return imp_key(imp[g]);
     default: return 0ull;
     }
 }
@@ -1234,9 +1245,9 @@ __device__ __forceinline__ uint32_t block_exscan_dpp(uint32_t v, PostShared<NT>&
 // of one thread overlap; indices past N are clamped (and their values
 // dropped) so that no load sits behind a branch.
 template <int NT, int KIND>
-__device__ __forceinline__ void stage_keys(const uint32_t* __restrict__ z, const uint32_t* __restrict__ d, int N,
-                                           uint64_t Ms, uint64_t Mt, uint32_t E, bool in_lds, uint64_t* keys,
-                                           uint32_t* hist, int shift, bool count)
+__device__ __forceinline__ void stage_keys(const uint32_t* __restrict__ z, const uint32_t* __restrict__ d,
+                                           const float* __restrict__ imp, int N, uint64_t Ms, uint64_t Mt, uint32_t E,
+                                           bool in_lds, uint64_t* keys, uint32_t* hist, int shift, bool count)
 {
     constexpr int U = 8;
     for (int i0 = threadIdx.x; i0 < N; i0 += U * NT) {
@@ -1246,13 +1257,14 @@ __device__ __forceinline__ void stage_keys(const uint32_t* __restrict__ z, const
             const int g = min(i0 + u * NT, N - 1);
             zz[u] = KIND == kKeyZ || KIND == kKeyFull ? z[g] : 0u;
             ee[u] = KIND == kKeyE || KIND == kKeyFull ? E - d[g] : 0u;
+            if constexpr (KIND == kKeyImp) zz[u] = (uint32_t)imp_key(imp[g]);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int i = i0 + u * NT;
             if (i < N) {
                 uint64_t key = 0ull;
-                if constexpr (KIND == kKeyZ) key = zz[u];
+                if constexpr (KIND == kKeyZ || KIND == kKeyImp) key = zz[u];
                 else if constexpr (KIND == kKeyE) key = ee[u];
                 else if constexpr (KIND == kKeyFull) key = Ms * (uint64_t)zz[u] + Mt * (uint64_t)ee[u];
                 if (in_lds) keys[i] = key;
@@ -1278,6 +1290,7 @@ struct KeySrc {
     const uint64_t* keys;
     const uint32_t* z;
     const uint32_t* d;
+    const float* imp;
     int kind;
     uint64_t Ms, Mt;
     uint32_t E;
@@ -1285,7 +1298,7 @@ struct KeySrc {
     __device__ __forceinline__ uint64_t at(int i) const
     {
         if constexpr (IN_LDS) return keys[i];
-        else return sel_key(z, d, i, kind, Ms, Mt, E);
+        else return sel_key(z, d, imp, i, kind, Ms, Mt, E);
     }
 };
 
@@ -1584,6 +1597,7 @@ __device__ void role_select(const PostArgs& a, int unit, PostShared<NT>& sh, uin
     const uint32_t E = su.E;
     const uint32_t* z = a.z + off;
     const uint32_t* d = a.d ? a.d + off : nullptr;
+    const float* imp = kind == kKeyImp ? t.proj + off : nullptr;  // learned run: Eq. 3 importance
     const bool in_lds = N <= keys_cap;
 
     // keys (staged in LDS) in [0, kmax], counted in the first digit's histogram
@@ -1593,14 +1607,15 @@ __device__ void role_select(const PostArgs& a, int unit, PostShared<NT>& sh, uin
     for (int b = tid; b < kRadixBins; b += NT) sh.hist[b] = 0u;
     __syncthreads();
     switch (kind) {
-    case kKeyZ: stage_keys<NT, kKeyZ>(z, d, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
-    case kKeyE: stage_keys<NT, kKeyE>(z, d, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
-    case kKeyFull: stage_keys<NT, kKeyFull>(z, d, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
-    default: stage_keys<NT, kKeyZero>(z, d, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, false); break;
+    case kKeyZ: stage_keys<NT, kKeyZ>(z, d, imp, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
+    case kKeyE: stage_keys<NT, kKeyE>(z, d, imp, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
+    case kKeyFull: stage_keys<NT, kKeyFull>(z, d, imp, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
+    case kKeyImp: stage_keys<NT, kKeyImp>(z, d, imp, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
+    default: stage_keys<NT, kKeyZero>(z, d, imp, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, false); break;
     }
     __syncthreads();
 
-    const KeySrc src{keys, z, d, kind, Ms, Mt, E};
+    const KeySrc src{keys, z, d, imp, kind, Ms, Mt, E};
     uint64_t* cand = keys + keys_cap;
     if (in_lds)
         select_and_compact<NT, true>(a, sh, src, cand, cand_cap_for(keys_cap), N, k, off, ioff, iadd, lo, hi, s0, s1, true);
@@ -1796,6 +1811,7 @@ __global__ __launch_bounds__(kHeadBlock) void k_head(HeadArgs a)
         const float v = sum / (float)((i1 - i0 + 1) * (j1 - j0 + 1)) + sg.head_b;
         const float M = 1.0f / (1.0f + expf(-v));
         if (a.importance) a.importance[base + q] = M;
+        t.proj[base + q] = M;  // the frame's projections are in LDS: the slot now holds M for a selection
         c += M < t.tau_s ? 1u : 0u;
     }
     c = wave_sum_u64(c);
