@@ -280,6 +280,21 @@ def learned_bench(args, dev, ctx, w, reps, fields):
     k_plain = kernels(lambda i: msao.msao_mas_score(reps[i], R, w.params, ctx=ctx, outputs=outs[i]))
     k_lrn = kernels(lambda i: msao.msao_mas_score_learned(reps[i], R, w.params, heads=heads, mlp=mlp, ctx=ctx,
                                                           outputs=outs[i]))
+    # the learned run through selection (image and audio by their Eq. 3 importance) and compaction
+    routs = [msao.Outputs(segs, R, token_fields=fields, compact=True) for segs in reps]
+    for i in range(len(reps)):
+        msao.msao_run_learned(reps[i], R, w.params, heads=heads, mlp=mlp, ctx=ctx, outputs=routs[i])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        msao.msao_run_learned(reps[i % len(reps)], R, w.params, heads=heads, mlp=mlp, ctx=ctx,
+                              outputs=routs[i % len(reps)])
+    e1.record()
+    torch.cuda.synchronize()
+    ms_run = e0.elapsed_time(e1) / steps
+    k_run = kernels(lambda i: msao.msao_run_learned(reps[i], R, w.params, heads=heads, mlp=mlp, ctx=ctx,
+                                                    outputs=routs[i]))
     ntok = w.n_tokens
     b_plain = w.input_bytes + 4 * len(fields) * ntok
     b_lrn = b_plain + 4 * ntok          # + the projection or the density importance of every token
@@ -294,6 +309,10 @@ def learned_bench(args, dev, ctx, w, reps, fields):
         "gpu_ms_per_call": total,
         "tokens_per_s": ntok / (total * 1e-3),
         "score_overhead": k_lrn[msao.binding.KERNEL_SCORE] / k_plain[msao.binding.KERNEL_SCORE] - 1.0,
+        "run_learned": {"ms_per_call": ms_run, "tokens_per_s": ntok / (ms_run * 1e-3),
+                        "kernel_ms": {"score": k_run[msao.binding.KERNEL_SCORE], "head": k_run[msao.binding.KERNEL_HEAD],
+                                      "post_mean_of_request_and_selection": k_run[msao.binding.KERNEL_POST],
+                                      "gather": k_run[msao.binding.KERNEL_GATHER]}},
         "algorithmic_bytes_score": b_lrn,
         "roofline": {"bound": "hbm", "kernel": "k_score<true>", "achieved": gbs, "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "traffic": committed_learned_traffic(w.config)},

@@ -1049,14 +1049,25 @@ __device__ void role_request_learned(const PostArgs& a, int r, PostShared<NT>& s
         const DevSeg& sg = t.seg[wr.seg];
         const bool head = sg.head_w != nullptr;
         if (part == 0 && lane == 0) cs += (uint64_t)sg.n_tok * (uint64_t)sg.C;
-        for (int w = wr.begin + part * kWave + lane; w < wr.end; w += kParts * kWave) {
-            const Partial pr = t.partial[w];
-            const PartialX px = t.partial_x[w];
-            if (!head) nsp += pr.nsparse;
-            ds += pr.dsum;
-            as += px.asum;
-            l1 += (double)px.l1;
-            l2 += (double)px.l2;
+        constexpr int U = 8;  // partials in flight per lane
+        for (int w0 = wr.begin + part * kWave + lane; w0 < wr.end; w0 += U * kParts * kWave) {
+            Partial pr[U];
+            PartialX px[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int w = min(w0 + u * kParts * kWave, wr.end - 1);
+                pr[u] = t.partial[w];
+                px[u] = t.partial_x[w];
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (w0 + u * kParts * kWave >= wr.end) break;
+                if (!head) nsp += pr[u].nsparse;
+                ds += pr[u].dsum;
+                as += px[u].asum;
+                l1 += (double)px[u].l1;
+                l2 += (double)px[u].l2;
+            }
         }
         if (head)
             for (int h = sg.hb_begin + part * kWave + lane; h < sg.hb_begin + sg.T; h += kParts * kWave)
