@@ -44,6 +44,9 @@ def parse():
                     help="skip the SimHash variant of Eq. 5 on the video clips")
     ap.add_argument("--no-learned", action="store_true",
                     help="skip the learned-head variant (Eq. 3 heads and the Eq. 6 MLP) of the scoring pass")
+    ap.add_argument("--no-learned-run", action="store_true",
+                    help="in the learned block, skip the learned run through selection (every learned scoring "
+                         "launch is then of one kind, for counter passes)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (calibrates HBM byte counters)")
     ap.add_argument("--no-configs", action="store_true",
@@ -280,21 +283,9 @@ def learned_bench(args, dev, ctx, w, reps, fields):
     k_plain = kernels(lambda i: msao.msao_mas_score(reps[i], R, w.params, ctx=ctx, outputs=outs[i]))
     k_lrn = kernels(lambda i: msao.msao_mas_score_learned(reps[i], R, w.params, heads=heads, mlp=mlp, ctx=ctx,
                                                           outputs=outs[i]))
-    # the learned run through selection (image and audio by their Eq. 3 importance) and compaction
-    routs = [msao.Outputs(segs, R, token_fields=fields, compact=True) for segs in reps]
-    for i in range(len(reps)):
-        msao.msao_run_learned(reps[i], R, w.params, heads=heads, mlp=mlp, ctx=ctx, outputs=routs[i])
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for i in range(steps):
-        msao.msao_run_learned(reps[i % len(reps)], R, w.params, heads=heads, mlp=mlp, ctx=ctx,
-                              outputs=routs[i % len(reps)])
-    e1.record()
-    torch.cuda.synchronize()
-    ms_run = e0.elapsed_time(e1) / steps
-    k_run = kernels(lambda i: msao.msao_run_learned(reps[i], R, w.params, heads=heads, mlp=mlp, ctx=ctx,
-                                                    outputs=routs[i]))
+    res_run = None
+    if not args.no_learned_run:
+        res_run = learned_run_timing(args, ctx, w, reps, fields, heads, mlp, steps, kernels)
     ntok = w.n_tokens
     b_plain = w.input_bytes + 4 * len(fields) * ntok
     b_lrn = b_plain + 4 * ntok          # + the projection or the density importance of every token
@@ -309,14 +300,39 @@ def learned_bench(args, dev, ctx, w, reps, fields):
         "gpu_ms_per_call": total,
         "tokens_per_s": ntok / (total * 1e-3),
         "score_overhead": k_lrn[msao.binding.KERNEL_SCORE] / k_plain[msao.binding.KERNEL_SCORE] - 1.0,
-        "run_learned": {"ms_per_call": ms_run, "tokens_per_s": ntok / (ms_run * 1e-3),
-                        "kernel_ms": {"score": k_run[msao.binding.KERNEL_SCORE], "head": k_run[msao.binding.KERNEL_HEAD],
-                                      "post_mean_of_request_and_selection": k_run[msao.binding.KERNEL_POST],
-                                      "gather": k_run[msao.binding.KERNEL_GATHER]}},
+        "run_learned": res_run,
         "algorithmic_bytes_score": b_lrn,
         "roofline": {"bound": "hbm", "kernel": "k_score<true>", "achieved": gbs, "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "traffic": committed_learned_traffic(w.config)},
     }
+
+
+def learned_run_timing(args, ctx, w, reps, fields, heads, mlp, steps, kernels):
+    """msao_run_learned (image and audio pruned by their Eq. 3 importance,
+    compaction) over the same rotated replicas."""
+    import torch
+
+    import paper_2604_02945_amd as msao
+
+    R, ntok = w.n_requests, w.n_tokens
+    routs = [msao.Outputs(segs, R, token_fields=fields, compact=True) for segs in reps]
+    for i in range(len(reps)):
+        msao.msao_run_learned(reps[i], R, w.params, heads=heads, mlp=mlp, ctx=ctx, outputs=routs[i])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        msao.msao_run_learned(reps[i % len(reps)], R, w.params, heads=heads, mlp=mlp, ctx=ctx,
+                              outputs=routs[i % len(reps)])
+    e1.record()
+    torch.cuda.synchronize()
+    ms_run = e0.elapsed_time(e1) / steps
+    k_run = kernels(lambda i: msao.msao_run_learned(reps[i], R, w.params, heads=heads, mlp=mlp, ctx=ctx,
+                                                    outputs=routs[i]))
+    return {"ms_per_call": ms_run, "tokens_per_s": ntok / (ms_run * 1e-3),
+            "kernel_ms": {"score": k_run[msao.binding.KERNEL_SCORE], "head": k_run[msao.binding.KERNEL_HEAD],
+                          "post_mean_of_request_and_selection": k_run[msao.binding.KERNEL_POST],
+                          "gather": k_run[msao.binding.KERNEL_GATHER]}}
 
 
 def simhash_bench(args, dev, ctx):
