@@ -223,6 +223,7 @@ def adversarial_cases():
         _rand_seg(rng, 1, VIDEO, 5, 6, 4096, "bf16", 0.5),        # 8 units: generic chain path
         _rand_seg(rng, 2, VIDEO, 40, 3, 1024, "bf16", 0.25, "static_video"),
         _rand_seg(rng, 2, IMAGE, 1, 50, 1024, "bf16", 0.25, "relu_bg"),
+        _rand_seg(rng, 3, VIDEO, 4, 7, 1024, "bf16", 1.0),        # kept whole: rows copied by the scoring pass
     ]
     cases["ties_and_specials"] = [
         _rand_seg(rng, 0, IMAGE, 1, 300, 64, "bf16", 0.37, "same"),   # tie storm
