@@ -787,6 +787,7 @@ struct PostShared {
     uint64_t asum[kWaves], csum[kWaves];
     double l1[kWaves], l2[kWaves];
     float fred[kWaves];
+    float fred4[kWaves][kNumMod];
     float alpha[kNumMod];
 };
 
@@ -1015,19 +1016,6 @@ __device__ __forceinline__ double wave_sum_f64(double v)
 
 // Block-wide float sum in a fixed order (wavefront DPP sums, then the
 // wavefronts in order), the same value in every thread.
-template <int NT>
-__device__ __forceinline__ float block_sum_f32(float v, PostShared<NT>& sh)
-{
-    v = wave_sum(v);
-    __syncthreads();
-    if ((threadIdx.x & (kWave - 1)) == 0) sh.fred[threadIdx.x >> 6] = v;
-    __syncthreads();
-    float s = 0.0f;
-#pragma unroll
-    for (int w = 0; w < NT / kWave; ++w) s += sh.fred[w];
-    return s;
-}
-
 // A learned call's request role: Eq. 4 counts from the heads' per-frame
 // counts (from the density test where a segment has no head), the
 // descriptor z_m of every modality, Eq. 6 on [p; z_m] when an MLP is given
@@ -1042,6 +1030,19 @@ __device__ void role_request_learned(const PostArgs& a, int r, PostShared<NT>& s
     const int wid = threadIdx.x >> 6, m = wid % kNumMod, part = wid / kNumMod;
     const int lane = threadIdx.x & (kWave - 1);
     const RmEntry e = t.rm[r * kNumMod + m];
+    // the MLP's weights of this thread's first hidden unit (the descriptor
+    // columns of W1, u = W1[:, :P] p + b1 from the head launch, and w2) are
+    // the same for every modality: read them now, so that their latency
+    // overlaps the aggregation
+    const int P = a.mlp.prompt_dim, IN = P + kDesc, H = a.mlp.hidden;
+    float w1u[kDesc], uu = 0.0f, w2u = 0.0f;
+    if (a.use_mlp && (int)threadIdx.x < H) {
+        const float* row = a.mlp.w1 + (int64_t)threadIdx.x * IN + P;
+#pragma unroll
+        for (int k = 0; k < kDesc; ++k) w1u[k] = row[k];
+        uu = a.mlp_u[(int64_t)r * H + threadIdx.x];
+        w2u = a.mlp.w2[threadIdx.x];
+    }
     uint64_t nsp = 0, ds = 0, as = 0, cs = 0;
     double l1 = 0.0, l2 = 0.0;
     for (int j = e.rng_begin; j < e.rng_end; ++j) {
@@ -1117,26 +1118,53 @@ __device__ void role_request_learned(const PostArgs& a, int r, PostShared<NT>& s
         if (pres[mm]) pre[mm] = mas_terms(t, g[mm], 1.0, mm);  // rho and the temporal term
         modality_descriptor(pres[mm], pre[mm], a1, c1, s1, s2, g[mm].ntok, z[mm]);
     }
-    // Eq. 6: alpha = w2 . relu(W1 [p; z] + b1) + b2, one modality at a time,
-    // with u = W1[:, :P] p + b1 from the head launch
+    // Eq. 6: alpha = w2 . relu(W1 [p; z] + b1) + b2 for every modality at
+    // once: each thread sums its hidden units' terms per modality, and one
+    // block reduction (each wavefront's sums, then the wavefronts in order)
+    // gives the four sums
     double al[kNumMod];
-    const int P = a.mlp.prompt_dim, IN = P + kDesc, H = a.mlp.hidden;
 #pragma unroll
-    for (int mm = 0; mm < kNumMod; ++mm) {
-        al[mm] = (double)t.alpha[r * kNumMod + mm];
-        if (!a.use_mlp || !pres[mm]) continue;
-        float zf[kDesc];
+    for (int mm = 0; mm < kNumMod; ++mm) al[mm] = (double)t.alpha[r * kNumMod + mm];
+    if (a.use_mlp) {
+        float zf[kNumMod][kDesc];
 #pragma unroll
-        for (int k = 0; k < kDesc; ++k) zf[k] = (float)z[mm][k];
-        float part_sum = 0.0f;
-        for (int j = threadIdx.x; j < H; j += NT) {
+        for (int mm = 0; mm < kNumMod; ++mm)
+#pragma unroll
+            for (int k = 0; k < kDesc; ++k) zf[mm][k] = (float)z[mm][k];
+        float ps[kNumMod] = {0.0f, 0.0f, 0.0f, 0.0f};
+        auto unit = [&](const float (&w1)[kDesc], float u, float w2) {
+#pragma unroll
+            for (int mm = 0; mm < kNumMod; ++mm) {
+                if (!pres[mm]) continue;
+                float h = u;
+#pragma unroll
+                for (int k = 0; k < kDesc; ++k) h = fmaf(w1[k], zf[mm][k], h);
+                ps[mm] = fmaf(w2, fmaxf(h, 0.0f), ps[mm]);
+            }
+        };
+        if ((int)threadIdx.x < H) unit(w1u, uu, w2u);
+        for (int j = threadIdx.x + NT; j < H; j += NT) {
             const float* row = a.mlp.w1 + (int64_t)j * IN + P;
-            float h = a.mlp_u[(int64_t)r * H + j];
+            float w1[kDesc];
 #pragma unroll
-            for (int k = 0; k < kDesc; ++k) h = fmaf(row[k], zf[k], h);
-            part_sum = fmaf(a.mlp.w2[j], fmaxf(h, 0.0f), part_sum);
+            for (int k = 0; k < kDesc; ++k) w1[k] = row[k];
+            unit(w1, a.mlp_u[(int64_t)r * H + j], a.mlp.w2[j]);
         }
-        al[mm] = (double)(a.mlp.b2 + block_sum_f32<NT>(part_sum, sh));
+#pragma unroll
+        for (int mm = 0; mm < kNumMod; ++mm) ps[mm] = wave_sum(ps[mm]);
+        if (lane == 0) {
+#pragma unroll
+            for (int mm = 0; mm < kNumMod; ++mm) sh.fred4[wid][mm] = ps[mm];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int mm = 0; mm < kNumMod; ++mm) {
+            if (!pres[mm]) continue;
+            float sum = 0.0f;
+#pragma unroll
+            for (int w = 0; w < NT / kWave; ++w) sum += sh.fred4[w][mm];
+            al[mm] = (double)(a.mlp.b2 + sum);
+        }
     }
     if (threadIdx.x != 0) return;
     double beta[kNumMod];
