@@ -144,6 +144,29 @@ def test_entry_points_reject_null_context():
     assert L.msao_select_tokens(None, arr, 1, 1, ctypes.byref(p), None, None, None, None, None, 0, None) == INVALID
 
 
+# entry points whose first argument is the context (or the plan): every one
+# rejects a NULL one before touching any other argument
+CTX_ENTRY_POINTS = ["msao_mas_score", "msao_temporal_redundancy", "msao_select_tokens", "msao_compact", "msao_run",
+                    "msao_run_noalloc", "msao_plan_create", "msao_plan_run", "msao_mas_score_learned",
+                    "msao_run_learned", "msao_temporal_simhash", "msao_run_simhash", "msao_draft_entropy",
+                    "msao_stream_read", "msao_set_profiling", "msao_kernel_times"]
+
+
+@pytest.mark.parametrize("name", CTX_ENTRY_POINTS)
+def test_every_entry_point_rejects_a_null_context(name):
+    L = B.lib()
+    fn = getattr(L, name)
+    args = []
+    for t in fn.argtypes:
+        if t in (ctypes.c_int, ctypes.c_int64, ctypes.c_size_t):
+            args.append(0)
+        elif t in (ctypes.c_float, ctypes.c_double):
+            args.append(0.0)
+        else:
+            args.append(None)
+    assert fn(*args) == INVALID
+
+
 def test_create_without_device_reports_hip_error():
     import torch
     if torch.cuda.is_available():

@@ -200,3 +200,16 @@ def test_argument_errors(dev):
     with pytest.raises(msao.MsaoError) as e:
         msao.msao_run_learned(dsegs, 1, w.params, heads=bad)
     assert e.value.status == 1
+
+
+@pytest.mark.parametrize("keep", [0.3, -1.0])
+def test_clip_with_a_head_beyond_lds_staging(keep, dev):
+    """A clip of 18,000 tokens with a head: more keys than the selection
+    stages in LDS, so every pass recomputes the importance keys from memory."""
+    rng = np.random.default_rng(31)
+    T, P, C = 3, 6000, 64
+    x = rng.standard_normal((T * P, C)).astype(np.float32)
+    clip = Segment(0, VIDEO, T, P, C, "bf16", keep, f32_to_bf16_bits(x))
+    img = Segment(0, IMAGE, 1, 576, C, "bf16", 0.25, f32_to_bf16_bits(rng.standard_normal((576, C)).astype(np.float32)))
+    heads = [make_head(clip, rng, 100, 3, 0.2)[1], make_head(img, rng, 24, 3, -0.4)[1]]
+    run_and_check([clip, img], 1, heads, None, dev)
