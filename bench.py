@@ -629,6 +629,15 @@ class Bench:
             if best is None or gbs > best["gbps"]:
                 best = {"gbps": gbs, "ms": ms, "bytes": self.buf_bytes, "chunk_kib": kib}
         best["frac_of_peak"] = best["gbps"] / PEAK_HBM_GBS
+        # the fixed cost of a launch by the same events: one wavefront reading 8 KiB
+        tiny = self.bufs[0][:8192]
+        for _ in range(8):
+            msao.msao_stream_read(tiny, 8, ctx=c, stream=self.streams[0], sink=sink)
+        c.set_profiling(True)
+        for _ in range(count):
+            msao.msao_stream_read(tiny, 8, ctx=c, stream=self.streams[0], sink=sink)
+        best["launch_floor_ms"] = c.kernel_times()[msao.binding.KERNEL_READ]
+        c.set_profiling(False)
         return best
 
     def close(self):
