@@ -37,6 +37,7 @@ struct msao_ctx {
     int chain_frames = 0;       // frames per temporal work item; 0 = automatic
     int xcd_order = -1;         // scoring block order: -1 automatic, 0 dispatch order, 1 one range per XCD
     int clip_fuse = 1;          // the SimHash run scores and hashes its clips in one pass (k_clip)
+    int pair_path = 1;          // bf16 clips with rows of at most 2 KiB are scored by k_pair
 };
 
 namespace {
@@ -152,6 +153,7 @@ struct Plan {
     int clip_dtype = -1, clip_bits = 0;
     std::vector<int32_t> cl_seg;   // segment of each k_clip block
     int n_wi_score = 0;            // k_score's work items [0, n_wi_score); the fused clips' follow
+    int n_wi_pair = 0;             // k_pair's work items [0, n_wi_pair), whole blocks
     size_t table_bytes = 0, off_partial = 0, total_bytes = 0;
 };
 
@@ -359,7 +361,28 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         }
         // scoring work items, one wavefront each
         int items = 0;
-        if (d.fused) {
+        const int64_t row_bytes = (int64_t)s.hidden * es;
+        if (d.temporal && !d.fused && !learned && !d.copy_in_score && (!ctx || ctx->pair_path) && s.dtype == MSAO_BF16 &&
+            row_bytes <= kPairMaxRowBytes && row_bytes % 512 == 0 && s.tokens_per_frame >= 2 &&
+            d.stride_bytes + row_bytes <= (1 << 30)) {
+            // k_pair: kPairWaves frame ranges of per_item frames per block of one
+            // pair of positions, tblk blocks along the clip (a block after the
+            // first reads the frame before its range as a halo)
+            const int F = s.n_frames <= kPairWaves * kPairMaxFrames ? (s.n_frames + kPairWaves - 1) / kPairWaves
+                                                                    : kPairMaxFrames;
+            const int tblk = (s.n_frames + kPairWaves * F - 1) / (kPairWaves * F);
+            const int64_t pitems = (int64_t)kPairWaves * ((s.tokens_per_frame + 1) / 2) * tblk;
+            if (pitems <= N) {
+                d.pair = 1;
+                d.tblk = tblk;
+                d.per_item = F;
+                items = (int)pitems;
+                pl.tseg.push_back(i);
+                pl.any_temporal = true;
+            }
+        }
+        if (d.pair) {
+        } else if (d.fused) {
             // tiles of at most 15 new frames of one position, the frames split
             // evenly; their work items follow all others
             d.ntiles = (s.n_frames + kClipFrames - 1) / kClipFrames;
@@ -385,10 +408,7 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         } else {
             d.per_item = 1;
         }
-        d.wi_begin = wi;
-        pl.wi_b[(size_t)i] = wi;
-        wi += items;
-        pl.wi_e[(size_t)i] = wi;
+        pl.wi_e[(size_t)i] = items;  // the item count until the ranges are laid out below
         d.g_begin = gi;
         if (!d.copy_in_score) gi += (d.cap + kGatherRows - 1) / kGatherRows;
         pl.seg_gi[(size_t)i + 1] = gi;
@@ -396,6 +416,20 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         if (d.copy_in_score) pl.any_copy = true;
         tok += N;
         if (d.temporal) frame += s.n_frames;
+    }
+    // work items: k_pair's clips first (whole blocks from item 0), then the
+    // other segments in table order, then the fused clips
+    for (int pass = 0; pass < 2; ++pass) {
+        for (int i = 0; i < n; ++i) {
+            DevSeg& d = pl.seg[(size_t)i];
+            if (d.fused || (d.pair != 0) != (pass == 0)) continue;
+            const int items = pl.wi_e[(size_t)i];
+            d.wi_begin = wi;
+            pl.wi_b[(size_t)i] = wi;
+            wi += items;
+            pl.wi_e[(size_t)i] = wi;
+        }
+        if (pass == 0) pl.n_wi_pair = wi;
     }
     pl.n_wi_score = wi;
     for (int i = 0; i < n; ++i) {
@@ -571,6 +605,7 @@ Tables device_tables(const Plan& pl, void* ws, int n, int R, const msao_params* 
     t.frame_seg = (const int32_t*)(b + pl.off_frseg);
     t.n_cl = (int32_t)pl.cl_seg.size();
     t.n_wi_score = pl.n_wi_score;
+    t.n_wi_pair = pl.n_wi_pair;
     t.n_hi = (int32_t)pl.hi_seg.size();
     t.n = n;
     t.R = R;
@@ -845,6 +880,7 @@ msao_status msao_create(msao_ctx** out, int device)
     if (const char* v = std::getenv("MSAO_CHAIN_FRAMES")) c->chain_frames = std::max(0, std::atoi(v));
     if (const char* v = std::getenv("MSAO_XCD_ORDER")) c->xcd_order = std::atoi(v) < 0 ? -1 : (std::atoi(v) ? 1 : 0);
     if (const char* v = std::getenv("MSAO_CLIP_FUSE")) c->clip_fuse = std::atoi(v) ? 1 : 0;
+    if (const char* v = std::getenv("MSAO_PAIR")) c->pair_path = std::atoi(v) ? 1 : 0;
     *out = c;
     return MSAO_OK;
 }

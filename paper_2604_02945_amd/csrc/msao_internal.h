@@ -58,6 +58,10 @@ struct DevSeg {
     int32_t fused;
     uint64_t key_ms, key_mt;
     int32_t cl_begin, ntiles;
+    // a bf16 clip with rows of at most 2 KiB scored by k_pair: a wavefront
+    // takes two adjacent positions (per_item frames of them), a block four
+    // consecutive frame ranges; tblk blocks of 4 per_item frames cover a clip
+    int32_t pair, tblk;
 };
 
 // Key kinds of a selection: Ms z + Mt (E - d) in general, z or E - d alone
@@ -142,6 +146,7 @@ struct Tables {
     const int32_t* cl_seg;   // [n_cl] segment of each k_clip block (fused clips)
     int32_t n_cl;
     int32_t n_wi_score;      // work items of k_score: [0, n_wi_score); the fused clips' follow
+    int32_t n_wi_pair;       // the first n_wi_pair of them (whole blocks) are k_pair's
     int32_t n_hi;
     int32_t n, R, n_wi, n_gwi, n_tseg, n_frames;
     float tau, tau_s;
@@ -206,6 +211,7 @@ struct ScoreArgs {
     int32_t xcd_order;    // 1: each XCD takes one contiguous range of workgroups
     int32_t learned;      // learned call: projections, importance of head-less tokens, PartialX
     float* importance;    // [Ntot] (learned calls; NULL: not written)
+    int32_t wi_first;     // k_score's first work item (set by the launcher: the pair items precede it)
 };
 
 // Pooling, sigmoid and the Eq. 4 test of the learned spatial head: one
@@ -314,6 +320,15 @@ int launch_simhash(const HashArgs& a, void* stream, void* ev0, void* ev1);
 int launch_hash_post(const HashArgs& a, void* stream, void* ev0, void* ev1);
 
 constexpr int kScoreBlock = 256;   // 4 wavefronts, one work item each
+#ifndef MSAO_PAIR_WAVES
+#define MSAO_PAIR_WAVES 4
+#endif
+constexpr int kPairWaves = MSAO_PAIR_WAVES;   // frame ranges of one pair of positions per k_pair block
+constexpr int kPairMaxRowBytes = 2048;        // rows k_pair takes: four 512-byte units per half-wavefront
+#ifndef MSAO_PAIR_MAX_FRAMES
+#define MSAO_PAIR_MAX_FRAMES 16
+#endif
+constexpr int kPairMaxFrames = MSAO_PAIR_MAX_FRAMES;  // frames per k_pair wavefront (the token buffer holds 2 per frame)
 #ifndef MSAO_POST_BLOCK
 #define MSAO_POST_BLOCK 256
 #endif

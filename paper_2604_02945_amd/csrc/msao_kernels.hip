@@ -725,7 +725,7 @@ template <bool LR>
 __global__ __launch_bounds__(kScoreBlock) __attribute__((amdgpu_waves_per_eu(5, 8))) void k_score(ScoreArgs a)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int w = uniform(score_block(a) * (kScoreBlock / kWave) + (threadIdx.x >> 6));
+    const int w = uniform(a.wi_first + score_block(a) * (kScoreBlock / kWave) + (threadIdx.x >> 6));
     if (w >= a.t.n_wi_score) return;
     const int s = uniform(a.t.wi_seg[w]);
     const DevSeg sg = a.t.seg[s];
@@ -761,6 +761,332 @@ __global__ __launch_bounds__(kScoreBlock) __attribute__((amdgpu_waves_per_eu(5, 
         pr.dsum = dsum;
         a.t.partial[w] = pr;
         if constexpr (LR) a.t.partial_x[w] = PartialX{lr.asum, lr.l1, lr.l2, 0u};
+    }
+}
+
+// ---------------------------------------------------------------- k_pair
+
+// bf16 clips whose rows are 512, 1024, 1536 or 2048 bytes (and that are not
+// kept whole, whose rows the chain pass copies out). A wavefront takes
+// two adjacent patch positions p0, p0 + 1 over a range of frames: lanes 0-31
+// hold the first position's row of a frame, lanes 32-63 the second's, so each
+// frame is one run of consecutive rows (4 KiB for 1024 channels). A block's
+// kPairWaves wavefronts take consecutive frame ranges of the same two
+// positions; the first frame of every range but the first has its
+// predecessor in the wavefront before, which derives that frame's temporal
+// terms at the end from a copy of the frame that its owner left in LDS (no
+// frame is read twice). Frames rotate through three register sets: the
+// current one, its predecessor, and the next one in flight; the frame after
+// that is loaded into the predecessor's registers once they are used. Per
+// channel the arithmetic is vector-only: the activity sign of tau - |x| as
+// packed 16-bit differences, four of them gathered into one word of 0x00/0xFF
+// bytes whose popcount (/8) gives the active count and, XOR the previous
+// frame's word, the changed count d; L1 and L2 as bf16 pair dot products; res
+// from the widened values of this and the previous frame. Half-wavefront sums
+// end in lanes 31 and 63 and are parked in a token buffer (lane 2i + h: frame
+// t0 + i, position p0 + h), written out once per wavefront, so the frame loop
+// issues no stores and every wait in it is for one known load.
+
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+
+// Sum over each 16-lane row (every lane of the row gets it), then rows 1 and
+// 3 add the sums of rows 0 and 2: lanes 16-31 hold the sum of lanes 0-31,
+// lanes 48-63 the sum of lanes 32-63.
+__device__ __forceinline__ float half_sum(float v)
+{
+    v += dpp_f<0xB1>(v);
+    v += dpp_f<0x4E>(v);
+    v += dpp_f<0x141>(v);
+    v += dpp_f<0x140>(v);
+    v += dpp_f<0x142>(v);
+    return v;
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_all_u(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+__device__ __forceinline__ uint32_t half_sum_u(uint32_t v)
+{
+    v += dpp_all_u<0xB1>(v);
+    v += dpp_all_u<0x4E>(v);
+    v += dpp_all_u<0x141>(v);
+    v += dpp_all_u<0x140>(v);
+    v += dpp_all_u<0x142>(v);
+    return v;
+}
+
+struct PairSums {
+    float l1, l2, res;
+    uint32_t act, chg;  // 8 per active channel, 8 per changed channel
+};
+
+// tau - |x| per 16-bit half: negative (sign bit set) iff the channel is active.
+__device__ __forceinline__ uint32_t act_sign(uint32_t th2, uint32_t x)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(s16x2, th2) - __builtin_bit_cast(s16x2, x & 0x7FFF7FFFu));
+}
+
+// One frame of this lane's position (4 NU dwords, 8 NU channels) against the
+// previous frame's raw words y and activity words pq; nq gets this frame's.
+// after(u) runs once unit u of y has been used.
+template <int NU, typename Hook>
+__device__ __forceinline__ PairSums pair_frame(const vec4 (&v)[NU], const vec4 (&y)[NU], uint32_t th2,
+                                               const uint32_t (&pq)[NU * 2], uint32_t (&nq)[NU * 2], Hook&& after)
+{
+    PairSums c{0.0f, 0.0f, 0.0f, 0u, 0u};
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+        uint32_t sg[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t x = v[u][e], yp = y[u][e];
+            sg[e] = act_sign(th2, x);
+            c.l1 = dot2(x & 0x7FFF7FFFu, kBf16OnePair, c.l1);
+            c.l2 = dot2(x, x, c.l2);
+            const float dlo = __uint_as_float(x << 16) - __uint_as_float(yp << 16);
+            const float dhi = __uint_as_float(x & 0xFFFF0000u) - __uint_as_float(yp & 0xFFFF0000u);
+            c.res = fmaf(dlo, dlo, c.res);
+            c.res = fmaf(dhi, dhi, c.res);
+        }
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            // bytes 0xFF / 0x00 from the sign bits 15 and 31 of two words
+            const uint32_t m = __builtin_amdgcn_perm(sg[2 * e + 1], sg[2 * e], 0x0B0A0908u);
+            c.act += (uint32_t)__builtin_popcount(m);
+            c.chg += (uint32_t)__builtin_popcount(m ^ pq[u * 2 + e]);
+            nq[u * 2 + e] = m;
+        }
+        after(u);
+    }
+    return c;
+}
+
+// Activity words of a frame (the halo frame before a block's range).
+template <int NU>
+__device__ __forceinline__ void pair_words(const vec4 (&v)[NU], uint32_t th2, uint32_t (&nq)[NU * 2])
+{
+#pragma unroll
+    for (int u = 0; u < NU; ++u)
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+            nq[u * 2 + e] = __builtin_amdgcn_perm(act_sign(th2, v[u][2 * e + 1]), act_sign(th2, v[u][2 * e]),
+                                                  0x0B0A0908u);
+}
+
+// The two positions' statistics of one frame (half sums in lanes 31 and 63).
+struct PairTok {
+    float l1, l2, res;
+    uint32_t cnt;  // active count | d << 16
+};
+
+__device__ __forceinline__ PairTok pair_reduce(const PairSums& c)
+{
+    return PairTok{half_sum(c.l1), half_sum(c.l2), half_sum(c.res), half_sum_u((c.act >> 3) | ((c.chg >> 3) << 16))};
+}
+
+// Lane slot of the buffer takes lane 31's value of v, lane slot + 1 lane 63's.
+template <typename T>
+__device__ __forceinline__ T park(T buf, T v, bool at0, bool at1)
+{
+    const T a = __builtin_bit_cast(T, __builtin_amdgcn_readlane((int)__builtin_bit_cast(uint32_t, v), 31));
+    const T b = __builtin_bit_cast(T, __builtin_amdgcn_readlane((int)__builtin_bit_cast(uint32_t, v), 63));
+    return at0 ? a : (at1 ? b : buf);
+}
+
+template <int NU>
+__device__ __forceinline__ void vcopy(vec4 (&d)[NU], const vec4 (&s)[NU])
+{
+#pragma unroll
+    for (int u = 0; u < NU; ++u) d[u] = s[u];
+}
+
+// Writes token (frame t, position p) with its statistics: main z, l1, l2 (and
+// the signature placeholder); temporal d, res, info.
+__device__ __forceinline__ void pair_write(const ScoreArgs& a, const DevSeg& sg, int g, const PairTok& s, bool main,
+                                           bool temporal)
+{
+    const TokenOut& o = a.tok;
+    const uint32_t act = s.cnt & 0xFFFFu, dd = s.cnt >> 16;
+    const uint32_t z = (uint32_t)sg.C - act;
+    if (main) {
+        if (a.mode == kModeScore) {
+            if (o.z) o.z[g] = z;
+            if (o.l1) o.l1[g] = s.l1;
+            if (o.l2) o.l2[g] = s.l2;
+        }
+        if (o.sig) o.sig[g] = 0ull;
+    }
+    if (temporal) {
+        if (a.mode == kModeScore && o.info) {
+            float red = sg.lam_s * (float)z;
+            red += sg.lam_t * (float)((uint32_t)sg.C - dd);
+            o.info[g] = 1.0f - red * __builtin_amdgcn_rcpf((float)sg.C);
+        }
+        if (o.d) o.d[g] = dd;
+        if (o.res) o.res[g] = s.res;
+    }
+}
+
+// Work item q of a k_pair segment (wavefront wv of its block).
+template <int NU>
+__device__ __forceinline__ void score_pair(const ScoreArgs& a, const DevSeg& sg, int q, int wv, int lane,
+                                           uint32_t* lds, uint32_t& nsp, uint32_t& dsum)
+{
+    constexpr int ND = NU * 4;
+    const int npairs = (sg.P + 1) >> 1;
+    const int qb = q / kPairWaves;
+    const int tbi = uniform(qb / npairs), j = uniform(qb - (qb / npairs) * npairs);
+    const int F = uniform(sg.per_item);
+    const int tb = tbi * kPairWaves * F;
+    const int tend = uniform(min(sg.T, tb + kPairWaves * F));
+    const int t0 = uniform(min(tend, tb + wv * F)), t1 = uniform(min(tend, t0 + F));
+    const int p0 = uniform(2 * j);
+    const int h = lane >> 5, l = lane & 31;
+    const bool two = uniform(p0 + 1 < sg.P ? 1 : 0) != 0;
+    const bool present = h == 0 || two;
+    const int rb = uniform(sg.nchunk * 16);
+    const int64_t fstride = (int64_t)sg.P * sg.stride_bytes;
+    const uint8_t* base = sg.data + (int64_t)p0 * sg.stride_bytes;
+    const int nrec = uniform(two ? (int)sg.stride_bytes + rb : rb);
+    // unit u of this lane's row at voff + 512 u; a missing second position
+    // reads as zeros (an offset past the resource)
+    const int voff = present ? h * (int)sg.stride_bytes + l * 16 : 0x7FFFFFF0;
+    // a frame past the range reads as zeros from an empty resource: every
+    // load is issued, so the waits count them exactly
+    auto frame_rsrc = [&](int t, bool ok) {
+        return make_rsrc(base + (ok ? (int64_t)t * fstride : 0), ok ? nrec : 0);
+    };
+    auto load = [&](vec4 (&v)[NU], int t, bool ok) {
+        const rsrc_t rs = frame_rsrc(t, ok);
+#pragma unroll
+        for (int u = 0; u < NU; ++u) v[u] = bload(rs, voff + u * 512);
+    };
+    const uint32_t lo = bf16_thresholds(a.t.tau).lo;
+    const uint32_t th2 = lo | (lo << 16);
+    // ranges after a block's first leave their first frame's temporal terms to
+    // the wavefront before; the first range of a block after the clip's first
+    // reads the frame before it (halo); the clip's frame 0 follows the zero frame
+    const bool deferred = wv > 0 && t0 < t1;
+    PairTok tok{0.0f, 0.0f, 0.0f, 0u};
+    // frame t in cur, its predecessor in prev; unit u of frame t + 2 is loaded
+    // into prev's registers once unit u of prev has been used
+    auto step = [&](const vec4 (&cur)[NU], vec4 (&prev)[NU], const uint32_t (&pq)[NU * 2],
+                    uint32_t (&nq)[NU * 2], int t) {
+        const rsrc_t rs = frame_rsrc(t + 2, t + 2 < t1);
+        const PairSums c = pair_frame<NU>(cur, prev, th2, pq, nq, [&](int u) {
+            prev[u] = bload(rs, voff + u * 512);
+            // keep the load here, where its registers have just been freed
+            __builtin_amdgcn_sched_barrier(0);
+        });
+        const PairTok r = pair_reduce(c);
+        const int slot = 2 * (t - t0);
+        const bool at0 = lane == slot, at1 = lane == slot + 1;
+        tok.l1 = park(tok.l1, r.l1, at0, at1);
+        tok.l2 = park(tok.l2, r.l2, at0, at1);
+        tok.res = park(tok.res, r.res, at0, at1);
+        tok.cnt = park(tok.cnt, r.cnt, at0, at1);
+    };
+    vec4 R0[NU], R1[NU], R2[NU], L[NU];
+    uint32_t Q0[NU * 2], Q1[NU * 2], Q2[NU * 2], LQ[NU * 2];
+    auto keep = [&](const vec4 (&v)[NU], const uint32_t (&w)[NU * 2]) {
+        vcopy<NU>(L, v);
+#pragma unroll
+        for (int i = 0; i < NU * 2; ++i) LQ[i] = w[i];
+    };
+    if (t0 < t1) {
+        // the frame before t0 in R2 (its words in Q2), t0 in R0, t0 + 1 in R1
+        load(R2, t0 - 1, wv == 0 && t0 > 0);
+        load(R0, t0, true);
+        load(R1, t0 + 1, t0 + 1 < t1);
+        pair_words<NU>(R2, th2, Q2);
+        if (deferred) {
+            uint32_t* slot = lds + (wv - 1) * ND * kWave;
+#pragma unroll
+            for (int u = 0; u < NU; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) slot[(u * 4 + e) * kWave + lane] = R0[u][e];
+        }
+        // frame t0 + i is in R[i % 3] with its words in Q[i % 3]; the last
+        // frame and its words are kept in L, LQ for the end
+        int t = t0;
+        while (true) {
+            step(R0, R2, Q2, Q0, t);
+            if (++t >= t1) {
+                keep(R0, Q0);
+                break;
+            }
+            step(R1, R0, Q0, Q1, t);
+            if (++t >= t1) {
+                keep(R1, Q1);
+                break;
+            }
+            step(R2, R1, Q1, Q2, t);
+            if (++t >= t1) {
+                keep(R2, Q2);
+                break;
+            }
+        }
+        // the range's tokens: lane 2i + h holds frame t0 + i, position p0 + h
+        const int nslot = 2 * (t1 - t0);
+        const int fi = lane >> 1, hh = lane & 1;
+        const bool mine = lane < nslot && (hh == 0 || two);
+        const bool temporal_ok = !(deferred && fi == 0);
+        const uint32_t act = tok.cnt & 0xFFFFu, dd = tok.cnt >> 16;
+        if (mine) pair_write(a, sg, sg.tok_off + (t0 + fi) * sg.P + p0 + hh, tok, true, temporal_ok);
+        nsp += (uint32_t)__popcll(__ballot(mine && act < (uint32_t)sg.A_s));
+        uint32_t dpart = mine && temporal_ok && t0 + fi >= 1 ? dd : 0u;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) dpart += (uint32_t)__shfl_xor((int)dpart, o);
+        dsum += dpart;
+    }
+    __syncthreads();
+    // the next range's first frame against this range's last (frame t1 - 1)
+    if (wv < kPairWaves - 1 && t1 == t0 + F && t1 < tend) {
+        const uint32_t* slot = lds + wv * ND * kWave;
+        vec4 nx[NU];
+#pragma unroll
+        for (int u = 0; u < NU; ++u)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) nx[u][e] = slot[(u * 4 + e) * kWave + lane];
+        const PairSums c = pair_frame<NU>(nx, L, th2, LQ, Q1, [](int) {});
+        const PairTok r = pair_reduce(c);
+        if (l == 31 && present) pair_write(a, sg, sg.tok_off + t1 * sg.P + p0 + h, r, false, true);
+        const uint32_t d0 = (uint32_t)__builtin_amdgcn_readlane((int)(r.cnt >> 16), 31);
+        const uint32_t d1 = two ? (uint32_t)__builtin_amdgcn_readlane((int)(r.cnt >> 16), 63) : 0u;
+        dsum += d0 + d1;
+    }
+}
+
+// One wavefront per k_pair work item; consecutive blocks (neighbouring pairs
+// of positions, whose statistics share cache lines) run on one XCD.
+__global__ __launch_bounds__(kPairWaves * 64) __attribute__((amdgpu_waves_per_eu(kPairWaves, kPairWaves)))
+void k_pair(ScoreArgs a)
+{
+    __shared__ uint32_t lds[(kPairWaves - 1) * (kPairMaxRowBytes / 128) * kWave];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = uniform(threadIdx.x >> 6);
+    const int nb = gridDim.x, b = blockIdx.x, x = b & 7, per = nb >> 3, rem = nb & 7;
+    const int vb = uniform(x * per + min(x, rem) + (b >> 3));
+    const int w = vb * kPairWaves + wv;
+    const int s = uniform(a.t.wi_seg[w]);
+    const DevSeg sg = a.t.seg[s];
+    const int q = w - sg.wi_begin;
+    uint32_t nsp = 0, dsum = 0;  // wave-uniform
+    switch (sg.nchunk >> 5) {  // rows of 512-byte units
+    case 1: score_pair<1>(a, sg, q, wv, lane, lds, nsp, dsum); break;
+    case 2: score_pair<2>(a, sg, q, wv, lane, lds, nsp, dsum); break;
+    case 3: score_pair<3>(a, sg, q, wv, lane, lds, nsp, dsum); break;
+    default: score_pair<4>(a, sg, q, wv, lane, lds, nsp, dsum); break;
+    }
+    if (lane == 0) {
+        Partial pr;
+        pr.nsparse = nsp;
+        pr.pad_ = 0u;
+        pr.dsum = dsum;
+        a.t.partial[w] = pr;
     }
 }
 
@@ -1868,23 +2194,36 @@ template <typename Args>
 static int launch(void (*kernel)(Args), dim3 grid, dim3 block, size_t lds, void* stream, const Args& a,
                   void* ev0, void* ev1)
 {
-    if (ev0 && ev1)
+    if (ev0 || ev1)
         hipExtLaunchKernelGGL(kernel, grid, block, lds, (hipStream_t)stream, (hipEvent_t)ev0, (hipEvent_t)ev1, 0, a);
     else
         hipLaunchKernelGGL(kernel, grid, block, lds, (hipStream_t)stream, a);
     return (int)hipGetLastError();
 }
 
+// k_pair's clips (work items [0, n_wi_pair)), then k_score for the rest:
+// ev0 is recorded at the first launch's start, ev1 at the last one's end.
 int launch_score(const ScoreArgs& a, void* stream, void* ev0, void* ev1)
 {
     if (a.t.n_wi_score <= 0) return kNoLaunch;
     const int waves = kScoreBlock / kWave;
-    const unsigned grid = (unsigned)((a.t.n_wi_score + waves - 1) / waves);
     if (a.learned) {
-        if (!a.t.partial_x || !a.t.proj) return (int)hipErrorInvalidValue;  // a learned plan's tables
+        if (!a.t.partial_x || !a.t.proj || a.t.n_wi_pair != 0) return (int)hipErrorInvalidValue;  // a learned plan's tables
+        const unsigned grid = (unsigned)((a.t.n_wi_score + waves - 1) / waves);
         return launch(k_score<true>, dim3(grid), dim3(kScoreBlock), 0, stream, a, ev0, ev1);
     }
-    return launch(k_score<false>, dim3(grid), dim3(kScoreBlock), 0, stream, a, ev0, ev1);
+    const int npair = a.t.n_wi_pair;
+    if (npair < 0 || npair % kPairWaves != 0 || npair > a.t.n_wi_score) return (int)hipErrorInvalidValue;
+    const bool rest = a.t.n_wi_score > npair;
+    if (npair > 0) {
+        const int rc = launch(k_pair, dim3((unsigned)(npair / kPairWaves)), dim3(kPairWaves * kWave), 0, stream, a, ev0,
+                              rest ? nullptr : ev1);
+        if (rc != 0 || !rest) return rc;
+    }
+    ScoreArgs b = a;
+    b.wi_first = npair;
+    const unsigned grid = (unsigned)((a.t.n_wi_score - npair + waves - 1) / waves);
+    return launch(k_score<false>, dim3(grid), dim3(kScoreBlock), 0, stream, b, npair > 0 ? nullptr : ev0, ev1);
 }
 
 template <int NT, bool LR>
