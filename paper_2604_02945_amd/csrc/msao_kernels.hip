@@ -1109,6 +1109,7 @@ struct PostShared {
     uint64_t vsel;            // selection: key of the wanted rank among few candidates
     uint64_t nsp[kWaves], dsum[kWaves], ntok[kNumMod], qbits[kNumMod];
     uint32_t digit, below, in_bin, ncand;
+    uint32_t ncopy;           // selection: candidates copied for a direct rank
     // learned calls
     uint64_t asum[kWaves], csum[kWaves];
     double l1[kWaves], l2[kWaves];
@@ -1605,7 +1606,8 @@ __device__ __forceinline__ uint32_t block_exscan_dpp(uint32_t v, PostShared<NT>&
 
 // Keys of tokens [0, N) of a selection staged into LDS (when in_lds), each
 // also counted in the histogram of the first radix digit, key >> shift (the
-// keys lie in [0, kmax], so the first digit needs no range of its own). U
+// keys lie in [0, kmax], so the first digit needs no range of its own), which
+// this zeroes first (every thread of the block calls it). U
 // tokens per thread are loaded before any is used, so that the global loads
 // of one thread overlap; indices past N are clamped (and their values
 // dropped) so that no load sits behind a branch.
@@ -1615,6 +1617,35 @@ __device__ __forceinline__ void stage_keys(const uint32_t* __restrict__ z, const
                                            bool in_lds, uint64_t* keys, uint32_t* hist, int shift, bool count)
 {
     constexpr int U = 8;
+    if (N <= U * NT) {
+        // one batch per thread: its loads are issued first and the histogram
+        // is zeroed while they are in flight (one barrier before the counting)
+        uint32_t zz[U], ee[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int g = min((int)threadIdx.x + u * NT, N - 1);
+            zz[u] = KIND == kKeyZ || KIND == kKeyFull ? z[g] : 0u;
+            ee[u] = KIND == kKeyE || KIND == kKeyFull ? E - d[g] : 0u;
+            if constexpr (KIND == kKeyImp) zz[u] = (uint32_t)imp_key(imp[g]);
+        }
+        for (int b = threadIdx.x; b < kRadixBins; b += NT) hist[b] = 0u;
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = (int)threadIdx.x + u * NT;
+            if (i < N) {
+                uint64_t key = 0ull;
+                if constexpr (KIND == kKeyZ || KIND == kKeyImp) key = zz[u];
+                else if constexpr (KIND == kKeyE) key = ee[u];
+                else if constexpr (KIND == kKeyFull) key = Ms * (uint64_t)zz[u] + Mt * (uint64_t)ee[u];
+                if (in_lds) keys[i] = key;
+                if (count) atomicAdd(&hist[(uint32_t)(key >> shift)], 1u);
+            }
+        }
+        return;
+    }
+    for (int b = threadIdx.x; b < kRadixBins; b += NT) hist[b] = 0u;
+    __syncthreads();
     for (int i0 = threadIdx.x; i0 < N; i0 += U * NT) {
         uint32_t zz[U], ee[U];
 #pragma unroll
@@ -1699,9 +1730,8 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
         const bool first = in_range == (uint32_t)N && below == 0u && prefix == 0ull;
         if (!built && collect && in_range <= (uint32_t)kSmallCand) {
             // so few keys are left that a copy of them and a direct rank among
-            // them cost less than the remaining digit passes
-            if (tid == 0) sh.ncand = 0u;
-            __syncthreads();
+            // them cost less than the remaining digit passes (their count was
+            // reset by the digit scan before its barrier)
             for (int base = wid * kWave; base < N; base += U * NT) {
                 uint64_t x[U];
 #pragma unroll
@@ -1712,17 +1742,17 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
                     const uint64_t m = __ballot(match);
                     if (m) {
                         uint32_t at = 0;
-                        if (lane == 0) at = atomicAdd(&sh.ncand, (uint32_t)__popcll(m));
+                        if (lane == 0) at = atomicAdd(&sh.ncopy, (uint32_t)__popcll(m));
                         at = (uint32_t)__shfl((int)at, 0);
                         if (match) cand[at + lanes_below(m)] = x[u];
                     }
                 }
             }
             __syncthreads();
+            const int m = (int)sh.ncopy;
             // candidate c = (w % cw) * 64 + lane is counted against the j-range
             // part w / cw of the candidates by wavefront w; the parts' counts
             // of smaller and of not larger candidates meet in LDS
-            const int m = (int)sh.ncand;
             const int cw = (m + kWave - 1) / kWave, nparts = kW / cw;
             const int c = (wid % cw) * kWave + lane, part = wid / cw;
             const int per = (m + nparts - 1) / nparts, j0 = min(m, part * per), j1 = min(m, j0 + per);
@@ -1764,10 +1794,12 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
             prefix = sh.vsel;
             below += sh.below;
             bits = 0;
-            __syncthreads();
             break;
         }
         if (!built) {
+            // (every thread has read the previous digit's fields, which the
+            // zeroing does not touch; the histogram was last read before the
+            // previous barrier)
             for (int b = tid; b < kRadixBins; b += NT) sh.hist[b] = 0u;
             if (tid == 0) sh.ncand = 0u;
             __syncthreads();
@@ -1804,23 +1836,31 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
             if (collect) ncand = (int)sh.ncand;
         }
         built = false;
-        uint32_t local = 0;
+        // the digit of rank `rank`, found by wavefront 0 alone (lane l sums
+        // bins [32 l, 32 l + 32), read in a rotated order so that the lanes
+        // hit different banks; a wavefront scan; the lane holding the rank
+        // walks its bins), so the other wavefronts wait at one barrier
+        if (wid == 0) {
+            constexpr int BPL = kRadixBins / kWave;
+            uint32_t local = 0;
 #pragma unroll
-        for (int j = 0; j < (kRadixBins / NT); ++j) local += sh.hist[tid * (kRadixBins / NT) + j];
-        uint32_t tot;
-        const uint32_t ex = block_exscan_dpp(local, sh, &tot);
-        if (ex <= rank && rank < ex + local) {
-            uint32_t cum = ex;
-            for (int j = 0; j < (kRadixBins / NT); ++j) {
-                const uint32_t h = sh.hist[tid * (kRadixBins / NT) + j];
-                if (rank < cum + h) {
-                    sh.digit = (uint32_t)(tid * (kRadixBins / NT) + j);
-                    sh.below = cum;
-                    sh.in_bin = h;
-                    break;
-                }
-                cum += h;
+            for (int j = 0; j < BPL; ++j) local += sh.hist[lane * BPL + ((j + lane) & (BPL - 1))];
+            const uint32_t incl = wave_incl_scan(local);
+            // the lane whose run of bins holds the rank; then its BPL bins, one
+            // per lane, scanned again to find the bin
+            const uint64_t hit = __ballot(incl - local <= rank && rank < incl);
+            const int owner = (int)__builtin_ctzll(hit | (1ull << 63));
+            const uint32_t ex = (uint32_t)__shfl((int)(incl - local), owner);
+            const uint32_t h = lane < BPL ? sh.hist[owner * BPL + lane] : 0u;
+            const uint32_t hin = wave_incl_scan(h);
+            const uint64_t at = __ballot(lane < BPL && rank < ex + hin);
+            const int j = (int)__builtin_ctzll(at | (1ull << 63));
+            if (lane == j) {
+                sh.digit = (uint32_t)(owner * BPL + j);
+                sh.below = ex + hin - h;
+                sh.in_bin = h;
             }
+            if (lane == 0) sh.ncopy = 0u;  // for a candidate copy that follows
         }
         __syncthreads();
         const uint32_t dg = sh.digit, bl = sh.below;
@@ -1829,7 +1869,6 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
         rank -= bl;
         prefix = (prefix << db) | dg;
         bits = shift;
-        __syncthreads();
     }
     const uint64_t vstar = lo + prefix;        // key of rank k-1
     const uint32_t ties = (uint32_t)k - below; // keys equal to vstar that are kept, lowest index first
@@ -1969,8 +2008,6 @@ __device__ void role_select(const PostArgs& a, int unit, PostShared<NT>& sh, uin
     const uint64_t lo = 0ull, hi = su.kmax;
     const int bits = hi > 0 ? 64 - __clzll((long long)hi) : 0;
     const int shift0 = bits > kRadixBits ? bits - kRadixBits : 0;
-    for (int b = tid; b < kRadixBins; b += NT) sh.hist[b] = 0u;
-    __syncthreads();
     switch (kind) {
     case kKeyZ: stage_keys<NT, kKeyZ>(z, d, imp, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
     case kKeyE: stage_keys<NT, kKeyE>(z, d, imp, N, Ms, Mt, E, in_lds, keys, sh.hist, shift0, bits > 0); break;
