@@ -135,11 +135,11 @@ def _committed(profile, kernel_file):
     return rec["traffic_bytes_per_launch"] if rec.get("kernel_source_sha256") == source_hash(kernel_file) else None
 
 
-TRAFFIC_PROFILES = {  # (config, compacting run) -> counter summary of that k_score launch
+TRAFFIC_PROFILES = {  # (config, compacting run) -> counter summary of that scoring launch
     (4, True): "k_score_trimodal_traffic.json",
     (4, False): "k_score_trimodal_scoreonly_traffic.json",
-    (3, True): "k_score_video_traffic.json",
-    (3, False): "k_score_video_scoreonly_traffic.json",
+    (3, True): "k_pair_video_traffic.json",
+    (3, False): "k_pair_video_scoreonly_traffic.json",
     (5, True): "k_score_highres_traffic.json",
     (5, False): "k_score_highres_scoreonly_traffic.json",
     (2, True): "k_score_imagebatch_traffic.json",
@@ -147,8 +147,12 @@ TRAFFIC_PROFILES = {  # (config, compacting run) -> counter summary of that k_sc
 }
 
 
+# the scoring kernel of each workload: the video clips (bf16, 2 KiB rows) take k_pair
+SCORE_KERNEL = {3: "k_pair"}
+
+
 def committed_traffic(config, compact=True):
-    """HBM bytes per k_score launch of a workload (committed counters)."""
+    """HBM bytes per scoring launch of a workload (committed counters)."""
     name = TRAFFIC_PROFILES.get((config, compact))
     return _committed(name, "msao_kernels.hip") if name else None
 
@@ -695,7 +699,8 @@ def measure(w, args, dev, n_str, graph=False, with_compact=True, with_score_sele
             "hbm_frac_step": b_step / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS,
             "algorithmic_bytes": {"score": b_score, "select": b_select, "gather_write": b_compact},
             "kernel_ms": {"score": float(k_ms[0]), "post": float(k_ms[1]), "gather": float(k_ms[2])},
-            "roofline": {"bound": "hbm", "kernel": "k_score", "achieved": score_gbs, "peak": PEAK_HBM_GBS,
+            "roofline": {"bound": "hbm", "kernel": SCORE_KERNEL.get(w.config, "k_score"), "achieved": score_gbs,
+                         "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": score_gbs / PEAK_HBM_GBS,
                          "traffic": committed_traffic(w.config, compact=True)},
         })
@@ -722,7 +727,8 @@ def measure(w, args, dev, n_str, graph=False, with_compact=True, with_score_sele
             "hbm_frac_one_stream": bb / (ms_ss_serial * 1e-3) / 1e9 / PEAK_HBM_GBS,
             "hbm_frac_one_stream_median": bb / (med_ss * 1e-3) / 1e9 / PEAK_HBM_GBS,
             "kernel_ms": {"score": float(k_ss[0]), "post": float(k_ss[1])},
-            "roofline": {"bound": "hbm", "kernel": "k_score (score only)", "achieved": gbs_s, "peak": PEAK_HBM_GBS,
+            "roofline": {"bound": "hbm", "kernel": SCORE_KERNEL.get(w.config, "k_score") + " (score only)",
+                         "achieved": gbs_s, "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": gbs_s / PEAK_HBM_GBS,
                          "traffic": committed_traffic(w.config, compact=False)},
         }
