@@ -296,7 +296,8 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         const int kind = by_imp ? kKeyImp
                          : d.temporal && d.L_t > 0 ? (d.L_s > 0 ? kKeyFull : kKeyE) : (d.L_s > 0 ? kKeyZ : kKeyZero);
         auto push_selection = [&](int frame, int n_u, int kfix) {
-            const int parts = n_u >= kSelSplitMin ? (n_u + kSelPartTokens - 1) / kSelPartTokens : 1;
+            const int part_tokens = n_u >= kPostBigSegment ? kSelBigPartTokens : kSelPartTokens;
+            const int parts = n_u >= kSelSplitMin ? (n_u + part_tokens - 1) / part_tokens : 1;
             for (int q = 0; q < parts; ++q) {
                 SelUnit u;
                 std::memset(&u, 0, sizeof u);

@@ -87,12 +87,21 @@ struct SelUnit {
     int32_t request, modality, pad_;
 };
 // Selections of at least kSelSplitMin tokens are split into blocks of about
-// kSelPartTokens tokens each for their counting and writing.
+// kSelPartTokens tokens each for their counting and writing; those of the
+// large-block launch (kPostBigSegment tokens or more, 1,024 threads) into
+// parts of kSelBigPartTokens, since each part stages all of the keys again.
 #ifndef MSAO_SEL_PART_TOKENS
-#define MSAO_SEL_PART_TOKENS 2048
+#define MSAO_SEL_PART_TOKENS 768
 #endif
 constexpr int kSelPartTokens = MSAO_SEL_PART_TOKENS;
-constexpr int kSelSplitMin = 4096;
+#ifndef MSAO_SEL_BIG_PART_TOKENS
+#define MSAO_SEL_BIG_PART_TOKENS 2048
+#endif
+constexpr int kSelBigPartTokens = MSAO_SEL_BIG_PART_TOKENS;
+#ifndef MSAO_SEL_SPLIT_MIN
+#define MSAO_SEL_SPLIT_MIN 1024
+#endif
+constexpr int kSelSplitMin = MSAO_SEL_SPLIT_MIN;
 
 // Integer partial sums of one scoring work item (no atomics, no zeroing).
 struct Partial {
