@@ -781,6 +781,25 @@ def msao_mas_score_learned(segments, n_requests, params=None, heads=None, mlp=No
     return o, extra
 
 
+def prepare_learned(segments, n_requests, outputs, params=None, heads=None, mlp=None, alpha=None, ctx=None,
+                    compact=True):
+    """msao_run_learned's arguments marshalled once (as prepare() does for the
+    other entry points): returns (call, extra); each call(stream) enqueues one
+    run on the same outputs and extra buffers (tables still uploaded per call)."""
+    device, ctx, segt, prm, harr, m, al, keep = _learned_args(segments, n_requests, params, heads, mlp, alpha, ctx)
+    o = outputs
+    n, R = len(segments), n_requests
+    extra = _learned_extra(o, R, device)
+    use_out = compact and o.out is not None
+    args = [ctx.handle, segt, n, R, _addr(prm), ctypes.cast(harr, _P) if harr is not None else None,
+            _addr(m) if m is not None else None, al, _addr(o.c_tok),
+            _ptr(extra["importance"]) if o.ntok else None, _addr(o.c_frm), _addr(o.c_req),
+            _ptr(extra["alpha"]), _ptr(extra["desc"]), _addr(o.c_sel),
+            _ptr(o.out) if use_out else None, o.out_off if use_out else None,
+            ctypes.c_int64(o.out_bytes if use_out else 0), _ptr(o.workspace), ctypes.c_size_t(o.ws_bytes), None]
+    return Call("msao_run_learned", args, ctx, keep + [o, extra]), extra
+
+
 def msao_run_learned(segments, n_requests, params=None, heads=None, mlp=None, alpha=None, ctx=None, outputs=None,
                      stream=None, compact=True):
     """msao_mas_score_learned plus the selection and compaction of msao_run,

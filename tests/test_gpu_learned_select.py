@@ -213,3 +213,29 @@ def test_clip_with_a_head_beyond_lds_staging(keep, dev):
     img = Segment(0, IMAGE, 1, 576, C, "bf16", 0.25, f32_to_bf16_bits(rng.standard_normal((576, C)).astype(np.float32)))
     heads = [make_head(clip, rng, 100, 3, 0.2)[1], make_head(img, rng, 24, 3, -0.4)[1]]
     run_and_check([clip, img], 1, heads, None, dev)
+
+
+def test_prepared_call_matches_one_shot(dev):
+    """prepare_learned marshals msao_run_learned once: two calls of it give the
+    one-shot call's outputs byte for byte (scores, selection, compacted rows)."""
+    w, heads, mlp = trimodal(3)
+    segs, R, p = w.segments, 3, w.params
+    dsegs = to_device(segs, dev)
+    dh, dm = device_heads(segs, heads, dev), device_mlp(mlp, dev)
+    one, oextra = msao.msao_run_learned(dsegs, R, p, heads=dh, mlp=dm)
+    outs = msao.Outputs(dsegs, R)
+    call, extra = msao.binding.prepare_learned(dsegs, R, outs, p, heads=dh, mlp=dm)
+    log("[learned select] prepared call, twice")
+    for _ in range(2):
+        call()
+        torch.cuda.synchronize()
+        a = {k: v.cpu().numpy() for k, v in one.results(R, len(segs)).items()}
+        b = {k: v.cpu().numpy() for k, v in outs.results(R, len(segs)).items()}
+        for k in a:
+            assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
+        assert np.array_equal(oextra["importance"].cpu().numpy().view(np.uint8),
+                              extra["importance"].cpu().numpy().view(np.uint8))
+        ra = msao.compacted_rows(dsegs, one, a["kept_count"])
+        rb = msao.compacted_rows(dsegs, outs, b["kept_count"])
+        for x, y in zip(ra, rb):
+            assert torch.equal(x.contiguous().view(torch.uint8), y.contiguous().view(torch.uint8))
