@@ -570,6 +570,40 @@ def msao_run_simhash(segments, n_requests, hashes, params=None, alpha=None, ctx=
     return o, sig
 
 
+def prepare_simhash(entry, segments, n_requests, hashes, outputs, sig, params=None, alpha=None, ctx=None,
+                    compact=True) -> Call:
+    """msao_run_simhash's or msao_temporal_simhash's arguments (entry) marshalled
+    once, as prepare() does for the other entry points; sig is the caller's
+    [total tokens] int64 signature tensor."""
+    device = _device_of(segments)
+    ctx = ctx or default_context(device.index if device.index is not None else torch.cuda.current_device())
+    o = outputs
+    segt = segment_table(segments)
+    prm = params_struct(params)
+    n, R = len(segments), n_requests
+    harr, keep = _hash_array(hashes, n)
+    al = None
+    if alpha is not None:
+        vals = list(alpha)
+        if len(vals) != R * NMOD:
+            raise ValueError("alpha needs n_requests * 4 logits")
+        al = (ctypes.c_float * len(vals))(*vals)
+    keep += [segt, prm, al, o, sig]
+    if entry == "msao_run_simhash":
+        use_out = compact and o.out is not None
+        args = [ctx.handle, segt, n, R, _addr(prm), ctypes.cast(harr, _P), al, _addr(o.c_tok),
+                _ptr(sig) if o.ntok else None, _addr(o.c_frm), _addr(o.c_req), _addr(o.c_sel),
+                _ptr(o.out) if use_out else None, o.out_off if use_out else None,
+                ctypes.c_int64(o.out_bytes if use_out else 0), _ptr(o.workspace), ctypes.c_size_t(o.ws_bytes), None]
+    elif entry == "msao_temporal_simhash":
+        args = [ctx.handle, segt, n, R, _addr(prm), ctypes.cast(harr, _P), _ptr(sig) if o.ntok else None,
+                _ptr(o.tok["d"]) if o.ntok else None, _addr(o.c_frm), _ptr(o.req["temporal"]), _ptr(o.workspace),
+                ctypes.c_size_t(o.ws_bytes), None]
+    else:
+        raise ValueError(f"unknown SimHash entry point {entry}")
+    return Call(entry, args, ctx, keep)
+
+
 def msao_select_tokens(segments, n_requests, z, d=None, mas=None, params=None, ctx=None, outputs=None,
                        stream=None):
     """Per-segment top-k selection from z (and d); mas for MAS-guided keep ratios."""

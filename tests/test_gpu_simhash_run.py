@@ -394,3 +394,40 @@ def test_errors_write_nothing(dev):
         msao.msao_run_simhash(dsegs, 1, [dict(planes=planes, bits=24)], outputs=out)
     torch.cuda.synchronize()
     assert int(out.sel["kept_count"][0]) == -7
+
+
+def test_prepared_calls_match_one_shot(dev):
+    """prepare_simhash marshals msao_run_simhash / msao_temporal_simhash once:
+    two calls of each give the one-shot calls' outputs byte for byte."""
+    segs, hashes = mixed_int_table(77, 32, "bf16")
+    R, p = 2, default_params()
+    dsegs = to_device(segs, dev)
+    dh = [None if h is None else dict(planes=dev_tensor(h["planes"], s.dtype, dev), bits=h["bits"])
+          for s, h in zip(segs, hashes)]
+    ntok = sum(s.n_tokens for s in segs)
+    log("[simhash-run] prepared calls, twice each")
+    one, sig1 = msao.msao_run_simhash(dsegs, R, dh, p)
+    t_one, tsig1 = msao.msao_temporal_simhash(dsegs, R, dh, p)
+    o_run = msao.Outputs(dsegs, R)
+    o_tmp = msao.Outputs(dsegs, R, compact=False)
+    sig2 = torch.empty(ntok, dtype=torch.int64, device=dev)
+    tsig2 = torch.empty(ntok, dtype=torch.int64, device=dev)
+    run = msao.binding.prepare_simhash("msao_run_simhash", dsegs, R, dh, o_run, sig2, p)
+    tmp = msao.binding.prepare_simhash("msao_temporal_simhash", dsegs, R, dh, o_tmp, tsig2, p)
+    for _ in range(2):
+        run()
+        tmp()
+        torch.cuda.synchronize()
+        a, b = one.results(R, len(segs)), o_run.results(R, len(segs))
+        for k in a:
+            assert torch.equal(a[k].view(torch.uint8), b[k].view(torch.uint8)), k
+        assert torch.equal(sig1, sig2)
+        ra = msao.compacted_rows(dsegs, one, host(a["kept_count"]))
+        rb = msao.compacted_rows(dsegs, o_run, host(b["kept_count"]))
+        for x, y in zip(ra, rb):
+            assert torch.equal(x.contiguous().view(torch.uint8), y.contiguous().view(torch.uint8))
+        assert torch.equal(tsig1, tsig2)
+        assert torch.equal(t_one.tok["d"], o_tmp.tok["d"])
+        assert torch.equal(t_one.req["temporal"], o_tmp.req["temporal"])
+        for k in ("dframe", "sim", "gamma"):
+            assert torch.equal(t_one.frm[k], o_tmp.frm[k]), k
