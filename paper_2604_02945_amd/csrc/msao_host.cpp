@@ -253,6 +253,12 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
     int64_t chains_total = 0;
     for (int i = 0; i < n; ++i)
         if (is_temporal(segs[i])) chains_total += segs[i].tokens_per_frame;
+    // selections before any split: mid-size ones are split only while the
+    // launch would otherwise leave CUs without a selection block
+    int64_t whole_sels = 0;
+    for (int i = 0; i < n; ++i)
+        whole_sels += per_frame && segs[i].n_frames >= 2 && segs[i].tokens_per_frame > 0 ? segs[i].n_frames : 1;
+    const bool split_mid = whole_sels < kSelSplitMaxSelections;
     for (int i = 0; i < n; ++i) {
         const msao_segment& s = segs[i];
         DevSeg& d = pl.seg[(size_t)i];
@@ -296,8 +302,9 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         const int kind = by_imp ? kKeyImp
                          : d.temporal && d.L_t > 0 ? (d.L_s > 0 ? kKeyFull : kKeyE) : (d.L_s > 0 ? kKeyZ : kKeyZero);
         auto push_selection = [&](int frame, int n_u, int kfix) {
-            const int part_tokens = n_u >= kPostBigSegment ? kSelBigPartTokens : kSelPartTokens;
-            const int parts = n_u >= kSelSplitMin ? (n_u + part_tokens - 1) / part_tokens : 1;
+            const int parts = n_u >= kPostBigSegment            ? (n_u + kSelBigPartTokens - 1) / kSelBigPartTokens
+                              : n_u >= kSelSplitMin && split_mid ? (n_u + kSelPartTokens - 1) / kSelPartTokens
+                                                                 : 1;
             for (int q = 0; q < parts; ++q) {
                 SelUnit u;
                 std::memset(&u, 0, sizeof u);

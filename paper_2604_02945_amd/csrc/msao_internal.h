@@ -86,10 +86,13 @@ struct SelUnit {
     int32_t seg_off;        // global token id of the segment's first token
     int32_t request, modality, pad_;
 };
-// Selections of at least kSelSplitMin tokens are split into blocks of about
-// kSelPartTokens tokens each for their counting and writing; those of the
-// large-block launch (kPostBigSegment tokens or more, 1,024 threads) into
-// parts of kSelBigPartTokens, since each part stages all of the keys again.
+// Selections of the large-block launch (kPostBigSegment tokens or more,
+// 1,024 threads) are split into parts of kSelBigPartTokens tokens for their
+// counting and writing, one block each. Selections of kSelSplitMin tokens or
+// more are split into parts of about kSelPartTokens tokens when the launch
+// has fewer than kSelSplitMaxSelections selections: more parts would only
+// queue behind each other on the CUs, since each part stages all of the keys
+// again.
 #ifndef MSAO_SEL_PART_TOKENS
 #define MSAO_SEL_PART_TOKENS 768
 #endif
@@ -102,6 +105,10 @@ constexpr int kSelBigPartTokens = MSAO_SEL_BIG_PART_TOKENS;
 #define MSAO_SEL_SPLIT_MIN 1024
 #endif
 constexpr int kSelSplitMin = MSAO_SEL_SPLIT_MIN;
+#ifndef MSAO_SEL_SPLIT_MAX_SELECTIONS
+#define MSAO_SEL_SPLIT_MAX_SELECTIONS 256
+#endif
+constexpr int kSelSplitMaxSelections = MSAO_SEL_SPLIT_MAX_SELECTIONS;
 
 // Integer partial sums of one scoring work item (no atomics, no zeroing).
 struct Partial {

@@ -409,6 +409,22 @@ def test_selection_beyond_lds_staging(dev):
     run_and_compare(segs, 2, default_params(), dev)
 
 
+@pytest.mark.parametrize("n_seg", [255, 256])
+def test_mid_size_selection_split_threshold(n_seg, dev):
+    """Selections of 1,024 to 4,095 tokens are split over several blocks only
+    while the launch has fewer than 256 selections: 255 segments take the split
+    path, 256 the whole one. Sizes span the split range (a part boundary within
+    a wavefront, one token short of the next part), fixed and MAS-guided keeps."""
+    rng = np.random.default_rng(400 + n_seg)
+    sizes = [1024, 1025, 1535, 1536, 1537, 2303, 2304, 4095] + list(rng.integers(1024, 4096, n_seg - 8))
+    mods = (IMAGE, AUDIO, TEXT)
+    segs = [_rand_seg(rng, i // 3, mods[i % 3], 1, int(n), 16, "bf16", -1.0 if i % 5 == 0 else 0.35, "relu_bg")
+            for i, n in enumerate(sizes)]
+    R = (n_seg + 2) // 3
+    log(f"[parity] {n_seg} selections of 1,024-4,095 tokens")
+    run_and_compare(segs, R, default_params(), dev)
+
+
 def test_plan_runs_match_oracle(dev):
     """msao_plan_create once, msao_plan_run several times (data rewritten in
     place between runs): every run matches the oracle on that run's data."""
