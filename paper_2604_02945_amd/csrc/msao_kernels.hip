@@ -1097,12 +1097,14 @@ constexpr int kRadixBits = 11;
 constexpr int kRadixBins = 1 << kRadixBits;
 
 // Shared state of a post-scoring block of NT threads.
+typedef unsigned int post_u32x4 __attribute__((ext_vector_type(4)));
+
 template <int NT>
 struct PostShared {
     static constexpr int kWaves = NT / kWave;
     static_assert(kWaves % kNumMod == 0, "the request role splits the wavefronts evenly over the modalities");
     static_assert(kRadixBins % NT == 0, "every thread owns the same number of radix bins");
-    uint32_t hist[kRadixBins];
+    alignas(16) uint32_t hist[kRadixBins];  // read 16 bytes at a time by the digit scan
     uint32_t scan[kWaves];
     uint32_t wcnt[kWaves][4];
     unsigned long long lo, hi, red;
@@ -1837,20 +1839,26 @@ __device__ void select_and_compact(const PostArgs& a, PostShared<NT>& sh, const 
         }
         built = false;
         // the digit of rank `rank`, found by wavefront 0 alone (lane l sums
-        // bins [32 l, 32 l + 32), read in a rotated order so that the lanes
-        // hit different banks; a wavefront scan; the lane holding the rank
-        // walks its bins), so the other wavefronts wait at one barrier
+        // bins [32 l, 32 l + 32) with eight 16-byte reads, taken in a rotated
+        // order so that the lanes served together hit different banks; a
+        // wavefront scan; the lane holding the rank walks its bins), so the
+        // other wavefronts wait at one barrier
         if (wid == 0) {
             constexpr int BPL = kRadixBins / kWave;
+            constexpr int VPL = BPL / 4;
+            const post_u32x4* hv = reinterpret_cast<const post_u32x4*>(sh.hist);
             uint32_t local = 0;
 #pragma unroll
-            for (int j = 0; j < BPL; ++j) local += sh.hist[lane * BPL + ((j + lane) & (BPL - 1))];
+            for (int j = 0; j < VPL; ++j) {
+                const post_u32x4 q = hv[lane * VPL + ((j + lane + (lane >> 3)) & (VPL - 1))];
+                local += (q.x + q.y) + (q.z + q.w);
+            }
             const uint32_t incl = wave_incl_scan(local);
             // the lane whose run of bins holds the rank; then its BPL bins, one
             // per lane, scanned again to find the bin
             const uint64_t hit = __ballot(incl - local <= rank && rank < incl);
             const int owner = (int)__builtin_ctzll(hit | (1ull << 63));
-            const uint32_t ex = (uint32_t)__shfl((int)(incl - local), owner);
+            const uint32_t ex = (uint32_t)__builtin_amdgcn_readlane((int)(incl - local), owner);
             const uint32_t h = lane < BPL ? sh.hist[owner * BPL + lane] : 0u;
             const uint32_t hin = wave_incl_scan(h);
             const uint64_t at = __ballot(lane < BPL && rank < ex + hin);
