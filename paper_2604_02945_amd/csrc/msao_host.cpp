@@ -410,8 +410,12 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
             pl.tseg.push_back(i);
             pl.any_temporal = true;
         } else if (N > 0) {
-            const int rb = (int)std::max<int64_t>(1, (ctx ? ctx->row_item_bytes : 8192) / ((int64_t)s.hidden * es));
-            d.per_item = rb;
+            // the fewest rows that reach the target bytes, unless they pass it
+            // by more than a quarter (then one row less, at least one)
+            const int64_t target = ctx ? ctx->row_item_bytes : 8192, row = (int64_t)s.hidden * es;
+            int64_t rb = (target + row - 1) / row;
+            if (rb > 1 && rb * row * 4 > target * 5) --rb;
+            d.per_item = (int32_t)rb;
             items = (int)((N + rb - 1) / rb);
         } else {
             d.per_item = 1;
