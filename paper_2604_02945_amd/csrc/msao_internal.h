@@ -340,6 +340,9 @@ constexpr int kScoreBlock = 256;   // 4 wavefronts, one work item each
 #define MSAO_PAIR_WAVES 4
 #endif
 constexpr int kPairWaves = MSAO_PAIR_WAVES;   // frame ranges of one pair of positions per k_pair block
+// k_pair's occupancy target (wavefronts per SIMD), whatever the block size:
+// its three frames of registers need about 125 VGPRs
+constexpr int kPairWavesPerEU = 4;
 constexpr int kPairMaxRowBytes = 2048;        // rows k_pair takes: four 512-byte units per half-wavefront
 #ifndef MSAO_PAIR_MAX_FRAMES
 #define MSAO_PAIR_MAX_FRAMES 16

@@ -1062,7 +1062,7 @@ __device__ __forceinline__ void score_pair(const ScoreArgs& a, const DevSeg& sg,
 
 // One wavefront per k_pair work item; consecutive blocks (neighbouring pairs
 // of positions, whose statistics share cache lines) run on one XCD.
-__global__ __launch_bounds__(kPairWaves * 64) __attribute__((amdgpu_waves_per_eu(kPairWaves, kPairWaves)))
+__global__ __launch_bounds__(kPairWaves * 64) __attribute__((amdgpu_waves_per_eu(kPairWavesPerEU, kPairWavesPerEU)))
 void k_pair(ScoreArgs a)
 {
     __shared__ uint32_t lds[(kPairWaves - 1) * (kPairMaxRowBytes / 128) * kWave];
