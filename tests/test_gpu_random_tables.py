@@ -6,7 +6,9 @@ modality, and the literal and per-frame flags. Same bar as the parity tests
 (run_and_compare): integers, kept indices and compacted rows bit-exact. The
 same kind of tables also go through the SimHash entry points and the learned
 heads at their bars; for msao_run_simhash the tables hold integer values, so
-that every projection is exact and the whole run is compared bit for bit."""
+that every projection is exact and the whole run is compared bit for bit.
+A second set of tables is drawn so that most of its clips take the paired
+scoring pass (bf16 rows of 512 to 2,048 bytes, up to 72 frames)."""
 import numpy as np
 import pytest
 import torch
@@ -55,6 +57,44 @@ def test_random_table(seed, dev):
     segs, R, p, pad = random_table(seed)
     log(f"[random] seed {seed}: {len(segs)} segments, R {R}, flags {p['flags']}, pad {pad}, "
         f"tokens {sum(s.n_tokens for s in segs)}")
+    run_and_compare(segs, R, p, dev, pad=pad)
+
+
+def random_pair_table(seed):
+    """Tables whose clips mostly take k_pair (bf16, 256 to 1,024 channels):
+    any frame count from 2 to 72 (several blocks along time past 64), odd
+    and even position counts, drifting and redrawn frames, beside a few
+    segments of the other passes."""
+    rng = np.random.default_rng(3000 + seed)
+    R = int(rng.integers(1, 4))
+    segs = []
+    for _ in range(int(rng.integers(1, 5))):
+        T, P = int(rng.integers(2, 73)), int(rng.integers(1, 40))
+        C = int(rng.choice([256, 512, 768, 1024]))
+        x = rng.standard_normal((T * P, C)).astype(np.float32)
+        if rng.random() < 0.5:
+            for t in range(1, T):
+                x[t * P:(t + 1) * P] = x[(t - 1) * P:t * P] + 0.02 * rng.standard_normal((P, C)).astype(np.float32)
+        keep = float(rng.choice([0.3, 0.5, -1.0, 0.07]))
+        segs.append(Segment(int(rng.integers(R)), VIDEO, T, P, C, "bf16", keep, f32_to_bf16_bits(x)))
+    for _ in range(int(rng.integers(0, 3))):
+        m = int(rng.choice([TEXT, IMAGE, AUDIO]))
+        C = int(rng.integers(1, 162)) * 8
+        P = int(rng.integers(1, 600))
+        x = rng.standard_normal((P, C)).astype(np.float32)
+        segs.append(Segment(int(rng.integers(R)), m, 1, P, C, "bf16", float(rng.choice([0.25, 1.0, -1.0])),
+                            f32_to_bf16_bits(x)))
+    p = default_params()
+    p["flags"] = int(rng.integers(4))
+    pad = int(rng.choice([0, 0, 8, 40]))
+    return segs, R, p, pad
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_pair_table(seed, dev):
+    segs, R, p, pad = random_pair_table(seed)
+    log(f"[random] pair seed {seed}: {len(segs)} segments, R {R}, flags {p['flags']}, pad {pad}, "
+        f"shapes {[(s.n_frames, s.tokens_per_frame, s.hidden) for s in segs]}")
     run_and_compare(segs, R, p, dev, pad=pad)
 
 
