@@ -139,6 +139,57 @@ def test_descriptor_temporal_entries():
     assert z[6] == 1.0 and z[5] == pytest.approx(o["temporal"][VIDEO], rel=1e-7) and z[5] > 0
 
 
+def _with(s, data, **kw):
+    f = dict(request=s.request, modality=s.modality, n_frames=s.n_frames, tokens_per_frame=s.tokens_per_frame,
+             hidden=s.hidden, dtype=s.dtype, keep_ratio=s.keep_ratio)
+    f.update(kw)
+    return Segment(f["request"], f["modality"], f["n_frames"], f["tokens_per_frame"], f["hidden"], f["dtype"],
+                   f["keep_ratio"], data)
+
+
+def test_descriptor_invariant_under_token_order():
+    """Entries 1-4 and 7 are sums over the modality's tokens divided by
+    totals: reordering the tokens of an image or audio segment leaves them
+    unchanged (up to the order of fp64 sums)."""
+    w = make_workload(4, n_requests=1)
+    rng = np.random.default_rng(11)
+    segs = [s if s.modality == TEXT else _with(s, np.ascontiguousarray(s.data[rng.permutation(s.n_tokens)]))
+            for s in w.segments]
+    a = oracle.run_learned(w.segments, 1, w.params)["desc"]
+    b = oracle.run_learned(segs, 1, w.params)["desc"]
+    np.testing.assert_allclose(b, a, rtol=1e-12, atol=0)
+
+
+def test_descriptor_scales_with_the_features():
+    """Doubling every feature (exact in fp32) and tau together keeps the
+    activity pattern, so rho and the active fraction stay, while the mean
+    magnitude and the root mean square double."""
+    w = make_workload(1)
+    p = dict(w.params)
+    segs2 = []
+    for s in w.segments:
+        assert s.dtype == "f32"
+        segs2.append(_with(s, (s.data * np.float32(2)).astype(np.float32)))
+    p2 = dict(p, tau=p["tau"] * 2)
+    a = oracle.run_learned(w.segments, 1, p)["desc"]
+    b = oracle.run_learned(segs2, 1, p2)["desc"]
+    for m in (TEXT, IMAGE):
+        np.testing.assert_array_equal(b[m][[0, 1, 2, 5, 6, 7]], a[m][[0, 1, 2, 5, 6, 7]])
+        np.testing.assert_allclose(b[m][[3, 4]], 2 * a[m][[3, 4]], rtol=1e-12)
+
+
+def test_descriptor_of_a_duplicated_segment():
+    """Two copies of a segment in one (request, modality): every mean and
+    fraction is that of one copy; only the token-count entry moves, to
+    ln(1 + 2N) / 16."""
+    w = make_workload(4, n_requests=1)
+    img = [s for s in w.segments if s.modality == IMAGE][0]
+    a = oracle.run_learned([img], 1, w.params)["desc"][IMAGE]
+    b = oracle.run_learned([img, img], 1, w.params)["desc"][IMAGE]
+    np.testing.assert_allclose(b[:7], a[:7], rtol=1e-12, atol=0)
+    assert b[7] == pytest.approx(math.log1p(2 * img.n_tokens) / 16, rel=1e-15)
+
+
 def mlp_for(R, P, H, rng):
     return dict(w1=rng.standard_normal((H, P + oracle.DESC)).astype(np.float32) * 0.3,
                 b1=rng.standard_normal(H).astype(np.float32) * 0.1,
