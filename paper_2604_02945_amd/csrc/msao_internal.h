@@ -356,10 +356,23 @@ constexpr int kPostBlock = MSAO_POST_BLOCK;  // threads per post-scoring block
 #define MSAO_POST_BIG_SEGMENT 4096
 #endif
 constexpr int kPostBigSegment = MSAO_POST_BIG_SEGMENT;  // larger selections use 1024-thread blocks
+// k_gather block size: one wavefront per block for launches of many kept
+// rows, larger blocks for launches of at most kGatherFewItems work items
+// (with other batches' scoring in flight, the few-row launches finish their
+// share sooner in larger blocks; a long one of one-wavefront blocks
+// interleaves better).
 #ifndef MSAO_GATHER_BLOCK
 #define MSAO_GATHER_BLOCK 64
 #endif
 constexpr int kGatherBlock = MSAO_GATHER_BLOCK;
+#ifndef MSAO_GATHER_BLOCK_FEW
+#define MSAO_GATHER_BLOCK_FEW 512
+#endif
+constexpr int kGatherBlockFew = MSAO_GATHER_BLOCK_FEW;
+#ifndef MSAO_GATHER_FEW_ITEMS
+#define MSAO_GATHER_FEW_ITEMS 98304
+#endif
+constexpr int kGatherFewItems = MSAO_GATHER_FEW_ITEMS;
 #ifndef MSAO_GATHER_ROWS
 #define MSAO_GATHER_ROWS 1
 #endif

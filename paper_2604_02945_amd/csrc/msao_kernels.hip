@@ -2119,10 +2119,11 @@ __device__ void gather_rows_generic(const GatherArgs& a, const DevSeg& sg, int j
     }
 }
 
-__global__ __launch_bounds__(kGatherBlock) void k_gather(GatherArgs a)
+template <int NT>
+__global__ __launch_bounds__(NT) void k_gather(GatherArgs a)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int w = uniform(blockIdx.x * (kGatherBlock / kWave) + (threadIdx.x >> 6));
+    const int w = uniform(blockIdx.x * (NT / kWave) + (threadIdx.x >> 6));
     if (w >= a.t.n_gwi) return;
     const int s = uniform(a.t.gi_seg[w]);
     const DevSeg sg = a.t.seg[s];
@@ -2318,9 +2319,14 @@ int launch_head(const HeadArgs& a, void* stream, void* ev0, void* ev1)
 int launch_gather(const GatherArgs& a, void* stream, void* ev0, void* ev1)
 {
     if (a.t.n_gwi <= 0) return kNoLaunch;
-    const int waves = kGatherBlock / kWave;
+    if (a.t.n_gwi <= kGatherFewItems) {
+        constexpr int waves = kGatherBlockFew / kWave;
+        const unsigned grid = (unsigned)((a.t.n_gwi + waves - 1) / waves);
+        return launch(k_gather<kGatherBlockFew>, dim3(grid), dim3(kGatherBlockFew), 0, stream, a, ev0, ev1);
+    }
+    constexpr int waves = kGatherBlock / kWave;
     const unsigned grid = (unsigned)((a.t.n_gwi + waves - 1) / waves);
-    return launch(k_gather, dim3(grid), dim3(kGatherBlock), 0, stream, a, ev0, ev1);
+    return launch(k_gather<kGatherBlock>, dim3(grid), dim3(kGatherBlock), 0, stream, a, ev0, ev1);
 }
 
 }  // namespace msao
