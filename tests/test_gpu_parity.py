@@ -425,6 +425,18 @@ def test_mid_size_selection_split_threshold(n_seg, dev):
     run_and_compare(segs, R, default_params(), dev)
 
 
+@pytest.mark.parametrize("keep", [0.49, 0.5])
+def test_gather_block_switch(keep, dev):
+    """A segment of 200,000 narrow rows keeping 98,001 (gather blocks of eight
+    wavefronts) or 100,000 (one-wavefront blocks, above 98,304 rows) beside
+    a small image: compacted rows byte-exact either way."""
+    rng = np.random.default_rng(int(keep * 100))
+    segs = [_rand_seg(rng, 0, AUDIO, 1, 200_000, 8, "bf16", keep, "relu_bg"),
+            _rand_seg(rng, 0, IMAGE, 1, 300, 256, "bf16", 0.3)]
+    log(f"[parity] gather of {int(200_000 * keep)} rows")
+    run_and_compare(segs, 1, default_params(), dev)
+
+
 def test_plan_runs_match_oracle(dev):
     """msao_plan_create once, msao_plan_run several times (data rewritten in
     place between runs): every run matches the oracle on that run's data."""
