@@ -38,6 +38,7 @@ struct msao_ctx {
     int xcd_order = -1;         // scoring block order: -1 automatic, 0 dispatch order, 1 one range per XCD
     int clip_fuse = 1;          // the SimHash run scores and hashes its clips in one pass (k_clip)
     int pair_path = 1;          // bf16 clips with rows of at most 2 KiB are scored by k_pair
+    int post_big_segment = kPostBigSegment;  // selections this large take 1024-thread blocks
 };
 
 namespace {
@@ -134,6 +135,7 @@ struct Plan {
     int64_t ntok = 0, nframes = 0;
     int n_wi = 0, n_gwi = 0;
     int max_n = 0;                 // largest selection (LDS key staging)
+    int big_seg = kPostBigSegment; // selections this large take 1024-thread blocks
     std::vector<SelUnit> sel_unit; // one selection block each: a segment, or a frame (per-frame scope)
     std::vector<int32_t> hi_seg;   // SimHash calls: segment of each hash tile
     bool any_temporal = false, any_guided = false;
@@ -216,6 +218,7 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
                 bool select_imp = false)
 {
     const bool per_frame = (p->flags & MSAO_FLAG_SELECT_PER_FRAME) != 0;
+    pl.big_seg = ctx ? ctx->post_big_segment : kPostBigSegment;
     pl.sel_unit.clear();
     pl.hi_seg.clear();
     pl.max_n = 0;
@@ -302,7 +305,7 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         const int kind = by_imp ? kKeyImp
                          : d.temporal && d.L_t > 0 ? (d.L_s > 0 ? kKeyFull : kKeyE) : (d.L_s > 0 ? kKeyZ : kKeyZero);
         auto push_selection = [&](int frame, int n_u, int kfix) {
-            const int parts = n_u >= kPostBigSegment            ? (n_u + kSelBigPartTokens - 1) / kSelBigPartTokens
+            const int parts = n_u >= pl.big_seg                 ? (n_u + kSelBigPartTokens - 1) / kSelBigPartTokens
                               : n_u >= kSelSplitMin && split_mid ? (n_u + kSelPartTokens - 1) / kSelPartTokens
                                                                  : 1;
             for (int q = 0; q < parts; ++q) {
@@ -893,6 +896,7 @@ msao_status msao_create(msao_ctx** out, int device)
     if (const char* v = std::getenv("MSAO_XCD_ORDER")) c->xcd_order = std::atoi(v) < 0 ? -1 : (std::atoi(v) ? 1 : 0);
     if (const char* v = std::getenv("MSAO_CLIP_FUSE")) c->clip_fuse = std::atoi(v) ? 1 : 0;
     if (const char* v = std::getenv("MSAO_PAIR")) c->pair_path = std::atoi(v) ? 1 : 0;
+    if (const char* v = std::getenv("MSAO_POST_BIG_SEGMENT")) c->post_big_segment = std::max(1, std::atoi(v));
     *out = c;
     return MSAO_OK;
 }
@@ -1082,6 +1086,7 @@ msao_status msao_select_tokens(msao_ctx* ctx, const msao_segment* segs, int n, i
     pa.mas_in = mas;
     pa.n_sel_blocks = (int)pl.sel_unit.size();
     pa.keys_cap = std::min(pl.max_n, kMaxLdsKeys);
+    pa.big_block = pl.max_n >= pl.big_seg ? 1 : 0;
     return launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa);
 }
 
@@ -1357,6 +1362,7 @@ msao_status enqueue_run(msao_ctx* ctx, const Plan& pl, const Tables& t, const ms
     pa.n_frame_blocks = want_frames ? (int)pl.nframes : 0;
     pa.n_sel_blocks = (int)pl.sel_unit.size();
     pa.keys_cap = std::min(pl.max_n, kMaxLdsKeys);
+    pa.big_block = pl.max_n >= pl.big_seg ? 1 : 0;
     MSAO_TRY(launched(ctx, MSAO_KERNEL_POST, st, run_post, &pa));
     if (!out || t.n_gwi == 0) return MSAO_OK;
     GatherArgs ga;
@@ -1534,6 +1540,7 @@ msao_status msao_run_learned(msao_ctx* ctx, const msao_segment* segs, int n, int
     ps.mas_in = mas_ws;
     ps.n_sel_blocks = (int)pl.sel_unit.size();
     ps.keys_cap = std::min(pl.max_n, kMaxLdsKeys);
+    ps.big_block = pl.max_n >= pl.big_seg ? 1 : 0;
     MSAO_TRY(launched(ctx, MSAO_KERNEL_POST, st, run_post, &ps));
     if (!out || t.n_gwi == 0) return MSAO_OK;
     GatherArgs ga;

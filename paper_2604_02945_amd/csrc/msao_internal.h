@@ -209,6 +209,7 @@ struct PostArgs {
     int32_t n_frame_blocks;// then one per temporal frame
     int32_t temporal_only;// request role writes only the temporal term
     int32_t keys_cap;     // selection keys staged in LDS per block (larger segments re-read z, d)
+    int32_t big_block;    // 1: the launch's selections take 1024-thread blocks
     // learned calls: head counts and descriptors feed Eq. 4, Eq. 6 gives alpha
     int32_t learned;
     int32_t use_mlp;

@@ -2283,10 +2283,11 @@ static int launch_post_nt(const PostArgs& a, int blocks, size_t lds, void* strea
     return launch(k_post<NT, LR>, dim3((unsigned)blocks), dim3(NT), lds, stream, a, ev0, ev1);
 }
 
-// Segments of kPostBigSegment tokens or more are selected by 1024-thread
-// blocks (their loops are latency-bound with one wavefront per SIMD);
-// otherwise kPostBlock threads, which leave room for the scoring of other
-// batches in flight.
+// Launches with a selection of kPostBigSegment tokens or more (the host's
+// big_block; the threshold can be changed at context creation) take
+// 1024-thread blocks (their loops are latency-bound with one wavefront per
+// SIMD); otherwise kPostBlock threads, which leave room for the scoring of
+// other batches in flight.
 int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1)
 {
     const int blocks = a.n_req_blocks + a.n_frame_blocks + a.n_sel_blocks;
@@ -2294,7 +2295,7 @@ int launch_post(const PostArgs& a, void* stream, void* ev0, void* ev1)
     const size_t lds = (size_t)(a.keys_cap + cand_cap_for(a.keys_cap)) * sizeof(uint64_t);
     if (a.learned && (!a.t.partial_x || !a.t.head_count || (a.use_mlp && !a.mlp_u))) return (int)hipErrorInvalidValue;
     if (a.learned) return launch_post_nt<kPostBlock, true>(a, a.n_req_blocks + a.n_frame_blocks, lds, stream, ev0, ev1);
-    if (a.n_sel_blocks > 0 && a.keys_cap >= kPostBigSegment)
+    if (a.n_sel_blocks > 0 && a.big_block)
         return launch_post_nt<1024, false>(a, blocks, lds, stream, ev0, ev1);
     return launch_post_nt<kPostBlock, false>(a, blocks, lds, stream, ev0, ev1);
 }

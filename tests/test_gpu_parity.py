@@ -425,6 +425,23 @@ def test_mid_size_selection_split_threshold(n_seg, dev):
     run_and_compare(segs, R, default_params(), dev)
 
 
+@pytest.mark.parametrize("big", ["1073741824", "1024"])
+def test_selection_block_size_knob(big, dev, monkeypatch):
+    """MSAO_POST_BIG_SEGMENT moves the threshold of the 1024-thread selection
+    blocks: above every selection (the video clips then take 256-thread
+    blocks and parts of 768 tokens), or down to 1,024 tokens (the tri-modal
+    audio selections take the large blocks). Same results as the oracle."""
+    monkeypatch.setenv("MSAO_POST_BIG_SEGMENT", big)
+    ctx = B.Context(0)
+    segs = make_workload(3, n_requests=3).segments + make_workload(4, n_requests=2).segments
+    segs = [Segment(s.request + (3 if s.modality != VIDEO else 0), s.modality, s.n_frames, s.tokens_per_frame,
+                    s.hidden, s.dtype, s.keep_ratio, s.data) for s in segs]
+    log(f"[parity] MSAO_POST_BIG_SEGMENT={big}")
+    run_and_compare(segs, 5, default_params(), dev, ctx=ctx)
+    run_and_compare(segs, 5, default_params(), dev, ctx=ctx, compact=False)
+    ctx.close()
+
+
 @pytest.mark.parametrize("keep", [0.49, 0.5])
 def test_gather_block_switch(keep, dev):
     """A segment of 200,000 narrow rows keeping 98,001 (gather blocks of eight
