@@ -764,6 +764,22 @@ def config_block(c, args, dev):
     res = {"workload": f"{CONFIG_NAMES[c]} (config {c})", "requests": w.n_requests, "segments": len(w.segments),
            "tokens": w.n_tokens, "input_bytes": w.input_bytes}
     res.update(measure(w, args, dev, args.streams, max_replicas=128 if c != 1 else 100))
+    if max(s.n_tokens for s in w.segments) >= 4096:
+        # the other trade of the selection of large segments: 256-thread blocks
+        # (throughput with batches in flight) instead of 1024-thread ones (latency)
+        knob, prev = "MSAO_POST_BIG_SEGMENT", os.environ.get("MSAO_POST_BIG_SEGMENT")
+        os.environ[knob] = str(2**31 - 1)
+        try:
+            t = measure(w, args, dev, args.streams, with_compact=False)["score_select"]
+        finally:
+            if prev is None:
+                os.environ.pop(knob)
+            else:
+                os.environ[knob] = prev
+        res["score_select_throughput_mode"] = {
+            "knob": f"{knob}={2**31 - 1} (every selection in 256-thread blocks)",
+            **{k: t[k] for k in ("ms_per_step", "ms_per_step_one_stream_median", "tokens_per_s", "hbm_frac",
+                                 "hbm_frac_one_stream_median", "kernel_ms")}}
     if not args.no_cpu_baseline:
         sample = {1: None, 2: 8, 3: 1, 5: 4}.get(c)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds / 4, sample)
