@@ -160,7 +160,17 @@ typedef struct {
 
 /* ---- context and helpers (host only) ------------------------------------ */
 
-/* Create a context bound to HIP device `device`. MSAO_ERR_HIP if it is absent. */
+/* Create a context bound to HIP device `device`. MSAO_ERR_HIP if it is absent.
+ * Tuning read from the environment at creation (launch shapes only: every
+ * output is the same for any value): MSAO_ROW_ITEM_BYTES (bytes of rows per
+ * scoring wavefront, 8192), MSAO_CHAIN_FRAMES (frames per wavefront of the
+ * chain pass over clips, 0 = automatic), MSAO_XCD_ORDER (scoring block order:
+ * -1 automatic, 0 dispatch order, 1 one range per XCD), MSAO_CLIP_FUSE (1:
+ * the run with SimHash scores and hashes its clips in one pass), MSAO_PAIR
+ * (1: bf16 clips with rows of 512 to 2,048 bytes take the paired pass) and
+ * MSAO_POST_BIG_SEGMENT (selections of at least this many tokens take
+ * 1,024-thread blocks, 4096: lower latency per batch; a larger value favours
+ * throughput with several batches in flight). */
 msao_status msao_create(msao_ctx** ctx, int device);
 /* Destroy a context (NULL is ignored). Waits for the context's pending uploads. */
 void msao_destroy(msao_ctx* ctx);
