@@ -376,13 +376,14 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
         if (d.temporal && !d.fused && !learned && !d.copy_in_score && (!ctx || ctx->pair_path) && s.dtype == MSAO_BF16 &&
             row_bytes <= kPairMaxRowBytes && row_bytes % 512 == 0 && s.tokens_per_frame >= 2 &&
             d.stride_bytes + row_bytes <= (1 << 30)) {
-            // k_pair: kPairWaves frame ranges of per_item frames per block of one
-            // pair of positions, tblk blocks along the clip (a block after the
-            // first reads the frame before its range as a halo)
-            const int F = s.n_frames <= kPairWaves * kPairMaxFrames ? (s.n_frames + kPairWaves - 1) / kPairWaves
-                                                                    : kPairMaxFrames;
-            const int tblk = (s.n_frames + kPairWaves * F - 1) / (kPairWaves * F);
-            const int64_t pitems = (int64_t)kPairWaves * ((s.tokens_per_frame + 1) / 2) * tblk;
+            // k_pair: one wavefront per pair of positions and range of at most
+            // kPairMaxFrames frames (a range after the first reads the frame
+            // before it as a halo), the items rounded up to whole blocks (the
+            // extra ones have no frames)
+            const int F = std::min(s.n_frames, kPairMaxFrames);
+            const int tblk = (s.n_frames + F - 1) / F;
+            const int64_t pitems =
+                ((int64_t)((s.tokens_per_frame + 1) / 2) * tblk + kPairWaves - 1) / kPairWaves * kPairWaves;
             if (pitems <= N) {
                 d.pair = 1;
                 d.tblk = tblk;

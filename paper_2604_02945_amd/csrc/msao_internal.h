@@ -59,8 +59,8 @@ struct DevSeg {
     uint64_t key_ms, key_mt;
     int32_t cl_begin, ntiles;
     // a bf16 clip with rows of at most 2 KiB scored by k_pair: a wavefront
-    // takes two adjacent positions (per_item frames of them), a block four
-    // consecutive frame ranges; tblk blocks of 4 per_item frames cover a clip
+    // takes two adjacent positions over a range of per_item frames (tblk
+    // ranges cover the clip; its items are rounded up to whole blocks)
     int32_t pair, tblk;
 };
 
@@ -340,15 +340,18 @@ constexpr int kScoreBlock = 256;   // 4 wavefronts, one work item each
 #ifndef MSAO_PAIR_WAVES
 #define MSAO_PAIR_WAVES 4
 #endif
-constexpr int kPairWaves = MSAO_PAIR_WAVES;   // frame ranges of one pair of positions per k_pair block
-// k_pair's occupancy target (wavefronts per SIMD), whatever the block size:
-// its three frames of registers need about 125 VGPRs
-constexpr int kPairWavesPerEU = 4;
+// k_pair block: wavefronts on consecutive pairs of positions over the same
+// frames (four: a clip batch of 1,024 wavefronts puts one on every SIMD)
+constexpr int kPairWaves = MSAO_PAIR_WAVES;
+// k_pair's register budget: a ring of four frames needs about 146 VGPRs
+constexpr int kPairWavesPerEU = 2;
+constexpr int kPairRing = 4;                  // frames in registers per k_pair wavefront (even)
 constexpr int kPairMaxRowBytes = 2048;        // rows k_pair takes: four 512-byte units per half-wavefront
 #ifndef MSAO_PAIR_MAX_FRAMES
-#define MSAO_PAIR_MAX_FRAMES 16
+#define MSAO_PAIR_MAX_FRAMES 32
 #endif
 constexpr int kPairMaxFrames = MSAO_PAIR_MAX_FRAMES;  // frames per k_pair wavefront (the token buffer holds 2 per frame)
+static_assert(kPairMaxFrames >= 1 && kPairMaxFrames <= 32, "k_pair parks two tokens per frame in 64 lanes");
 #ifndef MSAO_POST_BLOCK
 #define MSAO_POST_BLOCK 256
 #endif

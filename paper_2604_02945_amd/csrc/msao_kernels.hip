@@ -767,25 +767,25 @@ __global__ __launch_bounds__(kScoreBlock) __attribute__((amdgpu_waves_per_eu(5, 
 // ---------------------------------------------------------------- k_pair
 
 // bf16 clips whose rows are 512, 1024, 1536 or 2048 bytes (and that are not
-// kept whole, whose rows the chain pass copies out). A wavefront takes
-// two adjacent patch positions p0, p0 + 1 over a range of frames: lanes 0-31
-// hold the first position's row of a frame, lanes 32-63 the second's, so each
-// frame is one run of consecutive rows (4 KiB for 1024 channels). A block's
-// kPairWaves wavefronts take consecutive frame ranges of the same two
-// positions; the first frame of every range but the first has its
-// predecessor in the wavefront before, which derives that frame's temporal
-// terms at the end from a copy of the frame that its owner left in LDS (no
-// frame is read twice). Frames rotate through three register sets: the
-// current one, its predecessor, and the next one in flight; the frame after
-// that is loaded into the predecessor's registers once they are used. Per
-// channel the arithmetic is vector-only: the activity sign of tau - |x| as
-// packed 16-bit differences, four of them gathered into one word of 0x00/0xFF
-// bytes whose popcount (/8) gives the active count and, XOR the previous
-// frame's word, the changed count d; L1 and L2 as bf16 pair dot products; res
-// from the widened values of this and the previous frame. Half-wavefront sums
-// end in lanes 31 and 63 and are parked in a token buffer (lane 2i + h: frame
-// t0 + i, position p0 + h), written out once per wavefront, so the frame loop
-// issues no stores and every wait in it is for one known load.
+// kept whole, whose rows the chain pass copies out). A wavefront takes two
+// adjacent patch positions p0, p0 + 1 over a range of up to 32 frames: lanes
+// 0-31 hold the first position's row of a frame, lanes 32-63 the second's, so
+// each frame is one run of consecutive rows (4 KiB for 1024 channels), and a
+// block's kPairWaves wavefronts take consecutive pairs of positions over the
+// same frames. The frames of a range follow one another in a ring of
+// kPairRing register sets: frame t is scored against its predecessor in the
+// set before it, and once a unit of that predecessor has been used the same
+// unit of frame t + kPairRing - 1 is loaded into its registers, so two frames
+// beyond the next are in flight while one is scored. A range after a clip's
+// first reads the frame before it (halo). Per channel the arithmetic is
+// vector-only: the activity sign of tau - |x| as packed 16-bit differences,
+// four of them gathered into one word of 0x00/0xFF bytes whose popcount (/8)
+// gives the active count and, XOR the previous frame's word, the changed
+// count d; L1 and L2 as bf16 pair dot products; res from the widened values
+// of this and the previous frame. Half-wavefront sums end in lanes 31 and 63
+// and are parked in a token buffer (lane 2i + h: frame t0 + i, position
+// p0 + h), written out once per wavefront, so the frame loop issues no stores
+// and every wait in it is for one known load.
 
 typedef short s16x2 __attribute__((ext_vector_type(2)));
 
@@ -930,19 +930,20 @@ __device__ __forceinline__ void pair_write(const ScoreArgs& a, const DevSeg& sg,
     }
 }
 
-// Work item q of a k_pair segment (wavefront wv of its block).
+// Work item q of a k_pair segment: pair j = q mod the pair count, range
+// q / the pair count (none past the clip's end: the items of a segment are
+// rounded up to whole blocks).
 template <int NU>
-__device__ __forceinline__ void score_pair(const ScoreArgs& a, const DevSeg& sg, int q, int wv, int lane,
-                                           uint32_t* lds, uint32_t& nsp, uint32_t& dsum)
+__device__ __forceinline__ void score_pair(const ScoreArgs& a, const DevSeg& sg, int q, int lane, uint32_t& nsp,
+                                           uint32_t& dsum)
 {
-    constexpr int ND = NU * 4;
+    constexpr int RING = kPairRing;
+    static_assert(RING % 2 == 0 && RING >= 2, "activity words alternate between two sets with the frame's parity");
     const int npairs = (sg.P + 1) >> 1;
-    const int qb = q / kPairWaves;
-    const int tbi = uniform(qb / npairs), j = uniform(qb - (qb / npairs) * npairs);
+    const int tbi = uniform(q / npairs), j = uniform(q - (q / npairs) * npairs);
     const int F = uniform(sg.per_item);
-    const int tb = tbi * kPairWaves * F;
-    const int tend = uniform(min(sg.T, tb + kPairWaves * F));
-    const int t0 = uniform(min(tend, tb + wv * F)), t1 = uniform(min(tend, t0 + F));
+    const int t0 = uniform(min(sg.T, tbi * F)), t1 = uniform(min(sg.T, t0 + F));
+    if (t0 >= t1) return;
     const int p0 = uniform(2 * j);
     const int h = lane >> 5, l = lane & 31;
     const bool two = uniform(p0 + 1 < sg.P ? 1 : 0) != 0;
@@ -954,7 +955,7 @@ __device__ __forceinline__ void score_pair(const ScoreArgs& a, const DevSeg& sg,
     // unit u of this lane's row at voff + 512 u; a missing second position
     // reads as zeros (an offset past the resource)
     const int voff = present ? h * (int)sg.stride_bytes + l * 16 : 0x7FFFFFF0;
-    // a frame past the range reads as zeros from an empty resource: every
+    // a frame outside the range reads as zeros from an empty resource: every
     // load is issued, so the waits count them exactly
     auto frame_rsrc = [&](int t, bool ok) {
         return make_rsrc(base + (ok ? (int64_t)t * fstride : 0), ok ? nrec : 0);
@@ -966,106 +967,56 @@ __device__ __forceinline__ void score_pair(const ScoreArgs& a, const DevSeg& sg,
     };
     const uint32_t lo = bf16_thresholds(a.t.tau).lo;
     const uint32_t th2 = lo | (lo << 16);
-    // ranges after a block's first leave their first frame's temporal terms to
-    // the wavefront before; the first range of a block after the clip's first
-    // reads the frame before it (halo); the clip's frame 0 follows the zero frame
-    const bool deferred = wv > 0 && t0 < t1;
     PairTok tok{0.0f, 0.0f, 0.0f, 0u};
-    // frame t in cur, its predecessor in prev; unit u of frame t + 2 is loaded
-    // into prev's registers once unit u of prev has been used
-    auto step = [&](const vec4 (&cur)[NU], vec4 (&prev)[NU], const uint32_t (&pq)[NU * 2],
-                    uint32_t (&nq)[NU * 2], int t) {
-        const rsrc_t rs = frame_rsrc(t + 2, t + 2 < t1);
-        const PairSums c = pair_frame<NU>(cur, prev, th2, pq, nq, [&](int u) {
-            prev[u] = bload(rs, voff + u * 512);
-            // keep the load here, where its registers have just been freed
-            __builtin_amdgcn_sched_barrier(0);
-        });
-        const PairTok r = pair_reduce(c);
-        const int slot = 2 * (t - t0);
-        const bool at0 = lane == slot, at1 = lane == slot + 1;
-        tok.l1 = park(tok.l1, r.l1, at0, at1);
-        tok.l2 = park(tok.l2, r.l2, at0, at1);
-        tok.res = park(tok.res, r.res, at0, at1);
-        tok.cnt = park(tok.cnt, r.cnt, at0, at1);
-    };
-    vec4 R0[NU], R1[NU], R2[NU], L[NU];
-    uint32_t Q0[NU * 2], Q1[NU * 2], Q2[NU * 2], LQ[NU * 2];
-    auto keep = [&](const vec4 (&v)[NU], const uint32_t (&w)[NU * 2]) {
-        vcopy<NU>(L, v);
+    // frame t0 + i in R[i mod RING] with its activity words in Q[i mod 2];
+    // the frame before t0 (the zero frame before the clip's first) in
+    // R[RING - 1], its words in Q[1]
+    vec4 R[RING][NU];
+    uint32_t Q[2][NU * 2];
+    load(R[RING - 1], t0 - 1, t0 > 0);
 #pragma unroll
-        for (int i = 0; i < NU * 2; ++i) LQ[i] = w[i];
-    };
-    if (t0 < t1) {
-        // the frame before t0 in R2 (its words in Q2), t0 in R0, t0 + 1 in R1
-        load(R2, t0 - 1, wv == 0 && t0 > 0);
-        load(R0, t0, true);
-        load(R1, t0 + 1, t0 + 1 < t1);
-        pair_words<NU>(R2, th2, Q2);
-        if (deferred) {
-            uint32_t* slot = lds + (wv - 1) * ND * kWave;
+    for (int i = 0; i < RING - 1; ++i) load(R[i], t0 + i, t0 + i < t1);
+    pair_words<NU>(R[RING - 1], th2, Q[1]);
+    int t = t0;
+    while (t < t1) {
 #pragma unroll
-            for (int u = 0; u < NU; ++u)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) slot[(u * 4 + e) * kWave + lane] = R0[u][e];
+        for (int i = 0; i < RING; ++i) {
+            if (t >= t1) break;
+            const int pi = (i + RING - 1) % RING;
+            const rsrc_t rs = frame_rsrc(t + RING - 1, t + RING - 1 < t1);
+            const PairSums c = pair_frame<NU>(R[i], R[pi], th2, Q[(i + 1) & 1], Q[i & 1], [&](int u) {
+                R[pi][u] = bload(rs, voff + u * 512);
+                // keep the load here, where its registers have just been freed
+                __builtin_amdgcn_sched_barrier(0);
+            });
+            const PairTok r = pair_reduce(c);
+            const int slot = 2 * (t - t0);
+            const bool at0 = lane == slot, at1 = lane == slot + 1;
+            tok.l1 = park(tok.l1, r.l1, at0, at1);
+            tok.l2 = park(tok.l2, r.l2, at0, at1);
+            tok.res = park(tok.res, r.res, at0, at1);
+            tok.cnt = park(tok.cnt, r.cnt, at0, at1);
+            ++t;
         }
-        // frame t0 + i is in R[i % 3] with its words in Q[i % 3]; the last
-        // frame and its words are kept in L, LQ for the end
-        int t = t0;
-        while (true) {
-            step(R0, R2, Q2, Q0, t);
-            if (++t >= t1) {
-                keep(R0, Q0);
-                break;
-            }
-            step(R1, R0, Q0, Q1, t);
-            if (++t >= t1) {
-                keep(R1, Q1);
-                break;
-            }
-            step(R2, R1, Q1, Q2, t);
-            if (++t >= t1) {
-                keep(R2, Q2);
-                break;
-            }
-        }
-        // the range's tokens: lane 2i + h holds frame t0 + i, position p0 + h
-        const int nslot = 2 * (t1 - t0);
-        const int fi = lane >> 1, hh = lane & 1;
-        const bool mine = lane < nslot && (hh == 0 || two);
-        const bool temporal_ok = !(deferred && fi == 0);
-        const uint32_t act = tok.cnt & 0xFFFFu, dd = tok.cnt >> 16;
-        if (mine) pair_write(a, sg, sg.tok_off + (t0 + fi) * sg.P + p0 + hh, tok, true, temporal_ok);
-        nsp += (uint32_t)__popcll(__ballot(mine && act < (uint32_t)sg.A_s));
-        uint32_t dpart = mine && temporal_ok && t0 + fi >= 1 ? dd : 0u;
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) dpart += (uint32_t)__shfl_xor((int)dpart, o);
-        dsum += dpart;
     }
-    __syncthreads();
-    // the next range's first frame against this range's last (frame t1 - 1)
-    if (wv < kPairWaves - 1 && t1 == t0 + F && t1 < tend) {
-        const uint32_t* slot = lds + wv * ND * kWave;
-        vec4 nx[NU];
+    // the range's tokens: lane 2i + h holds frame t0 + i, position p0 + h
+    const int nslot = 2 * (t1 - t0);
+    const int fi = lane >> 1, hh = lane & 1;
+    const bool mine = lane < nslot && (hh == 0 || two);
+    const uint32_t act = tok.cnt & 0xFFFFu, dd = tok.cnt >> 16;
+    if (mine) pair_write(a, sg, sg.tok_off + (t0 + fi) * sg.P + p0 + hh, tok, true, true);
+    nsp += (uint32_t)__popcll(__ballot(mine && act < (uint32_t)sg.A_s));
+    uint32_t dpart = mine && t0 + fi >= 1 ? dd : 0u;
 #pragma unroll
-        for (int u = 0; u < NU; ++u)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) nx[u][e] = slot[(u * 4 + e) * kWave + lane];
-        const PairSums c = pair_frame<NU>(nx, L, th2, LQ, Q1, [](int) {});
-        const PairTok r = pair_reduce(c);
-        if (l == 31 && present) pair_write(a, sg, sg.tok_off + t1 * sg.P + p0 + h, r, false, true);
-        const uint32_t d0 = (uint32_t)__builtin_amdgcn_readlane((int)(r.cnt >> 16), 31);
-        const uint32_t d1 = two ? (uint32_t)__builtin_amdgcn_readlane((int)(r.cnt >> 16), 63) : 0u;
-        dsum += d0 + d1;
-    }
+    for (int o = 32; o >= 1; o >>= 1) dpart += (uint32_t)__shfl_xor((int)dpart, o);
+    dsum += dpart;
 }
 
 // One wavefront per k_pair work item; consecutive blocks (neighbouring pairs
 // of positions, whose statistics share cache lines) run on one XCD.
-__global__ __launch_bounds__(kPairWaves * 64) __attribute__((amdgpu_waves_per_eu(kPairWavesPerEU, kPairWavesPerEU)))
+__global__ __launch_bounds__(kPairWaves * 64) __attribute__((amdgpu_waves_per_eu(1, kPairWavesPerEU)))
 void k_pair(ScoreArgs a)
 {
-    __shared__ uint32_t lds[(kPairWaves - 1) * (kPairMaxRowBytes / 128) * kWave];
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = uniform(threadIdx.x >> 6);
     const int nb = gridDim.x, b = blockIdx.x, x = b & 7, per = nb >> 3, rem = nb & 7;
@@ -1076,10 +1027,10 @@ void k_pair(ScoreArgs a)
     const int q = w - sg.wi_begin;
     uint32_t nsp = 0, dsum = 0;  // wave-uniform
     switch (sg.nchunk >> 5) {  // rows of 512-byte units
-    case 1: score_pair<1>(a, sg, q, wv, lane, lds, nsp, dsum); break;
-    case 2: score_pair<2>(a, sg, q, wv, lane, lds, nsp, dsum); break;
-    case 3: score_pair<3>(a, sg, q, wv, lane, lds, nsp, dsum); break;
-    default: score_pair<4>(a, sg, q, wv, lane, lds, nsp, dsum); break;
+    case 1: score_pair<1>(a, sg, q, lane, nsp, dsum); break;
+    case 2: score_pair<2>(a, sg, q, lane, nsp, dsum); break;
+    case 3: score_pair<3>(a, sg, q, lane, nsp, dsum); break;
+    default: score_pair<4>(a, sg, q, lane, nsp, dsum); break;
     }
     if (lane == 0) {
         Partial pr;

@@ -1,11 +1,12 @@
 """GPU parity of k_pair, the scoring pass of bf16 clips whose rows are 512,
-1024, 1536 or 2048 bytes (two patch positions per wavefront, consecutive frame
-ranges per block, the first frame of a range finished by the wavefront before
-it), against the CPU oracle on seeded inputs.
+1024, 1536 or 2048 bytes (two patch positions per wavefront over a range of up
+to 32 frames, consecutive pairs of positions per block, a ring of four frames
+in registers), against the CPU oracle on seeded inputs.
 
 Covers every row width it takes, odd position counts (the last pair holds one
-position), clips shorter than a block's four ranges, clips long enough for
-several blocks along time (the halo frame), padded row strides, identical and
+position), pair counts that leave a block part empty, clips shorter than the
+ring, clips long enough for several ranges (the halo frame before each range
+after the first), padded row strides, identical and
 all-zero frames, a batch that mixes k_pair clips with clips and segments of the
 other paths (two scoring launches), the temporal-only entry point, and the
 same tables with k_pair switched off (MSAO_PAIR=0). Same bar as the other
@@ -33,16 +34,16 @@ def _clips(seed, shapes, kind="normal", keep=0.3):
 @pytest.mark.parametrize("C", [256, 512, 768, 1024])
 def test_row_widths_odd_positions(C, dev):
     """Rows of 1 to 4 units of 512 bytes, odd and even position counts, 2 to 9
-    frames (two frames of an odd position count take the chain pass: a block
-    of four ranges would need more work items than the clip has tokens)."""
+    frames (five pairs of positions: three wavefronts of the second block have
+    no frames)."""
     segs = _clips(10 + C, [(2, 8, C), (3, 7, C), (5, 9, C), (9, 2, C), (2, 7, C)])
     log(f"[pair] widths C={C}")
     run_and_compare(segs, 3, default_params(), dev)
 
 
 def test_long_clips_several_time_blocks(dev):
-    """70 and 130 frames: ranges of 16 frames, blocks of 64 frames along the
-    clip, each block after the first reading the frame before it."""
+    """70, 130, 64 and 65 frames: ranges of 32 frames (the last one of 6, 2, 32
+    and 1), each range after the first reading the frame before it."""
     segs = _clips(31, [(70, 5, 1024), (130, 4, 512), (64, 3, 1024), (65, 2, 256)], kind="static_video")
     log("[pair] long clips")
     run_and_compare(segs, 3, default_params(), dev)
