@@ -253,9 +253,12 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
     pl.tseg.clear();
     int64_t tok = 0, frame = 0;
     int wi = 0, gi = 0;
-    int64_t chains_total = 0;
+    int64_t chains_total = 0, pairs_total = 0;
     for (int i = 0; i < n; ++i)
-        if (is_temporal(segs[i])) chains_total += segs[i].tokens_per_frame;
+        if (is_temporal(segs[i])) {
+            chains_total += segs[i].tokens_per_frame;
+            pairs_total += (segs[i].tokens_per_frame + 1) / 2;
+        }
     // selections before any split: mid-size ones are split only while the
     // launch would otherwise leave CUs without a selection block
     int64_t whole_sels = 0;
@@ -380,7 +383,10 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
             // kPairMaxFrames frames (a range after the first reads the frame
             // before it as a halo), the items rounded up to whole blocks (the
             // extra ones have no frames)
-            const int F = std::min(s.n_frames, kPairMaxFrames);
+            int F = std::min(s.n_frames, kPairMaxFrames);
+            // shorter ranges (each after the first re-reads one frame) while the
+            // batch's pairs would leave SIMDs without a k_pair wavefront
+            while (F > kPairMinFrames && pairs_total * ((s.n_frames + F - 1) / F) < kPairTargetWaves) F = (F + 1) / 2;
             const int tblk = (s.n_frames + F - 1) / F;
             const int64_t pitems =
                 ((int64_t)((s.tokens_per_frame + 1) / 2) * tblk + kPairWaves - 1) / kPairWaves * kPairWaves;

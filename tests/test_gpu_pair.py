@@ -114,3 +114,15 @@ def test_pair_off_same_results(dev, monkeypatch):
         ctx.close()
     for k in ("z", "d", "kept_idx", "keep", "kept_count", "agg", "dframe"):
         assert np.array_equal(outs[0][k], outs[1][k]), k
+
+
+@pytest.mark.parametrize("requests", [1, 2, 4])
+def test_small_video_batches_shorter_ranges(requests, dev):
+    """One, two and four 32-frame clips of 256 positions: too few pairs of
+    positions to give every SIMD a wavefront, so the planner halves the
+    frame ranges (8, 8 and 16 frames: each range after the first re-reads
+    the frame before it)."""
+    from workloads import make_workload
+    w = make_workload(3, n_requests=requests)
+    log(f"[pair] video batch of {requests} clip(s)")
+    run_and_compare(w.segments, requests, w.params, dev)
