@@ -383,10 +383,26 @@ void build_plan(const msao_ctx* ctx, const msao_segment* segs, int n, int R, con
             // kPairMaxFrames frames (a range after the first reads the frame
             // before it as a halo), the items rounded up to whole blocks (the
             // extra ones have no frames)
+            // the range length (halved from the longest, down to
+            // kPairMinFrames) with the fewest frames read per SIMD: wavefronts
+            // beyond one per SIMD queue behind the first, and a range after a
+            // clip's first re-reads one frame; ties keep the longer range
             int F = std::min(s.n_frames, kPairMaxFrames);
-            // shorter ranges (each after the first re-reads one frame) while the
-            // batch's pairs would leave SIMDs without a k_pair wavefront
-            while (F > kPairMinFrames && pairs_total * ((s.n_frames + F - 1) / F) < kPairTargetWaves) F = (F + 1) / 2;
+            {
+                int best = F;
+                int64_t best_cost = INT64_MAX;
+                for (int f = F;; f = (f + 1) / 2) {
+                    const int64_t tb = (s.n_frames + f - 1) / f;
+                    const int64_t rounds = (pairs_total * tb + kPairTargetWaves - 1) / kPairTargetWaves;
+                    const int64_t cost = rounds * (f + (tb > 1 ? 1 : 0));
+                    if (cost < best_cost) {
+                        best_cost = cost;
+                        best = f;
+                    }
+                    if (f <= kPairMinFrames) break;
+                }
+                F = best;
+            }
             const int tblk = (s.n_frames + F - 1) / F;
             const int64_t pitems =
                 ((int64_t)((s.tokens_per_frame + 1) / 2) * tblk + kPairWaves - 1) / kPairWaves * kPairWaves;

@@ -352,8 +352,8 @@ constexpr int kPairMaxRowBytes = 2048;        // rows k_pair takes: four 512-byt
 #endif
 constexpr int kPairMaxFrames = MSAO_PAIR_MAX_FRAMES;  // frames per k_pair wavefront (the token buffer holds 2 per frame)
 static_assert(kPairMaxFrames >= 1 && kPairMaxFrames <= 32, "k_pair parks two tokens per frame in 64 lanes");
-// small batches: ranges longer than kPairMinFrames frames are halved until
-// the batch's k_pair wavefronts reach kPairTargetWaves (one per SIMD)
+// k_pair range length: halved from kPairMaxFrames down to kPairMinFrames to
+// spread a batch's frames evenly over kPairTargetWaves SIMDs
 constexpr int kPairMinFrames = 8;
 constexpr int kPairTargetWaves = 1024;
 #ifndef MSAO_POST_BLOCK
