@@ -2,19 +2,24 @@
 // analysis (Sec. 4.1) and of the MAS-guided token selection it drives.
 //
 // The path is HBM-bandwidth bound: every input byte is read once with 128-bit
-// loads, no step is a dense contraction (no MFMA). Three launches:
-//   k_score  one wavefront per work item (a run of rows, or one patch's run
-//            of frames). Per token: activity count by ballot + scalar
-//            popcount, L1/L2 by DPP wave reductions; for video the previous
-//            frame's values and activity masks stay in registers, so the
-//            temporal term (Eq. 5) costs no extra HBM traffic. Per work item
-//            it writes integer partials (sparse-token count, sum of d), so no
-//            atomics and no zeroing are needed and results are bit-stable.
+// loads, no step is a dense contraction (no MFMA). Three launch slots:
+//   scoring  k_pair for bf16 clips with rows of 512-2,048 bytes (a wavefront
+//            streams two neighbouring patch positions through a range of
+//            frames, a ring of frames in registers), k_score for the rest
+//            (one wavefront per work item: a run of rows, or one patch's run
+//            of frames). Per token: active count, L1/L2 and, for video, the
+//            temporal terms of Eq. 5 against the previous frame, whose values
+//            and activity bits stay in registers (no extra HBM traffic). Per
+//            work item they write integer partials (sparse-token count, sum
+//            of d), so no atomics and no zeroing are needed and results are
+//            bit-stable. (A call with learned heads launches k_head between
+//            the scoring pass and k_post: the heads' pooling and MLP.)
 //   k_post   block roles: one block per request (integer aggregation, modal
 //            softmax, Eq. 4 ratio, Eq. 7 MAS), one per video frame (Eq. 5
-//            per frame), one per segment (top-k by LDS radix select over
-//            exact integer keys, ties by index, block-scan compaction).
-//   k_gather one wavefront per few kept rows: packed bitwise copy.
+//            per frame), one or more per selection (top-k by LDS radix
+//            select over exact integer keys, ties by index, block-scan
+//            compaction).
+//   k_gather one wavefront per kept row: packed bitwise copy.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
