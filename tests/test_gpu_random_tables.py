@@ -62,9 +62,11 @@ def test_random_table(seed, dev):
 
 def random_pair_table(seed):
     """Tables whose clips mostly take k_pair (bf16, 256 to 1,024 channels):
-    any frame count from 2 to 72 (several blocks along time past 64), odd
-    and even position counts, drifting and redrawn frames, beside a few
-    segments of the other passes."""
+    any frame count from 2 to 72 (ranges of 8 to 32 frames, those after a
+    clip's first reading a halo frame; the range length depends on the
+    whole batch's pairs of positions), odd and even position counts,
+    drifting and redrawn frames, beside a few segments of the other
+    passes."""
     rng = np.random.default_rng(3000 + seed)
     R = int(rng.integers(1, 4))
     segs = []
@@ -90,7 +92,7 @@ def random_pair_table(seed):
     return segs, R, p, pad
 
 
-@pytest.mark.parametrize("seed", range(16))
+@pytest.mark.parametrize("seed", range(32))
 def test_random_pair_table(seed, dev):
     segs, R, p, pad = random_pair_table(seed)
     log(f"[random] pair seed {seed}: {len(segs)} segments, R {R}, flags {p['flags']}, pad {pad}, "
